@@ -1,0 +1,570 @@
+"""Pins for the CPU oracle, against what the paper and mathematics fix.
+
+None of these tests re-types an oracle formula: each checks the oracle
+against a closed form, an invariant, a library routine, brute force on small
+inputs, a value printed in the paper (tests/golden/), or an error bound.
+"""
+import math
+import os
+from decimal import Decimal, getcontext
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.linalg
+
+import workloads
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+U = 2.0 ** -24  # unit roundoff of binary32
+
+
+def gamma(j):
+    return j * U / (1 - j * U)
+
+
+def dense_h(orc, n):
+    """Explicit +-1 H_n = H_{2^k} (x) H_m, the Sylvester factor from scipy."""
+    k, m = orc.hadamard_factor(n)
+    h2 = scipy.linalg.hadamard(2 ** k).astype(np.int64)
+    return np.kron(h2, orc.hm_table(m).astype(np.int64))
+
+
+def times_h(orc, x, exact=False):
+    """x . H_n for rows x.  Small n: dense np.kron matrix.  Large n: the
+    Kronecker identity x (A (x) B) = vec(A^T X B) with X = x reshaped to
+    [2^k, m] (A = scipy's Sylvester matrix), using library matmuls."""
+    n = x.shape[1]
+    dt = np.float64  # exact for integer data while |sums| < 2^53
+    if n <= 4096:
+        out = x.astype(dt) @ dense_h(orc, n).astype(dt)
+    else:
+        k, m = orc.hadamard_factor(n)
+        A = scipy.linalg.hadamard(2 ** k).astype(dt)
+        B = orc.hm_table(m).astype(dt)
+        out = np.empty(x.shape, dt)
+        for r in range(x.shape[0]):
+            X = x[r].astype(dt).reshape(2 ** k, m)
+            out[r] = (A.T @ X @ B).reshape(-1)
+    if exact:
+        assert np.abs(x).max() * n < 2 ** 53
+        return out.astype(np.int64)
+    return out
+
+
+# --------------------------------------------------------------------------
+# number formats
+# --------------------------------------------------------------------------
+
+def test_f16_to_f32_all_values(orc):
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    h = bits.view(np.float16)
+    got = orc.f16_to_f32(h)
+    ref = h.astype(np.float32)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan].view(np.uint32), ref[~nan].view(np.uint32))
+
+
+def test_f32_to_f16_random_and_boundaries(orc):
+    rng = np.random.default_rng(1)
+    parts = [rng.integers(0, 2 ** 32, size=4_000_000, dtype=np.uint64).astype(np.uint32)]
+    # every fp16 value and its midpoints to both neighbours, exactly and
+    # one fp32 ulp around them (ties to even, subnormals, overflow edge)
+    h = np.arange(0, 0x7C01, dtype=np.uint32).astype(np.uint16).view(np.float16)
+    f = h.astype(np.float64)
+    mids = (f[:-1] + f[1:]) / 2
+    mids32 = mids.astype(np.float32)
+    for arr in (f.astype(np.float32), mids32, np.nextafter(mids32, np.float32(0)),
+                np.nextafter(mids32, np.float32(np.inf))):
+        parts.append(arr.view(np.uint32))
+        parts.append((-arr).view(np.uint32))
+    parts.append(np.array([np.float32(65519.996), np.float32(65520.0), np.float32(1e30),
+                           np.float32(2 ** -25), np.float32(2 ** -26), np.float32(3 * 2 ** -26)],
+                          np.float32).view(np.uint32))
+    allbits = np.concatenate(parts)
+    f32 = allbits.view(np.float32)
+    got = orc.f32_to_f16(f32)
+    with np.errstate(over="ignore"):
+        ref = f32.astype(np.float16)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan].view(np.uint16), ref[~nan].view(np.uint16))
+
+
+# --------------------------------------------------------------------------
+# Hadamard matrices (§3.1)
+# --------------------------------------------------------------------------
+
+def test_golden_eq1_h2(orc):
+    rows = []
+    norm = None
+    with open(os.path.join(GOLDEN, "eq1_sylvester_h2.txt")) as fh:
+        for line in fh:
+            if line.startswith("#") or not line.strip():
+                continue
+            tok = line.split()
+            if tok[0] == "row":
+                rows.append([int(t) for t in tok[1:]])
+            elif tok[0] == "normalization":
+                norm = tok[1]
+    assert norm == "1/sqrt(2)"
+    h2 = np.array(rows)
+    got = np.array([[orc.sylvester_entry(i, j) for j in range(2)] for i in range(2)])
+    assert np.array_equal(got, h2)
+    # the recursion of eq. (1): H_{2^n} = H_2 (x) H_{2^(n-1)}
+    h = h2
+    for n in range(2, 8):
+        h = np.kron(h2, h)
+        got = np.array([[orc.sylvester_entry(i, j) for j in range(2 ** n)]
+                        for i in range(2 ** n)])
+        assert np.array_equal(got, h)
+    # normalized H_2 is orthogonal
+    hn = h2 / math.sqrt(2)
+    assert np.allclose(hn @ hn.T, np.eye(2))
+
+
+def test_sylvester_matches_scipy(orc):
+    for k in (1, 3, 6, 9):
+        n = 2 ** k
+        got = np.array([[orc.sylvester_entry(i, j) for j in range(n)] for i in range(n)])
+        assert np.array_equal(got, scipy.linalg.hadamard(n))
+
+
+@pytest.mark.parametrize("m", [1, 12, 20, 28, 108, 172])
+def test_hm_table_is_hadamard(orc, m):
+    H = orc.hm_table(m).astype(np.int64)
+    assert set(np.unique(H)) <= {-1, 1}
+    assert np.array_equal(H @ H.T, m * np.eye(m, dtype=np.int64))
+
+
+@pytest.mark.parametrize("n", [128, 1024, 4096, 24, 56, 344, 160, 432, 3456])
+def test_kronecker_h_is_hadamard(orc, n):
+    H = dense_h(orc, n).astype(np.float64)  # +-1 sums up to n are exact in fp64
+    assert np.array_equal(H @ H.T, n * np.eye(n))
+
+
+def test_kronecker_identity_matches_dense(orc):
+    """The large-n reference (vec(A^T X B)) agrees with the dense kron."""
+    for n in (344, 448, 4096, 3456):
+        x = workloads.random_rows(n, 2, n).astype(np.float64)
+        k, m = orc.hadamard_factor(n)
+        A = scipy.linalg.hadamard(2 ** k).astype(np.float64)
+        B = orc.hm_table(m).astype(np.float64)
+        via_id = np.stack([(A.T @ r.reshape(2 ** k, m) @ B).reshape(-1) for r in x])
+        assert np.allclose(via_id, x @ dense_h(orc, n), rtol=0, atol=1e-9)
+
+
+def test_factorization(orc):
+    with open(os.path.join(GOLDEN, "paper_constants.txt")) as fh:
+        widths = [l.split()[1:] for l in fh if l.startswith("layer_widths")][0]
+    expect = {4096: (12, 1), 5120: (8, 20), 8192: (13, 1), 11008: (6, 172),
+              13824: (7, 108), 28672: (10, 28)}
+    for w in map(int, widths):
+        assert orc.hadamard_factor(w) == expect[w]
+        k, m = expect[w]
+        assert 2 ** k * m == w
+    for bad in (0, 3, 6, 14, 100, 172 * 3, 30):
+        assert orc.hadamard_factor(bad) is None
+
+
+def test_rotation_scale_correctly_rounded(orc):
+    getcontext().prec = 60
+    for n in (2, 128, 4096, 8192, 11008, 28672, 5120, 13824, 172, 28):
+        exact = Decimal(1) / Decimal(n).sqrt()
+        c = orc.rotation_scale(n)
+        # c is the binary32 nearest to 1/sqrt(n)
+        lo = np.nextafter(c, np.float32(0))
+        hi = np.nextafter(c, np.float32(1))
+        d = abs(Decimal(float(c)) - exact)
+        assert d <= abs(Decimal(float(lo)) - exact)
+        assert d <= abs(Decimal(float(hi)) - exact)
+
+
+# --------------------------------------------------------------------------
+# rotation
+# --------------------------------------------------------------------------
+
+def test_rotation_unit_vectors_exact(orc):
+    """x = e_i gives y = c * (row i of H_n): fixes row-vector convention,
+    Kronecker order and every sign (H_172 is not symmetric)."""
+    for n in (128, 56, 344, 160, 432, 48):
+        H = dense_h(orc, n)
+        c = orc.rotation_scale(n)
+        rows = np.arange(n) if n <= 512 else np.arange(0, n, 7)
+        x = np.zeros((len(rows), n), np.float16)
+        x[np.arange(len(rows)), rows] = 1
+        y = orc.rotate_f16(x)
+        ref = (H[rows].astype(np.float64) * np.float64(c)).astype(np.float32)
+        assert np.array_equal(y, ref), n
+
+
+def test_rotation_columns_of_h_give_scaled_basis(orc):
+    """x = column i of H_n: x H_n = n e_i exactly, so y = RN(n c) e_i."""
+    for n in (128, 56, 344, 4096):
+        H = dense_h(orc, n)
+        c = orc.rotation_scale(n)
+        idx = np.random.default_rng(n).choice(n, 8, replace=False)
+        x = H[:, idx].T.astype(np.float16)
+        y = orc.rotate_f16(x)
+        ref = np.zeros((8, n), np.float32)
+        ref[np.arange(8), idx] = np.float32(np.float64(n) * np.float64(c))
+        assert np.array_equal(y, ref)
+
+
+@pytest.mark.parametrize("n", [128, 4096, 8192, 11008, 28672, 5120, 13824, 344, 112])
+def test_rotation_exact_on_small_integers(orc, n):
+    """Small-integer rows keep every partial sum exact in binary32, so the
+    result must equal RN32(c * (x H)) computed with exact integers."""
+    rng = np.random.default_rng(n + 7)
+    rows = 4
+    # keep |partial sums| < 2^24: |x| <= 2^24 / n
+    lim = max(1, min(64, (2 ** 24) // n - 1))
+    x = rng.integers(-lim, lim + 1, size=(rows, n)).astype(np.int64)
+    exact = times_h(orc, x, exact=True)
+    c = np.float64(orc.rotation_scale(n))
+    ref = (exact.astype(np.float64) * c).astype(np.float32)
+    y = orc.rotate_f16(x.astype(np.float16))
+    assert np.array_equal(y, ref)
+
+
+@pytest.mark.parametrize("n,dist", [(128, "normal"), (4096, "normal"), (11008, "student_t3"),
+                                    (8192, "normal"), (28672, "normal"), (344, "uniform"),
+                                    (5120, "normal"), (13824, "normal")])
+def test_rotation_vs_dense_fp64_bound(orc, n, dist):
+    """Brute force: dense fp64 x H / sqrt(n) within the standard summation
+    bound gamma_{k+m} * c * ||x||_1 (+ one rounding of the product)."""
+    rows = 3 if n > 8192 else 6
+    x = workloads.random_rows(n, rows, n, dist)
+    k, m = orc.hadamard_factor(n)
+    ref = times_h(orc, x) / math.sqrt(n)
+    y = orc.rotate_f16(x).astype(np.float64)
+    l1 = np.abs(x.astype(np.float64)).sum(axis=1, keepdims=True)
+    bound = (gamma(k + m) + 2 * U) * l1 / math.sqrt(n)
+    err = np.abs(y - ref)
+    assert np.all(err <= bound)
+    # and a planted mistake of one term would be far outside it
+    assert np.all(np.abs(x.astype(np.float64)).max(axis=1) / math.sqrt(n) > 4 * bound.ravel())
+
+
+@pytest.mark.parametrize("n", [128, 4096, 56, 28 * 16])
+def test_rotation_involution_symmetric_h(orc, n):
+    """Sylvester and the Paley-II H_28 are symmetric, so (H/sqrt n)^2 = I."""
+    k, m = orc.hadamard_factor(n)
+    assert np.array_equal(orc.hm_table(m), orc.hm_table(m).T)
+    x = workloads.random_rows(3, 4, n).astype(np.float32)
+    y2 = orc.rotate_f32(orc.rotate_f32(x))
+    assert np.allclose(y2, x, atol=1e-5 * np.abs(x).max(), rtol=0)
+
+
+@pytest.mark.parametrize("n", [128, 11008, 28672, 13824])
+def test_rotation_preserves_norm(orc, n):
+    x = workloads.random_rows(5, 3, n, "student_t3")
+    y = orc.rotate_f16(x).astype(np.float64)
+    nx = np.linalg.norm(x.astype(np.float64), axis=1)
+    ny = np.linalg.norm(y, axis=1)
+    assert np.allclose(nx, ny, rtol=1e-5)
+
+
+@pytest.mark.parametrize("n", [128, 11008, 28672])
+def test_computational_invariance(orc, n):
+    """§3.4 / §4 Stage 1b: rotating activations and weight rows by the same
+    orthonormal H leaves x w^T unchanged (the transform fused into W)."""
+    x = workloads.random_rows(11, 4, n)
+    w = workloads.random_rows(12, 5, n, scale=0.02)
+    rx = orc.rotate_f16(x).astype(np.float64)
+    rw = orc.rotate_f16(w).astype(np.float64)
+    ref = x.astype(np.float64) @ w.astype(np.float64).T
+    got = rx @ rw.T
+    tol = 1e-5 * np.linalg.norm(x.astype(np.float64), axis=1)[:, None] * \
+        np.linalg.norm(w.astype(np.float64), axis=1)[None, :]
+    assert np.all(np.abs(got - ref) <= tol)
+    # with a transposed factor on one side the identity breaks (H_172 is not symmetric)
+    if n == 11008:
+        k, m = orc.hadamard_factor(n)
+        Hm = orc.hm_table(m).astype(np.float64)
+        assert not np.array_equal(Hm, Hm.T)
+
+
+def test_rotation_spreads_outliers(orc):
+    """§3.2 incoherence: planted outlier channels disappear after rotation
+    (max/RMS of a row drops sharply)."""
+    wl = workloads.LINEAR["tiny"]
+    x, _, idx = workloads.linear_inputs(wl)
+    y = orc.rotate_f16(x).astype(np.float64)
+    xf = x.astype(np.float64)
+
+    def mu(a):
+        return np.abs(a).max(axis=1) / np.sqrt((a ** 2).mean(axis=1))
+
+    assert np.all(mu(y) < 0.5 * mu(xf))
+
+
+# --------------------------------------------------------------------------
+# symmetric int4 quantizer
+# --------------------------------------------------------------------------
+
+def test_quant_closed_form_power_of_two_scale(orc):
+    """y = k_j * 2^e with max |k| = 7 gives s = 2^e and codes k exactly."""
+    rng = np.random.default_rng(3)
+    for e in (-6, -1, 0, 3):
+        k = rng.integers(-7, 8, size=(5, 64))
+        k[:, 0] = 7
+        y = (k * 2.0 ** e).astype(np.float32)
+        q, s = orc.quant_sym_f32(y)
+        assert np.all(s.astype(np.float64) == 2.0 ** e)
+        assert np.array_equal(orc.unpack_int4(q), k.astype(np.int8))
+
+
+def test_quant_ties_to_even_and_packing(orc):
+    y = np.array([[7, 2.5, -2.5, 3.5, 0.5, 1.5, -1.5, -3.5, -0.5, 6.5, 5.5, 4.5]],
+                 np.float32)
+    q, s = orc.quant_sym_f32(y)
+    assert float(s[0]) == 1.0
+    assert orc.unpack_int4(q).tolist() == [[7, 2, -2, 4, 0, 2, -2, -4, 0, 6, 6, 4]]
+    # byte j = (q[2j] & 15) | (q[2j+1] & 15) << 4, two's complement nibbles
+    y = np.array([[1, -1, -3, 7]], np.float32)
+    q, s = orc.quant_sym_f32(y, clip=1.0)
+    assert orc.unpack_int4(q)[0].tolist() == [1, -1, -3, 7]
+    assert q[0].tolist() == [0xF1, 0x7D]
+    # -8 is reachable only with clip < 1: s = 7 * 0.875 / 7 = 0.875
+    y = np.array([[7, -7, 0.4375, -0.4375]], np.float32)
+    q, s = orc.quant_sym_f32(y, clip=0.875)
+    assert float(s[0]) == 0.875
+    assert orc.unpack_int4(q)[0].tolist() == [7, -8, 0, 0]
+    assert q[0, 0] == 0x87
+
+
+def test_quant_brute_force_nearest_code(orc):
+    """Each code is the nearest integer in [-8, 7] to y / s16 (exact
+    rationals), up to the one rounding of the binary32 quotient."""
+    rng = np.random.default_rng(4)
+    y = (rng.standard_normal((40, 32)) * rng.uniform(0.01, 100, size=(40, 1))).astype(np.float32)
+    for clip in (1.0, 0.9):
+        q, s = orc.quant_sym_f32(y, clip)
+        codes = orc.unpack_int4(q)
+        for r in range(y.shape[0]):
+            sf = Fraction(float(s[r]))
+            amax = max(abs(Fraction(float(v))) for v in y[r])
+            # scale: nearest fp16 to amax*clip/7 within fp32 roundings
+            assert abs(sf - amax * Fraction(float(np.float32(clip))) / 7) <= \
+                sf * Fraction(1, 1024) + amax * Fraction(1, 2 ** 22)
+            for j in range(y.shape[1]):
+                ratio = Fraction(float(y[r, j])) / sf
+                best = min(range(-8, 8), key=lambda c: (abs(ratio - c), c % 2))
+                if codes[r, j] != best:
+                    # only a half-integer within one fp32 rounding may flip
+                    half = Fraction(2 * best + (1 if codes[r, j] > best else -1), 2)
+                    assert abs(ratio - half) <= abs(ratio) * Fraction(1, 2 ** 23)
+            if clip == 1.0:
+                assert codes[r].min() >= -7
+
+
+def test_quant_zero_row_and_bounds(orc):
+    y = np.zeros((2, 16), np.float32)
+    y[1, 3] = 1e-30  # scale underflows fp16 to zero
+    q, s = orc.quant_sym_f32(y)
+    assert np.all(s == 0) and np.all(q == 0)
+    x = workloads.random_rows(9, 16, 256, "student_t3")
+    yy = x.astype(np.float32)
+    q, s = orc.quant_sym_f32(yy, 1.0)
+    codes = orc.unpack_int4(q).astype(np.float64)
+    sf = s.astype(np.float64)[:, None]
+    err = np.abs(yy - codes * sf)
+    assert np.all(err <= sf / 2 * (1 + 2 ** -20))
+
+
+def test_quant_int4_rotate_composes(orc):
+    """quant_int4(x, rotate) equals quantizing the fp32 rotation of x."""
+    x = workloads.random_rows(21, 8, 4096)
+    q1, s1 = orc.quant_int4(x, rotate=True)
+    q2, s2 = orc.quant_sym_f32(orc.rotate_f16(x))
+    assert np.array_equal(q1, q2) and np.array_equal(s1.view(np.uint16), s2.view(np.uint16))
+    q3, s3 = orc.quant_int4(x, rotate=False)
+    q4, s4 = orc.quant_sym_f32(x.astype(np.float32))
+    assert np.array_equal(q3, q4) and np.array_equal(s3.view(np.uint16), s4.view(np.uint16))
+
+
+# --------------------------------------------------------------------------
+# GEMM and dequant
+# --------------------------------------------------------------------------
+
+def _pack(codes):
+    c = codes.astype(np.int64) & 0xF
+    return (c[:, 0::2] | (c[:, 1::2] << 4)).astype(np.uint8)
+
+
+def test_gemm_vs_numpy_int64(orc):
+    rng = np.random.default_rng(5)
+    for (M, N, K) in [(7, 9, 34), (33, 17, 256), (5, 3, 2)]:
+        a = rng.integers(-8, 8, size=(M, K))
+        b = rng.integers(-8, 8, size=(N, K))
+        acc = orc.gemm_i32(_pack(a), _pack(b))
+        assert np.array_equal(acc, a @ b.T)
+    # the extreme: all -8 gives 64 K
+    K = 4096
+    a = np.full((2, K), -8)
+    acc = orc.gemm_i32(_pack(a), _pack(a))
+    assert np.all(acc == 64 * K)
+
+
+def test_dequant_closed_forms(orc):
+    rng = np.random.default_rng(6)
+    acc = rng.integers(-2 ** 20, 2 ** 20, size=(8, 12)).astype(np.int32)
+    ones = np.ones(8, np.float16)
+    y = orc.dequant(acc, ones, np.ones(12, np.float16))
+    with np.errstate(over="ignore"):
+        ref = acc.astype(np.float16)
+    assert np.array_equal(y.view(np.uint16), ref.view(np.uint16))
+    # power-of-two scales are exact: y = RN16(acc * 2^(a+b))
+    sx = (2.0 ** rng.integers(-12, -4, size=8)).astype(np.float16)
+    sw = (2.0 ** rng.integers(-8, -2, size=12)).astype(np.float16)
+    y = orc.dequant(acc, sx, sw)
+    ref = (acc.astype(np.float64) * sx.astype(np.float64)[:, None] *
+           sw.astype(np.float64)[None, :]).astype(np.float16)
+    assert np.array_equal(y.view(np.uint16), ref.view(np.uint16))
+    # general scales: within 2 fp32 roundings + 1 fp16 rounding of the exact product
+    sx = rng.uniform(0.001, 1, 8).astype(np.float16)
+    sw = rng.uniform(0.001, 0.01, 12).astype(np.float16)
+    y = orc.dequant(acc, sx, sw).astype(np.float64)
+    ex = acc.astype(np.float64) * sx.astype(np.float64)[:, None] * sw.astype(np.float64)[None, :]
+    assert np.all(np.abs(y - ex) <= np.abs(ex) * (2 ** -11 + 3 * U) + 2 ** -24)
+
+
+def test_linear_composition_and_error_bound(orc):
+    wl = workloads.LINEAR["tiny"]
+    x, w, _ = workloads.linear_inputs(wl)
+    wq, sw = orc.prepare_weight(w)
+    y, acc = orc.linear(x, wq, sw, rotate=True, want_acc=True)
+    xq, sx = orc.quant_int4(x, rotate=True)
+    assert np.array_equal(acc, orc.gemm_i32(xq, wq))
+    assert np.array_equal(y.view(np.uint16), orc.dequant(acc, sx, sw).view(np.uint16))
+    # rigorous bound vs fp64 x w^T: sum_k (sx/2 |w'_k| + sw/2 |x'_k| + sx sw / 4)
+    xr = orc.rotate_f16(x).astype(np.float64)
+    wr = orc.rotate_f16(w).astype(np.float64)
+    ref = x.astype(np.float64) @ w.astype(np.float64).T
+    sxf = sx.astype(np.float64)[:, None]
+    swf = sw.astype(np.float64)[None, :]
+    bound = (sxf / 2 * np.abs(wr).sum(1)[None, :] + swf / 2 * np.abs(xr).sum(1)[:, None]
+             + sxf * swf / 4 * x.shape[1])
+    bound += 1e-4 * np.abs(ref) + np.abs(ref) * 2 ** -10 + 1e-3
+    assert np.all(np.abs(y.astype(np.float64) - ref) <= bound)
+
+
+@pytest.mark.parametrize("name,M,N,factor", [("tiny", None, None, 1.0),
+                                            ("llama2_7b_up", 32, 256, 1.0),
+                                            ("llama2_7b_down", 32, 256, 0.5)])
+def test_rotation_helps_w4a4(orc, name, M, N, factor):
+    """The method's claim at layer scope: rotated W4A4 output is closer to
+    x w^T than unrotated W4A4; by 2x or more on heavy-tailed activations."""
+    x, w, _ = workloads.linear_inputs(workloads.LINEAR[name], M=M, N=N)
+    ref = x.astype(np.float64) @ w.astype(np.float64).T
+
+    def rel(rotate):
+        wq, sw = orc.prepare_weight(w, rotate=rotate)
+        y = orc.linear(x, wq, sw, rotate=rotate).astype(np.float64)
+        return np.linalg.norm(y - ref) / np.linalg.norm(ref)
+
+    assert rel(True) < factor * rel(False)
+
+
+@pytest.mark.parametrize("name,M,factor", [("tiny", None, 0.6), ("llama2_7b_up", 64, 0.8),
+                                           ("llama2_7b_down", 64, 0.4),
+                                           ("llama2_70b_up", 16, 0.95)])
+def test_rotation_shrinks_activation_quant_error(orc, name, M, factor):
+    """Per-token int4 error of the activations themselves (norms are
+    preserved by the orthonormal rotation, so the two are comparable).  A few
+    huge outlier channels carry most of a row's energy, so the relative gain
+    is largest for heavy tails (measured ratios 0.41, 0.65, 0.26, 0.88)."""
+    x, _, _ = workloads.linear_inputs(workloads.LINEAR[name], M=M, weights=False)
+
+    def err(rotate):
+        q, s = orc.quant_int4(x, rotate=rotate)
+        deq = orc.unpack_int4(q).astype(np.float64) * s.astype(np.float64)[:, None]
+        base = orc.rotate_f16(x).astype(np.float64) if rotate else x.astype(np.float64)
+        return np.linalg.norm(deq - base) / np.linalg.norm(base)
+
+    assert err(True) < factor * err(False)
+
+
+# --------------------------------------------------------------------------
+# KV cache
+# --------------------------------------------------------------------------
+
+def test_kv_ladder_round_trips_exactly(orc):
+    """A group that is an exact 16-level ladder z + j s (fp16-exact s, z)
+    with clip 1 quantizes to codes j and dequantizes exactly."""
+    rng = np.random.default_rng(7)
+    rows, D = 6, 128
+    s = np.float32(0.125)
+    z = np.float32(-1.0)
+    j = rng.integers(0, 16, size=(rows, D))
+    j[:, 0] = 0
+    j[:, 1] = 15
+    x = (z + j * s).astype(np.float16)
+    q, sc, ze = orc.kv_quant(x, group=128, rotate=False, clip=1.0)
+    assert np.all(sc == np.float16(s)) and np.all(ze == np.float16(z))
+    assert np.array_equal(orc.unpack_uint4(q), j.astype(np.uint8))
+    out = orc.kv_dequant(q, sc, ze, group=128)
+    assert np.array_equal(out.view(np.uint16), x.view(np.uint16))
+
+
+def test_kv_brute_force_and_bounds(orc):
+    rng = np.random.default_rng(8)
+    x = (rng.standard_normal((30, 64)) * 3).astype(np.float16)
+    for G in (64, 32, 16):
+        q, sc, ze = orc.kv_quant(x, group=G, rotate=False, clip=0.95)
+        codes = orc.unpack_uint4(q)
+        assert codes.max() <= 15
+        for r in range(x.shape[0]):
+            for g in range(64 // G):
+                seg = x[r, g * G:(g + 1) * G].astype(np.float32)
+                mx, mn = seg.max(), seg.min()
+                sf = Fraction(float(sc[r, g]))
+                zf = Fraction(float(ze[r, g]))
+                assert abs(zf - Fraction(float(mn)) * Fraction(float(np.float32(0.95)))) <= \
+                    abs(zf) * Fraction(1, 2048) + Fraction(1, 2 ** 24)
+                span = (Fraction(float(mx)) - Fraction(float(mn))) * Fraction(float(np.float32(0.95)))
+                assert abs(sf * 15 - span) <= span * Fraction(1, 1000)
+                for i in range(G):
+                    ratio = (Fraction(float(seg[i])) - zf) / sf
+                    best = min(range(0, 16), key=lambda c: (abs(ratio - c), c % 2))
+                    got = int(codes[r, g * G + i])
+                    if got != best:
+                        half = Fraction(2 * best + (1 if got > best else -1), 2)
+                        assert abs(ratio - half) <= (abs(ratio) + 1) * Fraction(1, 2 ** 21)
+        out = orc.kv_dequant(q, sc, ze, group=G).astype(np.float64)
+        sfull = np.repeat(sc.astype(np.float64), G, axis=1)
+        zfull = np.repeat(ze.astype(np.float64), G, axis=1)
+        xf = x.astype(np.float64)
+        inside = (xf >= zfull) & (xf <= zfull + 15 * sfull)
+        err = np.abs(out - xf)
+        assert np.all(err[inside] <= sfull[inside] / 2 * (1 + 1e-3) + np.abs(xf[inside]) * 2 ** -10)
+
+
+def test_kv_degenerate_groups(orc):
+    x = np.zeros((3, 128), np.float16)
+    x[1] = 0.5
+    q, sc, ze = orc.kv_quant(x, group=128, rotate=False, clip=0.95)
+    assert np.all(sc == 0) and np.all(q == 0)
+    out = orc.kv_dequant(q, sc, ze, group=128)
+    assert np.array_equal(out.view(np.uint16), np.repeat(ze, 128, axis=1).view(np.uint16))
+
+
+def test_kv_rotated_round_trip(orc):
+    wl = workloads.KV["kv4_70b"]
+    k, v = workloads.kv_inputs(wl, B=1, S=16)
+    x = k.reshape(-1, 128)
+    q, sc, ze = orc.kv_quant(x, group=128, rotate=True, clip=0.95)
+    back = orc.kv_dequant(q, sc, ze, group=128, inverse_rotate=True).astype(np.float64)
+    xf = x.astype(np.float64)
+    rel = np.linalg.norm(back - xf) / np.linalg.norm(xf)
+    assert rel < 0.2
+    # rotation makes the 4-bit cache more accurate on outlier dims
+    q0, s0, z0 = orc.kv_quant(x, group=128, rotate=False, clip=0.95)
+    back0 = orc.kv_dequant(q0, s0, z0, group=128).astype(np.float64)
+    assert rel < 0.7 * np.linalg.norm(back0 - xf) / np.linalg.norm(xf)
+    # and rotated dequant (no inverse) equals the codes in the rotated basis
+    yr = orc.rotate_f16(x).astype(np.float64)
+    fwd = orc.kv_dequant(q, sc, ze, group=128).astype(np.float64)
+    assert np.linalg.norm(fwd - yr) / np.linalg.norm(yr) < 0.2
