@@ -1,0 +1,254 @@
+"""MI355X (gfx950) QuaRot W4A4 rotated-linear hot path.
+
+A thin ctypes binding over ``libquarot.so`` (HIP kernels behind the C ABI in
+``include/quarot.h``).  Every function here only marshals arguments: torch
+tensors provide device memory and the current stream, and every step of the
+path runs in the library's kernels.  There is no CPU fallback; if the
+library is missing or no gfx950 device is present the calls raise.
+
+Paper: Ashkboos et al., "QuaRot: Outlier-Free 4-Bit Inference in Rotated
+LLMs", arXiv 2404.00456 (§3.1 Hadamard construction, §4 Stage 1b/1d/2b,
+§5 Setup, App. A.10 4-bit linear layer).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch  # first: the library then binds to torch's HIP runtime
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libquarot.so")
+
+STATUS = {
+    0: "QUAROT_OK",
+    1: "QUAROT_ERR_INVALID_ARG",
+    2: "QUAROT_ERR_UNSUPPORTED_SIZE",
+    3: "QUAROT_ERR_ALIGNMENT",
+    4: "QUAROT_ERR_WORKSPACE",
+    5: "QUAROT_ERR_NO_DEVICE",
+    6: "QUAROT_ERR_HIP",
+}
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I = ctypes.c_int
+_F = ctypes.c_float
+
+# name -> (restype, argtypes), exactly the declarations of include/quarot.h
+SIGNATURES = {
+    "quarot_status_string": (ctypes.c_char_p, [_I]),
+    "quarot_last_hip_error": (_I, []),
+    "quarot_version": (_I, []),
+    "quarot_hadamard_factor": (_I, [_I64, _P, _P]),
+    "quarot_hadamard_factor_table": (_I, [_I, _P]),
+    "quarot_hadamard": (_I, [_P, _P, _I64, _I64, _P]),
+    "quarot_quant_int4": (_I, [_P, _P, _P, _I64, _I64, _I, _F, _P]),
+    "quarot_w4a4_gemm": (_I, [_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P]),
+    "quarot_linear_workspace_size": (ctypes.c_size_t, [_I64, _I64]),
+    "quarot_linear": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P, ctypes.c_size_t, _P]),
+    "quarot_kv_quant": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P]),
+    "quarot_kv_dequant": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _P]),
+}
+
+_lib = None
+
+
+class QuarotError(RuntimeError):
+    def __init__(self, call: str, status: int, hip_error: int = 0):
+        self.status = status
+        self.hip_error = hip_error
+        msg = f"{call} failed: {STATUS.get(status, status)}"
+        if hip_error:
+            msg += f" (hipError {hip_error})"
+        super().__init__(msg)
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2404_00456_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(call: str, st: int):
+    if st != 0:
+        raise QuarotError(call, st, lib().quarot_last_hip_error() if st == 6 else 0)
+
+
+def _ptr(t: Optional[torch.Tensor], dtype: torch.dtype, name: str):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream: Optional[torch.cuda.Stream]):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _rows(t: torch.Tensor, n: int) -> int:
+    return t.numel() // n if n else 0
+
+
+# -- host-side queries ------------------------------------------------------
+
+def quarot_version() -> int:
+    return lib().quarot_version()
+
+
+def quarot_hadamard_factor(n: int) -> Optional[Tuple[int, int]]:
+    k = ctypes.c_int()
+    m = ctypes.c_int()
+    st = lib().quarot_hadamard_factor(n, ctypes.byref(k), ctypes.byref(m))
+    return None if st else (k.value, m.value)
+
+
+def quarot_hadamard_factor_table(m: int):
+    import numpy as np
+    out = np.empty((m, m), np.int8)
+    _check("quarot_hadamard_factor_table",
+           lib().quarot_hadamard_factor_table(m, out.ctypes.data_as(ctypes.c_void_p)))
+    return out
+
+
+def quarot_linear_workspace_size(M: int, K: int) -> int:
+    return int(lib().quarot_linear_workspace_size(M, K))
+
+
+# -- device calls -----------------------------------------------------------
+
+def quarot_hadamard(x: torch.Tensor, y: Optional[torch.Tensor] = None,
+                    stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """y = RN16(x . H_n / sqrt(n)) row by row; x fp16 [..., n]."""
+    n = x.shape[-1]
+    if y is None:
+        y = torch.empty_like(x)
+    _check("quarot_hadamard", lib().quarot_hadamard(
+        _ptr(x, torch.float16, "x"), _ptr(y, torch.float16, "y"), _rows(x, n), n,
+        _stream(stream)))
+    return y
+
+
+def quarot_quant_int4(x: torch.Tensor, rotate: bool = True, clip_ratio: float = 1.0,
+                      q: Optional[torch.Tensor] = None, scale: Optional[torch.Tensor] = None,
+                      stream: Optional[torch.cuda.Stream] = None):
+    """Per-row symmetric int4 (optionally of the rotated row).
+    Returns (codes uint8 [..., n/2], scale fp16 [...])."""
+    n = x.shape[-1]
+    rows = _rows(x, n)
+    if q is None:
+        q = torch.empty(x.shape[:-1] + (n // 2,), dtype=torch.uint8, device=x.device)
+    if scale is None:
+        scale = torch.empty(x.shape[:-1], dtype=torch.float16, device=x.device)
+    _check("quarot_quant_int4", lib().quarot_quant_int4(
+        _ptr(x, torch.float16, "x"), _ptr(q, torch.uint8, "q"),
+        _ptr(scale, torch.float16, "scale"), rows, n, int(bool(rotate)), float(clip_ratio),
+        _stream(stream)))
+    return q, scale
+
+
+def quarot_w4a4_gemm(xq: torch.Tensor, sx: torch.Tensor, wq: torch.Tensor, sw: torch.Tensor,
+                     y: Optional[torch.Tensor] = None, acc_out: Optional[torch.Tensor] = None,
+                     want_acc: bool = False, stream: Optional[torch.cuda.Stream] = None):
+    """y = dequant(Xq Wq^T); returns y, or (y, acc) with want_acc."""
+    M, Kh = xq.shape
+    N = wq.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=xq.device)
+    if want_acc and acc_out is None:
+        acc_out = torch.empty((M, N), dtype=torch.int32, device=xq.device)
+    _check("quarot_w4a4_gemm", lib().quarot_w4a4_gemm(
+        _ptr(xq, torch.uint8, "xq"), _ptr(sx, torch.float16, "sx"), _ptr(wq, torch.uint8, "wq"),
+        _ptr(sw, torch.float16, "sw"), _ptr(y, torch.float16, "y"),
+        _ptr(acc_out, torch.int32, "acc_out"), M, N, 2 * Kh, _stream(stream)))
+    return (y, acc_out) if (want_acc or acc_out is not None) else y
+
+
+def quarot_linear(x: torch.Tensor, wq: torch.Tensor, sw: torch.Tensor, rotate: bool = True,
+                  clip_ratio: float = 1.0, y: Optional[torch.Tensor] = None,
+                  workspace: Optional[torch.Tensor] = None,
+                  stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """The 4-bit linear layer: rotate+quantize x, W4A4 GEMM, dequant."""
+    M, K = x.shape
+    N = wq.shape[0]
+    need = quarot_linear_workspace_size(M, K)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    _check("quarot_linear", lib().quarot_linear(
+        _ptr(x, torch.float16, "x"), _ptr(wq, torch.uint8, "wq"), _ptr(sw, torch.float16, "sw"),
+        _ptr(y, torch.float16, "y"), M, N, K, int(bool(rotate)), float(clip_ratio),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream)))
+    return y
+
+
+def prepare_weight(w: torch.Tensor, rotate: bool = True, clip_ratio: float = 1.0,
+                   stream: Optional[torch.cuda.Stream] = None):
+    """Offline weight prep: each output-channel row of W [N, K] rotated like
+    an activation row, then quantized per row (per output channel)."""
+    return quarot_quant_int4(w, rotate=rotate, clip_ratio=clip_ratio, stream=stream)
+
+
+def quarot_kv_quant(kv: torch.Tensor, group: int = 128, rotate: bool = True,
+                    clip_ratio: float = 0.95, q: Optional[torch.Tensor] = None,
+                    scale: Optional[torch.Tensor] = None, zero: Optional[torch.Tensor] = None,
+                    stream: Optional[torch.cuda.Stream] = None):
+    """4-bit asymmetric KV cache: kv fp16 [..., head_dim] ->
+    (codes uint8 [..., head_dim/2], scale, zero fp16 [..., head_dim/group])."""
+    D = kv.shape[-1]
+    rows = _rows(kv, D)
+    lead = kv.shape[:-1]
+    if q is None:
+        q = torch.empty(lead + (D // 2,), dtype=torch.uint8, device=kv.device)
+    if scale is None:
+        scale = torch.empty(lead + (D // group,), dtype=torch.float16, device=kv.device)
+    if zero is None:
+        zero = torch.empty(lead + (D // group,), dtype=torch.float16, device=kv.device)
+    _check("quarot_kv_quant", lib().quarot_kv_quant(
+        _ptr(kv, torch.float16, "kv"), _ptr(q, torch.uint8, "q"),
+        _ptr(scale, torch.float16, "scale"), _ptr(zero, torch.float16, "zero"), rows, D, group,
+        int(bool(rotate)), float(clip_ratio), _stream(stream)))
+    return q, scale, zero
+
+
+def quarot_kv_dequant(q: torch.Tensor, scale: torch.Tensor, zero: torch.Tensor,
+                      group: int = 128, inverse_rotate: bool = False,
+                      out: Optional[torch.Tensor] = None,
+                      stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    D = 2 * q.shape[-1]
+    rows = _rows(q, D // 2)
+    if out is None:
+        out = torch.empty(q.shape[:-1] + (D,), dtype=torch.float16, device=q.device)
+    _check("quarot_kv_dequant", lib().quarot_kv_dequant(
+        _ptr(q, torch.uint8, "q"), _ptr(scale, torch.float16, "scale"),
+        _ptr(zero, torch.float16, "zero"), _ptr(out, torch.float16, "out"), rows, D, group,
+        int(bool(inverse_rotate)), _stream(stream)))
+    return out
+
+
+__all__ = [
+    "QuarotError", "lib", "quarot_version", "quarot_hadamard_factor",
+    "quarot_hadamard_factor_table", "quarot_linear_workspace_size", "quarot_hadamard",
+    "quarot_quant_int4", "quarot_w4a4_gemm", "quarot_linear", "prepare_weight",
+    "quarot_kv_quant", "quarot_kv_dequant",
+]

@@ -1,0 +1,371 @@
+// C ABI of libquarot: argument validation, size dispatch, launches.
+// Every check runs on the host before any device work; on error no output
+// is touched.
+#include "../../include/quarot.h"
+
+#include <cmath>
+#include <cstring>
+
+#include "common.hpp"
+#include "hadamard_factors.hpp"
+
+using namespace quarot;
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+constexpr int kMaxN = 32768;
+
+bool aligned16(const void *p)
+{
+    return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
+}
+
+// n = 2^k * m with m picked by the odd part of n.
+bool factor(int64_t n, int *k, int *m)
+{
+    if (n <= 0)
+        return false;
+    static const int ms[6] = {1, 12, 20, 28, 108, 172};
+    for (int t = 0; t < 6; ++t) {
+        if (n % ms[t])
+            continue;
+        const int64_t p = n / ms[t];
+        if (p & (p - 1))
+            continue;
+        int kk = 0;
+        while ((int64_t(1) << kk) < p)
+            ++kk;
+        *k = kk;
+        *m = ms[t];
+        return true;
+    }
+    return false;
+}
+
+// RN32(1/sqrt(n)), through double (exact square root, one division).
+float rotation_scale(int64_t n)
+{
+    return (float)(1.0 / std::sqrt((double)n));
+}
+
+bool clip_ok(float c)
+{
+    return c > 0.0f && c <= 1.0f;
+}
+
+quarot_status hip_fail(hipError_t e)
+{
+    g_last_hip_error = (int)e;
+    return QUAROT_ERR_HIP;
+}
+
+// The device of the calling thread must be a gfx950.  Cached per thread
+// and device (a host-side query, no device work).
+quarot_status check_device()
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        return QUAROT_ERR_NO_DEVICE;
+    }
+    thread_local int ok_dev = -1;
+    if (ok_dev == dev)
+        return QUAROT_OK;
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        return QUAROT_ERR_NO_DEVICE;
+    }
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return QUAROT_ERR_NO_DEVICE;
+    ok_dev = dev;
+    return QUAROT_OK;
+}
+
+quarot_status check_rot_size(int64_t n, bool rotate, int epi, int *k, int *m)
+{
+    if (n <= 0 || n > kMaxN || (n & 7))
+        return n <= 0 ? QUAROT_ERR_INVALID_ARG : QUAROT_ERR_UNSUPPORTED_SIZE;
+    *k = 0;
+    *m = 1;
+    if (rotate || epi == EPI_KV) {
+        if (!factor(n, k, m))
+            return QUAROT_ERR_UNSUPPORTED_SIZE;
+    }
+    if (!rotate_supported(epi, rotate, *k, *m, (int)n))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    return QUAROT_OK;
+}
+
+quarot_status check_gemm_sizes(int64_t M, int64_t N, int64_t K)
+{
+    if (M < 0 || N < 0 || K <= 0)
+        return QUAROT_ERR_INVALID_ARG;
+    if (K % 64 || K > 65536 || M > (int64_t(1) << 30) || N > (int64_t(1) << 30))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (M > 0 && N > 0 && (int64_t)((M + 255) / 256) * ((N + 255) / 256) > 0x7FFFFFFF)
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    return QUAROT_OK;
+}
+
+quarot_status check_gemm(const uint8_t *xq, const quarot_f16 *sx, const uint8_t *wq,
+                         const quarot_f16 *sw, const quarot_f16 *y, const int32_t *acc,
+                         int64_t M, int64_t N, int64_t K)
+{
+    quarot_status st = check_gemm_sizes(M, N, K);
+    if (st || M == 0 || N == 0)
+        return st;
+    if (!xq || !sx || !wq || !sw || !y)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(xq) || !aligned16(wq) || !aligned16(y) || !aligned16(sx) ||
+        !aligned16(sw) || (acc && !aligned16(acc)))
+        return QUAROT_ERR_ALIGNMENT;
+    return QUAROT_OK;
+}
+
+size_t codes_bytes(int64_t M, int64_t K)
+{
+    return ((size_t)M * (size_t)(K / 2) + 255) & ~(size_t)255;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *quarot_status_string(int status)
+{
+    switch (status) {
+    case QUAROT_OK: return "QUAROT_OK";
+    case QUAROT_ERR_INVALID_ARG: return "QUAROT_ERR_INVALID_ARG";
+    case QUAROT_ERR_UNSUPPORTED_SIZE: return "QUAROT_ERR_UNSUPPORTED_SIZE";
+    case QUAROT_ERR_ALIGNMENT: return "QUAROT_ERR_ALIGNMENT";
+    case QUAROT_ERR_WORKSPACE: return "QUAROT_ERR_WORKSPACE";
+    case QUAROT_ERR_NO_DEVICE: return "QUAROT_ERR_NO_DEVICE";
+    case QUAROT_ERR_HIP: return "QUAROT_ERR_HIP";
+    }
+    return "QUAROT_ERR_UNKNOWN";
+}
+
+int quarot_last_hip_error(void)
+{
+    return g_last_hip_error;
+}
+
+int quarot_version(void)
+{
+    return 100;  // 0.1.0
+}
+
+quarot_status quarot_hadamard_factor(int64_t n, int *log2_pow2, int *m)
+{
+    if (!log2_pow2 || !m || n <= 0)
+        return QUAROT_ERR_INVALID_ARG;
+    int k, mm;
+    if (n > kMaxN || (n & 7) || !factor(n, &k, &mm) ||
+        !rotate_supported(EPI_SYM, true, k, mm, (int)n))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    *log2_pow2 = k;
+    *m = mm;
+    return QUAROT_OK;
+}
+
+quarot_status quarot_hadamard_factor_table(int m, int8_t *out)
+{
+    if (!out)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!hm_supported(m))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    for (int r = 0; r < m; ++r)
+        for (int s = 0; s < m; ++s)
+            out[r * m + s] = (int8_t)hm_sign(m, r, s);
+    return QUAROT_OK;
+}
+
+quarot_status quarot_hadamard(const quarot_f16 *x, quarot_f16 *y, int64_t rows, int64_t n,
+                              void *stream)
+{
+    if (rows < 0)
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;
+    quarot_status st = check_rot_size(n, true, EPI_F16, &k, &m);
+    if (st)
+        return st;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!x || !y)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(y))
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    RotArgs a{};
+    a.x = x;
+    a.out = y;
+    a.rows = rows;
+    a.n = (int)n;
+    a.c = rotation_scale(n);
+    a.clip = 1.0f;
+    hipError_t e = launch_rotate(a, EPI_F16, true, k, m, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+quarot_status quarot_quant_int4(const quarot_f16 *x, uint8_t *q, quarot_f16 *scale,
+                                int64_t rows, int64_t n, int rotate, float clip_ratio,
+                                void *stream)
+{
+    if (rows < 0 || !clip_ok(clip_ratio))
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;
+    quarot_status st = check_rot_size(n, rotate != 0, EPI_SYM, &k, &m);
+    if (st)
+        return st;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!x || !q || !scale)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(q) || !aligned16(scale))
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    RotArgs a{};
+    a.x = x;
+    a.out = q;
+    a.scale = scale;
+    a.rows = rows;
+    a.n = (int)n;
+    a.c = rotation_scale(n);
+    a.clip = clip_ratio;
+    hipError_t e = launch_rotate(a, EPI_SYM, rotate != 0, k, m, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+quarot_status quarot_w4a4_gemm(const uint8_t *xq, const quarot_f16 *sx, const uint8_t *wq,
+                               const quarot_f16 *sw, quarot_f16 *y, int32_t *acc_out,
+                               int64_t M, int64_t N, int64_t K, void *stream)
+{
+    quarot_status st = check_gemm(xq, sx, wq, sw, y, acc_out, M, N, K);
+    if (st || M == 0 || N == 0)
+        return st;
+    if ((st = check_device()))
+        return st;
+    GemmArgs a{xq, sx, wq, sw, y, acc_out, (int)M, (int)N, (int)K};
+    hipError_t e = launch_gemm(a, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+size_t quarot_linear_workspace_size(int64_t M, int64_t K)
+{
+    if (M < 0 || K <= 0 || (K & 1))
+        return 0;
+    const size_t scales = ((size_t)M * 2 + 255) & ~(size_t)255;
+    return codes_bytes(M, K) + scales;
+}
+
+quarot_status quarot_linear(const quarot_f16 *x, const uint8_t *wq, const quarot_f16 *sw,
+                            quarot_f16 *y, int64_t M, int64_t N, int64_t K, int rotate,
+                            float clip_ratio, void *workspace, size_t workspace_bytes,
+                            void *stream)
+{
+    if (M < 0 || N < 0 || !clip_ok(clip_ratio))
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;
+    quarot_status st = check_rot_size(K, rotate != 0, EPI_SYM, &k, &m);
+    if (st)
+        return st;
+    if ((st = check_gemm_sizes(M, N, K)))
+        return st;
+    if (M == 0 || N == 0)
+        return QUAROT_OK;
+    if (!x || !wq || !sw || !y)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(wq) || !aligned16(sw) || !aligned16(y))
+        return QUAROT_ERR_ALIGNMENT;
+    if (!workspace || workspace_bytes < quarot_linear_workspace_size(M, K))
+        return QUAROT_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    uint8_t *xq = static_cast<uint8_t *>(workspace);
+    quarot_f16 *sx = reinterpret_cast<quarot_f16 *>(xq + codes_bytes(M, K));
+    RotArgs ra{};
+    ra.x = x;
+    ra.out = xq;
+    ra.scale = sx;
+    ra.rows = M;
+    ra.n = (int)K;
+    ra.c = rotation_scale(K);
+    ra.clip = clip_ratio;
+    hipError_t e = launch_rotate(ra, EPI_SYM, rotate != 0, k, m, (hipStream_t)stream);
+    if (e != hipSuccess)
+        return hip_fail(e);
+    GemmArgs ga{xq, sx, wq, sw, y, nullptr, (int)M, (int)N, (int)K};
+    e = launch_gemm(ga, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+quarot_status quarot_kv_quant(const quarot_f16 *kv, uint8_t *q, quarot_f16 *scale,
+                              quarot_f16 *zero, int64_t rows, int64_t head_dim, int64_t group,
+                              int rotate, float clip_ratio, void *stream)
+{
+    if (rows < 0 || !clip_ok(clip_ratio) || head_dim <= 0 || group <= 0)
+        return QUAROT_ERR_INVALID_ARG;
+    if (head_dim < 8 || head_dim > 512 || (head_dim & (head_dim - 1)) || group < 8 ||
+        group > head_dim || (group & (group - 1)))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    int k, m;
+    quarot_status st = check_rot_size(head_dim, rotate != 0, EPI_KV, &k, &m);
+    if (st)
+        return st;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!kv || !q || !scale || !zero)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(kv) || !aligned16(q) || !aligned16(scale) || !aligned16(zero))
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    RotArgs a{};
+    a.x = kv;
+    a.out = q;
+    a.scale = scale;
+    a.zero = zero;
+    a.rows = rows;
+    a.n = (int)head_dim;
+    a.group = (int)group;
+    a.c = rotation_scale(head_dim);
+    a.clip = clip_ratio;
+    hipError_t e = launch_rotate(a, EPI_KV, rotate != 0, k, m, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+quarot_status quarot_kv_dequant(const uint8_t *q, const quarot_f16 *scale,
+                                const quarot_f16 *zero, quarot_f16 *out, int64_t rows,
+                                int64_t head_dim, int64_t group, int inverse_rotate,
+                                void *stream)
+{
+    if (rows < 0 || head_dim <= 0 || group <= 0)
+        return QUAROT_ERR_INVALID_ARG;
+    if (head_dim < 8 || head_dim > 512 || (head_dim & (head_dim - 1)) || group < 8 ||
+        group > head_dim || (group & (group - 1)))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!q || !scale || !zero || !out)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(scale) || !aligned16(zero) || !aligned16(out))
+        return QUAROT_ERR_ALIGNMENT;
+    quarot_status st = check_device();
+    if (st)
+        return st;
+    KvDeqArgs a{q, scale, zero, out, rows, (int)head_dim, (int)group,
+                rotation_scale(head_dim)};
+    hipError_t e = launch_kv_dequant(a, inverse_rotate != 0, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+}  // extern "C"

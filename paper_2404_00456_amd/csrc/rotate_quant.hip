@@ -1,0 +1,787 @@
+// Online Hadamard rotation fused with quantization (§3.1, §4 Stage 1b/2b,
+// §5 Setup), for gfx950.
+//
+// A row of width n = 2^k * m is rotated as y = x . (H_{2^k} (x) H_m) * c,
+// c = RN32(1/sqrt(n)), element index i = a*m + b (m fast), in this binary32
+// order: the m-factor sum over b left to right; the Walsh-Hadamard
+// butterflies over a, bit 0 first; one multiply by c.  Each kernel keeps
+// that order exactly, whatever lane, register or wave holds an element, so
+// the fp32 y (and every code derived from it) is reproducible bit for bit.
+//
+// Kernels:
+//   k_rot_pow2    m = 1, n = 2^k <= 32768.  Each lane owns 16-byte chunks of
+//                 8 consecutive elements: i = ((cc*W + w)*L + l)*8 + e, so
+//                 bits 0-2 live in registers, the next log2(L) bits across
+//                 lanes, then across the W waves (LDS), then across chunks.
+//   k_rot_smallm  m = 12, 20, 28: each lane owns whole groups of m elements
+//                 (the m-factor runs in registers with compile-time signs).
+//   k_rot_largem  m = 108, 172: one group per lane, output columns of the
+//                 m-factor in a loop with signs from constant memory, the
+//                 rotated row staged in LDS.
+//   k_quant_plain quantization without rotation, any n multiple of 8.
+//   k_kv_dequant  4-bit KV cache back to fp16, optional inverse rotation.
+#include "common.hpp"
+#include "hadamard_factors.hpp"
+
+namespace quarot {
+
+__constant__ HmColumns<108> c_hm108 = HmColumns<108>();
+__constant__ HmColumns<172> c_hm172 = HmColumns<172>();
+
+namespace {
+
+constexpr int ilog2(int v)
+{
+    int r = 0;
+    while ((1 << r) < v)
+        ++r;
+    return r;
+}
+
+// Symmetric int4 code of y with the stored fp16 scale sf (§4 Stage 2b):
+// clamp(rint_even(RN(y / sf)), -8, 7); sf == 0 gives 0.  IEEE division.
+__device__ __forceinline__ uint32_t sym_code(float y, float sf)
+{
+    if (sf == 0.0f)
+        return 0u;
+    float r = rintf(y / sf);
+    r = fminf(fmaxf(r, -8.0f), 7.0f);
+    return (uint32_t)(int)r & 0xFu;
+}
+
+// Asymmetric uint4 code: clamp(rint_even(RN(RN(y - zf) / sf)), 0, 15).
+__device__ __forceinline__ uint32_t asym_code(float y, float sf, float zf)
+{
+    if (sf == 0.0f)
+        return 0u;
+    float r = rintf((y - zf) / sf);
+    r = fminf(fmaxf(r, 0.0f), 15.0f);
+    return (uint32_t)(int)r;
+}
+
+__device__ __forceinline__ void load8(const uint16_t *p, float *v)
+{
+    uint4 raw = *reinterpret_cast<const uint4 *>(p);
+    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[2 * i] = h2f((uint16_t)(w[i] & 0xFFFFu));
+        v[2 * i + 1] = h2f((uint16_t)(w[i] >> 16));
+    }
+}
+
+__device__ __forceinline__ void store8(uint16_t *p, const float *v)
+{
+    uint4 raw;
+    raw.x = (uint32_t)f2h(v[0]) | ((uint32_t)f2h(v[1]) << 16);
+    raw.y = (uint32_t)f2h(v[2]) | ((uint32_t)f2h(v[3]) << 16);
+    raw.z = (uint32_t)f2h(v[4]) | ((uint32_t)f2h(v[5]) << 16);
+    raw.w = (uint32_t)f2h(v[6]) | ((uint32_t)f2h(v[7]) << 16);
+    *reinterpret_cast<uint4 *>(p) = raw;
+}
+
+__device__ __forceinline__ void load4(const uint16_t *p, float *v)
+{
+    uint2 raw = *reinterpret_cast<const uint2 *>(p);
+    v[0] = h2f((uint16_t)(raw.x & 0xFFFFu));
+    v[1] = h2f((uint16_t)(raw.x >> 16));
+    v[2] = h2f((uint16_t)(raw.y & 0xFFFFu));
+    v[3] = h2f((uint16_t)(raw.y >> 16));
+}
+
+__device__ __forceinline__ void store4(uint16_t *p, const float *v)
+{
+    uint2 raw;
+    raw.x = (uint32_t)f2h(v[0]) | ((uint32_t)f2h(v[1]) << 16);
+    raw.y = (uint32_t)f2h(v[2]) | ((uint32_t)f2h(v[3]) << 16);
+    *reinterpret_cast<uint2 *>(p) = raw;
+}
+
+// Max over the L-lane group (xor butterfly), then over the W waves.
+template <int LOGL, int W>
+__device__ __forceinline__ float row_absmax(float amax, int w, float *red)
+{
+#pragma unroll
+    for (int j = 0; j < LOGL; ++j)
+        amax = fmaxf(amax, __shfl_xor(amax, 1 << j));
+    if constexpr (W > 1) {
+        if ((threadIdx.x & 63) == 0)
+            red[w] = amax;
+        __syncthreads();
+        amax = red[0];
+#pragma unroll
+        for (int i = 1; i < W; ++i)
+            amax = fmaxf(amax, red[i]);
+    }
+    return amax;
+}
+
+// ------------------------------------------------------------ m = 1 -----
+
+template <int LOGL, int W, int C, int EPI, bool ROT>
+__global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
+{
+    constexpr int L = 1 << LOGL;
+    constexpr int LOGW = ilog2(W);
+    constexpr int RPW = (W == 1) ? 64 / L : 1;  // rows per wave
+    constexpr int RPB = (W == 1) ? 4 * RPW : 1; // rows per block
+    constexpr int N = 8 * L * W * C;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int ll = lane & (L - 1);
+    int64_t row;
+    int w;
+    if constexpr (W == 1) {
+        row = (int64_t)blockIdx.x * RPB + wave * RPW + (lane >> LOGL);
+        w = 0;
+        if (row >= a.rows)
+            return;
+    } else {
+        row = blockIdx.x;
+        w = wave;
+    }
+
+    float v[C][8];
+    const uint16_t *xr = a.x + row * N;
+#pragma unroll
+    for (int cc = 0; cc < C; ++cc)
+        load8(xr + ((cc * W + w) * L + ll) * 8, v[cc]);
+
+    if constexpr (ROT) {
+        // element bits 0..2: inside each chunk
+#pragma unroll
+        for (int h = 1; h < 8; h <<= 1)
+#pragma unroll
+            for (int cc = 0; cc < C; ++cc)
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (!(e & h)) {
+                        float p = v[cc][e], q = v[cc][e + h];
+                        v[cc][e] = p + q;
+                        v[cc][e + h] = p - q;
+                    }
+        // next LOGL bits: across lanes
+#pragma unroll
+        for (int j = 0; j < LOGL; ++j)
+#pragma unroll
+            for (int cc = 0; cc < C; ++cc)
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    v[cc][e] = bfly_lane(v[cc][e], ll, 1 << j);
+        // next LOGW bits: across waves, through LDS one chunk at a time
+        if constexpr (W > 1) {
+            __shared__ float xs[W][8][64];
+#pragma unroll
+            for (int j = 0; j < LOGW; ++j)
+#pragma unroll
+                for (int cc = 0; cc < C; ++cc) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        xs[w][e][lane] = v[cc][e];
+                    __syncthreads();
+                    const int pw = w ^ (1 << j);
+                    const bool hi = (w >> j) & 1;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        float o = xs[pw][e][lane];
+                        v[cc][e] = hi ? (o - v[cc][e]) : (v[cc][e] + o);
+                    }
+                    __syncthreads();
+                }
+        }
+        // top bits: across the chunks of a lane
+#pragma unroll
+        for (int h = 1; h < C; h <<= 1)
+#pragma unroll
+            for (int cc = 0; cc < C; ++cc)
+                if (!(cc & h)) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        float p = v[cc][e], q = v[cc + h][e];
+                        v[cc][e] = p + q;
+                        v[cc + h][e] = p - q;
+                    }
+                }
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc)
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                v[cc][e] = v[cc][e] * a.c;
+    }
+
+    if constexpr (EPI == EPI_F16) {
+        uint16_t *yr = static_cast<uint16_t *>(a.out) + row * N;
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc)
+            store8(yr + ((cc * W + w) * L + ll) * 8, v[cc]);
+    } else if constexpr (EPI == EPI_SYM) {
+        __shared__ float red[W > 1 ? W : 1];
+        float amax = 0.0f;
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc)
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                amax = fmaxf(amax, fabsf(v[cc][e]));
+        amax = row_absmax<LOGL, W>(amax, w, red);
+        const float s32 = (amax * a.clip) / 7.0f;
+        const uint16_t s16 = f2h(s32);
+        const float sf = h2f(s16);
+        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (N / 2);
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc) {
+            uint32_t pk = 0;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                pk |= sym_code(v[cc][e], sf) << (4 * e);
+            *reinterpret_cast<uint32_t *>(qr + ((cc * W + w) * L + ll) * 4) = pk;
+        }
+        if (ll == 0 && w == 0)
+            a.scale[row] = s16;
+    } else {  // EPI_KV: W == 1, C == 1, a group is G/8 consecutive lanes
+        static_assert(W == 1 && C == 1, "KV rows fit one wave");
+        float mx = v[0][0], mn = v[0][0];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) {
+            mx = fmaxf(mx, v[0][e]);
+            mn = fminf(mn, v[0][e]);
+        }
+        const int gl = a.group >> 3;  // lanes per group
+        for (int j = 1; j < gl; j <<= 1) {
+            mx = fmaxf(mx, __shfl_xor(mx, j));
+            mn = fminf(mn, __shfl_xor(mn, j));
+        }
+        const float mxc = mx * a.clip, mnc = mn * a.clip;
+        const float s32 = (mxc - mnc) / 15.0f;
+        const uint16_t s16 = f2h(s32), z16 = f2h(mnc);
+        const float sf = h2f(s16), zf = h2f(z16);
+        uint32_t pk = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            pk |= asym_code(v[0][e], sf, zf) << (4 * e);
+        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (N / 2);
+        *reinterpret_cast<uint32_t *>(qr + ll * 4) = pk;
+        if ((ll & (gl - 1)) == 0) {
+            const int64_t gi = row * (N / a.group) + ll / gl;
+            a.scale[gi] = s16;
+            a.zero[gi] = z16;
+        }
+    }
+}
+
+// ---------------------------------------------------- m = 12, 20, 28 -----
+
+template <int M, int LOGL, int W, int C, int EPI>
+__global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
+{
+    static_assert(M % 4 == 0, "groups load as 8-byte pieces");
+    constexpr int L = 1 << LOGL;
+    constexpr int LOGW = ilog2(W);
+    constexpr int RPW = (W == 1) ? 64 / L : 1;
+    constexpr int RPB = (W == 1) ? 4 * RPW : 1;
+    constexpr int N = M * L * W * C;
+    constexpr HmTable<M> H{};
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int ll = lane & (L - 1);
+    int64_t row;
+    int w;
+    if constexpr (W == 1) {
+        row = (int64_t)blockIdx.x * RPB + wave * RPW + (lane >> LOGL);
+        w = 0;
+        if (row >= a.rows)
+            return;
+    } else {
+        row = blockIdx.x;
+        w = wave;
+    }
+
+    float v[C][M];
+    const uint16_t *xr = a.x + row * N;
+#pragma unroll
+    for (int cc = 0; cc < C; ++cc) {
+        const int g = (cc * W + w) * L + ll;
+#pragma unroll
+        for (int p = 0; p < M / 4; ++p)
+            load4(xr + g * M + 4 * p, &v[cc][4 * p]);
+    }
+
+    // m-factor: u[b'] = sum_b H[b][b'] t[b], left to right
+#pragma unroll
+    for (int cc = 0; cc < C; ++cc) {
+        float t[M];
+#pragma unroll
+        for (int b = 0; b < M; ++b)
+            t[b] = v[cc][b];
+#pragma unroll
+        for (int bp = 0; bp < M; ++bp) {
+            float acc = (H.v[0][bp] > 0.0f) ? t[0] : -t[0];
+#pragma unroll
+            for (int b = 1; b < M; ++b)
+                acc = (H.v[b][bp] > 0.0f) ? (acc + t[b]) : (acc - t[b]);
+            v[cc][bp] = acc;
+        }
+    }
+    // group bits 0..LOGL-1 across lanes
+#pragma unroll
+    for (int j = 0; j < LOGL; ++j)
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc)
+#pragma unroll
+            for (int b = 0; b < M; ++b)
+                v[cc][b] = bfly_lane(v[cc][b], ll, 1 << j);
+    if constexpr (W > 1) {
+        __shared__ float xs[W][M][64];
+#pragma unroll
+        for (int j = 0; j < LOGW; ++j)
+#pragma unroll
+            for (int cc = 0; cc < C; ++cc) {
+#pragma unroll
+                for (int b = 0; b < M; ++b)
+                    xs[w][b][lane] = v[cc][b];
+                __syncthreads();
+                const int pw = w ^ (1 << j);
+                const bool hi = (w >> j) & 1;
+#pragma unroll
+                for (int b = 0; b < M; ++b) {
+                    float o = xs[pw][b][lane];
+                    v[cc][b] = hi ? (o - v[cc][b]) : (v[cc][b] + o);
+                }
+                __syncthreads();
+            }
+    }
+#pragma unroll
+    for (int h = 1; h < C; h <<= 1)
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc)
+            if (!(cc & h)) {
+#pragma unroll
+                for (int b = 0; b < M; ++b) {
+                    float p = v[cc][b], q = v[cc + h][b];
+                    v[cc][b] = p + q;
+                    v[cc + h][b] = p - q;
+                }
+            }
+#pragma unroll
+    for (int cc = 0; cc < C; ++cc)
+#pragma unroll
+        for (int b = 0; b < M; ++b)
+            v[cc][b] = v[cc][b] * a.c;
+
+    if constexpr (EPI == EPI_F16) {
+        uint16_t *yr = static_cast<uint16_t *>(a.out) + row * N;
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc) {
+            const int g = (cc * W + w) * L + ll;
+#pragma unroll
+            for (int p = 0; p < M / 4; ++p)
+                store4(yr + g * M + 4 * p, &v[cc][4 * p]);
+        }
+    } else {
+        static_assert(EPI == EPI_SYM, "small-m kernels serve activations");
+        __shared__ float red[W > 1 ? W : 1];
+        float amax = 0.0f;
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc)
+#pragma unroll
+            for (int b = 0; b < M; ++b)
+                amax = fmaxf(amax, fabsf(v[cc][b]));
+        amax = row_absmax<LOGL, W>(amax, w, red);
+        const float s32 = (amax * a.clip) / 7.0f;
+        const uint16_t s16 = f2h(s32);
+        const float sf = h2f(s16);
+        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (N / 2);
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc) {
+            const int g = (cc * W + w) * L + ll;
+#pragma unroll
+            for (int p = 0; p < M / 4; ++p) {
+                uint32_t pk = sym_code(v[cc][4 * p], sf) | (sym_code(v[cc][4 * p + 1], sf) << 4) |
+                              (sym_code(v[cc][4 * p + 2], sf) << 8) |
+                              (sym_code(v[cc][4 * p + 3], sf) << 12);
+                *reinterpret_cast<uint16_t *>(qr + g * (M / 2) + 2 * p) = (uint16_t)pk;
+            }
+        }
+        if (ll == 0 && w == 0)
+            a.scale[row] = s16;
+    }
+}
+
+// ------------------------------------------------------- m = 108, 172 -----
+
+template <int M>
+__device__ __forceinline__ const float *hm_columns();
+template <>
+__device__ __forceinline__ const float *hm_columns<108>()
+{
+    return &c_hm108.col[0][0];
+}
+template <>
+__device__ __forceinline__ const float *hm_columns<172>()
+{
+    return &c_hm172.col[0][0];
+}
+
+// One row per block; thread g < A = n/M owns group g.  The rotated row
+// (before the scale) is staged in LDS as A rows of M+1 floats.
+template <int M, int W, int EPI>
+__global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
+{
+    constexpr int CB = 4;  // output columns per pass
+    static_assert(M % CB == 0 && M % 4 == 0, "column blocking");
+    constexpr int LD = M + 1;
+    extern __shared__ float rowbuf[];
+    __shared__ float red[W];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int n = a.n, A = n / M;
+    const int k = 31 - __clz(A);
+    const int64_t row = blockIdx.x;
+    const bool act = tid < A;
+    const float *hc = hm_columns<M>();
+
+    float t[M];
+    if (act) {
+        const uint16_t *xg = a.x + row * n + (int64_t)tid * M;
+#pragma unroll
+        for (int p = 0; p < M / 4; ++p)
+            load4(xg + 4 * p, &t[4 * p]);
+    } else {
+#pragma unroll
+        for (int b = 0; b < M; ++b)
+            t[b] = 0.0f;
+    }
+    const int klane = k < 6 ? k : 6;
+    // rolled: one pass is 4 * M fused multiply-adds; unrolling all M/CB
+    // passes would not fit the instruction cache
+#pragma unroll 1
+    for (int cb = 0; cb < M; cb += CB) {
+        float u[CB];
+#pragma unroll
+        for (int q = 0; q < CB; ++q) {
+            const float *sg = hc + (cb + q) * M;  // signs of column cb+q
+            float acc = sg[0] * t[0];
+#pragma unroll
+            for (int b = 1; b < M; ++b)
+                acc = __builtin_fmaf(sg[b], t[b], acc);  // exactly acc +- t[b]
+            u[q] = acc;
+        }
+        for (int j = 0; j < klane; ++j)
+#pragma unroll
+            for (int q = 0; q < CB; ++q)
+                u[q] = bfly_lane(u[q], lane, 1 << j);
+        if (act)
+#pragma unroll
+            for (int q = 0; q < CB; ++q)
+                rowbuf[tid * LD + cb + q] = u[q];
+    }
+    __syncthreads();
+    // group bits 6.. (across waves): butterflies on the staged row
+    for (int j = 6; j < k; ++j) {
+        const int h = 1 << j;
+        const int total = (A / 2) * M;
+        for (int idx = tid; idx < total; idx += 64 * W) {
+            const int pr = idx / M, b = idx - pr * M;
+            const int p = (pr / h) * 2 * h + (pr % h), q = p + h;
+            const float up = rowbuf[p * LD + b], uq = rowbuf[q * LD + b];
+            rowbuf[p * LD + b] = up + uq;
+            rowbuf[q * LD + b] = up - uq;
+        }
+        __syncthreads();
+    }
+    const float c = a.c;
+    const int chunks = n / 8;
+    if constexpr (EPI == EPI_F16) {
+        uint16_t *yr = static_cast<uint16_t *>(a.out) + row * n;
+        for (int ch = tid; ch < chunks; ch += 64 * W) {
+            float y[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
+                y[e] = rowbuf[gi * LD + b] * c;
+            }
+            store8(yr + ch * 8, y);
+        }
+    } else {
+        static_assert(EPI == EPI_SYM, "large-m kernels serve activations");
+        float amax = 0.0f;
+        for (int ch = tid; ch < chunks; ch += 64 * W)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
+                amax = fmaxf(amax, fabsf(rowbuf[gi * LD + b] * c));
+            }
+#pragma unroll
+        for (int j = 0; j < 6; ++j)
+            amax = fmaxf(amax, __shfl_xor(amax, 1 << j));
+        if (lane == 0)
+            red[tid >> 6] = amax;
+        __syncthreads();
+        amax = red[0];
+#pragma unroll
+        for (int i = 1; i < W; ++i)
+            amax = fmaxf(amax, red[i]);
+        const float s32 = (amax * a.clip) / 7.0f;
+        const uint16_t s16 = f2h(s32);
+        const float sf = h2f(s16);
+        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (n / 2);
+        for (int ch = tid; ch < chunks; ch += 64 * W) {
+            uint32_t pk = 0;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
+                pk |= sym_code(rowbuf[gi * LD + b] * c, sf) << (4 * e);
+            }
+            *reinterpret_cast<uint32_t *>(qr + ch * 4) = pk;
+        }
+        if (tid == 0)
+            a.scale[row] = s16;
+    }
+}
+
+// ------------------------------------------------- no rotation, any n -----
+
+__global__ __launch_bounds__(256) void k_quant_plain(RotArgs a)
+{
+    __shared__ float red[4];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int64_t row = blockIdx.x;
+    const int n = a.n, chunks = n / 8;
+    const uint16_t *xr = a.x + row * n;
+    float amax = 0.0f;
+    for (int ch = tid; ch < chunks; ch += 256) {
+        float v[8];
+        load8(xr + ch * 8, v);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            amax = fmaxf(amax, fabsf(v[e]));
+    }
+#pragma unroll
+    for (int j = 0; j < 6; ++j)
+        amax = fmaxf(amax, __shfl_xor(amax, 1 << j));
+    if (lane == 0)
+        red[tid >> 6] = amax;
+    __syncthreads();
+    amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    const float s32 = (amax * a.clip) / 7.0f;
+    const uint16_t s16 = f2h(s32);
+    const float sf = h2f(s16);
+    uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (n / 2);
+    for (int ch = tid; ch < chunks; ch += 256) {
+        float v[8];
+        load8(xr + ch * 8, v);
+        uint32_t pk = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            pk |= sym_code(v[e], sf) << (4 * e);
+        *reinterpret_cast<uint32_t *>(qr + ch * 4) = pk;
+    }
+    if (tid == 0)
+        a.scale[row] = s16;
+}
+
+// ------------------------------------------------------ KV dequant -------
+
+template <int LOGL, bool INV>
+__global__ __launch_bounds__(256) void k_kv_dequant(KvDeqArgs a)
+{
+    constexpr int L = 1 << LOGL;
+    constexpr int RPW = 64 / L, RPB = 4 * RPW, N = 8 * L;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int ll = lane & (L - 1);
+    const int64_t row = (int64_t)blockIdx.x * RPB + wave * RPW + (lane >> LOGL);
+    if (row >= a.rows)
+        return;
+    const uint32_t pk = *reinterpret_cast<const uint32_t *>(a.q + row * (N / 2) + ll * 4);
+    const int64_t gi = row * (N / a.group) + (ll * 8) / a.group;
+    const float sf = h2f(a.scale[gi]), zf = h2f(a.zero[gi]);
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float t = (float)((pk >> (4 * e)) & 0xFu) * sf;
+        v[e] = t + zf;
+    }
+    if constexpr (INV) {
+#pragma unroll
+        for (int h = 1; h < 8; h <<= 1)
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (!(e & h)) {
+                    float p = v[e], q = v[e + h];
+                    v[e] = p + q;
+                    v[e + h] = p - q;
+                }
+#pragma unroll
+        for (int j = 0; j < LOGL; ++j)
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                v[e] = bfly_lane(v[e], ll, 1 << j);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            v[e] = v[e] * a.c;
+    }
+    store8(a.out + row * N + ll * 8, v);
+}
+
+// ---------------------------------------------------------- dispatch -----
+
+template <int LOGL, int W, int C, int EPI, bool ROT>
+hipError_t go_pow2(const RotArgs &a, hipStream_t s)
+{
+    constexpr int L = 1 << LOGL;
+    constexpr int RPB = (W == 1) ? 4 * (64 / L) : 1;
+    const int64_t blocks = (a.rows + RPB - 1) / RPB;
+    hipLaunchKernelGGL((k_rot_pow2<LOGL, W, C, EPI, ROT>), dim3((unsigned)blocks),
+                       dim3(W == 1 ? 256 : 64 * W), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int M, int LOGL, int W, int C, int EPI>
+hipError_t go_smallm(const RotArgs &a, hipStream_t s)
+{
+    constexpr int L = 1 << LOGL;
+    constexpr int RPB = (W == 1) ? 4 * (64 / L) : 1;
+    const int64_t blocks = (a.rows + RPB - 1) / RPB;
+    hipLaunchKernelGGL((k_rot_smallm<M, LOGL, W, C, EPI>), dim3((unsigned)blocks),
+                       dim3(W == 1 ? 256 : 64 * W), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int M, int W, int EPI>
+hipError_t go_largem(const RotArgs &a, hipStream_t s)
+{
+    const size_t lds = (size_t)(a.n / M) * (M + 1) * sizeof(float);
+    hipLaunchKernelGGL((k_rot_largem<M, W, EPI>), dim3((unsigned)a.rows), dim3(64 * W), lds, s, a);
+    return hipGetLastError();
+}
+
+template <int EPI, bool ROT>
+hipError_t dispatch_pow2(const RotArgs &a, int k, hipStream_t s)
+{
+    switch (k) {
+    case 3: return go_pow2<0, 1, 1, EPI, ROT>(a, s);
+    case 4: return go_pow2<1, 1, 1, EPI, ROT>(a, s);
+    case 5: return go_pow2<2, 1, 1, EPI, ROT>(a, s);
+    case 6: return go_pow2<3, 1, 1, EPI, ROT>(a, s);
+    case 7: return go_pow2<4, 1, 1, EPI, ROT>(a, s);
+    case 8: return go_pow2<5, 1, 1, EPI, ROT>(a, s);
+    case 9: return go_pow2<6, 1, 1, EPI, ROT>(a, s);
+    }
+    if constexpr (EPI != EPI_KV) {
+        switch (k) {
+        case 10: return go_pow2<6, 1, 2, EPI, ROT>(a, s);
+        case 11: return go_pow2<6, 1, 4, EPI, ROT>(a, s);
+        case 12: return go_pow2<6, 1, 8, EPI, ROT>(a, s);
+        case 13: return go_pow2<6, 1, 16, EPI, ROT>(a, s);
+        case 14: return go_pow2<6, 4, 8, EPI, ROT>(a, s);
+        case 15: return go_pow2<6, 8, 8, EPI, ROT>(a, s);
+        }
+    }
+    return hipErrorInvalidValue;
+}
+
+// groups A = 2^k; C = min(A/64, CMAX) chunks per lane, W = A/(64 C) waves
+template <int M, int CMAX, int EPI>
+hipError_t dispatch_smallm(const RotArgs &a, int k, hipStream_t s)
+{
+    switch (k) {
+    case 0: return go_smallm<M, 0, 1, 1, EPI>(a, s);
+    case 1: return go_smallm<M, 1, 1, 1, EPI>(a, s);
+    case 2: return go_smallm<M, 2, 1, 1, EPI>(a, s);
+    case 3: return go_smallm<M, 3, 1, 1, EPI>(a, s);
+    case 4: return go_smallm<M, 4, 1, 1, EPI>(a, s);
+    case 5: return go_smallm<M, 5, 1, 1, EPI>(a, s);
+    case 6: return go_smallm<M, 6, 1, 1, EPI>(a, s);
+    case 7: return go_smallm<M, 6, 1, 2, EPI>(a, s);
+    case 8: return go_smallm<M, 6, 1, 4, EPI>(a, s);
+    case 9: return go_smallm<M, 6, (CMAX >= 8 ? 1 : 2), (CMAX >= 8 ? 8 : 4), EPI>(a, s);
+    case 10: return go_smallm<M, 6, (CMAX >= 8 ? 2 : 4), (CMAX >= 8 ? 8 : 4), EPI>(a, s);
+    case 11:
+        if constexpr (CMAX >= 8)
+            return go_smallm<M, 6, 4, 8, EPI>(a, s);
+        break;
+    }
+    return hipErrorInvalidValue;
+}
+
+template <int EPI>
+hipError_t dispatch_rotated(const RotArgs &a, int k, int m, hipStream_t s)
+{
+    switch (m) {
+    case 1: return dispatch_pow2<EPI, true>(a, k, s);
+    case 12: return dispatch_smallm<12, 8, EPI>(a, k, s);
+    case 20: return dispatch_smallm<20, 4, EPI>(a, k, s);
+    case 28: return dispatch_smallm<28, 4, EPI>(a, k, s);
+    case 108: return (k <= 6) ? go_largem<108, 1, EPI>(a, s) : go_largem<108, 2, EPI>(a, s);
+    case 172: return go_largem<172, 1, EPI>(a, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+template <int LOGL>
+hipError_t go_kvdeq(const KvDeqArgs &a, bool inv, hipStream_t s)
+{
+    constexpr int RPB = 4 * (64 >> LOGL);
+    const int64_t blocks = (a.rows + RPB - 1) / RPB;
+    if (inv)
+        hipLaunchKernelGGL((k_kv_dequant<LOGL, true>), dim3((unsigned)blocks), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((k_kv_dequant<LOGL, false>), dim3((unsigned)blocks), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool rotate_supported(int epi, bool rotate, int k, int m, int n)
+{
+    if (n <= 0 || n % 8 != 0 || n > 32768)
+        return false;
+    if (!rotate)
+        return epi == EPI_SYM || (epi == EPI_KV && m == 1 && k >= 3 && k <= 9);
+    if (epi == EPI_KV)
+        return m == 1 && k >= 3 && k <= 9;
+    switch (m) {
+    case 1: return k >= 3 && k <= 15;
+    case 12: return k >= 1 && k <= 11;
+    case 20:
+    case 28: return k >= 1 && k <= 10;
+    case 108: return k >= 1 && k <= 7;
+    case 172: return k >= 1 && k <= 6;
+    }
+    return false;
+}
+
+hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, hipStream_t s)
+{
+    if (a.rows == 0)
+        return hipSuccess;
+    if (!rotate) {
+        if (epi == EPI_SYM) {
+            hipLaunchKernelGGL(k_quant_plain, dim3((unsigned)a.rows), dim3(256), 0, s, a);
+            return hipGetLastError();
+        }
+        if (epi == EPI_KV)
+            return dispatch_pow2<EPI_KV, false>(a, k, s);
+        return hipErrorInvalidValue;
+    }
+    switch (epi) {
+    case EPI_F16: return dispatch_rotated<EPI_F16>(a, k, m, s);
+    case EPI_SYM: return dispatch_rotated<EPI_SYM>(a, k, m, s);
+    case EPI_KV: return dispatch_pow2<EPI_KV, true>(a, k, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_kv_dequant(const KvDeqArgs &a, bool inverse_rotate, hipStream_t s)
+{
+    if (a.rows == 0)
+        return hipSuccess;
+    switch (a.n) {
+    case 8: return go_kvdeq<0>(a, inverse_rotate, s);
+    case 16: return go_kvdeq<1>(a, inverse_rotate, s);
+    case 32: return go_kvdeq<2>(a, inverse_rotate, s);
+    case 64: return go_kvdeq<3>(a, inverse_rotate, s);
+    case 128: return go_kvdeq<4>(a, inverse_rotate, s);
+    case 256: return go_kvdeq<5>(a, inverse_rotate, s);
+    case 512: return go_kvdeq<6>(a, inverse_rotate, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace quarot

@@ -1,0 +1,140 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol
+that include/quarot.h declares, answers host-only queries, and rejects bad
+arguments before touching any device.  No kernel is launched here."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2404_00456_amd as q
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "quarot.h")
+
+OK, INVALID, UNSUPPORTED, ALIGN, WORKSPACE, NODEV, HIP = range(7)
+
+# fake, aligned, never dereferenced device addresses for validation tests
+P = ctypes.c_void_p(1 << 20)
+P2 = ctypes.c_void_p((1 << 20) + 4096)
+UNALIGNED = ctypes.c_void_p((1 << 20) + 8)
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(quarot_[a-z0-9_]+)\s*\(", src)))
+
+
+def has_gpu():
+    import torch
+    return torch.cuda.device_count() > 0
+
+
+@pytest.fixture(scope="module")
+def L():
+    return q.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert len(names) >= 12
+    for name in names:
+        assert hasattr(L, name), name
+    # and the binding declares exactly those signatures
+    assert sorted(q.SIGNATURES) == names
+
+
+def test_status_strings(L):
+    for code, name in q.STATUS.items():
+        assert L.quarot_status_string(code).decode() == name
+    assert L.quarot_status_string(99).decode() == "QUAROT_ERR_UNKNOWN"
+    assert q.quarot_version() == 100
+
+
+def test_hadamard_factor_matches_oracle(orc):
+    for n in (8, 16, 128, 1024, 4096, 8192, 16384, 32768, 11008, 28672, 5120, 13824, 14336,
+              24, 40, 56, 344, 216, 20480, 24576):
+        assert q.quarot_hadamard_factor(n) == orc.hadamard_factor(n), n
+    for bad in (0, -8, 4, 12, 100, 65536, 172 * 128, 28 * 2048, 72, 20 * 2048):
+        assert q.quarot_hadamard_factor(bad) is None, bad
+
+
+@pytest.mark.parametrize("m", [12, 20, 28, 108, 172])
+def test_library_tables_match_oracle(orc, m):
+    """The library and the oracle build H_m independently from the same
+    published constructions; they must agree entry for entry."""
+    lib_t = q.quarot_hadamard_factor_table(m)
+    assert np.array_equal(lib_t, orc.hm_table(m))
+    H = lib_t.astype(np.int64)
+    assert np.array_equal(H @ H.T, m * np.eye(m, dtype=np.int64))
+
+
+def test_workspace_size(L):
+    assert q.quarot_linear_workspace_size(16384, 8192) == 16384 * 4096 + 32768
+    assert q.quarot_linear_workspace_size(3, 128) == 256 + 256
+    assert q.quarot_linear_workspace_size(0, 128) == 256 * 0 + 0
+    assert q.quarot_linear_workspace_size(-1, 128) == 0
+    assert q.quarot_linear_workspace_size(4, 0) == 0
+    assert q.quarot_linear_workspace_size(4, 7) == 0
+
+
+def test_invalid_arguments_rejected_before_device(L):
+    S = None  # null stream
+    # hadamard
+    assert L.quarot_hadamard(P, P2, -1, 128, S) == INVALID
+    assert L.quarot_hadamard(P, P2, 4, 0, S) == INVALID
+    assert L.quarot_hadamard(P, P2, 4, 100, S) == UNSUPPORTED
+    assert L.quarot_hadamard(P, P2, 4, 65536, S) == UNSUPPORTED
+    assert L.quarot_hadamard(None, P2, 4, 128, S) == INVALID
+    assert L.quarot_hadamard(UNALIGNED, P2, 4, 128, S) == ALIGN
+    assert L.quarot_hadamard(None, None, 0, 128, S) == OK  # empty is a no-op
+    # quant
+    assert L.quarot_quant_int4(P, P2, P2, 4, 128, 1, 0.0, S) == INVALID
+    assert L.quarot_quant_int4(P, P2, P2, 4, 128, 1, 1.5, S) == INVALID
+    assert L.quarot_quant_int4(P, P2, P2, 4, 12, 0, 1.0, S) == UNSUPPORTED
+    assert L.quarot_quant_int4(P, P2, P2, 4, 11008 * 3, 1, 1.0, S) == UNSUPPORTED
+    assert L.quarot_quant_int4(P, None, P2, 4, 128, 1, 1.0, S) == INVALID
+    assert L.quarot_quant_int4(P, P2, UNALIGNED, 4, 128, 1, 1.0, S) == ALIGN
+    assert L.quarot_quant_int4(None, None, None, 0, 128, 1, 1.0, S) == OK
+    # gemm
+    assert L.quarot_w4a4_gemm(P, P, P, P, P, None, 4, 4, 100, S) == UNSUPPORTED
+    assert L.quarot_w4a4_gemm(P, P, P, P, P, None, -1, 4, 128, S) == INVALID
+    assert L.quarot_w4a4_gemm(P, P, P, P, P, None, 4, 4, 0, S) == INVALID
+    assert L.quarot_w4a4_gemm(P, P, P, P, P, None, 4, 4, 65536 + 64, S) == UNSUPPORTED
+    assert L.quarot_w4a4_gemm(P, None, P, P, P, None, 4, 4, 128, S) == INVALID
+    assert L.quarot_w4a4_gemm(P, P, P, P, P, UNALIGNED, 4, 4, 128, S) == ALIGN
+    assert L.quarot_w4a4_gemm(None, None, None, None, None, None, 0, 4, 128, S) == OK
+    # linear
+    assert L.quarot_linear(P, P, P, P, 4, 4, 128, 1, 1.0, None, 0, S) == WORKSPACE
+    assert L.quarot_linear(P, P, P, P, 4, 4, 128, 1, 1.0, P, 10, S) == WORKSPACE
+    assert L.quarot_linear(P, P, P, P, 4, 4, 128, 1, 1.0, ctypes.c_void_p((1 << 20) + 16),
+                           4096, S) == ALIGN
+    assert L.quarot_linear(P, P, P, P, 4, 4, 96, 1, 1.0, P, 4096, S) == UNSUPPORTED
+    assert L.quarot_linear(P, P, P, P, 4, 4, 128, 1, -0.5, P, 4096, S) == INVALID
+    # kv
+    assert L.quarot_kv_quant(P, P, P, P, 4, 128, 256, 1, 0.95, S) == UNSUPPORTED
+    assert L.quarot_kv_quant(P, P, P, P, 4, 96, 32, 1, 0.95, S) == UNSUPPORTED
+    assert L.quarot_kv_quant(P, P, P, P, 4, 128, 4, 1, 0.95, S) == UNSUPPORTED
+    assert L.quarot_kv_quant(P, P, P, P, 4, 1024, 128, 1, 0.95, S) == UNSUPPORTED
+    assert L.quarot_kv_quant(P, P, P, None, 4, 128, 128, 1, 0.95, S) == INVALID
+    assert L.quarot_kv_dequant(P, P, P, P, 4, 128, 0, 0, S) == INVALID
+    assert L.quarot_kv_dequant(P, P, UNALIGNED, P, 4, 128, 128, 0, S) == ALIGN
+
+
+@pytest.mark.skipif(has_gpu(), reason="valid arguments would reach a real device")
+def test_no_device_reported(L):
+    """With valid arguments and no GPU the call stops at the device check
+    (fake pointers are never dereferenced because nothing launches)."""
+    assert L.quarot_quant_int4(P, P2, P2, 4, 128, 1, 1.0, None) == NODEV
+    assert L.quarot_w4a4_gemm(P, P, P, P, P, None, 4, 4, 128, None) == NODEV
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    x = torch.zeros(4, 128, dtype=torch.float16)
+    with pytest.raises(ValueError):
+        q.quarot_hadamard(x, y=torch.zeros_like(x))
+    with pytest.raises(TypeError):
+        q.quarot_hadamard(x.float(), y=torch.zeros_like(x))
