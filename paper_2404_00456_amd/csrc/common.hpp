@@ -64,8 +64,12 @@ __device__ __forceinline__ float h2f(uint16_t h)
     return __half2float(__ushort_as_half(h));
 }
 
+// RN16 of a rounded binary32 value.  The empty asm pins f to a VGPR first:
+// without it the backend folds "fp32 multiply (or add), then convert" into
+// one v_fma_mix*_f16, which rounds once to fp16 instead of RN16(RN32(.)).
 __device__ __forceinline__ uint16_t f2h(float f)
 {
+    __asm__ volatile("" : "+v"(f));
     return __half_as_ushort(__float2half_rn(f));
 }
 
