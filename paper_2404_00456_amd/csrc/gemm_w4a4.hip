@@ -66,7 +66,7 @@ constexpr int THREADS = 512;
 constexpr int WN = 64;   // n per wave
 constexpr int NI = WN / 16;  // n slices per wave (MFMA A operands)
 
-__global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
+__global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_k64(GemmArgs a)
 {
     extern __shared__ __align__(16) uint8_t lds[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -211,20 +211,197 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
     }
 }
 
+
+// ------------------------------------------------------------------------
+// Main kernel (K a multiple of 128).  Same tile, waves and epilogue as the
+// fallback above, but the operand tiles travel HBM -> LDS with
+// global_load_lds_dwordx4 (no VGRP staging) into a ring of S stages, issued
+// two k-steps ahead of the MFMAs, with one barrier per k-step.  The DMA
+// writes a wave's 64 lanes contiguously (1 KB = 16 rows x 64 B), so rows are
+// unpadded and bank conflicts are avoided by an XOR swizzle instead: the
+// 16-byte chunk c of row r sits at chunk position c ^ ((r >> 2) & 3).
+constexpr int S = 3;                       // LDS ring stages
+constexpr int RING_STAGE = (BM + BN) * BKB;  // 32 KB: X rows then W rows
+constexpr int RING_BYTES = S * RING_STAGE;
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 16 bytes per lane from global memory straight into LDS at
+// lds_base + 16 * lane.  Issued as inline asm on purpose: for the compiler's
+// own LDS-DMA builtin the waitcnt pass cannot tell the DMA target from the
+// stage being read and waits for every DMA before each LDS read, which
+// serializes the ring.  Here only the explicit s_waitcnt below orders it.
+// The kernel uses M0 for nothing else (checked in its ISA).
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds_base)
+{
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(g), "s"(lds_base)
+                 : "memory");
+}
+
+__global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 2, wn = wave & 3;
+    const int M = a.M, N = a.N, K = a.K;
+    const int TM = (M + BM - 1) / BM, TN = (N + BN - 1) / BN;
+    int tm, tn;
+    tile_of(blockIdx.x, gridDim.x, TM, TN, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int64_t ldk = K / 2;
+    const int KT = K / 128;
+
+    // DMA sources: instruction i of wave w moves 16 rows of X (i < 2) or W
+    // (i >= 2): rows 16*(w + 8*(i&1)) + lane/4, LDS chunk position lane%4,
+    // global chunk (lane%4) ^ swizzle(row)
+    const uint8_t *src[4];
+    int dst[4];
+    {
+        const int rsub = lane >> 2;
+        const int c = (lane & 3) ^ ((lane >> 4) & 3);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int q = wave + 8 * (i & 1);
+            const int r = 16 * q + rsub;
+            if (i < 2) {
+                src[i] = a.xq + (int64_t)min(m0 + r, M - 1) * ldk + c * 16;
+                dst[i] = q * 1024;
+            } else {
+                src[i] = a.wq + (int64_t)min(n0 + r, N - 1) * ldk + c * 16;
+                dst[i] = BM * BKB + q * 1024;
+            }
+        }
+    }
+    const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void *)lds;
+    auto issue = [&](int kt, int stage) {
+        const uint32_t sbase = lds_base + stage * RING_STAGE;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            dma16(src[i] + (int64_t)kt * BKB, __builtin_amdgcn_readfirstlane(sbase + dst[i]));
+    };
+
+    v4i acc[NI][8];
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            acc[i][j] = v4i{0, 0, 0, 0};
+
+    // operand reads: row (lane & 15) of a 16-row slice, k chunk 2*kk + lane/32,
+    // byte 8 * ((lane >> 4) & 1) of it, at the swizzled chunk position
+    const int orow = lane & 15;
+    const int rsw = (orow >> 2) & 3;
+    int ooff[2];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+        ooff[kk] = (((2 * kk + (lane >> 5)) ^ rsw) << 4) + (((lane >> 4) & 1) << 3);
+    const int brow = (wm * 128 + orow) * BKB;        // X slice rows (B operand)
+    const int arow = (BM + wn * WN + orow) * BKB;    // W slice rows (A operand)
+
+    // Loads are issued unconditionally: past the last k-step they re-fetch
+    // step KT-1 into a stage that is never read again.  That keeps exactly
+    // two stages (8 DMAs per thread) in flight at every wait, and keeps the
+    // compiler from inserting a vmcnt(0) where a conditional issue joins.
+    issue(0, 0);
+    issue(min(1, KT - 1), 1 % S);
+    for (int kt = 0; kt < KT; ++kt) {
+        // my DMAs for stage kt are done (stage kt+1's 4 may still fly); after
+        // the barrier everyone's are, and everyone has finished reading the
+        // stage that the next issue overwrites.  A bare s_barrier:
+        // __syncthreads' fence would wait for every DMA in flight.
+        __builtin_amdgcn_s_waitcnt(0xF74);  // vmcnt(4) expcnt(7) lgkmcnt(15)
+        __builtin_amdgcn_s_barrier();
+        issue(min(kt + 2, KT - 1), (kt + 2) % S);
+        const uint8_t *sb = lds + (kt % S) * RING_STAGE;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            v4i bq[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                bq[j] = widen(*reinterpret_cast<const uint2 *>(sb + brow + j * 16 * BKB + ooff[kk]));
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                const v4i aq =
+                    widen(*reinterpret_cast<const uint2 *>(sb + arow + i * 16 * BKB + ooff[kk]));
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aq, bq[j], acc[i][j], 0, 0, 0);
+            }
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0xF70);  // no DMA may outlive the block's LDS
+
+    float sxf[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int m = m0 + wm * 128 + j * 16 + orow;
+        sxf[j] = h2f(a.sx[min(m, M - 1)]);
+    }
+    const bool vec = (N & 3) == 0;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+        const int nb = n0 + wn * WN + i * 16 + (lane >> 4) * 4;
+        float swf[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            swf[r] = h2f(a.sw[min(nb + r, N - 1)]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int m = m0 + wm * 128 + j * 16 + orow;
+            if (m >= M)
+                continue;
+            int iv[4];
+            uint16_t hv[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                iv[r] = acc[i][j][r] >> 8;
+                const float t = (float)iv[r] * sxf[j];
+                hv[r] = f2h(t * swf[r]);
+            }
+            uint16_t *yrow = a.y + (int64_t)m * N;
+            int32_t *arw = a.acc ? a.acc + (int64_t)m * N : nullptr;
+            if (vec && nb + 3 < N) {
+                uint2 pk;
+                pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
+                pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
+                *reinterpret_cast<uint2 *>(yrow + nb) = pk;
+                if (arw)
+                    *reinterpret_cast<int4 *>(arw + nb) = make_int4(iv[0], iv[1], iv[2], iv[3]);
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (nb + r < N) {
+                        yrow[nb + r] = hv[r];
+                        if (arw)
+                            arw[nb + r] = iv[r];
+                    }
+            }
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s)
 {
     if (a.M == 0 || a.N == 0)
         return hipSuccess;
+    const int TM = (a.M + BM - 1) / BM, TN = (a.N + BN - 1) / BN;
+    const bool main = (a.K % 128) == 0;
+    const void *fn = main ? (const void *)k_gemm_w4a4 : (const void *)k_gemm_w4a4_k64;
+    const int lds_bytes = main ? RING_BYTES : LDS_BYTES;
     // more than 64 KB of dynamic LDS: raise the kernel's limit (per call, so
     // that every device the caller uses gets it; the call is host-side only)
-    hipError_t e = hipFuncSetAttribute((const void *)k_gemm_w4a4,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
     if (e != hipSuccess)
         return e;
-    const int TM = (a.M + BM - 1) / BM, TN = (a.N + BN - 1) / BN;
-    hipLaunchKernelGGL(k_gemm_w4a4, dim3((unsigned)(TM * TN)), dim3(THREADS), LDS_BYTES, s, a);
+    if (main)
+        hipLaunchKernelGGL(k_gemm_w4a4, dim3((unsigned)(TM * TN)), dim3(THREADS), lds_bytes, s, a);
+    else
+        hipLaunchKernelGGL(k_gemm_w4a4_k64, dim3((unsigned)(TM * TN)), dim3(THREADS), lds_bytes, s,
+                           a);
     return hipGetLastError();
 }
 
