@@ -213,14 +213,22 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_k64(GemmArgs a)
 
 
 // ------------------------------------------------------------------------
-// Main kernel (K a multiple of 128).  Same tile, waves and epilogue as the
-// fallback above, but the operand tiles travel HBM -> LDS with
-// global_load_lds_dwordx4 (no VGRP staging) into a ring of S stages, issued
-// two k-steps ahead of the MFMAs, with one barrier per k-step.  The DMA
-// writes a wave's 64 lanes contiguously (1 KB = 16 rows x 64 B), so rows are
-// unpadded and bank conflicts are avoided by an XOR swizzle instead: the
-// 16-byte chunk c of row r sits at chunk position c ^ ((r >> 2) & 3).
-constexpr int S = 3;                       // LDS ring stages
+// Main kernel (K a multiple of 128).  Same block tile, waves and epilogue as
+// the fallback above; the operand path differs:
+//
+//  * HBM -> LDS with global_load_lds_dwordx4 (no VGPR staging) into a ring
+//    of S stages, three k-steps ahead of the MFMAs, one barrier per k-step.
+//  * k assignment: within a k-step (128 k = 64 packed bytes per row), lane
+//    group g = lane/16 of an operand owns the 16-byte unit g of its row and
+//    uses its first 8 bytes in MFMA substep 0 and the last 8 in substep 1.
+//    Every byte of the row is used once, by the same lane slot in A and B,
+//    so the dot products are unchanged, and each operand is a single
+//    ds_read_b128 per k-step.
+//  * LDS rows are unpadded (the DMA writes a wave's lanes contiguously:
+//    1 KB = 16 rows x 64 B); unit c of row r sits at unit c ^ ((r >> 1) & 3),
+//    which makes the 16-byte reads of 8 consecutive rows hit 8 distinct bank
+//    groups.
+constexpr int S = 3;                         // LDS ring stages
 constexpr int RING_STAGE = (BM + BN) * BKB;  // 32 KB: X rows then W rows
 constexpr int RING_BYTES = S * RING_STAGE;
 
@@ -254,13 +262,13 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
     const int KT = K / 128;
 
     // DMA sources: instruction i of wave w moves 16 rows of X (i < 2) or W
-    // (i >= 2): rows 16*(w + 8*(i&1)) + lane/4, LDS chunk position lane%4,
-    // global chunk (lane%4) ^ swizzle(row)
+    // (i >= 2): rows 16*(w + 8*(i&1)) + lane/4 land at unit lane%4 of their
+    // LDS row, so they must fetch global unit (lane%4) ^ swizzle(row)
     const uint8_t *src[4];
     int dst[4];
     {
         const int rsub = lane >> 2;
-        const int c = (lane & 3) ^ ((lane >> 4) & 3);
+        const int c = (lane & 3) ^ ((lane >> 3) & 3);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int q = wave + 8 * (i & 1);
@@ -289,47 +297,64 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
         for (int j = 0; j < 8; ++j)
             acc[i][j] = v4i{0, 0, 0, 0};
 
-    // operand reads: row (lane & 15) of a 16-row slice, k chunk 2*kk + lane/32,
-    // byte 8 * ((lane >> 4) & 1) of it, at the swizzled chunk position
+    // operand reads: row (lane & 15) of a 16-row slice, unit lane >> 4 of it
     const int orow = lane & 15;
-    const int rsw = (orow >> 2) & 3;
-    int ooff[2];
+    const int ounit = ((lane >> 4) ^ ((orow >> 1) & 3)) << 4;
+    const int brow = (wm * 128 + orow) * BKB + ounit;        // X slice rows (B operand)
+    const int arow = (BM + wn * WN + orow) * BKB + ounit;    // W slice rows (A operand)
+    auto read_step = [&](uint4 (&ops)[8 + NI], int stage) {
+        const uint8_t *sb = lds + stage * RING_STAGE;
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-        ooff[kk] = (((2 * kk + (lane >> 5)) ^ rsw) << 4) + (((lane >> 4) & 1) << 3);
-    const int brow = (wm * 128 + orow) * BKB;        // X slice rows (B operand)
-    const int arow = (BM + wn * WN + orow) * BKB;    // W slice rows (A operand)
-
-    // Loads are issued unconditionally: past the last k-step they re-fetch
-    // step KT-1 into a stage that is never read again.  That keeps exactly
-    // two stages (8 DMAs per thread) in flight at every wait, and keeps the
-    // compiler from inserting a vmcnt(0) where a conditional issue joins.
-    issue(0, 0);
-    issue(min(1, KT - 1), 1 % S);
-    for (int kt = 0; kt < KT; ++kt) {
-        // my DMAs for stage kt are done (stage kt+1's 4 may still fly); after
-        // the barrier everyone's are, and everyone has finished reading the
-        // stage that the next issue overwrites.  A bare s_barrier:
-        // __syncthreads' fence would wait for every DMA in flight.
-        __builtin_amdgcn_s_waitcnt(0xF74);  // vmcnt(4) expcnt(7) lgkmcnt(15)
-        __builtin_amdgcn_s_barrier();
-        issue(min(kt + 2, KT - 1), (kt + 2) % S);
-        const uint8_t *sb = lds + (kt % S) * RING_STAGE;
+        for (int j = 0; j < 8; ++j)
+            ops[j] = *reinterpret_cast<const uint4 *>(sb + brow + j * 16 * BKB);
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            v4i bq[8];
+        for (int i = 0; i < NI; ++i)
+            ops[8 + i] = *reinterpret_cast<const uint4 *>(sb + arow + i * 16 * BKB);
+    };
+    // one MFMA substep: the A operands (W rows) widened up front, each B
+    // operand (X rows) widened just before its NI MFMAs
+    auto substep = [&](const uint4 (&ops)[8 + NI], int h) {
+        v4i aq[NI];
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                bq[j] = widen(*reinterpret_cast<const uint2 *>(sb + brow + j * 16 * BKB + ooff[kk]));
+        for (int i = 0; i < NI; ++i)
+            aq[i] = widen(h ? make_uint2(ops[8 + i].z, ops[8 + i].w)
+                            : make_uint2(ops[8 + i].x, ops[8 + i].y));
 #pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                const v4i aq =
-                    widen(*reinterpret_cast<const uint2 *>(sb + arow + i * 16 * BKB + ooff[kk]));
+        for (int j = 0; j < 8; ++j) {
+            const v4i bq = widen(h ? make_uint2(ops[j].z, ops[j].w) : make_uint2(ops[j].x, ops[j].y));
 #pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aq, bq[j], acc[i][j], 0, 0, 0);
-            }
+            for (int i = 0; i < NI; ++i)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aq[i], bq, acc[i][j], 0, 0, 0);
         }
+    };
+
+    // Iteration kt: substep 0 of step kt; wait for my DMA of step kt+1 and
+    // my LDS reads, barrier (now every DMA of kt+1 has landed and nobody
+    // reads stage kt any more); DMA of step kt+3 into stage kt; read step
+    // kt+1 while substep 1 of step kt runs.  DMAs are issued
+    // unconditionally (past the last step they re-fetch step KT-1 into a
+    // stage never read again) so that exactly two steps are in flight at
+    // every wait; the read after the last step touches a landed, unused
+    // stage.
+    issue(0, 0);
+    issue(min(1, KT - 1), 1);
+    issue(min(2, KT - 1), 2);
+    __builtin_amdgcn_s_waitcnt(0xF78);  // vmcnt(8): step 0 landed
+    __builtin_amdgcn_s_barrier();
+    // (rolled: unrolled by two, so that R and Rn alternate instead of being
+    // copied, the kernel no longer fits 256 VGPRs)
+    uint4 R[8 + NI], Rn[8 + NI];
+    read_step(R, 0);
+    for (int kt = 0; kt < KT; ++kt) {
+        substep(R, 0);
+        __builtin_amdgcn_s_waitcnt(0x074);  // vmcnt(4) expcnt(7) lgkmcnt(0)
+        __builtin_amdgcn_s_barrier();
+        issue(min(kt + 3, KT - 1), kt % S);
+        read_step(Rn, (kt + 1) % S);
+        substep(R, 1);
+#pragma unroll
+        for (int o = 0; o < 8 + NI; ++o)
+            R[o] = Rn[o];
     }
     __builtin_amdgcn_s_waitcnt(0xF70);  // no DMA may outlive the block's LDS
 
