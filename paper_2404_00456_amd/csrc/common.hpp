@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 namespace quarot {
 
@@ -73,13 +74,96 @@ __device__ __forceinline__ uint16_t f2h(float f)
     return __half_as_ushort(__float2half_rn(f));
 }
 
-// One butterfly of the Walsh-Hadamard transform across lanes: lane pairs
-// (p, p ^ mask); the lane with the bit clear keeps u_p + u_q, the other
-// keeps u_p - u_q (each one rounded op, as in the canonical order).
-__device__ __forceinline__ float bfly_lane(float v, int lane, int mask)
+// Value of lane (lane ^ (1 << J)), J = 0..3, by DPP: quad_perm for bits 0
+// and 1; for bits 2 and 3 a mirror within 8 (lane ^ 7) or 16 (lane ^ 15)
+// lanes composed with a second DPP.
+template <int J>
+__device__ __forceinline__ float lane_xor_dpp(float v)
 {
-    float o = __shfl_xor(v, mask);
-    return (lane & mask) ? (o - v) : (v + o);
+    static_assert(J >= 0 && J <= 3, "bits 0..3");
+    const int vi = __float_as_int(v);
+    int p;
+    if constexpr (J == 0) {
+        p = __builtin_amdgcn_update_dpp(vi, vi, 0xB1, 0xF, 0xF, false);  // quad_perm 1,0,3,2
+    } else if constexpr (J == 1) {
+        p = __builtin_amdgcn_update_dpp(vi, vi, 0x4E, 0xF, 0xF, false);  // quad_perm 2,3,0,1
+    } else if constexpr (J == 2) {
+        const int t = __builtin_amdgcn_update_dpp(vi, vi, 0x141, 0xF, 0xF, false);  // lane ^ 7
+        p = __builtin_amdgcn_update_dpp(t, t, 0x1B, 0xF, 0xF, false);  // then ^ 3
+    } else {
+        const int t = __builtin_amdgcn_update_dpp(vi, vi, 0x140, 0xF, 0xF, false);  // lane ^ 15
+        p = __builtin_amdgcn_update_dpp(t, t, 0x141, 0xF, 0xF, false);  // then ^ 7
+    }
+    return __int_as_float(p);
+}
+
+// The pair across lane bit J (4 or 5) by v_permlane{16,32}_swap: .x holds
+// the value of the lane with bit J clear, .y that of the lane with it set.
+template <int J>
+__device__ __forceinline__ float2 lane_pair_swap(float v)
+{
+    static_assert(J == 4 || J == 5, "bits 4, 5");
+    const unsigned u = __float_as_uint(v);
+    if constexpr (J == 4) {
+        const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+        return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    } else {
+        const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+        return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    }
+}
+
+// One Walsh-Hadamard butterfly across lane bit J: lanes with the bit clear
+// get RN(u_lo + u_hi), lanes with it set RN(u_lo - u_hi), each exactly one
+// rounded operation as in the canonical order: fma(x, +-1, y) = RN(y +- x).
+// s is +1 on lanes with bit J clear and -1 where it is set.
+template <int J>
+__device__ __forceinline__ float bfly_lane(float v, float s)
+{
+    if constexpr (J <= 3) {
+        return __builtin_fmaf(v, s, lane_xor_dpp<J>(v));  // v is u_lo (s=+1) or u_hi (s=-1)
+    } else {
+        const float2 p = lane_pair_swap<J>(v);
+        return __builtin_fmaf(p.y, s, p.x);
+    }
+}
+
+template <int J>
+__device__ __forceinline__ float lane_max(float v)
+{
+    if constexpr (J <= 3)
+        return fmaxf(v, lane_xor_dpp<J>(v));
+    else {
+        const float2 p = lane_pair_swap<J>(v);
+        return fmaxf(p.x, p.y);
+    }
+}
+
+template <int J>
+__device__ __forceinline__ float lane_min(float v)
+{
+    if constexpr (J <= 3)
+        return fminf(v, lane_xor_dpp<J>(v));
+    else {
+        const float2 p = lane_pair_swap<J>(v);
+        return fminf(p.x, p.y);
+    }
+}
+
+// Compile-time loop helper: f(std::integral_constant<int, J>) for J < N.
+template <int N, int J = 0, typename F>
+__device__ __forceinline__ void static_for(F &&f)
+{
+    if constexpr (J < N) {
+        f(std::integral_constant<int, J>());
+        static_for<N, J + 1>(f);
+    }
+}
+
+// Lane signs for the butterflies: +1 where lane bit J is clear, -1 where set.
+__device__ __forceinline__ float lane_sign(int lane, int J)
+{
+    return ((lane >> J) & 1) ? -1.0f : 1.0f;
 }
 
 }  // namespace quarot

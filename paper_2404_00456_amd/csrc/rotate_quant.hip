@@ -38,25 +38,46 @@ constexpr int ilog2(int v)
     return r;
 }
 
-// Symmetric int4 code of y with the stored fp16 scale sf (§4 Stage 2b):
-// clamp(rint_even(RN(y / sf)), -8, 7); sf == 0 gives 0.  IEEE division.
-__device__ __forceinline__ uint32_t sym_code(float y, float sf)
+// The quantizers divide by a stored fp16 scale sf.  RN(y / sf) is formed
+// with Markstein's correction from rf = RN(1 / sf), computed once per row or
+// group: q0 = RN(y rf), e = y - q0 sf (exact, one fma), q = RN(q0 + e rf).
+// With a correctly rounded reciprocal this equals the IEEE quotient except
+// where it underflows (|q| < 2^-100), where both give code 0; checked
+// against IEEE division for every positive fp16 divisor.  A zero or
+// infinite scale gives code 0 (y / inf = 0 as well).
+struct Divisor {
+    float s, r;
+    bool ok;
+};
+
+__device__ __forceinline__ Divisor make_divisor(float sf)
 {
-    if (sf == 0.0f)
-        return 0u;
-    float r = rintf(y / sf);
-    r = fminf(fmaxf(r, -8.0f), 7.0f);
-    return (uint32_t)(int)r & 0xFu;
+    Divisor d;
+    d.s = sf;
+    d.ok = sf > 0.0f && sf < __builtin_inff();
+    d.r = d.ok ? 1.0f / sf : 0.0f;
+    return d;
+}
+
+__device__ __forceinline__ float quotient(float y, const Divisor &d)
+{
+    const float q0 = y * d.r;
+    const float e = __builtin_fmaf(-q0, d.s, y);
+    return __builtin_fmaf(e, d.r, q0);
+}
+
+// Symmetric int4 code (§4 Stage 2b): clamp(rint_even(RN(y / sf)), -8, 7).
+__device__ __forceinline__ uint32_t sym_code(float y, const Divisor &d)
+{
+    const float c = fminf(fmaxf(rintf(quotient(y, d)), -8.0f), 7.0f);
+    return d.ok ? ((uint32_t)(int)c & 0xFu) : 0u;
 }
 
 // Asymmetric uint4 code: clamp(rint_even(RN(RN(y - zf) / sf)), 0, 15).
-__device__ __forceinline__ uint32_t asym_code(float y, float sf, float zf)
+__device__ __forceinline__ uint32_t asym_code(float y, const Divisor &d, float zf)
 {
-    if (sf == 0.0f)
-        return 0u;
-    float r = rintf((y - zf) / sf);
-    r = fminf(fmaxf(r, 0.0f), 15.0f);
-    return (uint32_t)(int)r;
+    const float c = fminf(fmaxf(rintf(quotient(y - zf, d)), 0.0f), 15.0f);
+    return d.ok ? (uint32_t)(int)c : 0u;
 }
 
 __device__ __forceinline__ void load8(const uint16_t *p, float *v)
@@ -101,9 +122,7 @@ __device__ __forceinline__ void store4(uint16_t *p, const float *v)
 template <int LOGL, int W>
 __device__ __forceinline__ float row_absmax(float amax, int w, float *red)
 {
-#pragma unroll
-    for (int j = 0; j < LOGL; ++j)
-        amax = fmaxf(amax, __shfl_xor(amax, 1 << j));
+    static_for<LOGL>([&](auto J) { amax = lane_max<J>(amax); });
     if constexpr (W > 1) {
         if ((threadIdx.x & 63) == 0)
             red[w] = amax;
@@ -160,13 +179,14 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
                         v[cc][e + h] = p - q;
                     }
         // next LOGL bits: across lanes
-#pragma unroll
-        for (int j = 0; j < LOGL; ++j)
+        static_for<LOGL>([&](auto J) {
+            const float sg = lane_sign(lane, J);
 #pragma unroll
             for (int cc = 0; cc < C; ++cc)
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    v[cc][e] = bfly_lane(v[cc][e], ll, 1 << j);
+                    v[cc][e] = bfly_lane<J>(v[cc][e], sg);
+        });
         // next LOGW bits: across waves, through LDS one chunk at a time
         if constexpr (W > 1) {
             __shared__ float xs[W][8][64];
@@ -224,14 +244,14 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
         amax = row_absmax<LOGL, W>(amax, w, red);
         const float s32 = (amax * a.clip) / 7.0f;
         const uint16_t s16 = f2h(s32);
-        const float sf = h2f(s16);
+        const Divisor dv = make_divisor(h2f(s16));
         uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (N / 2);
 #pragma unroll
         for (int cc = 0; cc < C; ++cc) {
             uint32_t pk = 0;
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                pk |= sym_code(v[cc][e], sf) << (4 * e);
+                pk |= sym_code(v[cc][e], dv) << (4 * e);
             *reinterpret_cast<uint32_t *>(qr + ((cc * W + w) * L + ll) * 4) = pk;
         }
         if (ll == 0 && w == 0)
@@ -245,18 +265,21 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
             mn = fminf(mn, v[0][e]);
         }
         const int gl = a.group >> 3;  // lanes per group
-        for (int j = 1; j < gl; j <<= 1) {
-            mx = fmaxf(mx, __shfl_xor(mx, j));
-            mn = fminf(mn, __shfl_xor(mn, j));
-        }
+        static_for<LOGL>([&](auto J) {
+            if ((1 << J) < gl) {
+                mx = lane_max<J>(mx);
+                mn = lane_min<J>(mn);
+            }
+        });
         const float mxc = mx * a.clip, mnc = mn * a.clip;
         const float s32 = (mxc - mnc) / 15.0f;
         const uint16_t s16 = f2h(s32), z16 = f2h(mnc);
-        const float sf = h2f(s16), zf = h2f(z16);
+        const Divisor dv = make_divisor(h2f(s16));
+        const float zf = h2f(z16);
         uint32_t pk = 0;
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-            pk |= asym_code(v[0][e], sf, zf) << (4 * e);
+            pk |= asym_code(v[0][e], dv, zf) << (4 * e);
         uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (N / 2);
         *reinterpret_cast<uint32_t *>(qr + ll * 4) = pk;
         if ((ll & (gl - 1)) == 0) {
@@ -320,13 +343,14 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
         }
     }
     // group bits 0..LOGL-1 across lanes
-#pragma unroll
-    for (int j = 0; j < LOGL; ++j)
+    static_for<LOGL>([&](auto J) {
+        const float sg = lane_sign(lane, J);
 #pragma unroll
         for (int cc = 0; cc < C; ++cc)
 #pragma unroll
             for (int b = 0; b < M; ++b)
-                v[cc][b] = bfly_lane(v[cc][b], ll, 1 << j);
+                v[cc][b] = bfly_lane<J>(v[cc][b], sg);
+    });
     if constexpr (W > 1) {
         __shared__ float xs[W][M][64];
 #pragma unroll
@@ -386,16 +410,16 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
         amax = row_absmax<LOGL, W>(amax, w, red);
         const float s32 = (amax * a.clip) / 7.0f;
         const uint16_t s16 = f2h(s32);
-        const float sf = h2f(s16);
+        const Divisor dv = make_divisor(h2f(s16));
         uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (N / 2);
 #pragma unroll
         for (int cc = 0; cc < C; ++cc) {
             const int g = (cc * W + w) * L + ll;
 #pragma unroll
             for (int p = 0; p < M / 4; ++p) {
-                uint32_t pk = sym_code(v[cc][4 * p], sf) | (sym_code(v[cc][4 * p + 1], sf) << 4) |
-                              (sym_code(v[cc][4 * p + 2], sf) << 8) |
-                              (sym_code(v[cc][4 * p + 3], sf) << 12);
+                uint32_t pk = sym_code(v[cc][4 * p], dv) | (sym_code(v[cc][4 * p + 1], dv) << 4) |
+                              (sym_code(v[cc][4 * p + 2], dv) << 8) |
+                              (sym_code(v[cc][4 * p + 3], dv) << 12);
                 *reinterpret_cast<uint16_t *>(qr + g * (M / 2) + 2 * p) = (uint16_t)pk;
             }
         }
@@ -462,10 +486,14 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
                 acc = __builtin_fmaf(sg[b], t[b], acc);  // exactly acc +- t[b]
             u[q] = acc;
         }
-        for (int j = 0; j < klane; ++j)
+        static_for<6>([&](auto J) {
+            if (J < klane) {
+                const float sg = lane_sign(lane, J);
 #pragma unroll
-            for (int q = 0; q < CB; ++q)
-                u[q] = bfly_lane(u[q], lane, 1 << j);
+                for (int q = 0; q < CB; ++q)
+                    u[q] = bfly_lane<J>(u[q], sg);
+            }
+        });
         if (act)
 #pragma unroll
             for (int q = 0; q < CB; ++q)
@@ -507,9 +535,7 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
                 const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
                 amax = fmaxf(amax, fabsf(rowbuf[gi * LD + b] * c));
             }
-#pragma unroll
-        for (int j = 0; j < 6; ++j)
-            amax = fmaxf(amax, __shfl_xor(amax, 1 << j));
+        static_for<6>([&](auto J) { amax = lane_max<J>(amax); });
         if (lane == 0)
             red[tid >> 6] = amax;
         __syncthreads();
@@ -519,14 +545,14 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
             amax = fmaxf(amax, red[i]);
         const float s32 = (amax * a.clip) / 7.0f;
         const uint16_t s16 = f2h(s32);
-        const float sf = h2f(s16);
+        const Divisor dv = make_divisor(h2f(s16));
         uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (n / 2);
         for (int ch = tid; ch < chunks; ch += 64 * W) {
             uint32_t pk = 0;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
-                pk |= sym_code(rowbuf[gi * LD + b] * c, sf) << (4 * e);
+                pk |= sym_code(rowbuf[gi * LD + b] * c, dv) << (4 * e);
             }
             *reinterpret_cast<uint32_t *>(qr + ch * 4) = pk;
         }
@@ -552,16 +578,14 @@ __global__ __launch_bounds__(256) void k_quant_plain(RotArgs a)
         for (int e = 0; e < 8; ++e)
             amax = fmaxf(amax, fabsf(v[e]));
     }
-#pragma unroll
-    for (int j = 0; j < 6; ++j)
-        amax = fmaxf(amax, __shfl_xor(amax, 1 << j));
+    static_for<6>([&](auto J) { amax = lane_max<J>(amax); });
     if (lane == 0)
         red[tid >> 6] = amax;
     __syncthreads();
     amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
     const float s32 = (amax * a.clip) / 7.0f;
     const uint16_t s16 = f2h(s32);
-    const float sf = h2f(s16);
+    const Divisor dv = make_divisor(h2f(s16));
     uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (n / 2);
     for (int ch = tid; ch < chunks; ch += 256) {
         float v[8];
@@ -569,7 +593,7 @@ __global__ __launch_bounds__(256) void k_quant_plain(RotArgs a)
         uint32_t pk = 0;
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-            pk |= sym_code(v[e], sf) << (4 * e);
+            pk |= sym_code(v[e], dv) << (4 * e);
         *reinterpret_cast<uint32_t *>(qr + ch * 4) = pk;
     }
     if (tid == 0)
@@ -607,11 +631,12 @@ __global__ __launch_bounds__(256) void k_kv_dequant(KvDeqArgs a)
                     v[e] = p + q;
                     v[e + h] = p - q;
                 }
-#pragma unroll
-        for (int j = 0; j < LOGL; ++j)
+        static_for<LOGL>([&](auto J) {
+            const float sg = lane_sign(lane, J);
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                v[e] = bfly_lane(v[e], ll, 1 << j);
+                v[e] = bfly_lane<J>(v[e], sg);
+        });
 #pragma unroll
         for (int e = 0; e < 8; ++e)
             v[e] = v[e] * a.c;
