@@ -50,6 +50,9 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=64,
                     help="rows per layer of the oracle's CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after timing, copy a buffer of this many MiB once (a plain copy "
+                         "kernel of known size, to scale hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU; multi-GPU runs are not "
@@ -135,6 +138,15 @@ def main():
             "gemm_TOPS": round(ops[li] / (gemm_ms[li] * 1e-3) / 1e12, 1),
             "linear_TOPS": round(ops[li] / ((gemm_ms[li] + rot_ms[li]) * 1e-3) / 1e12, 1),
         }
+
+    if args.copy_mib:
+        src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

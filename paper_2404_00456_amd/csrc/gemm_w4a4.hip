@@ -248,6 +248,12 @@ __device__ __forceinline__ void dma16(const void *g, uint32_t lds_base)
                  : "memory");
 }
 
+// Persistent: each block walks a range of tiles.  Block b sits on XCD b % 8
+// (the dispatcher deals blocks round-robin), so the 8 XCDs own contiguous
+// eighths of the tile order and the blocks of one XCD take consecutive
+// tiles, as the one-tile-per-block kernel above does.  The ring keeps
+// running across tiles: the last three k-steps of a tile issue the DMAs of
+// the next tile's first three, which land during the epilogue.
 __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
 {
     extern __shared__ __align__(16) uint8_t lds[];
@@ -255,156 +261,224 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
     const int wm = wave >> 2, wn = wave & 3;
     const int M = a.M, N = a.N, K = a.K;
     const int TM = (M + BM - 1) / BM, TN = (N + BN - 1) / BN;
-    int tm, tn;
-    tile_of(blockIdx.x, gridDim.x, TM, TN, tm, tn);
-    const int m0 = tm * BM, n0 = tn * BN;
+    const int T = TM * TN;
+    const int G = gridDim.x, b = blockIdx.x;
     const int64_t ldk = K / 2;
     const int KT = K / 128;
 
+    // this block's tiles: logical positions b, b + G, ... within a
+    // per-XCD ordering when the grid and the tile count allow it
+    const bool xcd = (G % 8 == 0) && (T % 8 == 0) && G <= T;
+    auto tile_pos = [&](int it) -> int {  // it-th tile of this block, or -1
+        if (xcd) {
+            const int per_x = T / 8, gx = G / 8;
+            const int r = (b >> 3) + it * gx;
+            return r < per_x ? (b & 7) * per_x + r : -1;
+        }
+        const int t = b + it * G;
+        return t < T ? t : -1;
+    };
+    auto tile_mn = [&](int t, int &m0, int &n0) {
+        const int gsize = GM * TN;
+        const int g = t / gsize;
+        const int first = g * GM;
+        const int gm = min(TM - first, GM);
+        const int r = t - g * gsize;
+        m0 = (first + r % gm) * BM;
+        n0 = (r / gm) * BN;
+    };
+
     // DMA sources: instruction i of wave w moves 16 rows of X (i < 2) or W
     // (i >= 2): rows 16*(w + 8*(i&1)) + lane/4 land at unit lane%4 of their
-    // LDS row, so they must fetch global unit (lane%4) ^ swizzle(row)
-    const uint8_t *src[4];
+    // LDS row, so they fetch global unit (lane%4) ^ swizzle(row)
+    const int rsub = lane >> 2;
+    const int cunit = (lane & 3) ^ ((lane >> 3) & 3);
     int dst[4];
-    {
-        const int rsub = lane >> 2;
-        const int c = (lane & 3) ^ ((lane >> 3) & 3);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        dst[i] = (i < 2 ? 0 : BM * BKB) + (wave + 8 * (i & 1)) * 1024;
+    auto sources = [&](int m0, int n0, const uint8_t *(&src)[4]) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int q = wave + 8 * (i & 1);
-            const int r = 16 * q + rsub;
-            if (i < 2) {
-                src[i] = a.xq + (int64_t)min(m0 + r, M - 1) * ldk + c * 16;
-                dst[i] = q * 1024;
-            } else {
-                src[i] = a.wq + (int64_t)min(n0 + r, N - 1) * ldk + c * 16;
-                dst[i] = BM * BKB + q * 1024;
-            }
+            const int r = 16 * (wave + 8 * (i & 1)) + rsub;
+            src[i] = (i < 2) ? a.xq + (int64_t)min(m0 + r, M - 1) * ldk + cunit * 16
+                             : a.wq + (int64_t)min(n0 + r, N - 1) * ldk + cunit * 16;
         }
-    }
+    };
     const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void *)lds;
-    auto issue = [&](int kt, int stage) {
+    auto issue = [&](const uint8_t *const (&src)[4], int kt, int stage) {
         const uint32_t sbase = lds_base + stage * RING_STAGE;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
             dma16(src[i] + (int64_t)kt * BKB, __builtin_amdgcn_readfirstlane(sbase + dst[i]));
     };
 
-    v4i acc[NI][8];
-#pragma unroll
-    for (int i = 0; i < NI; ++i)
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-            acc[i][j] = v4i{0, 0, 0, 0};
-
-    // operand reads: row (lane & 15) of a 16-row slice, unit lane >> 4 of it
     const int orow = lane & 15;
     const int ounit = ((lane >> 4) ^ ((orow >> 1) & 3)) << 4;
     const int brow = (wm * 128 + orow) * BKB + ounit;        // X slice rows (B operand)
     const int arow = (BM + wn * WN + orow) * BKB + ounit;    // W slice rows (A operand)
-    auto read_step = [&](uint4 (&ops)[8 + NI], int stage) {
-        const uint8_t *sb = lds + stage * RING_STAGE;
+
+    int t = tile_pos(0);
+    if (t < 0)
+        return;
+    int m0, n0;
+    tile_mn(t, m0, n0);
+    const uint8_t *src[4];
+    sources(m0, n0, src);
+    // ring position: global step g of this block lives in stage g % S
+    int g = 0;
+    issue(src, 0, 0);
+    issue(src, min(1, KT - 1), 1);
+    issue(src, min(2, KT - 1), 2);
+
+    for (int it = 0; t >= 0; ++it) {
+        const int tn_ = tile_pos(it + 1);
+        int m1 = 0, n1 = 0;
+        const uint8_t *nsrc[4];
+        if (tn_ >= 0) {
+            tile_mn(tn_, m1, n1);
+            sources(m1, n1, nsrc);
+        } else {
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-            ops[j] = *reinterpret_cast<const uint4 *>(sb + brow + j * 16 * BKB);
+            for (int i = 0; i < 4; ++i)
+                nsrc[i] = src[i];
+        }
+
+        v4i acc[NI][8];
 #pragma unroll
         for (int i = 0; i < NI; ++i)
-            ops[8 + i] = *reinterpret_cast<const uint4 *>(sb + arow + i * 16 * BKB);
-    };
-    // one MFMA substep: the A operands (W rows) widened up front, each B
-    // operand (X rows) widened just before its NI MFMAs
-    auto substep = [&](const uint4 (&ops)[8 + NI], int h) {
-        v4i aq[NI];
 #pragma unroll
-        for (int i = 0; i < NI; ++i)
-            aq[i] = widen(h ? make_uint2(ops[8 + i].z, ops[8 + i].w)
-                            : make_uint2(ops[8 + i].x, ops[8 + i].y));
+            for (int j = 0; j < 8; ++j)
+                acc[i][j] = v4i{0, 0, 0, 0};
+
+        auto read_step = [&](uint4 (&ops)[8 + NI], int stage) {
+            const uint8_t *sb = lds + stage * RING_STAGE;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const v4i bq = widen(h ? make_uint2(ops[j].z, ops[j].w) : make_uint2(ops[j].x, ops[j].y));
+            for (int j = 0; j < 8; ++j)
+                ops[j] = *reinterpret_cast<const uint4 *>(sb + brow + j * 16 * BKB);
 #pragma unroll
             for (int i = 0; i < NI; ++i)
-                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aq[i], bq, acc[i][j], 0, 0, 0);
+                ops[8 + i] = *reinterpret_cast<const uint4 *>(sb + arow + i * 16 * BKB);
+        };
+        auto substep = [&](const uint4 (&ops)[8 + NI], int h) {
+            v4i aq[NI];
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+                aq[i] = widen(h ? make_uint2(ops[8 + i].z, ops[8 + i].w)
+                                : make_uint2(ops[8 + i].x, ops[8 + i].y));
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const v4i bq =
+                    widen(h ? make_uint2(ops[j].z, ops[j].w) : make_uint2(ops[j].x, ops[j].y));
+#pragma unroll
+                for (int i = 0; i < NI; ++i)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aq[i], bq, acc[i][j], 0, 0, 0);
+            }
+        };
+
+        // Step 0 of this tile (global step g) must have landed for every
+        // wave.  For the first tile: wait for it (two steps, 8 DMAs, stay in
+        // flight) and synchronize.  For later tiles it was already waited
+        // for, by every wave, before the last barrier of the previous tile
+        // (and a wait here would also wait for the epilogue's stores, which
+        // count in vmcnt).
+        if (it == 0) {
+            __asm__ volatile("" ::: "memory");
+            __builtin_amdgcn_s_waitcnt(0xF78);  // vmcnt(8)
+            __builtin_amdgcn_s_barrier();
+            __asm__ volatile("" ::: "memory");
         }
-    };
+        uint4 R[8 + NI], Rn[8 + NI];
+        read_step(R, g % S);
+        for (int kt = 0; kt < KT; ++kt, ++g) {
+            substep(R, 0);
+            // The s_waitcnt and s_barrier builtins do not order memory
+            // accesses for the compiler; the empty asm statements do: every
+            // LDS read of stage g is issued before the wait (and completes
+            // by it), and no read of stage g+1 moves above the barrier.
+            __asm__ volatile("" ::: "memory");
+            __builtin_amdgcn_s_waitcnt(0x074);  // vmcnt(4) expcnt(7) lgkmcnt(0)
+            __builtin_amdgcn_s_barrier();
+            __asm__ volatile("" ::: "memory");
+            // DMA of global step g+3: this tile's step kt+3, else the next
+            // tile's step kt+3-KT, else (no next tile) a harmless re-fetch.
+            // Selected without a branch, which would split the scheduling
+            // region of the loop body.
+            {
+                const bool here = kt + 3 < KT;
+                const int sk = here ? kt + 3 : (tn_ >= 0 ? min(kt + 3 - KT, KT - 1) : KT - 1);
+                const uint32_t sbase = lds_base + (g % S) * RING_STAGE;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    dma16((here ? src[i] : nsrc[i]) + (int64_t)sk * BKB,
+                          __builtin_amdgcn_readfirstlane(sbase + dst[i]));
+            }
+            read_step(Rn, (g + 1) % S);
+            substep(R, 1);
+#pragma unroll
+            for (int o = 0; o < 8 + NI; ++o)
+                R[o] = Rn[o];
+        }
+        // the extra read after the last step touched stage g % S (the next
+        // tile's step 0, landed) and is discarded
 
-    // Iteration kt: substep 0 of step kt; wait for my DMA of step kt+1 and
-    // my LDS reads, barrier (now every DMA of kt+1 has landed and nobody
-    // reads stage kt any more); DMA of step kt+3 into stage kt; read step
-    // kt+1 while substep 1 of step kt runs.  DMAs are issued
-    // unconditionally (past the last step they re-fetch step KT-1 into a
-    // stage never read again) so that exactly two steps are in flight at
-    // every wait; the read after the last step touches a landed, unused
-    // stage.
-    issue(0, 0);
-    issue(min(1, KT - 1), 1);
-    issue(min(2, KT - 1), 2);
-    __builtin_amdgcn_s_waitcnt(0xF78);  // vmcnt(8): step 0 landed
-    __builtin_amdgcn_s_barrier();
-    // (rolled: unrolled by two, so that R and Rn alternate instead of being
-    // copied, the kernel no longer fits 256 VGPRs)
-    uint4 R[8 + NI], Rn[8 + NI];
-    read_step(R, 0);
-    for (int kt = 0; kt < KT; ++kt) {
-        substep(R, 0);
-        __builtin_amdgcn_s_waitcnt(0x074);  // vmcnt(4) expcnt(7) lgkmcnt(0)
-        __builtin_amdgcn_s_barrier();
-        issue(min(kt + 3, KT - 1), kt % S);
-        read_step(Rn, (kt + 1) % S);
-        substep(R, 1);
-#pragma unroll
-        for (int o = 0; o < 8 + NI; ++o)
-            R[o] = Rn[o];
-    }
-    __builtin_amdgcn_s_waitcnt(0xF70);  // no DMA may outlive the block's LDS
-
-    float sxf[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int m = m0 + wm * 128 + j * 16 + orow;
-        sxf[j] = h2f(a.sx[min(m, M - 1)]);
-    }
-    const bool vec = (N & 3) == 0;
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-        const int nb = n0 + wn * WN + i * 16 + (lane >> 4) * 4;
-        float swf[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            swf[r] = h2f(a.sw[min(nb + r, N - 1)]);
+        float sxf[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int m = m0 + wm * 128 + j * 16 + orow;
-            if (m >= M)
-                continue;
-            int iv[4];
-            uint16_t hv[4];
+            sxf[j] = h2f(a.sx[min(m, M - 1)]);
+        }
+        const bool vec = (N & 3) == 0;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                iv[r] = acc[i][j][r] >> 8;
-                const float t = (float)iv[r] * sxf[j];
-                hv[r] = f2h(t * swf[r]);
-            }
-            uint16_t *yrow = a.y + (int64_t)m * N;
-            int32_t *arw = a.acc ? a.acc + (int64_t)m * N : nullptr;
-            if (vec && nb + 3 < N) {
-                uint2 pk;
-                pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
-                pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
-                *reinterpret_cast<uint2 *>(yrow + nb) = pk;
-                if (arw)
-                    *reinterpret_cast<int4 *>(arw + nb) = make_int4(iv[0], iv[1], iv[2], iv[3]);
-            } else {
+        for (int i = 0; i < NI; ++i) {
+            const int nb = n0 + wn * WN + i * 16 + (lane >> 4) * 4;
+            float swf[4];
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    if (nb + r < N) {
-                        yrow[nb + r] = hv[r];
-                        if (arw)
-                            arw[nb + r] = iv[r];
-                    }
+            for (int r = 0; r < 4; ++r)
+                swf[r] = h2f(a.sw[min(nb + r, N - 1)]);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int m = m0 + wm * 128 + j * 16 + orow;
+                if (m >= M)
+                    continue;
+                int iv[4];
+                uint16_t hv[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    iv[r] = acc[i][j][r] >> 8;
+                    const float tt = (float)iv[r] * sxf[j];
+                    hv[r] = f2h(tt * swf[r]);
+                }
+                uint16_t *yrow = a.y + (int64_t)m * N;
+                int32_t *arw = a.acc ? a.acc + (int64_t)m * N : nullptr;
+                if (vec && nb + 3 < N) {
+                    uint2 pk;
+                    pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
+                    pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
+                    *reinterpret_cast<uint2 *>(yrow + nb) = pk;
+                    if (arw)
+                        *reinterpret_cast<int4 *>(arw + nb) = make_int4(iv[0], iv[1], iv[2], iv[3]);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (nb + r < N) {
+                            yrow[nb + r] = hv[r];
+                            if (arw)
+                                arw[nb + r] = iv[r];
+                        }
+                }
             }
         }
+
+        t = tn_;
+        m0 = m1;
+        n0 = n1;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            src[i] = nsrc[i];
     }
+    __asm__ volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xF70);  // no DMA may outlive the block's LDS
 }
 
 }  // namespace
@@ -422,8 +496,18 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s)
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
     if (e != hipSuccess)
         return e;
-    if (main)
-        hipLaunchKernelGGL(k_gemm_w4a4, dim3((unsigned)(TM * TN)), dim3(THREADS), lds_bytes, s, a);
+    if (main) {
+        // persistent: one block per CU (256 on MI355X), or fewer for small
+        // problems; the LDS ring allows one resident block per CU
+        int dev = 0, cus = 256;
+        if (hipGetDevice(&dev) == hipSuccess)
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        const int tiles = TM * TN;
+        int grid = tiles < cus ? tiles : cus;
+        if (grid >= 8 && tiles % 8 == 0)
+            grid -= grid % 8;
+        hipLaunchKernelGGL(k_gemm_w4a4, dim3((unsigned)grid), dim3(THREADS), lds_bytes, s, a);
+    }
     else
         hipLaunchKernelGGL(k_gemm_w4a4_k64, dim3((unsigned)(TM * TN)), dim3(THREADS), lds_bytes, s,
                            a);
