@@ -231,6 +231,7 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_k64(GemmArgs a)
 constexpr int S = 3;                         // LDS ring stages
 constexpr int RING_STAGE = (BM + BN) * BKB;  // 32 KB: X rows then W rows
 constexpr int RING_BYTES = S * RING_STAGE;
+constexpr int DPW = RING_STAGE / 1024 / (THREADS / 64);  // DMAs per wave per k-step
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -239,21 +240,31 @@ typedef __attribute__((address_space(3))) void lds_void;
 // own LDS-DMA builtin the waitcnt pass cannot tell the DMA target from the
 // stage being read and waits for every DMA before each LDS read, which
 // serializes the ring.  Here only the explicit s_waitcnt below orders it.
-// The kernel uses M0 for nothing else (checked in its ISA).
+// The kernel uses M0 for nothing else (checked in its ISA); the s_nop is
+// the wait state the ISA asks for between an SALU write of M0 and a VMEM
+// instruction with LDS destination.
 __device__ __forceinline__ void dma16(const void *g, uint32_t lds_base)
 {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                  :
                  : "v"(g), "s"(lds_base)
                  : "memory");
+}
+
+// s_waitcnt immediate: vmcnt(vm) expcnt(7) lgkmcnt(lgkm) in the gfx9 layout
+constexpr int waitcnt_imm(int vm, int lgkm)
+{
+    return (vm & 15) | (((vm >> 4) & 3) << 14) | (7 << 4) | ((lgkm & 15) << 8);
 }
 
 // Persistent: each block walks a range of tiles.  Block b sits on XCD b % 8
 // (the dispatcher deals blocks round-robin), so the 8 XCDs own contiguous
 // eighths of the tile order and the blocks of one XCD take consecutive
 // tiles, as the one-tile-per-block kernel above does.  The ring keeps
-// running across tiles: the last three k-steps of a tile issue the DMAs of
-// the next tile's first three, which land during the epilogue.
+// running across tiles: the last S k-steps of a tile issue the DMAs of the
+// next tile's first S, which land during the epilogue.  That needs at least
+// S k-steps per tile; the launcher gives every block a single tile
+// otherwise.
 __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
 {
     extern __shared__ __align__(16) uint8_t lds[];
@@ -293,23 +304,24 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
     // LDS row, so they fetch global unit (lane%4) ^ swizzle(row)
     const int rsub = lane >> 2;
     const int cunit = (lane & 3) ^ ((lane >> 3) & 3);
-    int dst[4];
+    static_assert(DPW == 4, "two X and two W chunks per wave");
+    int dst[DPW];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < DPW; ++i)
         dst[i] = (i < 2 ? 0 : BM * BKB) + (wave + 8 * (i & 1)) * 1024;
-    auto sources = [&](int m0, int n0, const uint8_t *(&src)[4]) {
+    auto sources = [&](int m0, int n0, const uint8_t *(&src)[DPW]) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < DPW; ++i) {
             const int r = 16 * (wave + 8 * (i & 1)) + rsub;
             src[i] = (i < 2) ? a.xq + (int64_t)min(m0 + r, M - 1) * ldk + cunit * 16
                              : a.wq + (int64_t)min(n0 + r, N - 1) * ldk + cunit * 16;
         }
     };
     const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void *)lds;
-    auto issue = [&](const uint8_t *const (&src)[4], int kt, int stage) {
+    auto issue = [&](const uint8_t *const (&src)[DPW], int kt, int stage) {
         const uint32_t sbase = lds_base + stage * RING_STAGE;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < DPW; ++i)
             dma16(src[i] + (int64_t)kt * BKB, __builtin_amdgcn_readfirstlane(sbase + dst[i]));
     };
 
@@ -323,24 +335,24 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
         return;
     int m0, n0;
     tile_mn(t, m0, n0);
-    const uint8_t *src[4];
+    const uint8_t *src[DPW];
     sources(m0, n0, src);
     // ring position: global step g of this block lives in stage g % S
     int g = 0;
-    issue(src, 0, 0);
-    issue(src, min(1, KT - 1), 1);
-    issue(src, min(2, KT - 1), 2);
+#pragma unroll
+    for (int i = 0; i < S; ++i)
+        issue(src, min(i, KT - 1), i);
 
     for (int it = 0; t >= 0; ++it) {
         const int tn_ = tile_pos(it + 1);
         int m1 = 0, n1 = 0;
-        const uint8_t *nsrc[4];
+        const uint8_t *nsrc[DPW];
         if (tn_ >= 0) {
             tile_mn(tn_, m1, n1);
             sources(m1, n1, nsrc);
         } else {
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < DPW; ++i)
                 nsrc[i] = src[i];
         }
 
@@ -377,14 +389,14 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
         };
 
         // Step 0 of this tile (global step g) must have landed for every
-        // wave.  For the first tile: wait for it (two steps, 8 DMAs, stay in
+        // wave.  For the first tile: wait for it (S - 1 steps of DMAs stay in
         // flight) and synchronize.  For later tiles it was already waited
         // for, by every wave, before the last barrier of the previous tile
         // (and a wait here would also wait for the epilogue's stores, which
         // count in vmcnt).
         if (it == 0) {
             __asm__ volatile("" ::: "memory");
-            __builtin_amdgcn_s_waitcnt(0xF78);  // vmcnt(8)
+            __builtin_amdgcn_s_waitcnt(waitcnt_imm((S - 1) * DPW, 15));
             __builtin_amdgcn_s_barrier();
             __asm__ volatile("" ::: "memory");
         }
@@ -397,19 +409,19 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
             // LDS read of stage g is issued before the wait (and completes
             // by it), and no read of stage g+1 moves above the barrier.
             __asm__ volatile("" ::: "memory");
-            __builtin_amdgcn_s_waitcnt(0x074);  // vmcnt(4) expcnt(7) lgkmcnt(0)
+            __builtin_amdgcn_s_waitcnt(waitcnt_imm((S - 2) * DPW, 0));
             __builtin_amdgcn_s_barrier();
             __asm__ volatile("" ::: "memory");
-            // DMA of global step g+3: this tile's step kt+3, else the next
-            // tile's step kt+3-KT, else (no next tile) a harmless re-fetch.
+            // DMA of global step g+S: this tile's step kt+S, else the next
+            // tile's step kt+S-KT, else (no next tile) a harmless re-fetch.
             // Selected without a branch, which would split the scheduling
             // region of the loop body.
             {
-                const bool here = kt + 3 < KT;
-                const int sk = here ? kt + 3 : (tn_ >= 0 ? min(kt + 3 - KT, KT - 1) : KT - 1);
+                const bool here = kt + S < KT;
+                const int sk = here ? kt + S : (tn_ >= 0 ? kt + S - KT : KT - 1);
                 const uint32_t sbase = lds_base + (g % S) * RING_STAGE;
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
+                for (int i = 0; i < DPW; ++i)
                     dma16((here ? src[i] : nsrc[i]) + (int64_t)sk * BKB,
                           __builtin_amdgcn_readfirstlane(sbase + dst[i]));
             }
@@ -474,11 +486,11 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
         m0 = m1;
         n0 = n1;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < DPW; ++i)
             src[i] = nsrc[i];
     }
     __asm__ volatile("" ::: "memory");
-    __builtin_amdgcn_s_waitcnt(0xF70);  // no DMA may outlive the block's LDS
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));  // no DMA may outlive the block's LDS
 }
 
 }  // namespace
@@ -498,12 +510,15 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s)
         return e;
     if (main) {
         // persistent: one block per CU (256 on MI355X), or fewer for small
-        // problems; the LDS ring allows one resident block per CU
-        int dev = 0, cus = 256;
-        if (hipGetDevice(&dev) == hipSuccess)
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        // problems; the LDS ring allows one resident block per CU.  With
+        // fewer than S k-steps, one tile per block (see the kernel).
+        int dev = 0, cus = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
         const int tiles = TM * TN;
-        int grid = tiles < cus ? tiles : cus;
+        int grid = (tiles < cus || a.K / 128 < S) ? tiles : cus;
         if (grid >= 8 && tiles % 8 == 0)
             grid -= grid % 8;
         hipLaunchKernelGGL(k_gemm_w4a4, dim3((unsigned)grid), dim3(THREADS), lds_bytes, s, a);

@@ -164,6 +164,26 @@ def test_gemm_exact(dev, orc, M, N, K):
     assert_fp16_close(H(y), orc.dequant(racc, sx, sw), f"y M={M} N={N} K={K}")
 
 
+@pytest.mark.parametrize("M,N,K", [(2048, 8448, 128), (2048, 8448, 256), (2048, 8448, 384),
+                                   (2048, 8448, 640), (2304, 8448, 512), (2200, 8400, 1024)])
+def test_gemm_many_tiles(dev, orc, M, N, K):
+    """More 256 x 256 tiles than one wave of blocks (264 and 297 tiles), so
+    that blocks walk several tiles: k-step counts below, at and above the
+    LDS ring depth, tile counts with and without a multiple of 8, ragged
+    edges."""
+    import paper_2404_00456_amd as q
+    say(f"gemm many tiles M={M} N={N} K={K}")
+    rng = np.random.default_rng(M + N + K)
+    xq = rand_codes(rng, M, K)
+    wq = rand_codes(rng, N, K)
+    sx = rng.uniform(0.01, 2.0, M).astype(np.float16)
+    sw = rng.uniform(0.0005, 0.05, N).astype(np.float16)
+    y, acc = q.quarot_w4a4_gemm(T(xq, dev), T(sx, dev), T(wq, dev), T(sw, dev), want_acc=True)
+    racc = orc.gemm_i32(xq, wq)
+    assert_same(H(acc), racc, f"acc M={M} N={N} K={K}")
+    assert_fp16_close(H(y), orc.dequant(racc, sx, sw), f"y M={M} N={N} K={K}")
+
+
 def test_gemm_extreme_codes(dev, orc):
     """All -8 codes: |acc| = 64 K, the largest magnitude (K = 65536: 2^22)."""
     import paper_2404_00456_amd as q
