@@ -29,6 +29,8 @@ namespace quarot {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef float f2 __attribute__((ext_vector_type(2)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 
 constexpr int BM = 256;   // X rows per block
 constexpr int BN = 256;   // W rows per block
@@ -232,6 +234,10 @@ constexpr int S = 3;                         // LDS ring stages
 constexpr int RING_STAGE = (BM + BN) * BKB;  // 32 KB: X rows then W rows
 constexpr int RING_BYTES = S * RING_STAGE;
 constexpr int DPW = RING_STAGE / 1024 / (THREADS / 64);  // DMAs per wave per k-step
+// Scales of a tile (256 sx then 256 sw, fp16) live in LDS after the ring,
+// double buffered by tile parity.
+constexpr int SCALE_BYTES = 2 * (BM + BN) * 2;
+constexpr int MAIN_LDS_BYTES = RING_BYTES + SCALE_BYTES;
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -246,6 +252,15 @@ typedef __attribute__((address_space(3))) void lds_void;
 __device__ __forceinline__ void dma16(const void *g, uint32_t lds_base)
 {
     asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(g), "s"(lds_base)
+                 : "memory");
+}
+
+// 4 bytes per lane into LDS at lds_base + 4 * lane (same rules as dma16).
+__device__ __forceinline__ void dma4(const void *g, uint32_t lds_base)
+{
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
                  :
                  : "v"(g), "s"(lds_base)
                  : "memory");
@@ -330,6 +345,23 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
     const int brow = (wm * 128 + orow) * BKB + ounit;        // X slice rows (B operand)
     const int arow = (BM + wn * WN + orow) * BKB + ounit;    // W slice rows (A operand)
 
+    // Tiles wholly inside the matrices (and no int32 output) take the fast
+    // epilogue, with the scales staged in LDS: one 4-byte DMA per wave
+    // (waves w and w+4 fetch the same quarter: sx rows 0-127, 128-255, sw
+    // 0-127, 128-255), issued ahead of the tile's operand DMAs so that the
+    // k-loop's waits cover it.  Scale loads in the epilogue itself would
+    // wait for the next tile's operand DMAs in flight (vmcnt is in order).
+    auto fast_tile = [&](int m0_, int n0_) {
+        return m0_ + BM <= M && n0_ + BN <= N && (N & 3) == 0 && a.acc == nullptr;
+    };
+    auto scale_dma = [&](int m0_, int n0_, int buf) {
+        const int part = wave & 3;
+        const uint16_t *gs = (part < 2 ? a.sx + m0_ + 128 * part : a.sw + n0_ + 128 * (part - 2));
+        dma4(gs + 2 * lane,
+             __builtin_amdgcn_readfirstlane(lds_base + RING_BYTES + buf * (SCALE_BYTES / 2) +
+                                            part * 256));
+    };
+
     int t = tile_pos(0);
     if (t < 0)
         return;
@@ -337,6 +369,8 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
     tile_mn(t, m0, n0);
     const uint8_t *src[DPW];
     sources(m0, n0, src);
+    if (fast_tile(m0, n0))
+        scale_dma(m0, n0, 0);
     // ring position: global step g of this block lives in stage g % S
     int g = 0;
 #pragma unroll
@@ -434,6 +468,47 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
         // the extra read after the last step touched stage g % S (the next
         // tile's step 0, landed) and is discarded
 
+        // the next tile's scales: its buffer was last read by the epilogue
+        // two tiles back, which every wave finished before this tile's
+        // barriers
+        if (tn_ >= 0 && fast_tile(m1, n1))
+            scale_dma(m1, n1, (it + 1) & 1);
+
+        if (fast_tile(m0, n0)) {
+            // y = RN16(RN(RN(f32(acc) sx) sw)).  The accumulators hold 256 acc
+            // and f32(256 acc) = 256 f32(acc), so multiplying by sx / 256
+            // (exact) gives the same RN(f32(acc) sx) without the shift.
+            const uint8_t *sc = lds + RING_BYTES + (it & 1) * (SCALE_BYTES / 2);
+            const uint16_t *lsx = reinterpret_cast<const uint16_t *>(sc);
+            const uint16_t *lsw = lsx + BM;
+            float sxs[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                sxs[j] = h2f(lsx[wm * 128 + j * 16 + orow]) * 0x1p-8f;
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                const int nl = wn * WN + i * 16 + (lane >> 4) * 4;
+                const uint2 swp = *reinterpret_cast<const uint2 *>(lsw + nl);
+                const float sw0 = h2f((uint16_t)swp.x), sw1 = h2f((uint16_t)(swp.x >> 16));
+                const float sw2 = h2f((uint16_t)swp.y), sw3 = h2f((uint16_t)(swp.y >> 16));
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    float u0 = ((float)acc[i][j][0] * sxs[j]) * sw0;
+                    float u1 = ((float)acc[i][j][1] * sxs[j]) * sw1;
+                    float u2 = ((float)acc[i][j][2] * sxs[j]) * sw2;
+                    float u3 = ((float)acc[i][j][3] * sxs[j]) * sw3;
+                    // pinned so the multiply is not fused into the conversion
+                    __asm__ volatile("" : "+v"(u0), "+v"(u1), "+v"(u2), "+v"(u3));
+                    const h2 lo = __builtin_convertvector((f2){u0, u1}, h2);
+                    const h2 hi = __builtin_convertvector((f2){u2, u3}, h2);
+                    uint2 pk;
+                    pk.x = __builtin_bit_cast(uint32_t, lo);
+                    pk.y = __builtin_bit_cast(uint32_t, hi);
+                    const int m = m0 + wm * 128 + j * 16 + orow;
+                    *reinterpret_cast<uint2 *>(a.y + (int64_t)m * N + n0 + nl) = pk;
+                }
+            }
+        } else {
         float sxf[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -481,6 +556,7 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
                 }
             }
         }
+        }
 
         t = tn_;
         m0 = m1;
@@ -502,7 +578,7 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s)
     const int TM = (a.M + BM - 1) / BM, TN = (a.N + BN - 1) / BN;
     const bool main = (a.K % 128) == 0;
     const void *fn = main ? (const void *)k_gemm_w4a4 : (const void *)k_gemm_w4a4_k64;
-    const int lds_bytes = main ? RING_BYTES : LDS_BYTES;
+    const int lds_bytes = main ? MAIN_LDS_BYTES : LDS_BYTES;
     // more than 64 KB of dynamic LDS: raise the kernel's limit (per call, so
     // that every device the caller uses gets it; the call is host-side only)
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);

@@ -158,10 +158,14 @@ def test_gemm_exact(dev, orc, M, N, K):
     wq = rand_codes(rng, N, K)
     sx = rng.uniform(0.01, 2.0, M).astype(np.float16)
     sw = rng.uniform(0.0005, 0.05, N).astype(np.float16)
-    y, acc = q.quarot_w4a4_gemm(T(xq, dev), T(sx, dev), T(wq, dev), T(sw, dev), want_acc=True)
+    args = (T(xq, dev), T(sx, dev), T(wq, dev), T(sw, dev))
+    y, acc = q.quarot_w4a4_gemm(*args, want_acc=True)
+    y_only = q.quarot_w4a4_gemm(*args)  # no int32 output: the fast epilogue on full tiles
     racc = orc.gemm_i32(xq, wq)
     assert_same(H(acc), racc, f"acc M={M} N={N} K={K}")
-    assert_fp16_close(H(y), orc.dequant(racc, sx, sw), f"y M={M} N={N} K={K}")
+    ry = orc.dequant(racc, sx, sw)
+    assert_fp16_close(H(y), ry, f"y M={M} N={N} K={K}")
+    assert_fp16_close(H(y_only), ry, f"y (no acc) M={M} N={N} K={K}")
 
 
 @pytest.mark.parametrize("M,N,K", [(2048, 8448, 128), (2048, 8448, 256), (2048, 8448, 384),
@@ -178,10 +182,37 @@ def test_gemm_many_tiles(dev, orc, M, N, K):
     wq = rand_codes(rng, N, K)
     sx = rng.uniform(0.01, 2.0, M).astype(np.float16)
     sw = rng.uniform(0.0005, 0.05, N).astype(np.float16)
-    y, acc = q.quarot_w4a4_gemm(T(xq, dev), T(sx, dev), T(wq, dev), T(sw, dev), want_acc=True)
+    args = (T(xq, dev), T(sx, dev), T(wq, dev), T(sw, dev))
+    y, acc = q.quarot_w4a4_gemm(*args, want_acc=True)
+    y_only = q.quarot_w4a4_gemm(*args)  # no int32 output: the fast epilogue on full tiles
     racc = orc.gemm_i32(xq, wq)
     assert_same(H(acc), racc, f"acc M={M} N={N} K={K}")
-    assert_fp16_close(H(y), orc.dequant(racc, sx, sw), f"y M={M} N={N} K={K}")
+    ry = orc.dequant(racc, sx, sw)
+    assert_fp16_close(H(y), ry, f"y M={M} N={N} K={K}")
+    assert_fp16_close(H(y_only), ry, f"y (no acc) M={M} N={N} K={K}")
+
+
+def test_gemm_tiny_scales(dev, orc):
+    """Scales down to fp16 subnormals, so that y spans the fp16 subnormal
+    range and underflows to zero: the conversions of both epilogues (full
+    tiles without int32 output, and the general one) against the oracle."""
+    import paper_2404_00456_amd as q
+    M, N, K = 512, 768, 2048
+    rng = np.random.default_rng(11)
+    xq = rand_codes(rng, M, K)
+    wq = rand_codes(rng, N, K)
+    sx = (2.0 ** rng.uniform(-24, -10, M)).astype(np.float16)
+    sw = (2.0 ** rng.uniform(-14, -6, N)).astype(np.float16)
+    args = (T(xq, dev), T(sx, dev), T(wq, dev), T(sw, dev))
+    y, acc = q.quarot_w4a4_gemm(*args, want_acc=True)
+    y_only = q.quarot_w4a4_gemm(*args)
+    racc = orc.gemm_i32(xq, wq)
+    ry = orc.dequant(racc, sx, sw)
+    sub = np.abs(ry.astype(np.float32)) < 2.0 ** -14
+    assert sub.mean() > 0.2 and (ry == 0).any()  # the case is exercised
+    assert_same(H(acc), racc, "tiny-scale acc")
+    assert_fp16_close(H(y), ry, "tiny-scale y")
+    assert_fp16_close(H(y_only), ry, "tiny-scale y (no acc)")
 
 
 def test_gemm_extreme_codes(dev, orc):
