@@ -485,18 +485,27 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
 #pragma unroll
             for (int j = 0; j < 8; ++j)
                 sxs[j] = h2f(lsx[wm * 128 + j * 16 + orow]) * 0x1p-8f;
+            float swf[NI][4];
 #pragma unroll
             for (int i = 0; i < NI; ++i) {
                 const int nl = wn * WN + i * 16 + (lane >> 4) * 4;
                 const uint2 swp = *reinterpret_cast<const uint2 *>(lsw + nl);
-                const float sw0 = h2f((uint16_t)swp.x), sw1 = h2f((uint16_t)(swp.x >> 16));
-                const float sw2 = h2f((uint16_t)swp.y), sw3 = h2f((uint16_t)(swp.y >> 16));
+                swf[i][0] = h2f((uint16_t)swp.x);
+                swf[i][1] = h2f((uint16_t)(swp.x >> 16));
+                swf[i][2] = h2f((uint16_t)swp.y);
+                swf[i][3] = h2f((uint16_t)(swp.y >> 16));
+            }
+            // row by row: the NI stores of one j cover 128 contiguous bytes
+            // of each of 16 rows, back to back, so L2 lines fill at once
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    float u0 = ((float)acc[i][j][0] * sxs[j]) * sw0;
-                    float u1 = ((float)acc[i][j][1] * sxs[j]) * sw1;
-                    float u2 = ((float)acc[i][j][2] * sxs[j]) * sw2;
-                    float u3 = ((float)acc[i][j][3] * sxs[j]) * sw3;
+            for (int j = 0; j < 8; ++j) {
+#pragma unroll
+                for (int i = 0; i < NI; ++i) {
+                    const int nl = wn * WN + i * 16 + (lane >> 4) * 4;
+                    float u0 = ((float)acc[i][j][0] * sxs[j]) * swf[i][0];
+                    float u1 = ((float)acc[i][j][1] * sxs[j]) * swf[i][1];
+                    float u2 = ((float)acc[i][j][2] * sxs[j]) * swf[i][2];
+                    float u3 = ((float)acc[i][j][3] * sxs[j]) * swf[i][3];
                     // pinned so the multiply is not fused into the conversion
                     __asm__ volatile("" : "+v"(u0), "+v"(u1), "+v"(u2), "+v"(u3));
                     const h2 lo = __builtin_convertvector((f2){u0, u1}, h2);
