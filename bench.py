@@ -36,6 +36,23 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+# HBM-side bytes per k_gemm_w4a4 launch on this workload, averaged over the
+# up and down launches: FETCH_SIZE x 2 + WRITE_SIZE x 1 (KiB, scaled by what
+# the counters read for a plain 1 GiB copy), from the two rocprofv3 --pmc runs
+# summarized in profiles/.  Valid only for the kernel source they were taken
+# with; after any change to it the figure is reported as null.
+GEMM_TRAFFIC = {"source_sha256_16": "40414b49ac9c251e", "bytes_per_launch": 3.452e9}
+
+
+def gemm_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("gemm_w4a4.hip", "common.hpp"):
+        with open(os.path.join(ROOT, "paper_2404_00456_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
 def rotate_bytes(M, K):
     """Algorithmic HBM bytes of rotate+quantize: read fp16 x, write packed
     int4 codes and one fp16 scale per row."""
@@ -164,6 +181,8 @@ def main():
                "sample": f"first {R} of {layers[0]['wl'].M} token rows of each layer "
                          f"(rotate+quantize+GEMM+dequant), {dt:.1f} s"}
 
+    traffic = (GEMM_TRAFFIC["bytes_per_launch"]
+               if gemm_source_hash() == GEMM_TRAFFIC["source_sha256_16"] else None)
     out = {
         "metric": "W4A4 rotated-linear TOPS + % int8-MFMA peak; Hadamard/quant GB/s "
                   "(Llama2 shapes)",
@@ -185,7 +204,7 @@ def main():
         "pct_int8_peak": round(100 * value / PEAK_I8_TOPS, 2),
         "roofline": {"bound": "mfma", "kernel": "k_gemm_w4a4",
                      "achieved": round(gemm_tops, 1), "peak": PEAK_I8_TOPS, "unit": "TOP/s",
-                     "frac": round(gemm_tops / PEAK_I8_TOPS, 4), "traffic": None},
+                     "frac": round(gemm_tops / PEAK_I8_TOPS, 4), "traffic": traffic},
         "kernels": kernels,
         "cpu_baseline": cpu,
     }
