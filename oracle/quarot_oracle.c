@@ -23,9 +23,12 @@
  *  - Evaluation order of the rotation (the paper is silent; fp32 addition is
  *    not associative, so the order is part of the definition):
  *      1. t_i = f32(x_i)
- *      2. m-factor: for each a and output column b', accumulate
- *         sum_b Hm[b][b'] * t[a*m+b] left to right, starting from
- *         Hm[0][b'] * t[a*m], each step one rounded add or subtract.
+ *      2. m-factor: for each a and output column b',
+ *         u[a*m+b'] = RN32( sum_b Hm[b][b'] * t[a*m+b] ), the sum taken
+ *         exactly and rounded once.  For fp16 inputs every partial sum is a
+ *         multiple of 2^-24 below 172 * 65504 < 2^24 in magnitude, so an
+ *         fp64 accumulation (any order) is exact; it is done here left to
+ *         right in fp64.
  *      3. FWHT over a, butterfly bit j = 0, 1, ..., k-1 in increasing order;
  *         for p with bit j clear and q = p + 2^j:
  *         (u_p, u_q) <- (RN(u_p + u_q), RN(u_p - u_q)).
@@ -317,14 +320,15 @@ static void rotate_row(const float *t, float *y, float *u, int64_t n, int k, int
                        const int8_t *Hm, float c)
 {
     int64_t A = n / m;
-    /* step 2: m-factor, u[a*m + b'] = sum_b Hm[b][b'] t[a*m + b] */
+    /* step 2: m-factor, u[a*m + b'] = RN32(sum_b Hm[b][b'] t[a*m + b]),
+     * summed in fp64 (exact for fp16-valued t) and rounded once */
     for (int64_t a = 0; a < A; a++) {
         const float *ta = t + a * m;
         for (int bp = 0; bp < m; bp++) {
-            float acc = Hm[0 * m + bp] > 0 ? ta[0] : -ta[0];
-            for (int b = 1; b < m; b++)
-                acc = Hm[b * m + bp] > 0 ? acc + ta[b] : acc - ta[b];
-            u[a * m + bp] = acc;
+            double acc = 0.0;
+            for (int b = 0; b < m; b++)
+                acc = Hm[b * m + bp] > 0 ? acc + (double)ta[b] : acc - (double)ta[b];
+            u[a * m + bp] = (float)acc;
         }
     }
     /* step 3: FWHT over a, bits low to high */

@@ -228,6 +228,46 @@ def test_rotation_exact_on_small_integers(orc, n):
     assert np.array_equal(y, ref)
 
 
+@pytest.mark.parametrize("m", [12, 20, 28, 108, 172])
+def test_mfactor_exact_sum_rounded_once(orc, m):
+    """The m-factor of H_{2^k} (x) H_m (§3.1) is defined as the exact sum
+    rounded once to binary32.  With k = 1 the output is
+    y = RN(RN(u_0 +- u_1) * c), u_j = RN32(t_j H_m) computed here with
+    Python integers (fp16 values are integer multiples of 2^-24), on rows
+    mixing magnitudes from 2^-24 to 2^15, where a left-to-right binary32
+    sum would round differently."""
+    n = 2 * m
+    assert orc.hadamard_factor(n) == (1, m)
+    rng = np.random.default_rng(m)
+    rows = 64
+    mag = 2.0 ** rng.integers(-24, 16, size=(rows, n))
+    x = (rng.uniform(1, 2, size=(rows, n)) * mag * rng.choice([-1, 1], size=(rows, n)))
+    x = x.astype(np.float16)
+    Hm = orc.hm_table(m).astype(np.int64)
+    xi = (x.astype(np.float64) * 2.0 ** 24).astype(np.int64)  # exact integers
+    assert np.array_equal(xi.astype(np.float64) * 2.0 ** -24, x.astype(np.float64))
+    u = np.empty((rows, n), np.float32)
+    seq = np.empty((rows, n), np.float32)
+    for r in range(rows):
+        for a in range(2):
+            blk = [int(v) for v in xi[r, a * m:(a + 1) * m]]
+            for bp in range(m):
+                exact = sum(int(Hm[b, bp]) * blk[b] for b in range(m))  # Python int
+                u[r, a * m + bp] = np.float32(float(exact) * 2.0 ** -24)
+                acc = np.float32(0)
+                for b in range(m):  # the left-to-right binary32 sum, for contrast
+                    acc = np.float32(acc + np.float32(Hm[b, bp]) * x[r, a * m + b].astype(np.float32))
+                seq[r, a * m + bp] = acc
+    c = orc.rotation_scale(n)
+    y = np.empty_like(u)
+    y[:, :m] = (u[:, :m] + u[:, m:]) * c
+    y[:, m:] = (u[:, :m] - u[:, m:]) * c
+    got = orc.rotate_f16(x)
+    assert np.array_equal(got.view(np.uint32), y.view(np.uint32))
+    # the inputs do discriminate: a sequential binary32 m-factor differs
+    assert (seq != u).any()
+
+
 @pytest.mark.parametrize("n,dist", [(128, "normal"), (4096, "normal"), (11008, "student_t3"),
                                     (8192, "normal"), (28672, "normal"), (344, "uniform"),
                                     (5120, "normal"), (13824, "normal")])
