@@ -32,7 +32,8 @@
  *      3. FWHT over a, butterfly bit j = 0, 1, ..., k-1 in increasing order;
  *         for p with bit j clear and q = p + 2^j:
  *         (u_p, u_q) <- (RN(u_p + u_q), RN(u_p - u_q)).
- *      4. y = RN(u * c) with c = RN32(1/sqrt(n)).
+ *      4. y = RN(u * c) with c = RN32(1/sqrt(n)); a zero y is +0 (the sign
+ *         of a zero is not part of the result: y = RN(RN(u * c) + 0)).
  *  - Symmetric int4 (§4 Stage 2b, scale = absmax / 7):
  *      s32 = RN(RN(absmax * clip) / 7), s16 = RN16(s32), and the codes use
  *      the stored s16: q = clamp(rint_even(RN(y / f32(s16))), -8, 7);
@@ -345,9 +346,10 @@ static void rotate_row(const float *t, float *y, float *u, int64_t n, int k, int
             }
         }
     }
-    /* step 4: one scale multiply */
+    /* step 4: one scale multiply; adding +0 turns a -0 into +0 and leaves
+     * every other value as it is */
     for (int64_t i = 0; i < n; i++)
-        y[i] = u[i] * c;
+        y[i] = u[i] * c + 0.0f;
 }
 
 struct rot_plan {

@@ -113,19 +113,112 @@ __device__ __forceinline__ float2 lane_pair_swap(float v)
     }
 }
 
-// One Walsh-Hadamard butterfly across lane bit J: lanes with the bit clear
-// get RN(u_lo + u_hi), lanes with it set RN(u_lo - u_hi), each exactly one
-// rounded operation as in the canonical order: fma(x, +-1, y) = RN(y +- x).
-// s is +1 on lanes with bit J clear and -1 where it is set.
-template <int J>
-__device__ __forceinline__ float bfly_lane(float v, float s)
+// Compile-time loop helper: f(std::integral_constant<int, J>) for J < N.
+template <int N, int J = 0, typename F>
+__device__ __forceinline__ void static_for(F &&f)
 {
-    if constexpr (J <= 3) {
-        return __builtin_fmaf(v, s, lane_xor_dpp<J>(v));  // v is u_lo (s=+1) or u_hi (s=-1)
-    } else {
-        const float2 p = lane_pair_swap<J>(v);
-        return __builtin_fmaf(p.y, s, p.x);
+    if constexpr (J < N) {
+        f(std::integral_constant<int, J>());
+        static_for<N, J + 1>(f);
     }
+}
+
+// ---- butterflies across lanes --------------------------------------------
+//
+// A row segment of L = 2^LOGL lanes holds positions 0..L-1 (the lane bits of
+// the element index).  Lane l holds position pos(l) = l ^ 3*b2(l) ^ 4*b3(l)
+// (b2, b3 the bits 2 and 3 of l).  With this placement the DPP patterns that
+// exist on gfx950 pair the right positions: quad_perm swaps position bits 0
+// and 1, row_half_mirror (l -> l^7) flips position bit 2 and row_mirror
+// (l -> l^15) flips position bit 3.
+__device__ __forceinline__ int lane_pos(int lane)
+{
+    return lane ^ (((lane >> 2) & 1) * 3) ^ (((lane >> 3) & 1) * 4);
+}
+
+// +1 where position bit J is clear, -1 where it is set.
+__device__ __forceinline__ float pos_sign(int pos, int J)
+{
+    return ((pos >> J) & 1) ? -1.0f : 1.0f;
+}
+
+// Butterfly across position bit J < 4 as one v_fmac_f32_dpp per register:
+// v <- partner * s + v with s = pos_sign(pos, J).  The lane with the bit
+// clear gets u_lo + u_hi; the lane with it set gets u_hi - u_lo, the
+// negative of the Walsh-Hadamard output.  Each is one rounding of an exact
+// sum, and RN(-x) = -RN(x), so the lanes carry their outputs up to a known
+// sign: after the DPP stages a lane holds sigma * u with
+// sigma = (-1)^popcount(pos & dpp_bits), and partners in later stages share
+// sigma.  The kernels fold sigma into the final scale multiply.
+//
+// The compiler does not fuse a DPP move into v_fmac, hence inline asm.  A
+// DPP read needs two wait states after a VALU write of its source, which
+// the compiler cannot see through asm: each block starts with s_nop 1, and
+// within a block every instruction reads a register that no earlier one in
+// the block writes.
+#define QUAROT_DPP_FMAC4(CTL)                                                                \
+    asm volatile("s_nop 1\n\t"                                                               \
+                 "v_fmac_f32_dpp %0, %0, %4 " CTL " row_mask:0xf bank_mask:0xf\n\t"        \
+                 "v_fmac_f32_dpp %1, %1, %4 " CTL " row_mask:0xf bank_mask:0xf\n\t"        \
+                 "v_fmac_f32_dpp %2, %2, %4 " CTL " row_mask:0xf bank_mask:0xf\n\t"        \
+                 "v_fmac_f32_dpp %3, %3, %4 " CTL " row_mask:0xf bank_mask:0xf"            \
+                 : "+v"(a), "+v"(b), "+v"(c), "+v"(d)                                        \
+                 : "v"(s))
+
+template <int J>
+__device__ __forceinline__ void dpp_fmac4(float &a, float &b, float &c, float &d, float s)
+{
+    static_assert(J >= 0 && J <= 3, "DPP butterflies cover position bits 0..3");
+    if constexpr (J == 0)
+        QUAROT_DPP_FMAC4("quad_perm:[1,0,3,2]");
+    else if constexpr (J == 1)
+        QUAROT_DPP_FMAC4("quad_perm:[2,3,0,1]");
+    else if constexpr (J == 2)
+        QUAROT_DPP_FMAC4("row_half_mirror");
+    else
+        QUAROT_DPP_FMAC4("row_mirror");
+}
+#undef QUAROT_DPP_FMAC4
+
+// One Walsh-Hadamard stage across position bit J on R registers (R a
+// multiple of 4), s = pos_sign(pos, J).  J < 4: DPP as above (flips the
+// sign of the lanes with the bit set).  J = 4, 5 (lane ^ 16 by ds_swizzle,
+// lane ^ 32 by ds_bpermute, both through the LDS crossbar, no LDS memory):
+// v <- fma(v, s, partner), which is u_lo + u_hi or u_lo - u_hi exactly
+// rounded, with no sign change.
+template <int J, int R>
+__device__ __forceinline__ void lane_stage(float *v, float s, int lane)
+{
+    static_assert(R % 4 == 0, "register count");
+    if constexpr (J <= 3) {
+#pragma unroll
+        for (int i = 0; i < R; i += 4)
+            dpp_fmac4<J>(v[i], v[i + 1], v[i + 2], v[i + 3], s);
+    } else if constexpr (J == 4) {
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const float p = __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v[i]), 0x401F));
+            v[i] = __builtin_fmaf(v[i], s, p);
+        }
+    } else {
+        static_assert(J == 5, "lane bits 0..5");
+        const int addr = (lane ^ 32) << 2;
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const float p = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(v[i])));
+            v[i] = __builtin_fmaf(v[i], s, p);
+        }
+    }
+}
+
+// All lane stages J < LOGL (in increasing J, the canonical order) on R
+// registers; returns sigma, the sign the lane's values now carry.
+template <int LOGL, int R>
+__device__ __forceinline__ float lane_stages(float *v, int lane, int pos)
+{
+    static_for<LOGL>([&](auto J) { lane_stage<J, R>(v, pos_sign(pos, J), lane); });
+    constexpr int dpp_bits = (1 << (LOGL < 4 ? LOGL : 4)) - 1;
+    return (__builtin_popcount(pos & dpp_bits) & 1) ? -1.0f : 1.0f;
 }
 
 template <int J>
@@ -150,20 +243,5 @@ __device__ __forceinline__ float lane_min(float v)
     }
 }
 
-// Compile-time loop helper: f(std::integral_constant<int, J>) for J < N.
-template <int N, int J = 0, typename F>
-__device__ __forceinline__ void static_for(F &&f)
-{
-    if constexpr (J < N) {
-        f(std::integral_constant<int, J>());
-        static_for<N, J + 1>(f);
-    }
-}
-
-// Lane signs for the butterflies: +1 where lane bit J is clear, -1 where set.
-__device__ __forceinline__ float lane_sign(int lane, int J)
-{
-    return ((lane >> J) & 1) ? -1.0f : 1.0f;
-}
 
 }  // namespace quarot

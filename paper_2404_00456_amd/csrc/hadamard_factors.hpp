@@ -134,17 +134,18 @@ struct HmTable {
     }
 };
 
-// Column-major copy: col[s][r] = H[r][s], so the M signs of one output
-// column are contiguous (scalar loads in the large-m kernel).
-template <int M>
-struct HmColumns {
-    float col[M][M];
-    constexpr HmColumns() : col()
+// Signs as doubles for the large-m kernel, which forms CB output columns
+// per pass: blk[p][r][q] = H[r][p*CB + q], so one pass reads the CB signs of
+// each input r as one contiguous scalar load.
+template <int M, int CB>
+struct HmColumnBlocks {
+    double blk[M / CB][M][CB];
+    constexpr HmColumnBlocks() : blk()
     {
         const Gs43Rows g{};
         for (int r = 0; r < M; ++r)
             for (int s = 0; s < M; ++s)
-                col[s][r] = (float)(M == 172 ? gs172_sign(g, r, s) : hm_sign(M, r, s));
+                blk[s / CB][r][s % CB] = (double)(M == 172 ? gs172_sign(g, r, s) : hm_sign(M, r, s));
     }
 };
 

@@ -2,31 +2,36 @@
 // §5 Setup), for gfx950.
 //
 // A row of width n = 2^k * m is rotated as y = x . (H_{2^k} (x) H_m) * c,
-// c = RN32(1/sqrt(n)), element index i = a*m + b (m fast), in this binary32
-// order: the m-factor sum over b left to right; the Walsh-Hadamard
-// butterflies over a, bit 0 first; one multiply by c.  Each kernel keeps
-// that order exactly, whatever lane, register or wave holds an element, so
-// the fp32 y (and every code derived from it) is reproducible bit for bit.
+// c = RN32(1/sqrt(n)), element index i = a*m + b (m fast):
+//   1. the m-factor u[a,b'] = RN32(sum_b H_m[b][b'] t[a,b]), the exact sum
+//      rounded once (exact in fp64 for fp16 inputs, in any order);
+//   2. the Walsh-Hadamard butterflies over a in binary32, bit 0 first, each
+//      output one rounded add or subtract;
+//   3. one multiply by c.
+// Every kernel keeps this arithmetic exactly, whatever lane, register or
+// wave holds an element, so the fp32 y (and every code derived from it) is
+// reproducible bit for bit.
 //
 // Kernels:
 //   k_rot_pow2    m = 1, n = 2^k <= 32768.  Each lane owns 16-byte chunks of
-//                 8 consecutive elements: i = ((cc*W + w)*L + l)*8 + e, so
+//                 8 consecutive elements: i = ((cc*W + w)*L + pos)*8 + e, so
 //                 bits 0-2 live in registers, the next log2(L) bits across
 //                 lanes, then across the W waves (LDS), then across chunks.
-//   k_rot_smallm  m = 12, 20, 28: each lane owns whole groups of m elements
-//                 (the m-factor runs in registers with compile-time signs).
-//   k_rot_largem  m = 108, 172: one group per lane, output columns of the
-//                 m-factor in a loop with signs from constant memory, the
-//                 rotated row staged in LDS.
+//   k_rot_smallm  m = 12, 20, 28: each lane owns whole groups of m elements;
+//                 the m-factor is an fp64 sum with shared partial sums.
+//   k_rot_largem  m = 108, 172: one group per lane, CB output columns of the
+//                 m-factor per pass in fp64, the rotated row staged in LDS.
 //   k_quant_plain quantization without rotation, any n multiple of 8.
 //   k_kv_dequant  4-bit KV cache back to fp16, optional inverse rotation.
+// Lane butterflies use the placement and sign bookkeeping of lane_stages().
 #include "common.hpp"
 #include "hadamard_factors.hpp"
 
 namespace quarot {
 
-__constant__ HmColumns<108> c_hm108 = HmColumns<108>();
-__constant__ HmColumns<172> c_hm172 = HmColumns<172>();
+constexpr int kLargeCB = 4;  // output columns per pass in k_rot_largem
+__constant__ HmColumnBlocks<108, kLargeCB> c_hm108 = HmColumnBlocks<108, kLargeCB>();
+__constant__ HmColumnBlocks<172, kLargeCB> c_hm172 = HmColumnBlocks<172, kLargeCB>();
 
 namespace {
 
@@ -146,7 +151,8 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
     constexpr int RPB = (W == 1) ? 4 * RPW : 1; // rows per block
     constexpr int N = 8 * L * W * C;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int ll = lane & (L - 1);
+    // position of this lane in its row segment (see lane_pos)
+    const int pos = lane_pos(lane) & (L - 1);
     int64_t row;
     int w;
     if constexpr (W == 1) {
@@ -163,7 +169,7 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
     const uint16_t *xr = a.x + row * N;
 #pragma unroll
     for (int cc = 0; cc < C; ++cc)
-        load8(xr + ((cc * W + w) * L + ll) * 8, v[cc]);
+        load8(xr + ((cc * W + w) * L + pos) * 8, v[cc]);
 
     if constexpr (ROT) {
         // element bits 0..2: inside each chunk
@@ -179,34 +185,27 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
                         v[cc][e + h] = p - q;
                     }
         // next LOGL bits: across lanes
-        static_for<LOGL>([&](auto J) {
-            const float sg = lane_sign(lane, J);
-#pragma unroll
-            for (int cc = 0; cc < C; ++cc)
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    v[cc][e] = bfly_lane<J>(v[cc][e], sg);
-        });
-        // next LOGW bits: across waves, through LDS one chunk at a time
+        const float sigma = lane_stages<LOGL, 8 * C>(&v[0][0], lane, pos);
+        // next LOGW bits: across waves, through LDS one chunk at a time; the
+        // partner wave holds the same lane position (the same sigma)
         if constexpr (W > 1) {
             __shared__ float xs[W][8][64];
 #pragma unroll
-            for (int j = 0; j < LOGW; ++j)
+            for (int j = 0; j < LOGW; ++j) {
+                const int pw = w ^ (1 << j);
+                const float sw = ((w >> j) & 1) ? -1.0f : 1.0f;
 #pragma unroll
                 for (int cc = 0; cc < C; ++cc) {
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
                         xs[w][e][lane] = v[cc][e];
                     __syncthreads();
-                    const int pw = w ^ (1 << j);
-                    const bool hi = (w >> j) & 1;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        float o = xs[pw][e][lane];
-                        v[cc][e] = hi ? (o - v[cc][e]) : (v[cc][e] + o);
-                    }
+                    for (int e = 0; e < 8; ++e)  // u_lo + u_hi, or u_lo - u_hi
+                        v[cc][e] = __builtin_fmaf(v[cc][e], sw, xs[pw][e][lane]);
                     __syncthreads();
                 }
+            }
         }
         // top bits: across the chunks of a lane
 #pragma unroll
@@ -221,18 +220,21 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
                         v[cc + h][e] = p - q;
                     }
                 }
+        // y = u * c: sigma * c is exact and RN(sigma u * sigma c) = RN(u c);
+        // the fma with +0 makes a zero +0 (the sign folding can leave -0)
+        const float sc = sigma * a.c;
 #pragma unroll
         for (int cc = 0; cc < C; ++cc)
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                v[cc][e] = v[cc][e] * a.c;
+                v[cc][e] = __builtin_fmaf(v[cc][e], sc, 0.0f);
     }
 
     if constexpr (EPI == EPI_F16) {
         uint16_t *yr = static_cast<uint16_t *>(a.out) + row * N;
 #pragma unroll
         for (int cc = 0; cc < C; ++cc)
-            store8(yr + ((cc * W + w) * L + ll) * 8, v[cc]);
+            store8(yr + ((cc * W + w) * L + pos) * 8, v[cc]);
     } else if constexpr (EPI == EPI_SYM) {
         __shared__ float red[W > 1 ? W : 1];
         float amax = 0.0f;
@@ -252,11 +254,11 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
 #pragma unroll
             for (int e = 0; e < 8; ++e)
                 pk |= sym_code(v[cc][e], dv) << (4 * e);
-            *reinterpret_cast<uint32_t *>(qr + ((cc * W + w) * L + ll) * 4) = pk;
+            *reinterpret_cast<uint32_t *>(qr + ((cc * W + w) * L + pos) * 4) = pk;
         }
-        if (ll == 0 && w == 0)
+        if (pos == 0 && w == 0)
             a.scale[row] = s16;
-    } else {  // EPI_KV: W == 1, C == 1, a group is G/8 consecutive lanes
+    } else {  // EPI_KV: W == 1, C == 1, a group is G/8 consecutive positions
         static_assert(W == 1 && C == 1, "KV rows fit one wave");
         float mx = v[0][0], mn = v[0][0];
 #pragma unroll
@@ -264,6 +266,8 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
             mx = fmaxf(mx, v[0][e]);
             mn = fminf(mn, v[0][e]);
         }
+        // the lanes of one group are an aligned block of gl lanes (lane_pos
+        // maps aligned blocks of 2, 4, 8, 16 lanes onto themselves)
         const int gl = a.group >> 3;  // lanes per group
         static_for<LOGL>([&](auto J) {
             if ((1 << J) < gl) {
@@ -281,9 +285,9 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
         for (int e = 0; e < 8; ++e)
             pk |= asym_code(v[0][e], dv, zf) << (4 * e);
         uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (N / 2);
-        *reinterpret_cast<uint32_t *>(qr + ll * 4) = pk;
-        if ((ll & (gl - 1)) == 0) {
-            const int64_t gi = row * (N / a.group) + ll / gl;
+        *reinterpret_cast<uint32_t *>(qr + pos * 4) = pk;
+        if ((pos & (gl - 1)) == 0) {
+            const int64_t gi = row * (N / a.group) + pos / gl;
             a.scale[gi] = s16;
             a.zero[gi] = z16;
         }
@@ -291,6 +295,46 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
 }
 
 // ---------------------------------------------------- m = 12, 20, 28 -----
+
+// The m-factor of one group of M fp16-valued inputs, exactly: each output
+// u[b'] = RN32(sum_b H[b][b'] t[b]).  The sum runs in fp64, where every
+// partial sum of fp16 values (multiples of 2^-24 below 2^21 in magnitude)
+// is exact, so the order is free: inputs go in blocks of four (a, b, c, d),
+// whose 8 signed sums a +- b +- c +- d cost 12 adds, and each output adds
+// one signed block sum per block (the block's signs, normalised so that a
+// enters with +, select which).  M = 28: 7 * 12 + 28 * 6 adds instead of
+// 28 * 27.
+template <int M>
+__device__ __forceinline__ void mfactor_exact(float *t)
+{
+    static_assert(M % 4 == 0, "blocks of four");
+    constexpr HmTable<M> H{};
+    constexpr int G = M / 4;
+    double acc[M];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        const double a = t[4 * g], b = t[4 * g + 1], c = t[4 * g + 2], d = t[4 * g + 3];
+        const double P[2] = {a + b, a - b}, Q[2] = {c + d, c - d};
+        const double cp[2][2] = {{P[0] + Q[0], P[0] + Q[1]}, {P[1] + Q[0], P[1] + Q[1]}};
+        const double cm[2][2] = {{P[0] - Q[0], P[0] - Q[1]}, {P[1] - Q[0], P[1] - Q[1]}};
+#pragma unroll
+        for (int bp = 0; bp < M; ++bp) {
+            // contribution h0 a + h1 b + h2 c + h3 d
+            //   = h0 ((a + h0h1 b) + h0h2 (c + h2h3 d))
+            const float h0 = H.v[4 * g][bp], h1 = H.v[4 * g + 1][bp];
+            const float h2 = H.v[4 * g + 2][bp], h3 = H.v[4 * g + 3][bp];
+            const int i1 = (h0 * h1 < 0.0f), i3 = (h2 * h3 < 0.0f);
+            const double blk = (h0 * h2 < 0.0f) ? cm[i1][i3] : cp[i1][i3];
+            if (g == 0)
+                acc[bp] = (h0 > 0.0f) ? blk : -blk;
+            else
+                acc[bp] = (h0 > 0.0f) ? acc[bp] + blk : acc[bp] - blk;
+        }
+    }
+#pragma unroll
+    for (int bp = 0; bp < M; ++bp)
+        t[bp] = (float)acc[bp];  // the one rounding
+}
 
 template <int M, int LOGL, int W, int C, int EPI>
 __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
@@ -301,9 +345,8 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
     constexpr int RPW = (W == 1) ? 64 / L : 1;
     constexpr int RPB = (W == 1) ? 4 * RPW : 1;
     constexpr int N = M * L * W * C;
-    constexpr HmTable<M> H{};
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int ll = lane & (L - 1);
+    const int pos = lane_pos(lane) & (L - 1);
     int64_t row;
     int w;
     if constexpr (W == 1) {
@@ -320,56 +363,36 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
     const uint16_t *xr = a.x + row * N;
 #pragma unroll
     for (int cc = 0; cc < C; ++cc) {
-        const int g = (cc * W + w) * L + ll;
+        const int g = (cc * W + w) * L + pos;
 #pragma unroll
         for (int p = 0; p < M / 4; ++p)
             load4(xr + g * M + 4 * p, &v[cc][4 * p]);
     }
 
-    // m-factor: u[b'] = sum_b H[b][b'] t[b], left to right
 #pragma unroll
-    for (int cc = 0; cc < C; ++cc) {
-        float t[M];
-#pragma unroll
-        for (int b = 0; b < M; ++b)
-            t[b] = v[cc][b];
-#pragma unroll
-        for (int bp = 0; bp < M; ++bp) {
-            float acc = (H.v[0][bp] > 0.0f) ? t[0] : -t[0];
-#pragma unroll
-            for (int b = 1; b < M; ++b)
-                acc = (H.v[b][bp] > 0.0f) ? (acc + t[b]) : (acc - t[b]);
-            v[cc][bp] = acc;
-        }
-    }
+    for (int cc = 0; cc < C; ++cc)
+        mfactor_exact<M>(v[cc]);
+
     // group bits 0..LOGL-1 across lanes
-    static_for<LOGL>([&](auto J) {
-        const float sg = lane_sign(lane, J);
-#pragma unroll
-        for (int cc = 0; cc < C; ++cc)
-#pragma unroll
-            for (int b = 0; b < M; ++b)
-                v[cc][b] = bfly_lane<J>(v[cc][b], sg);
-    });
+    const float sigma = lane_stages<LOGL, C * M>(&v[0][0], lane, pos);
     if constexpr (W > 1) {
         __shared__ float xs[W][M][64];
 #pragma unroll
-        for (int j = 0; j < LOGW; ++j)
+        for (int j = 0; j < LOGW; ++j) {
+            const int pw = w ^ (1 << j);
+            const float sw = ((w >> j) & 1) ? -1.0f : 1.0f;
 #pragma unroll
             for (int cc = 0; cc < C; ++cc) {
 #pragma unroll
                 for (int b = 0; b < M; ++b)
                     xs[w][b][lane] = v[cc][b];
                 __syncthreads();
-                const int pw = w ^ (1 << j);
-                const bool hi = (w >> j) & 1;
 #pragma unroll
-                for (int b = 0; b < M; ++b) {
-                    float o = xs[pw][b][lane];
-                    v[cc][b] = hi ? (o - v[cc][b]) : (v[cc][b] + o);
-                }
+                for (int b = 0; b < M; ++b)
+                    v[cc][b] = __builtin_fmaf(v[cc][b], sw, xs[pw][b][lane]);
                 __syncthreads();
             }
+        }
     }
 #pragma unroll
     for (int h = 1; h < C; h <<= 1)
@@ -383,17 +406,18 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
                     v[cc + h][b] = p - q;
                 }
             }
+    const float sc = sigma * a.c;  // as in k_rot_pow2: zeros come out +0
 #pragma unroll
     for (int cc = 0; cc < C; ++cc)
 #pragma unroll
         for (int b = 0; b < M; ++b)
-            v[cc][b] = v[cc][b] * a.c;
+            v[cc][b] = __builtin_fmaf(v[cc][b], sc, 0.0f);
 
     if constexpr (EPI == EPI_F16) {
         uint16_t *yr = static_cast<uint16_t *>(a.out) + row * N;
 #pragma unroll
         for (int cc = 0; cc < C; ++cc) {
-            const int g = (cc * W + w) * L + ll;
+            const int g = (cc * W + w) * L + pos;
 #pragma unroll
             for (int p = 0; p < M / 4; ++p)
                 store4(yr + g * M + 4 * p, &v[cc][4 * p]);
@@ -414,7 +438,7 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
         uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (N / 2);
 #pragma unroll
         for (int cc = 0; cc < C; ++cc) {
-            const int g = (cc * W + w) * L + ll;
+            const int g = (cc * W + w) * L + pos;
 #pragma unroll
             for (int p = 0; p < M / 4; ++p) {
                 uint32_t pk = sym_code(v[cc][4 * p], dv) | (sym_code(v[cc][4 * p + 1], dv) << 4) |
@@ -423,7 +447,7 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
                 *reinterpret_cast<uint16_t *>(qr + g * (M / 2) + 2 * p) = (uint16_t)pk;
             }
         }
-        if (ll == 0 && w == 0)
+        if (pos == 0 && w == 0)
             a.scale[row] = s16;
     }
 }
@@ -431,24 +455,27 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
 // ------------------------------------------------------- m = 108, 172 -----
 
 template <int M>
-__device__ __forceinline__ const float *hm_columns();
+__device__ __forceinline__ const double *hm_blocks();
 template <>
-__device__ __forceinline__ const float *hm_columns<108>()
+__device__ __forceinline__ const double *hm_blocks<108>()
 {
-    return &c_hm108.col[0][0];
+    return &c_hm108.blk[0][0][0];
 }
 template <>
-__device__ __forceinline__ const float *hm_columns<172>()
+__device__ __forceinline__ const double *hm_blocks<172>()
 {
-    return &c_hm172.col[0][0];
+    return &c_hm172.blk[0][0][0];
 }
 
-// One row per block; thread g < A = n/M owns group g.  The rotated row
-// (before the scale) is staged in LDS as A rows of M+1 floats.
+// One row per block; thread g < A = n/M owns group g (placed at lane
+// position pos, see lane_pos).  The m-factor runs CB output columns per
+// pass, each an fp64 sum of +-t (exact, see mfactor_exact) rounded once.
+// The rotated row (before the scale) is staged in LDS as A rows of M+1
+// floats, with the lanes' sign sigma removed.
 template <int M, int W, int EPI>
 __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
 {
-    constexpr int CB = 4;  // output columns per pass
+    constexpr int CB = kLargeCB;
     static_assert(M % CB == 0 && M % 4 == 0, "column blocking");
     constexpr int LD = M + 1;
     extern __shared__ float rowbuf[];
@@ -457,12 +484,14 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
     const int n = a.n, A = n / M;
     const int k = 31 - __clz(A);
     const int64_t row = blockIdx.x;
-    const bool act = tid < A;
-    const float *hc = hm_columns<M>();
+    const int pos = lane_pos(lane);
+    const int g = (tid & ~63) | pos;  // this thread's group
+    const bool act = g < A;
+    const double *hb = hm_blocks<M>();
 
     float t[M];
     if (act) {
-        const uint16_t *xg = a.x + row * n + (int64_t)tid * M;
+        const uint16_t *xg = a.x + row * n + (int64_t)g * M;
 #pragma unroll
         for (int p = 0; p < M / 4; ++p)
             load4(xg + 4 * p, &t[4 * p]);
@@ -472,32 +501,42 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
             t[b] = 0.0f;
     }
     const int klane = k < 6 ? k : 6;
-    // rolled: one pass is 4 * M fused multiply-adds; unrolling all M/CB
-    // passes would not fit the instruction cache
+    // rolled: one pass is CB * M fma; unrolling all M/CB passes would not
+    // fit the instruction cache
 #pragma unroll 1
-    for (int cb = 0; cb < M; cb += CB) {
+    for (int cb = 0; cb < M / CB; ++cb) {
+        const double *sg = hb + cb * M * CB;  // signs [b][q] of columns cb*CB + q
+        double acc[CB];
+#pragma unroll
+        for (int q = 0; q < CB; ++q)
+            acc[q] = 0.0;
+#pragma unroll
+        for (int b = 0; b < M; ++b) {
+            const double tb = t[b];
+#pragma unroll
+            for (int q = 0; q < CB; ++q)
+                acc[q] = __builtin_fma(sg[b * CB + q], tb, acc[q]);  // exactly acc +- t[b]
+        }
         float u[CB];
 #pragma unroll
-        for (int q = 0; q < CB; ++q) {
-            const float *sg = hc + (cb + q) * M;  // signs of column cb+q
-            float acc = sg[0] * t[0];
-#pragma unroll
-            for (int b = 1; b < M; ++b)
-                acc = __builtin_fmaf(sg[b], t[b], acc);  // exactly acc +- t[b]
-            u[q] = acc;
+        for (int q = 0; q < CB; ++q)
+            u[q] = (float)acc[q];
+        // group bits below min(k, 6) across lanes; the count is uniform, so
+        // every lane of the wave takes the same branches
+        float sigma = 1.0f;
+        switch (klane) {
+        case 1: sigma = lane_stages<1, CB>(u, lane, pos & 1); break;
+        case 2: sigma = lane_stages<2, CB>(u, lane, pos & 3); break;
+        case 3: sigma = lane_stages<3, CB>(u, lane, pos & 7); break;
+        case 4: sigma = lane_stages<4, CB>(u, lane, pos & 15); break;
+        case 5: sigma = lane_stages<5, CB>(u, lane, pos & 31); break;
+        case 6: sigma = lane_stages<6, CB>(u, lane, pos); break;
+        default: break;
         }
-        static_for<6>([&](auto J) {
-            if (J < klane) {
-                const float sg = lane_sign(lane, J);
-#pragma unroll
-                for (int q = 0; q < CB; ++q)
-                    u[q] = bfly_lane<J>(u[q], sg);
-            }
-        });
         if (act)
 #pragma unroll
             for (int q = 0; q < CB; ++q)
-                rowbuf[tid * LD + cb + q] = u[q];
+                rowbuf[g * LD + cb * CB + q] = u[q] * sigma;
     }
     __syncthreads();
     // group bits 6.. (across waves): butterflies on the staged row
@@ -522,7 +561,7 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
-                y[e] = rowbuf[gi * LD + b] * c;
+                y[e] = __builtin_fmaf(rowbuf[gi * LD + b], c, 0.0f);  // zeros +0
             }
             store8(yr + ch * 8, y);
         }
@@ -533,7 +572,7 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
-                amax = fmaxf(amax, fabsf(rowbuf[gi * LD + b] * c));
+                amax = fmaxf(amax, fabsf(rowbuf[gi * LD + b] * c));  // |y|: sign of 0 moot
             }
         static_for<6>([&](auto J) { amax = lane_max<J>(amax); });
         if (lane == 0)
@@ -608,12 +647,12 @@ __global__ __launch_bounds__(256) void k_kv_dequant(KvDeqArgs a)
     constexpr int L = 1 << LOGL;
     constexpr int RPW = 64 / L, RPB = 4 * RPW, N = 8 * L;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int ll = lane & (L - 1);
+    const int pos = lane_pos(lane) & (L - 1);
     const int64_t row = (int64_t)blockIdx.x * RPB + wave * RPW + (lane >> LOGL);
     if (row >= a.rows)
         return;
-    const uint32_t pk = *reinterpret_cast<const uint32_t *>(a.q + row * (N / 2) + ll * 4);
-    const int64_t gi = row * (N / a.group) + (ll * 8) / a.group;
+    const uint32_t pk = *reinterpret_cast<const uint32_t *>(a.q + row * (N / 2) + pos * 4);
+    const int64_t gi = row * (N / a.group) + (pos * 8) / a.group;
     const float sf = h2f(a.scale[gi]), zf = h2f(a.zero[gi]);
     float v[8];
 #pragma unroll
@@ -631,17 +670,12 @@ __global__ __launch_bounds__(256) void k_kv_dequant(KvDeqArgs a)
                     v[e] = p + q;
                     v[e + h] = p - q;
                 }
-        static_for<LOGL>([&](auto J) {
-            const float sg = lane_sign(lane, J);
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-                v[e] = bfly_lane<J>(v[e], sg);
-        });
+        const float sc = lane_stages<LOGL, 8>(v, lane, pos) * a.c;
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-            v[e] = v[e] * a.c;
+            v[e] = __builtin_fmaf(v[e], sc, 0.0f);  // zeros +0, as in k_rot_pow2
     }
-    store8(a.out + row * N + ll * 8, v);
+    store8(a.out + row * N + pos * 8, v);
 }
 
 // ---------------------------------------------------------- dispatch -----

@@ -268,6 +268,24 @@ def test_mfactor_exact_sum_rounded_once(orc, m):
     assert (seq != u).any()
 
 
+@pytest.mark.parametrize("n", [128, 56, 344, 4096])
+def test_rotation_zero_outputs_are_positive(orc, n):
+    """A zero rotation output is +0, whatever the signs of the zeros that
+    produced it; every nonzero output is untouched (checked against the
+    dense fp64 product, in which these small-integer cases are exact)."""
+    rows = np.zeros((4, n), np.float16)
+    rows[0] = -0.0                     # all negative zeros
+    rows[1] = 0.25                     # constant: one nonzero output per Kronecker block
+    rows[2, ::2] = -0.0
+    rows[3, : n // 2] = 3.0
+    rows[3, n // 2:] = -3.0
+    y = orc.rotate_f16(rows)
+    assert not np.signbit(y[y == 0]).any()
+    ref = times_h(orc, rows.astype(np.float64)) * np.float64(orc.rotation_scale(n))
+    assert np.array_equal(y != 0, ref != 0)
+    assert (y == 0).sum() > n  # the cases do produce zeros
+
+
 @pytest.mark.parametrize("n,dist", [(128, "normal"), (4096, "normal"), (11008, "student_t3"),
                                     (8192, "normal"), (28672, "normal"), (344, "uniform"),
                                     (5120, "normal"), (13824, "normal")])
