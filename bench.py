@@ -13,6 +13,13 @@ with fused dequant (quarot_w4a4_gemm).  HIP events on the launch stream
 bracket every kernel, so the per-kernel averages over the timed steps give
 the roofline figures.  value = 2*M*N*K summed over both layers / step time.
 
+The same run then times the 4-bit KV cache path on its own workload (K and V
+fp16 [batch 16, 64 heads, 4096 tokens, head_dim 128], 1 GiB each):
+rotate + asymmetric int4 quantization per head row (quarot_kv_quant) and the
+dequantization back to fp16 (quarot_kv_dequant), reported as HBM GB/s
+against 8 TB/s under "kv" (HBM-bound kernels; each tensor is 4x the 256 MB
+last-level cache, so the traffic is HBM traffic).
+
 Prints one JSON line.
 """
 from __future__ import annotations
@@ -59,14 +66,77 @@ def rotate_bytes(M, K):
     return M * K * 2 + M * K // 2 + M * 2
 
 
+def kv_bytes(rows, D, group):
+    """Algorithmic HBM bytes of one KV tensor: fp16 values, packed uint4
+    codes, fp16 scale and zero per group (read one side, write the other)."""
+    return rows * D * 2 + rows * D // 2 + rows * (D // group) * 4
+
+
+def bench_kv(q, workloads, torch, np, dev, stream, iters):
+    wl = workloads.KV["kv4_70b"]
+    log(f"generating {wl.name}: K, V [{wl.B}, {wl.H}, {wl.S}, {wl.D}]")
+    k, v = workloads.kv_inputs(wl)
+    rows = wl.rows
+    tens = []
+    for t in (k, v):
+        xd = torch.from_numpy(t.reshape(rows, wl.D)).to(dev)
+        codes = torch.empty((rows, wl.D // 2), dtype=torch.uint8, device=dev)
+        sc = torch.empty((rows, wl.D // wl.group), dtype=torch.float16, device=dev)
+        ze = torch.empty_like(sc)
+        out = torch.empty_like(xd)
+        tens.append((xd, codes, sc, ze, out))
+    del k, v
+    torch.cuda.synchronize()
+
+    def once(ev=None):
+        for ti, (xd, codes, sc, ze, out) in enumerate(tens):
+            if ev is not None:
+                ev[3 * ti].record(stream)
+            q.quarot_kv_quant(xd, group=wl.group, rotate=True, clip_ratio=wl.clip, q=codes,
+                              scale=sc, zero=ze)
+            if ev is not None:
+                ev[3 * ti + 1].record(stream)
+            q.quarot_kv_dequant(codes, sc, ze, group=wl.group, inverse_rotate=False, out=out)
+            if ev is not None:
+                ev[3 * ti + 2].record(stream)
+
+    once()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(iters)]
+    log(f"timing kv x{iters}")
+    for it in range(iters):
+        once(evs[it])
+    torch.cuda.synchronize()
+    qt = [ev[3 * ti].elapsed_time(ev[3 * ti + 1]) for ev in evs for ti in range(2)]
+    dt = [ev[3 * ti + 1].elapsed_time(ev[3 * ti + 2]) for ev in evs for ti in range(2)]
+    nbytes = kv_bytes(rows, wl.D, wl.group)
+    q_us, d_us = float(np.mean(qt)) * 1e3, float(np.mean(dt)) * 1e3
+    q_gbs, d_gbs = nbytes / (q_us * 1e-6) / 1e9, nbytes / (d_us * 1e-6) / 1e9
+    res = {"workload": f"{wl.name}: K and V fp16 [{wl.B}, {wl.H}, {wl.S}, {wl.D}], "
+                       f"H_{wl.D} per head row, asymmetric uint4, group {wl.group}, "
+                       f"clip {wl.clip}",
+           "bytes_per_tensor": nbytes,
+           "quant_us": round(q_us, 1), "quant_GBps": round(q_gbs, 1),
+           "quant_frac_hbm": round(q_gbs / PEAK_HBM_GBS, 4),
+           "dequant_us": round(d_us, 1), "dequant_GBps": round(d_gbs, 1),
+           "dequant_frac_hbm": round(d_gbs / PEAK_HBM_GBS, 4)}
+    for t in tens:
+        del t
+    tens.clear()
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--cpu-rows", type=int, default=64,
+    ap.add_argument("--cpu-rows", type=int, default=384,
                     help="rows per layer of the oracle's CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kv", action="store_true", help="skip the KV-cache leg")
+    ap.add_argument("--kv-iters", type=int, default=5)
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB once (a plain copy "
                          "kernel of known size, to scale hardware byte counters)")
@@ -156,6 +226,8 @@ def main():
             "linear_TOPS": round(ops[li] / ((gemm_ms[li] + rot_ms[li]) * 1e-3) / 1e12, 1),
         }
 
+    kv = None if args.no_kv else bench_kv(q, workloads, torch, np, dev, stream, args.kv_iters)
+
     if args.copy_mib:
         src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -206,6 +278,7 @@ def main():
                      "achieved": round(gemm_tops, 1), "peak": PEAK_I8_TOPS, "unit": "TOP/s",
                      "frac": round(gemm_tops / PEAK_I8_TOPS, 4), "traffic": traffic},
         "kernels": kernels,
+        "kv": kv,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -9,9 +9,11 @@
  *
  *   rotation   y = x . H_n / sqrt(n) for each row, H_n = H_{2^k} (x) H_m
  *              (§3.1 Kronecker construction; §4 Stage 1b online Hadamard),
- *              computed in binary32 (App. A.7) in one fixed order:
- *              the m-factor sum left to right, then the Walsh-Hadamard
- *              butterflies bit 0 first, then one multiply by RN32(1/sqrt(n)).
+ *              computed in binary32 (App. A.7): element i = a*m + b; the
+ *              m-factor sum over b taken exactly and rounded once to
+ *              binary32; then the Walsh-Hadamard butterflies over a, bit 0
+ *              first, each output one rounded add or subtract; then one
+ *              multiply by RN32(1/sqrt(n)); a zero output is +0.
  *   quantize   per row (token) symmetric int4 (§4 Stage 2b):
  *              s = RN16(RN(RN(absmax * clip) / 7)),
  *              q = clamp(rint_even(RN(y / s)), -8, 7).
@@ -144,6 +146,59 @@ quarot_status quarot_linear(const quarot_f16 *x, const uint8_t *wq, const quarot
                             quarot_f16 *y, int64_t M, int64_t N, int64_t K, int rotate,
                             float clip_ratio, void *workspace, size_t workspace_bytes,
                             void *stream);
+
+/*
+ * The elementwise SwiGLU product alone: h = RN16(RN(silu(gate) * up)) with
+ * the binary32 silu recipe of quarot_swiglu_quant_int4 below.
+ * gate, up, h fp16 [count]; count a multiple of 8 (0 is a no-op).
+ */
+quarot_status quarot_swiglu(const quarot_f16 *gate, const quarot_f16 *up, quarot_f16 *h,
+                            int64_t count, void *stream);
+
+/*
+ * The down-projection input of a SwiGLU FFN, rotated and quantized in one
+ * launch (§4 Stage 1b: the online Hadamard sits between silu(gate) * up
+ * and the 4-bit W_down):
+ *   h = RN16(RN(silu(gate) * up)) elementwise, then exactly
+ *   quarot_quant_int4(h, rotate = 1, clip_ratio), without storing h.
+ * silu is binary32 by a fixed sequence of IEEE operations, so that its
+ * result is reproducible (a Cody-Waite reduced exp, Taylor degree 7):
+ *   x = clamp(-g, -88, 88), kf = rint_even(RN(x * RN32(1/ln 2))),
+ *   r = fma(-kf, LN2_HI, x), r = fma(-kf, LN2_LO, r),
+ *   p = 1 + r(1 + r(1/2! + r(1/3! + ... + r/7!))) by fma (RN32 coefficients),
+ *   silu(g) = RN(g / RN(1 + ldexp(p, kf)))
+ * with LN2_HI = 0x1.62e4p-1, LN2_LO = 0x1.7f7d1cp-20 (within 4 binary32
+ * ulps of g/(1+exp(-g)) for every fp16 g).
+ *   gate, up fp16 [rows, n]; q uint8 [rows, n/2]; scale fp16 [rows];
+ *   n supported by quarot_hadamard_factor; clip_ratio in (0, 1].
+ */
+quarot_status quarot_swiglu_quant_int4(const quarot_f16 *gate, const quarot_f16 *up, uint8_t *q,
+                                       quarot_f16 *scale, int64_t rows, int64_t n,
+                                       float clip_ratio, void *stream);
+
+/*
+ * Hadamard transform across attention heads (§4 Stage 1c: with the
+ * per-head factor I (x) H_dh fused into W_v and W_out offline, the online
+ * part before out_proj is z <- z (H_nh (x) I_dh)).  Rows z [rows, n] with
+ * n = n_heads * head_dim, head-major (element h * head_dim + d):
+ *   y = RN16(z (H_nh (x) I_dh) / sqrt(n_heads)), the Walsh-Hadamard
+ *   butterflies over the head index (bit 0 first) in binary32, one
+ *   multiply by RN32(1/sqrt(n_heads)); a zero output is +0.
+ * n_heads a power of two >= 2, head_dim a power of two >= 8,
+ * n <= 32768.  z == y (in place) is allowed.
+ */
+quarot_status quarot_hadamard_heads(const quarot_f16 *z, quarot_f16 *y, int64_t rows,
+                                    int64_t n_heads, int64_t head_dim, void *stream);
+
+/*
+ * The out_proj input: the binary32 head-wise transform above quantized
+ * per row (token) to symmetric int4 exactly as quarot_quant_int4 does
+ * (scale from the row's absmax, codes by IEEE division by the stored fp16
+ * scale).  q uint8 [rows, n/2], scale fp16 [rows]; sizes as above.
+ */
+quarot_status quarot_hadamard_heads_quant_int4(const quarot_f16 *z, uint8_t *q,
+                                               quarot_f16 *scale, int64_t rows, int64_t n_heads,
+                                               int64_t head_dim, float clip_ratio, void *stream);
 
 /*
  * 4-bit KV cache quantization (§4 Stage 1d: head-wise rotation of keys,

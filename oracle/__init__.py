@@ -58,6 +58,11 @@ _SIGS = {
     "orc_linear": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I, _F]),
     "orc_kv_quant": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F]),
     "orc_kv_dequant": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I]),
+    "orc_silu_f32": (_F, [_F]),
+    "orc_swiglu_f16": (_I, [_P, _P, _P, _I64]),
+    "orc_swiglu_quant_int4": (_I, [_P, _P, _P, _P, _I64, _I64, _I, _F]),
+    "orc_heads_f16": (_I, [_P, _P, _I64, _I64, _I64]),
+    "orc_heads_quant_int4": (_I, [_P, _P, _P, _I64, _I64, _I64, _F]),
     "orc_set_threads": (None, [_I]),
     "orc_max_threads": (_I, []),
 }
@@ -261,6 +266,61 @@ def kv_dequant(q: np.ndarray, scale: np.ndarray, zero: np.ndarray, group: int = 
     _check(lib().orc_kv_dequant(_ptr(q), _ptr(_u16(scale)), _ptr(_u16(zero)), _ptr(out),
                                 rows, D, group, int(inverse_rotate)), "kv_dequant")
     return out.view(np.float16)
+
+
+# -- prologues of the two online-Hadamard sites -----------------------------
+
+def silu_f32(g: float) -> np.float32:
+    """The binary32 SiLU recipe (scalar)."""
+    return np.float32(lib().orc_silu_f32(float(np.float32(g))))
+
+
+def swiglu(gate: np.ndarray, up: np.ndarray) -> np.ndarray:
+    """h = RN16(RN(silu(gate) * up)), elementwise, fp16 in and out."""
+    g = _f16(gate)
+    u = _f16(up)
+    assert g.shape == u.shape
+    h = np.empty(g.shape, np.uint16)
+    _check(lib().orc_swiglu_f16(_ptr(_u16(g)), _ptr(_u16(u)), _ptr(h), g.size), "swiglu")
+    return h.view(np.float16)
+
+
+def swiglu_quant_int4(gate: np.ndarray, up: np.ndarray, rotate: bool = True,
+                      clip: float = 1.0):
+    """quant_int4(swiglu(gate, up)) per row: the down-projection input."""
+    g = _f16(gate)
+    u = _f16(up)
+    rows, n = g.shape
+    q = np.empty((rows, n // 2), np.uint8)
+    s = np.empty(rows, np.uint16)
+    _check(lib().orc_swiglu_quant_int4(_ptr(_u16(g)), _ptr(_u16(u)), _ptr(q), _ptr(s), rows,
+                                       n, int(rotate), clip), "swiglu_quant_int4")
+    return q, s.view(np.float16)
+
+
+def heads_f32(z: np.ndarray, n_heads: int) -> np.ndarray:
+    """Rows z [rows, n_heads * head_dim] (head-major) -> binary32
+    z (H_nh (x) I) / sqrt(nh)."""
+    z = _f16(z)
+    rows, n = z.shape
+    y = np.empty((rows, n), np.float32)
+    _check(lib().orc_heads_f16(_ptr(_u16(z)), _ptr(y), rows, n_heads, n // n_heads), "heads")
+    return y
+
+
+def hadamard_heads(z: np.ndarray, n_heads: int) -> np.ndarray:
+    """fp16 rows in, RN16 of the head-wise rotation out."""
+    return f32_to_f16(heads_f32(z, n_heads))
+
+
+def heads_quant_int4(z: np.ndarray, n_heads: int, clip: float = 1.0):
+    z = _f16(z)
+    rows, n = z.shape
+    q = np.empty((rows, n // 2), np.uint8)
+    s = np.empty(rows, np.uint16)
+    _check(lib().orc_heads_quant_int4(_ptr(_u16(z)), _ptr(q), _ptr(s), rows, n_heads,
+                                      n // n_heads, clip), "heads_quant_int4")
+    return q, s.view(np.float16)
 
 
 # -- packing helpers (test-side views of the packed format) -----------------

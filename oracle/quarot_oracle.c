@@ -510,6 +510,160 @@ int orc_quant_int4(const uint16_t *x, uint8_t *q, uint16_t *s, int64_t rows, int
 }
 
 /* ------------------------------------------------------------------------ */
+/* Prologues of the two online-Hadamard sites of a layer (§4 Stage 1b: the  */
+/* input of the FFN down-projection, silu(gate) * up; §4 Stage 1c: the      */
+/* attention output before out_proj, rotated across heads).                 */
+/* ------------------------------------------------------------------------ */
+
+/* SiLU in binary32 by a fixed sequence of IEEE operations (so that every
+ * implementation that performs the same operations gets the same bits):
+ *   x  = clamp(-g, -88, 88)
+ *   kf = rint_even(RN(x * log2(e)))
+ *   r  = fma(-kf, LN2_HI, x); r = fma(-kf, LN2_LO, r)   (Cody-Waite reduction)
+ *   p  = 1 + r (1 + r (1/2 + r (1/6 + ... + r/5040)))   (Taylor, Horner in fma)
+ *   E  = p * 2^kf                                      (ldexp)
+ *   silu(g) = RN(g / RN(1 + E))
+ * E approximates exp(-g) to a few binary32 ulps; |r| <= ln(2)/2, where the
+ * degree-7 Taylor remainder is below 2^-27. */
+static const float ORC_LOG2E = 0x1.715476p+0f;   /* RN32(1 / ln 2) */
+static const float ORC_LN2_HI = 0x1.62e4p-1f;     /* ln 2 to 16 bits: kf * LN2_HI is exact */
+static const float ORC_LN2_LO = 0x1.7f7d1cp-20f;  /* RN32(ln 2 - LN2_HI) */
+/* RN32(1/k!) for k = 7 .. 2 */
+static const float ORC_C7 = 0x1.a01a02p-13f, ORC_C6 = 0x1.6c16c2p-10f, ORC_C5 = 0x1.111112p-7f,
+                   ORC_C4 = 0x1.555556p-5f, ORC_C3 = 0x1.555556p-3f;
+
+float orc_silu_f32(float g)
+{
+    float x = -g;
+    if (x > 88.0f)
+        x = 88.0f;
+    if (x < -88.0f)
+        x = -88.0f;
+    float kf = rintf(x * ORC_LOG2E);
+    float r = fmaf(-kf, ORC_LN2_HI, x);
+    r = fmaf(-kf, ORC_LN2_LO, r);
+    float p = ORC_C7;
+    p = fmaf(p, r, ORC_C6);
+    p = fmaf(p, r, ORC_C5);
+    p = fmaf(p, r, ORC_C4);
+    p = fmaf(p, r, ORC_C3);
+    p = fmaf(p, r, 0.5f);
+    p = fmaf(p, r, 1.0f);
+    p = fmaf(p, r, 1.0f);
+    float e = ldexpf(p, (int)kf);
+    float den = 1.0f + e;
+    return g / den;
+}
+
+/* h = RN16(RN(silu(g) * u)): the fp16 input of the down-projection. */
+static uint16_t swiglu_one(uint16_t g, uint16_t u)
+{
+    float sg = orc_silu_f32(orc_f16_to_f32(g));
+    return orc_f32_to_f16(sg * orc_f16_to_f32(u));
+}
+
+int orc_swiglu_f16(const uint16_t *gate, const uint16_t *up, uint16_t *h, int64_t n)
+{
+    if (n < 0)
+        return ORC_ERR_ARG;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; i++)
+        h[i] = swiglu_one(gate[i], up[i]);
+    return ORC_OK;
+}
+
+/* The down-projection input, rotated and quantized per token: exactly
+ * orc_quant_int4 of orc_swiglu_f16(gate, up). */
+int orc_swiglu_quant_int4(const uint16_t *gate, const uint16_t *up, uint8_t *q, uint16_t *s,
+                          int64_t rows, int64_t n, int rotate, float clip)
+{
+    if (n <= 0 || (n & 1) || rows < 0)
+        return ORC_ERR_ARG;
+    uint16_t *h = (uint16_t *)malloc((size_t)(rows * n) * 2 + 2);
+    if (!h)
+        return ORC_ERR_NOMEM;
+    int st = orc_swiglu_f16(gate, up, h, rows * n);
+    if (st == ORC_OK)
+        st = orc_quant_int4(h, q, s, rows, n, rotate, clip);
+    free(h);
+    return st;
+}
+
+/* Hadamard across heads (§4 Stage 1c, "Hadamard heads"): a row z of width
+ * nh * dh (head-major: element h*dh + d) becomes y = z (H_nh (x) I_dh) /
+ * sqrt(nh).  For each d the Walsh-Hadamard butterflies run over the head
+ * index h, bit 0 first, in binary32; then one multiply by RN32(1/sqrt(nh));
+ * a zero y is +0.  nh must be a power of two. */
+static void heads_row(const float *t, float *y, int64_t nh, int64_t dh, float c)
+{
+    for (int64_t i = 0; i < nh * dh; i++)
+        y[i] = t[i];
+    for (int64_t h = 1; h < nh; h <<= 1)
+        for (int64_t p = 0; p < nh; p++) {
+            if (p & h)
+                continue;
+            for (int64_t d = 0; d < dh; d++) {
+                float up = y[p * dh + d], uq = y[(p + h) * dh + d];
+                y[p * dh + d] = up + uq;
+                y[(p + h) * dh + d] = up - uq;
+            }
+        }
+    for (int64_t i = 0; i < nh * dh; i++)
+        y[i] = y[i] * c + 0.0f;
+}
+
+static int heads_args(int64_t rows, int64_t nh, int64_t dh)
+{
+    if (rows < 0 || nh < 2 || dh < 1 || (nh & (nh - 1)))
+        return ORC_ERR_ARG;
+    return ORC_OK;
+}
+
+/* fp16 rows -> binary32 rotated rows [rows, nh*dh]. */
+int orc_heads_f16(const uint16_t *z, float *y, int64_t rows, int64_t nh, int64_t dh)
+{
+    int st = heads_args(rows, nh, dh);
+    if (st)
+        return st;
+    const int64_t n = nh * dh;
+    const float c = orc_rotation_scale(nh);
+    int err = 0;
+#pragma omp parallel for schedule(static) reduction(| : err)
+    for (int64_t r = 0; r < rows; r++) {
+        float *t = (float *)malloc((size_t)n * sizeof(float));
+        if (!t) {
+            err |= 1;
+            continue;
+        }
+        for (int64_t i = 0; i < n; i++)
+            t[i] = orc_f16_to_f32(z[r * n + i]);
+        heads_row(t, y + r * n, nh, dh, c);
+        free(t);
+    }
+    return err ? ORC_ERR_NOMEM : ORC_OK;
+}
+
+/* The out_proj input rotated across heads and quantized per token
+ * (symmetric int4, as orc_quant_sym_f32). */
+int orc_heads_quant_int4(const uint16_t *z, uint8_t *q, uint16_t *s, int64_t rows, int64_t nh,
+                         int64_t dh, float clip)
+{
+    int st = heads_args(rows, nh, dh);
+    if (st)
+        return st;
+    if ((nh * dh) & 1)
+        return ORC_ERR_ARG;
+    float *y = (float *)malloc((size_t)(rows * nh * dh) * sizeof(float) + 4);
+    if (!y)
+        return ORC_ERR_NOMEM;
+    st = orc_heads_f16(z, y, rows, nh, dh);
+    if (st == ORC_OK)
+        st = orc_quant_sym_f32(y, q, s, rows, nh * dh, clip);
+    free(y);
+    return st;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Integer GEMM and dequantization (§4 Stage 2b, App. A.10).                */
 /* ------------------------------------------------------------------------ */
 

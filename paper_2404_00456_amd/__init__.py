@@ -48,6 +48,10 @@ SIGNATURES = {
     "quarot_w4a4_gemm": (_I, [_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P]),
     "quarot_linear_workspace_size": (ctypes.c_size_t, [_I64, _I64]),
     "quarot_linear": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P, ctypes.c_size_t, _P]),
+    "quarot_swiglu": (_I, [_P, _P, _P, _I64, _P]),
+    "quarot_swiglu_quant_int4": (_I, [_P, _P, _P, _P, _I64, _I64, _F, _P]),
+    "quarot_hadamard_heads": (_I, [_P, _P, _I64, _I64, _I64, _P]),
+    "quarot_hadamard_heads_quant_int4": (_I, [_P, _P, _P, _I64, _I64, _I64, _F, _P]),
     "quarot_kv_quant": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P]),
     "quarot_kv_dequant": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _P]),
 }
@@ -209,6 +213,70 @@ def prepare_weight(w: torch.Tensor, rotate: bool = True, clip_ratio: float = 1.0
     return quarot_quant_int4(w, rotate=rotate, clip_ratio=clip_ratio, stream=stream)
 
 
+def quarot_swiglu(gate: torch.Tensor, up: torch.Tensor, h: Optional[torch.Tensor] = None,
+                  stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """h = RN16(silu(gate) * up) elementwise (binary32 silu recipe)."""
+    if tuple(up.shape) != tuple(gate.shape):
+        raise ValueError("gate and up must have the same shape")
+    if h is None:
+        h = torch.empty_like(gate)
+    _check("quarot_swiglu", lib().quarot_swiglu(
+        _ptr(gate, torch.float16, "gate"), _ptr(up, torch.float16, "up"),
+        _ptr(h, torch.float16, "h"), gate.numel(), _stream(stream)))
+    return h
+
+
+def quarot_swiglu_quant_int4(gate: torch.Tensor, up: torch.Tensor, clip_ratio: float = 1.0,
+                             q: Optional[torch.Tensor] = None,
+                             scale: Optional[torch.Tensor] = None,
+                             stream: Optional[torch.cuda.Stream] = None):
+    """Down-projection input: int4 codes of the rotated RN16(silu(gate) * up).
+    Returns (codes uint8 [..., n/2], scale fp16 [...])."""
+    n = gate.shape[-1]
+    if tuple(up.shape) != tuple(gate.shape):
+        raise ValueError("gate and up must have the same shape")
+    rows = _rows(gate, n)
+    if q is None:
+        q = torch.empty(gate.shape[:-1] + (n // 2,), dtype=torch.uint8, device=gate.device)
+    if scale is None:
+        scale = torch.empty(gate.shape[:-1], dtype=torch.float16, device=gate.device)
+    _check("quarot_swiglu_quant_int4", lib().quarot_swiglu_quant_int4(
+        _ptr(gate, torch.float16, "gate"), _ptr(up, torch.float16, "up"),
+        _ptr(q, torch.uint8, "q"), _ptr(scale, torch.float16, "scale"), rows, n,
+        float(clip_ratio), _stream(stream)))
+    return q, scale
+
+
+def quarot_hadamard_heads(z: torch.Tensor, n_heads: int, y: Optional[torch.Tensor] = None,
+                          stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """y = RN16(z (H_nh (x) I_dh) / sqrt(nh)); z fp16 [..., n_heads * head_dim]."""
+    n = z.shape[-1]
+    if y is None:
+        y = torch.empty_like(z)
+    _check("quarot_hadamard_heads", lib().quarot_hadamard_heads(
+        _ptr(z, torch.float16, "z"), _ptr(y, torch.float16, "y"), _rows(z, n), n_heads,
+        n // n_heads if n_heads > 0 else 0, _stream(stream)))
+    return y
+
+
+def quarot_hadamard_heads_quant_int4(z: torch.Tensor, n_heads: int, clip_ratio: float = 1.0,
+                                     q: Optional[torch.Tensor] = None,
+                                     scale: Optional[torch.Tensor] = None,
+                                     stream: Optional[torch.cuda.Stream] = None):
+    """out_proj input: per-token int4 codes of the head-wise rotation."""
+    n = z.shape[-1]
+    rows = _rows(z, n)
+    if q is None:
+        q = torch.empty(z.shape[:-1] + (n // 2,), dtype=torch.uint8, device=z.device)
+    if scale is None:
+        scale = torch.empty(z.shape[:-1], dtype=torch.float16, device=z.device)
+    _check("quarot_hadamard_heads_quant_int4", lib().quarot_hadamard_heads_quant_int4(
+        _ptr(z, torch.float16, "z"), _ptr(q, torch.uint8, "q"),
+        _ptr(scale, torch.float16, "scale"), rows, n_heads,
+        n // n_heads if n_heads > 0 else 0, float(clip_ratio), _stream(stream)))
+    return q, scale
+
+
 def quarot_kv_quant(kv: torch.Tensor, group: int = 128, rotate: bool = True,
                     clip_ratio: float = 0.95, q: Optional[torch.Tensor] = None,
                     scale: Optional[torch.Tensor] = None, zero: Optional[torch.Tensor] = None,
@@ -250,5 +318,6 @@ __all__ = [
     "QuarotError", "lib", "quarot_version", "quarot_hadamard_factor",
     "quarot_hadamard_factor_table", "quarot_linear_workspace_size", "quarot_hadamard",
     "quarot_quant_int4", "quarot_w4a4_gemm", "quarot_linear", "prepare_weight",
+    "quarot_swiglu", "quarot_swiglu_quant_int4", "quarot_hadamard_heads", "quarot_hadamard_heads_quant_int4",
     "quarot_kv_quant", "quarot_kv_dequant",
 ]

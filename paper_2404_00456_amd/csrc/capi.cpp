@@ -308,6 +308,120 @@ quarot_status quarot_linear(const quarot_f16 *x, const uint8_t *wq, const quarot
     return e == hipSuccess ? QUAROT_OK : hip_fail(e);
 }
 
+quarot_status quarot_swiglu(const quarot_f16 *gate, const quarot_f16 *up, quarot_f16 *h,
+                            int64_t count, void *stream)
+{
+    if (count < 0)
+        return QUAROT_ERR_INVALID_ARG;
+    if (count % 8)
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (count == 0)
+        return QUAROT_OK;
+    if (!gate || !up || !h)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(gate) || !aligned16(up) || !aligned16(h))
+        return QUAROT_ERR_ALIGNMENT;
+    quarot_status st = check_device();
+    if (st)
+        return st;
+    hipError_t e = launch_swiglu(gate, up, h, count, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+quarot_status quarot_swiglu_quant_int4(const quarot_f16 *gate, const quarot_f16 *up, uint8_t *q,
+                                       quarot_f16 *scale, int64_t rows, int64_t n,
+                                       float clip_ratio, void *stream)
+{
+    if (rows < 0 || !clip_ok(clip_ratio))
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;
+    quarot_status st = check_rot_size(n, true, EPI_SYM, &k, &m);
+    if (st)
+        return st;
+    if (!rotate_supported(EPI_SYM, true, k, m, (int)n, PRO_SWIGLU))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!gate || !up || !q || !scale)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(gate) || !aligned16(up) || !aligned16(q) || !aligned16(scale))
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    RotArgs a{};
+    a.x = gate;
+    a.x2 = up;
+    a.out = q;
+    a.scale = scale;
+    a.rows = rows;
+    a.n = (int)n;
+    a.c = rotation_scale(n);
+    a.clip = clip_ratio;
+    hipError_t e = launch_rotate(a, EPI_SYM, true, k, m, (hipStream_t)stream, PRO_SWIGLU);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Head-wise transform: n = n_heads * head_dim, both powers of two.
+quarot_status heads_launch(const quarot_f16 *z, void *out, quarot_f16 *scale, int64_t rows,
+                           int64_t n_heads, int64_t head_dim, float clip, int epi,
+                           void *stream)
+{
+    if (rows < 0 || n_heads <= 0 || head_dim <= 0 || !clip_ok(clip))
+        return QUAROT_ERR_INVALID_ARG;
+    if (n_heads < 2 || (n_heads & (n_heads - 1)) || head_dim < 8 ||
+        (head_dim & (head_dim - 1)) || n_heads * head_dim > kMaxN)
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    const int64_t n = n_heads * head_dim;
+    int k = 0, m = 1, s0 = 0;
+    while ((int64_t(1) << k) < n)
+        ++k;
+    while ((int64_t(1) << s0) < head_dim)
+        ++s0;
+    if (!rotate_supported(epi, true, k, m, (int)n))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!z || !out || (epi == EPI_SYM && !scale))
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(z) || !aligned16(out) || (scale && !aligned16(scale)))
+        return QUAROT_ERR_ALIGNMENT;
+    quarot_status st = check_device();
+    if (st)
+        return st;
+    RotArgs a{};
+    a.x = z;
+    a.out = out;
+    a.scale = scale;
+    a.rows = rows;
+    a.n = (int)n;
+    a.s0 = s0;
+    a.c = rotation_scale(n_heads);
+    a.clip = clip;
+    hipError_t e = launch_rotate(a, epi, true, k, m, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+quarot_status quarot_hadamard_heads(const quarot_f16 *z, quarot_f16 *y, int64_t rows,
+                                    int64_t n_heads, int64_t head_dim, void *stream)
+{
+    return heads_launch(z, y, nullptr, rows, n_heads, head_dim, 1.0f, EPI_F16, stream);
+}
+
+quarot_status quarot_hadamard_heads_quant_int4(const quarot_f16 *z, uint8_t *q,
+                                               quarot_f16 *scale, int64_t rows, int64_t n_heads,
+                                               int64_t head_dim, float clip_ratio, void *stream)
+{
+    return heads_launch(z, q, scale, rows, n_heads, head_dim, clip_ratio, EPI_SYM, stream);
+}
+
 quarot_status quarot_kv_quant(const quarot_f16 *kv, uint8_t *q, quarot_f16 *scale,
                               quarot_f16 *zero, int64_t rows, int64_t head_dim, int64_t group,
                               int rotate, float clip_ratio, void *stream)

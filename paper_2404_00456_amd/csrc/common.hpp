@@ -16,15 +16,23 @@ enum Epilogue : int {
     EPI_KV = 2,   // per-group asymmetric uint4 codes + fp16 scale, zero
 };
 
+// Load stages of the rotate kernels.
+enum Prologue : int {
+    PRO_PLAIN = 0,   // x is the row
+    PRO_SWIGLU = 1,  // the row is RN16(silu(x) * x2) (gate x, up x2)
+};
+
 struct RotArgs {
-    const uint16_t *x;  // fp16 [rows, n]
-    void *out;          // EPI_F16: fp16 [rows, n]; else uint8 codes [rows, n/2]
-    uint16_t *scale;    // EPI_SYM: [rows]; EPI_KV: [rows, n/group]
-    uint16_t *zero;     // EPI_KV: [rows, n/group]
+    const uint16_t *x;   // fp16 [rows, n]
+    const uint16_t *x2;  // PRO_SWIGLU: the up-projection, fp16 [rows, n]
+    void *out;           // EPI_F16: fp16 [rows, n]; else uint8 codes [rows, n/2]
+    uint16_t *scale;     // EPI_SYM: [rows]; EPI_KV: [rows, n/group]
+    uint16_t *zero;      // EPI_KV: [rows, n/group]
     int64_t rows;
     int n;
-    int group;          // EPI_KV group size
-    float c;            // RN32(1/sqrt(n))
+    int group;           // EPI_KV group size
+    int s0;              // first butterfly bit (0; log2(head_dim) across heads)
+    float c;             // RN32(1/sqrt(n)), or RN32(1/sqrt(heads)) across heads
     float clip;
 };
 
@@ -51,12 +59,15 @@ struct KvDeqArgs {
 
 // Launchers (return hipSuccess or the launch error).  `rotate` selects the
 // rotation; sizes have been validated by the caller.
-hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, hipStream_t s);
+hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, hipStream_t s,
+                         int pro = PRO_PLAIN);
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
 hipError_t launch_kv_dequant(const KvDeqArgs &a, bool inverse_rotate, hipStream_t s);
+hipError_t launch_swiglu(const uint16_t *g, const uint16_t *u, uint16_t *h, int64_t count,
+                         hipStream_t s);
 
 // Is (k, m) covered by a compiled rotate kernel for this epilogue?
-bool rotate_supported(int epi, bool rotate, int k, int m, int n);
+bool rotate_supported(int epi, bool rotate, int k, int m, int n, int pro = PRO_PLAIN);
 
 // ---------------------------------------------------------------- device --
 
@@ -212,13 +223,18 @@ __device__ __forceinline__ void lane_stage(float *v, float s, int lane)
 }
 
 // All lane stages J < LOGL (in increasing J, the canonical order) on R
-// registers; returns sigma, the sign the lane's values now carry.
+// registers, skipping J < j0 (j0 uniform across the wave); returns sigma,
+// the sign the lane's values now carry.
 template <int LOGL, int R>
-__device__ __forceinline__ float lane_stages(float *v, int lane, int pos)
+__device__ __forceinline__ float lane_stages(float *v, int lane, int pos, int j0 = 0)
 {
-    static_for<LOGL>([&](auto J) { lane_stage<J, R>(v, pos_sign(pos, J), lane); });
+    static_for<LOGL>([&](auto J) {
+        if (J >= j0)
+            lane_stage<J, R>(v, pos_sign(pos, J), lane);
+    });
     constexpr int dpp_bits = (1 << (LOGL < 4 ? LOGL : 4)) - 1;
-    return (__builtin_popcount(pos & dpp_bits) & 1) ? -1.0f : 1.0f;
+    const int done = j0 <= 0 ? dpp_bits : j0 >= 4 ? 0 : (dpp_bits & ~((1 << j0) - 1));
+    return (__builtin_popcount(pos & done) & 1) ? -1.0f : 1.0f;
 }
 
 template <int J>

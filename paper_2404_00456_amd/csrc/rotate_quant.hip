@@ -24,6 +24,8 @@
 //   k_quant_plain quantization without rotation, any n multiple of 8.
 //   k_kv_dequant  4-bit KV cache back to fp16, optional inverse rotation.
 // Lane butterflies use the placement and sign bookkeeping of lane_stages().
+#include <algorithm>
+
 #include "common.hpp"
 #include "hadamard_factors.hpp"
 
@@ -123,6 +125,69 @@ __device__ __forceinline__ void store4(uint16_t *p, const float *v)
     *reinterpret_cast<uint2 *>(p) = raw;
 }
 
+// SiLU in binary32 by a fixed sequence of IEEE operations (Cody-Waite
+// reduction of exp(-g) and a degree-7 Taylor polynomial in fma; the CPU
+// reference performs the same operations):
+//   x = clamp(-g, -88, 88), kf = rint_even(RN(x log2 e)),
+//   r = fma(-kf, LN2_HI, fma...)  (kf LN2_HI exact: LN2_HI has 16 bits),
+//   E = ldexp(p(r), kf), silu(g) = RN(g / RN(1 + E)).
+__device__ __forceinline__ float silu_f32(float g)
+{
+    const float x = fminf(fmaxf(-g, -88.0f), 88.0f);
+    const float kf = rintf(x * 0x1.715476p+0f);  // RN32(1 / ln 2)
+    float r = __builtin_fmaf(-kf, 0x1.62e4p-1f, x);  // ln 2 to 16 bits
+    r = __builtin_fmaf(-kf, 0x1.7f7d1cp-20f, r);     // RN32(ln 2 - that)
+    float p = 0x1.a01a02p-13f;                        // RN32(1/k!), k = 7 .. 2
+    p = __builtin_fmaf(p, r, 0x1.6c16c2p-10f);
+    p = __builtin_fmaf(p, r, 0x1.111112p-7f);
+    p = __builtin_fmaf(p, r, 0x1.555556p-5f);
+    p = __builtin_fmaf(p, r, 0x1.555556p-3f);
+    p = __builtin_fmaf(p, r, 0.5f);
+    p = __builtin_fmaf(p, r, 1.0f);
+    p = __builtin_fmaf(p, r, 1.0f);
+    const float e = __builtin_ldexpf(p, (int)kf);
+    return g / (1.0f + e);
+}
+
+// The down-projection input h = RN16(RN(silu(g) u)), as binary32.
+__device__ __forceinline__ float swiglu1(uint16_t g, uint16_t u)
+{
+    return h2f(f2h(silu_f32(h2f(g)) * h2f(u)));
+}
+
+// 8 (4) consecutive elements of the row at element offset off.
+template <int PRO>
+__device__ __forceinline__ void load_row8(const RotArgs &a, int64_t off, float *v)
+{
+    if constexpr (PRO == PRO_PLAIN) {
+        load8(a.x + off, v);
+    } else {
+        const uint4 g = *reinterpret_cast<const uint4 *>(a.x + off);
+        const uint4 u = *reinterpret_cast<const uint4 *>(a.x2 + off);
+        const uint32_t gw[4] = {g.x, g.y, g.z, g.w}, uw[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[2 * i] = swiglu1((uint16_t)(gw[i] & 0xFFFFu), (uint16_t)(uw[i] & 0xFFFFu));
+            v[2 * i + 1] = swiglu1((uint16_t)(gw[i] >> 16), (uint16_t)(uw[i] >> 16));
+        }
+    }
+}
+
+template <int PRO>
+__device__ __forceinline__ void load_row4(const RotArgs &a, int64_t off, float *v)
+{
+    if constexpr (PRO == PRO_PLAIN) {
+        load4(a.x + off, v);
+    } else {
+        const uint2 g = *reinterpret_cast<const uint2 *>(a.x + off);
+        const uint2 u = *reinterpret_cast<const uint2 *>(a.x2 + off);
+        v[0] = swiglu1((uint16_t)(g.x & 0xFFFFu), (uint16_t)(u.x & 0xFFFFu));
+        v[1] = swiglu1((uint16_t)(g.x >> 16), (uint16_t)(u.x >> 16));
+        v[2] = swiglu1((uint16_t)(g.y & 0xFFFFu), (uint16_t)(u.y & 0xFFFFu));
+        v[3] = swiglu1((uint16_t)(g.y >> 16), (uint16_t)(u.y >> 16));
+    }
+}
+
 // Max over the L-lane group (xor butterfly), then over the W waves.
 template <int LOGL, int W>
 __device__ __forceinline__ float row_absmax(float amax, int w, float *red)
@@ -142,7 +207,9 @@ __device__ __forceinline__ float row_absmax(float amax, int w, float *red)
 
 // ------------------------------------------------------------ m = 1 -----
 
-template <int LOGL, int W, int C, int EPI, bool ROT>
+// Butterflies run over element bits >= a.s0 only (0: the whole
+// Walsh-Hadamard transform; log2(head_dim): across heads).
+template <int LOGL, int W, int C, int EPI, bool ROT, int PRO = PRO_PLAIN>
 __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
 {
     constexpr int L = 1 << LOGL;
@@ -166,32 +233,35 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
     }
 
     float v[C][8];
-    const uint16_t *xr = a.x + row * N;
 #pragma unroll
     for (int cc = 0; cc < C; ++cc)
-        load8(xr + ((cc * W + w) * L + pos) * 8, v[cc]);
+        load_row8<PRO>(a, row * N + ((cc * W + w) * L + pos) * 8, v[cc]);
 
     if constexpr (ROT) {
+        const int s0 = a.s0;
         // element bits 0..2: inside each chunk
 #pragma unroll
-        for (int h = 1; h < 8; h <<= 1)
+        for (int h = 1, bit = 0; h < 8; h <<= 1, ++bit)
+            if (bit >= s0)
 #pragma unroll
-            for (int cc = 0; cc < C; ++cc)
+                for (int cc = 0; cc < C; ++cc)
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    if (!(e & h)) {
-                        float p = v[cc][e], q = v[cc][e + h];
-                        v[cc][e] = p + q;
-                        v[cc][e + h] = p - q;
-                    }
+                    for (int e = 0; e < 8; ++e)
+                        if (!(e & h)) {
+                            float p = v[cc][e], q = v[cc][e + h];
+                            v[cc][e] = p + q;
+                            v[cc][e + h] = p - q;
+                        }
         // next LOGL bits: across lanes
-        const float sigma = lane_stages<LOGL, 8 * C>(&v[0][0], lane, pos);
+        const float sigma = lane_stages<LOGL, 8 * C>(&v[0][0], lane, pos, s0 - 3);
         // next LOGW bits: across waves, through LDS one chunk at a time; the
         // partner wave holds the same lane position (the same sigma)
         if constexpr (W > 1) {
             __shared__ float xs[W][8][64];
 #pragma unroll
             for (int j = 0; j < LOGW; ++j) {
+                if (3 + LOGL + j < s0)
+                    continue;
                 const int pw = w ^ (1 << j);
                 const float sw = ((w >> j) & 1) ? -1.0f : 1.0f;
 #pragma unroll
@@ -209,17 +279,18 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
         }
         // top bits: across the chunks of a lane
 #pragma unroll
-        for (int h = 1; h < C; h <<= 1)
+        for (int h = 1, bit = 3 + LOGL + LOGW; h < C; h <<= 1, ++bit)
+            if (bit >= s0)
 #pragma unroll
-            for (int cc = 0; cc < C; ++cc)
-                if (!(cc & h)) {
+                for (int cc = 0; cc < C; ++cc)
+                    if (!(cc & h)) {
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        float p = v[cc][e], q = v[cc + h][e];
-                        v[cc][e] = p + q;
-                        v[cc + h][e] = p - q;
+                        for (int e = 0; e < 8; ++e) {
+                            float p = v[cc][e], q = v[cc + h][e];
+                            v[cc][e] = p + q;
+                            v[cc + h][e] = p - q;
+                        }
                     }
-                }
         // y = u * c: sigma * c is exact and RN(sigma u * sigma c) = RN(u c);
         // the fma with +0 makes a zero +0 (the sign folding can leave -0)
         const float sc = sigma * a.c;
@@ -336,7 +407,7 @@ __device__ __forceinline__ void mfactor_exact(float *t)
         t[bp] = (float)acc[bp];  // the one rounding
 }
 
-template <int M, int LOGL, int W, int C, int EPI>
+template <int M, int LOGL, int W, int C, int EPI, int PRO = PRO_PLAIN>
 __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
 {
     static_assert(M % 4 == 0, "groups load as 8-byte pieces");
@@ -360,13 +431,12 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
     }
 
     float v[C][M];
-    const uint16_t *xr = a.x + row * N;
 #pragma unroll
     for (int cc = 0; cc < C; ++cc) {
         const int g = (cc * W + w) * L + pos;
 #pragma unroll
         for (int p = 0; p < M / 4; ++p)
-            load4(xr + g * M + 4 * p, &v[cc][4 * p]);
+            load_row4<PRO>(a, row * N + g * M + 4 * p, &v[cc][4 * p]);
     }
 
 #pragma unroll
@@ -472,7 +542,7 @@ __device__ __forceinline__ const double *hm_blocks<172>()
 // pass, each an fp64 sum of +-t (exact, see mfactor_exact) rounded once.
 // The rotated row (before the scale) is staged in LDS as A rows of M+1
 // floats, with the lanes' sign sigma removed.
-template <int M, int W, int EPI>
+template <int M, int W, int EPI, int PRO = PRO_PLAIN>
 __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
 {
     constexpr int CB = kLargeCB;
@@ -491,10 +561,10 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
 
     float t[M];
     if (act) {
-        const uint16_t *xg = a.x + row * n + (int64_t)g * M;
+        const int64_t xg = row * n + (int64_t)g * M;
 #pragma unroll
         for (int p = 0; p < M / 4; ++p)
-            load4(xg + 4 * p, &t[4 * p]);
+            load_row4<PRO>(a, xg + 4 * p, &t[4 * p]);
     } else {
 #pragma unroll
         for (int b = 0; b < M; ++b)
@@ -639,6 +709,23 @@ __global__ __launch_bounds__(256) void k_quant_plain(RotArgs a)
         a.scale[row] = s16;
 }
 
+// ------------------------------------------------- elementwise SwiGLU -----
+
+// h = RN16(RN(silu(gate) up)), 8 elements per thread and step.
+__global__ __launch_bounds__(256) void k_swiglu(const uint16_t *g, const uint16_t *u,
+                                                uint16_t *h, int64_t chunks)
+{
+    RotArgs a{};
+    a.x = g;
+    a.x2 = u;
+    for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < chunks;
+         c += (int64_t)gridDim.x * 256) {
+        float v[8];
+        load_row8<PRO_SWIGLU>(a, c * 8, v);
+        store8(h + c * 8, v);  // exact: v holds fp16 values
+    }
+}
+
 // ------------------------------------------------------ KV dequant -------
 
 template <int LOGL, bool INV>
@@ -680,95 +767,96 @@ __global__ __launch_bounds__(256) void k_kv_dequant(KvDeqArgs a)
 
 // ---------------------------------------------------------- dispatch -----
 
-template <int LOGL, int W, int C, int EPI, bool ROT>
+template <int LOGL, int W, int C, int EPI, bool ROT, int PRO>
 hipError_t go_pow2(const RotArgs &a, hipStream_t s)
 {
     constexpr int L = 1 << LOGL;
     constexpr int RPB = (W == 1) ? 4 * (64 / L) : 1;
     const int64_t blocks = (a.rows + RPB - 1) / RPB;
-    hipLaunchKernelGGL((k_rot_pow2<LOGL, W, C, EPI, ROT>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((k_rot_pow2<LOGL, W, C, EPI, ROT, PRO>), dim3((unsigned)blocks),
                        dim3(W == 1 ? 256 : 64 * W), 0, s, a);
     return hipGetLastError();
 }
 
-template <int M, int LOGL, int W, int C, int EPI>
+template <int M, int LOGL, int W, int C, int EPI, int PRO>
 hipError_t go_smallm(const RotArgs &a, hipStream_t s)
 {
     constexpr int L = 1 << LOGL;
     constexpr int RPB = (W == 1) ? 4 * (64 / L) : 1;
     const int64_t blocks = (a.rows + RPB - 1) / RPB;
-    hipLaunchKernelGGL((k_rot_smallm<M, LOGL, W, C, EPI>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((k_rot_smallm<M, LOGL, W, C, EPI, PRO>), dim3((unsigned)blocks),
                        dim3(W == 1 ? 256 : 64 * W), 0, s, a);
     return hipGetLastError();
 }
 
-template <int M, int W, int EPI>
+template <int M, int W, int EPI, int PRO>
 hipError_t go_largem(const RotArgs &a, hipStream_t s)
 {
     const size_t lds = (size_t)(a.n / M) * (M + 1) * sizeof(float);
-    hipLaunchKernelGGL((k_rot_largem<M, W, EPI>), dim3((unsigned)a.rows), dim3(64 * W), lds, s, a);
+    hipLaunchKernelGGL((k_rot_largem<M, W, EPI, PRO>), dim3((unsigned)a.rows), dim3(64 * W), lds,
+                       s, a);
     return hipGetLastError();
 }
 
-template <int EPI, bool ROT>
+template <int EPI, bool ROT, int PRO>
 hipError_t dispatch_pow2(const RotArgs &a, int k, hipStream_t s)
 {
     switch (k) {
-    case 3: return go_pow2<0, 1, 1, EPI, ROT>(a, s);
-    case 4: return go_pow2<1, 1, 1, EPI, ROT>(a, s);
-    case 5: return go_pow2<2, 1, 1, EPI, ROT>(a, s);
-    case 6: return go_pow2<3, 1, 1, EPI, ROT>(a, s);
-    case 7: return go_pow2<4, 1, 1, EPI, ROT>(a, s);
-    case 8: return go_pow2<5, 1, 1, EPI, ROT>(a, s);
-    case 9: return go_pow2<6, 1, 1, EPI, ROT>(a, s);
+    case 3: return go_pow2<0, 1, 1, EPI, ROT, PRO>(a, s);
+    case 4: return go_pow2<1, 1, 1, EPI, ROT, PRO>(a, s);
+    case 5: return go_pow2<2, 1, 1, EPI, ROT, PRO>(a, s);
+    case 6: return go_pow2<3, 1, 1, EPI, ROT, PRO>(a, s);
+    case 7: return go_pow2<4, 1, 1, EPI, ROT, PRO>(a, s);
+    case 8: return go_pow2<5, 1, 1, EPI, ROT, PRO>(a, s);
+    case 9: return go_pow2<6, 1, 1, EPI, ROT, PRO>(a, s);
     }
     if constexpr (EPI != EPI_KV) {
         switch (k) {
-        case 10: return go_pow2<6, 1, 2, EPI, ROT>(a, s);
-        case 11: return go_pow2<6, 1, 4, EPI, ROT>(a, s);
-        case 12: return go_pow2<6, 1, 8, EPI, ROT>(a, s);
-        case 13: return go_pow2<6, 1, 16, EPI, ROT>(a, s);
-        case 14: return go_pow2<6, 4, 8, EPI, ROT>(a, s);
-        case 15: return go_pow2<6, 8, 8, EPI, ROT>(a, s);
+        case 10: return go_pow2<6, 1, 2, EPI, ROT, PRO>(a, s);
+        case 11: return go_pow2<6, 1, 4, EPI, ROT, PRO>(a, s);
+        case 12: return go_pow2<6, 1, 8, EPI, ROT, PRO>(a, s);
+        case 13: return go_pow2<6, 4, 4, EPI, ROT, PRO>(a, s);
+        case 14: return go_pow2<6, 4, 8, EPI, ROT, PRO>(a, s);
+        case 15: return go_pow2<6, 8, 8, EPI, ROT, PRO>(a, s);
         }
     }
     return hipErrorInvalidValue;
 }
 
 // groups A = 2^k; C = min(A/64, CMAX) chunks per lane, W = A/(64 C) waves
-template <int M, int CMAX, int EPI>
+template <int M, int CMAX, int EPI, int PRO>
 hipError_t dispatch_smallm(const RotArgs &a, int k, hipStream_t s)
 {
     switch (k) {
-    case 0: return go_smallm<M, 0, 1, 1, EPI>(a, s);
-    case 1: return go_smallm<M, 1, 1, 1, EPI>(a, s);
-    case 2: return go_smallm<M, 2, 1, 1, EPI>(a, s);
-    case 3: return go_smallm<M, 3, 1, 1, EPI>(a, s);
-    case 4: return go_smallm<M, 4, 1, 1, EPI>(a, s);
-    case 5: return go_smallm<M, 5, 1, 1, EPI>(a, s);
-    case 6: return go_smallm<M, 6, 1, 1, EPI>(a, s);
-    case 7: return go_smallm<M, 6, 1, 2, EPI>(a, s);
-    case 8: return go_smallm<M, 6, 1, 4, EPI>(a, s);
-    case 9: return go_smallm<M, 6, (CMAX >= 8 ? 1 : 2), (CMAX >= 8 ? 8 : 4), EPI>(a, s);
-    case 10: return go_smallm<M, 6, (CMAX >= 8 ? 2 : 4), (CMAX >= 8 ? 8 : 4), EPI>(a, s);
+    case 0: return go_smallm<M, 0, 1, 1, EPI, PRO>(a, s);
+    case 1: return go_smallm<M, 1, 1, 1, EPI, PRO>(a, s);
+    case 2: return go_smallm<M, 2, 1, 1, EPI, PRO>(a, s);
+    case 3: return go_smallm<M, 3, 1, 1, EPI, PRO>(a, s);
+    case 4: return go_smallm<M, 4, 1, 1, EPI, PRO>(a, s);
+    case 5: return go_smallm<M, 5, 1, 1, EPI, PRO>(a, s);
+    case 6: return go_smallm<M, 6, 1, 1, EPI, PRO>(a, s);
+    case 7: return go_smallm<M, 6, 1, 2, EPI, PRO>(a, s);
+    case 8: return go_smallm<M, 6, 1, 4, EPI, PRO>(a, s);
+    case 9: return go_smallm<M, 6, (CMAX >= 8 ? 1 : 2), (CMAX >= 8 ? 8 : 4), EPI, PRO>(a, s);
+    case 10: return go_smallm<M, 6, (CMAX >= 8 ? 2 : 4), (CMAX >= 8 ? 8 : 4), EPI, PRO>(a, s);
     case 11:
         if constexpr (CMAX >= 8)
-            return go_smallm<M, 6, 4, 8, EPI>(a, s);
+            return go_smallm<M, 6, 4, 8, EPI, PRO>(a, s);
         break;
     }
     return hipErrorInvalidValue;
 }
 
-template <int EPI>
+template <int EPI, int PRO>
 hipError_t dispatch_rotated(const RotArgs &a, int k, int m, hipStream_t s)
 {
     switch (m) {
-    case 1: return dispatch_pow2<EPI, true>(a, k, s);
-    case 12: return dispatch_smallm<12, 8, EPI>(a, k, s);
-    case 20: return dispatch_smallm<20, 4, EPI>(a, k, s);
-    case 28: return dispatch_smallm<28, 4, EPI>(a, k, s);
-    case 108: return (k <= 6) ? go_largem<108, 1, EPI>(a, s) : go_largem<108, 2, EPI>(a, s);
-    case 172: return go_largem<172, 1, EPI>(a, s);
+    case 1: return dispatch_pow2<EPI, true, PRO>(a, k, s);
+    case 12: return dispatch_smallm<12, 8, EPI, PRO>(a, k, s);
+    case 20: return dispatch_smallm<20, 4, EPI, PRO>(a, k, s);
+    case 28: return dispatch_smallm<28, 4, EPI, PRO>(a, k, s);
+    case 108: return (k <= 6) ? go_largem<108, 1, EPI, PRO>(a, s) : go_largem<108, 2, EPI, PRO>(a, s);
+    case 172: return go_largem<172, 1, EPI, PRO>(a, s);
     }
     return hipErrorInvalidValue;
 }
@@ -787,9 +875,11 @@ hipError_t go_kvdeq(const KvDeqArgs &a, bool inv, hipStream_t s)
 
 }  // namespace
 
-bool rotate_supported(int epi, bool rotate, int k, int m, int n)
+bool rotate_supported(int epi, bool rotate, int k, int m, int n, int pro)
 {
     if (n <= 0 || n % 8 != 0 || n > 32768)
+        return false;
+    if (pro == PRO_SWIGLU && (epi != EPI_SYM || !rotate))
         return false;
     if (!rotate)
         return epi == EPI_SYM || (epi == EPI_KV && m == 1 && k >= 3 && k <= 9);
@@ -806,25 +896,40 @@ bool rotate_supported(int epi, bool rotate, int k, int m, int n)
     return false;
 }
 
-hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, hipStream_t s)
+hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, hipStream_t s,
+                         int pro)
 {
     if (a.rows == 0)
         return hipSuccess;
+    if (pro == PRO_SWIGLU)
+        return (epi == EPI_SYM && rotate) ? dispatch_rotated<EPI_SYM, PRO_SWIGLU>(a, k, m, s)
+                                          : hipErrorInvalidValue;
     if (!rotate) {
         if (epi == EPI_SYM) {
             hipLaunchKernelGGL(k_quant_plain, dim3((unsigned)a.rows), dim3(256), 0, s, a);
             return hipGetLastError();
         }
         if (epi == EPI_KV)
-            return dispatch_pow2<EPI_KV, false>(a, k, s);
+            return dispatch_pow2<EPI_KV, false, PRO_PLAIN>(a, k, s);
         return hipErrorInvalidValue;
     }
     switch (epi) {
-    case EPI_F16: return dispatch_rotated<EPI_F16>(a, k, m, s);
-    case EPI_SYM: return dispatch_rotated<EPI_SYM>(a, k, m, s);
-    case EPI_KV: return dispatch_pow2<EPI_KV, true>(a, k, s);
+    case EPI_F16: return dispatch_rotated<EPI_F16, PRO_PLAIN>(a, k, m, s);
+    case EPI_SYM: return dispatch_rotated<EPI_SYM, PRO_PLAIN>(a, k, m, s);
+    case EPI_KV: return dispatch_pow2<EPI_KV, true, PRO_PLAIN>(a, k, s);
     }
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_swiglu(const uint16_t *g, const uint16_t *u, uint16_t *h, int64_t count,
+                         hipStream_t s)
+{
+    const int64_t chunks = count / 8;
+    if (chunks == 0)
+        return hipSuccess;
+    const int64_t blocks = std::min<int64_t>((chunks + 255) / 256, 256 * 16);
+    hipLaunchKernelGGL(k_swiglu, dim3((unsigned)blocks), dim3(256), 0, s, g, u, h, chunks);
+    return hipGetLastError();
 }
 
 hipError_t launch_kv_dequant(const KvDeqArgs &a, bool inverse_rotate, hipStream_t s)

@@ -121,6 +121,29 @@ def test_invalid_arguments_rejected_before_device(L):
     assert L.quarot_kv_quant(P, P, P, None, 4, 128, 128, 1, 0.95, S) == INVALID
     assert L.quarot_kv_dequant(P, P, P, P, 4, 128, 0, 0, S) == INVALID
     assert L.quarot_kv_dequant(P, P, UNALIGNED, P, 4, 128, 128, 0, S) == ALIGN
+    # swiglu prologue
+    assert L.quarot_swiglu(P, P2, P, 12, S) == UNSUPPORTED
+    assert L.quarot_swiglu(P, P2, P, -8, S) == INVALID
+    assert L.quarot_swiglu(P, None, P, 16, S) == INVALID
+    assert L.quarot_swiglu(P, P2, UNALIGNED, 16, S) == ALIGN
+    assert L.quarot_swiglu(None, None, None, 0, S) == OK
+    assert L.quarot_swiglu_quant_int4(P, P2, P, P2, -1, 128, 1.0, S) == INVALID
+    assert L.quarot_swiglu_quant_int4(P, P2, P, P2, 4, 128, 0.0, S) == INVALID
+    assert L.quarot_swiglu_quant_int4(P, P2, P, P2, 4, 100, 1.0, S) == UNSUPPORTED
+    assert L.quarot_swiglu_quant_int4(P, None, P, P2, 4, 128, 1.0, S) == INVALID
+    assert L.quarot_swiglu_quant_int4(P, UNALIGNED, P, P2, 4, 128, 1.0, S) == ALIGN
+    assert L.quarot_swiglu_quant_int4(None, None, None, None, 0, 11008, 1.0, S) == OK
+    # heads
+    assert L.quarot_hadamard_heads(P, P2, 4, 48, 128, S) == UNSUPPORTED   # 48 heads
+    assert L.quarot_hadamard_heads(P, P2, 4, 64, 96, S) == UNSUPPORTED    # head_dim 96
+    assert L.quarot_hadamard_heads(P, P2, 4, 512, 128, S) == UNSUPPORTED  # n > 32768
+    assert L.quarot_hadamard_heads(P, P2, 4, 1, 128, S) == UNSUPPORTED
+    assert L.quarot_hadamard_heads(P, P2, 4, 0, 128, S) == INVALID
+    assert L.quarot_hadamard_heads(P, None, 4, 64, 128, S) == INVALID
+    assert L.quarot_hadamard_heads(P, UNALIGNED, 4, 64, 128, S) == ALIGN
+    assert L.quarot_hadamard_heads(None, None, 0, 64, 128, S) == OK
+    assert L.quarot_hadamard_heads_quant_int4(P, P2, None, 4, 64, 128, 1.0, S) == INVALID
+    assert L.quarot_hadamard_heads_quant_int4(P, P2, P, 4, 64, 128, 2.0, S) == INVALID
 
 
 @pytest.mark.skipif(has_gpu(), reason="valid arguments would reach a real device")
@@ -129,6 +152,8 @@ def test_no_device_reported(L):
     (fake pointers are never dereferenced because nothing launches)."""
     assert L.quarot_quant_int4(P, P2, P2, 4, 128, 1, 1.0, None) == NODEV
     assert L.quarot_w4a4_gemm(P, P, P, P, P, None, 4, 4, 128, None) == NODEV
+    assert L.quarot_swiglu_quant_int4(P, P2, P, P2, 4, 28672, 1.0, None) == NODEV
+    assert L.quarot_hadamard_heads_quant_int4(P, P2, P, 4, 64, 128, 1.0, None) == NODEV
 
 
 def test_binding_rejects_host_tensors():
