@@ -102,6 +102,33 @@ def bench_kv(q, workloads, torch, np, dev, stream, iters):
 
     once()
     torch.cuda.synchronize()
+    # decode step over the whole quantized cache: one rotated query per
+    # (batch, head), seq_len = 4096 tokens
+    nq = wl.B * wl.H
+    kcache = tuple(x.view(nq, wl.S, -1) for x in tens[0][1:4])
+    vcache = tuple(x.view(nq, wl.S, -1) for x in tens[1][1:4])
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    qd = torch.randn((nq, wl.D), generator=g, device=dev).to(torch.float16)
+    qd = q.quarot_hadamard(qd)
+    att_out = torch.empty_like(qd)
+    ws_bytes = q.quarot_kv_attention_workspace_size(nq, wl.S, wl.D)
+    att_ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+
+    def attend():
+        q.quarot_kv_decode_attention(qd, kcache, vcache, wl.S, group=wl.group, out=att_out,
+                                     workspace=att_ws)
+
+    attend()
+    torch.cuda.synchronize()
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record(stream)
+    for _ in range(10 * iters):
+        attend()
+    a1.record(stream)
+    torch.cuda.synchronize()
+    att_us = a0.elapsed_time(a1) / (10 * iters) * 1e3
+    att_bytes = 2 * (rows * wl.D // 2 + rows * (wl.D // wl.group) * 4)  # K and V caches
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(iters)]
     log(f"timing kv x{iters}")
     for it in range(iters):
@@ -119,7 +146,12 @@ def bench_kv(q, workloads, torch, np, dev, stream, iters):
            "quant_us": round(q_us, 1), "quant_GBps": round(q_gbs, 1),
            "quant_frac_hbm": round(q_gbs / PEAK_HBM_GBS, 4),
            "dequant_us": round(d_us, 1), "dequant_GBps": round(d_gbs, 1),
-           "dequant_frac_hbm": round(d_gbs / PEAK_HBM_GBS, 4)}
+           "dequant_frac_hbm": round(d_gbs / PEAK_HBM_GBS, 4),
+           "decode_attention": {
+               "what": f"one rotated fp16 query per (batch, head) over {wl.S} cached tokens",
+               "us": round(att_us, 1), "cache_bytes": att_bytes,
+               "GBps": round(att_bytes / (att_us * 1e-6) / 1e9, 1),
+               "frac_hbm": round(att_bytes / (att_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}}
     for t in tens:
         del t
     tens.clear()

@@ -229,6 +229,54 @@ quarot_status quarot_kv_dequant(const uint8_t *q, const quarot_f16 *scale,
                                 int64_t head_dim, int64_t group, int inverse_rotate,
                                 void *stream);
 
+/*
+ * Append (App. A.10, decode step): quantize the new tokens' head vectors
+ * exactly as quarot_kv_quant does and store them at token position pos of
+ * caches laid out [rows, s_max, ...]:
+ *   kv_new fp16 [rows, head_dim]        (rows = batch * kv heads)
+ *   q_cache uint8 [rows, s_max, head_dim/2]
+ *   scale_cache, zero_cache fp16 [rows, s_max, head_dim/group]
+ * Only position pos of each row is written.  0 <= pos < s_max; other size
+ * rules as quarot_kv_quant.
+ */
+quarot_status quarot_kv_append(const quarot_f16 *kv_new, uint8_t *q_cache,
+                               quarot_f16 *scale_cache, quarot_f16 *zero_cache, int64_t rows,
+                               int64_t s_max, int64_t pos, int64_t head_dim, int64_t group,
+                               int rotate, float clip_ratio, void *stream);
+
+/*
+ * Bytes of device workspace quarot_kv_decode_attention needs for nq query
+ * rows over seq_len tokens (0 when the sequence is not split).  Host-only.
+ */
+size_t quarot_kv_attention_workspace_size(int64_t nq, int64_t seq_len, int64_t head_dim);
+
+/*
+ * Decode attention over the 4-bit KV cache (§4 Stage 2c: fp16 queries,
+ * the cache dequantized on the fly; App. A.10 "Decode").  The keys and
+ * values are in the rotated basis and the queries are rotated alike (by
+ * quarot_hadamard with n = head_dim), so q . khat is the attention score.
+ *   q fp16 [nq, head_dim]; query row i reads cache row i / (nq / nkv)
+ *   k_codes, v_codes uint8 [nkv, s_max, head_dim/2]
+ *   k_scale, k_zero, v_scale, v_zero fp16 [nkv, s_max, head_dim/group]
+ *   out fp16 [nq, head_dim]
+ * With khat = code * scale + zero (per group) and tokens t < seq_len:
+ *   out = RN16(softmax_t(sm_scale * q . khat_t) . vhat), computed with
+ *   binary32 accumulation and a running-max softmax (a floating-point
+ *   result: it agrees with the exact value to a stated tolerance, not bit
+ *   for bit).
+ * head_dim 64, 128 or 256; group a power of two with 32 <= group <=
+ * head_dim; nq a multiple of nkv; 1 <= seq_len <= s_max; workspace of at
+ * least quarot_kv_attention_workspace_size bytes (may be NULL when that
+ * is 0), 16-byte aligned.
+ */
+quarot_status quarot_kv_decode_attention(const quarot_f16 *q, const uint8_t *k_codes,
+                                         const quarot_f16 *k_scale, const quarot_f16 *k_zero,
+                                         const uint8_t *v_codes, const quarot_f16 *v_scale,
+                                         const quarot_f16 *v_zero, quarot_f16 *out, int64_t nq,
+                                         int64_t nkv, int64_t s_max, int64_t seq_len,
+                                         int64_t head_dim, int64_t group, float sm_scale,
+                                         void *workspace, size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

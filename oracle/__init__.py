@@ -63,6 +63,9 @@ _SIGS = {
     "orc_swiglu_quant_int4": (_I, [_P, _P, _P, _P, _I64, _I64, _I, _F]),
     "orc_heads_f16": (_I, [_P, _P, _I64, _I64, _I64]),
     "orc_heads_quant_int4": (_I, [_P, _P, _P, _I64, _I64, _I64, _F]),
+    "orc_kv_append": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I64, _I64, _I, _F]),
+    "orc_kv_attention": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _I64,
+                              _I64, _F]),
     "orc_set_threads": (None, [_I]),
     "orc_max_threads": (_I, []),
 }
@@ -265,6 +268,40 @@ def kv_dequant(q: np.ndarray, scale: np.ndarray, zero: np.ndarray, group: int = 
     out = np.empty((rows, D), np.uint16)
     _check(lib().orc_kv_dequant(_ptr(q), _ptr(_u16(scale)), _ptr(_u16(zero)), _ptr(out),
                                 rows, D, group, int(inverse_rotate)), "kv_dequant")
+    return out.view(np.float16)
+
+
+def kv_append(kv_new: np.ndarray, q_cache: np.ndarray, scale_cache: np.ndarray,
+              zero_cache: np.ndarray, pos: int, group: int = 128, rotate: bool = True,
+              clip: float = 0.95):
+    """Quantize kv_new [rows, D] into caches [rows, s_max, ...] at token pos
+    (in place on copies, which are returned)."""
+    kv_new = _f16(kv_new)
+    rows, D = kv_new.shape
+    qc = np.ascontiguousarray(q_cache, dtype=np.uint8).copy()
+    sc = _f16(scale_cache).copy()
+    zc = _f16(zero_cache).copy()
+    s_max = qc.shape[1]
+    _check(lib().orc_kv_append(_ptr(_u16(kv_new)), _ptr(qc), _ptr(_u16(sc)), _ptr(_u16(zc)),
+                               rows, s_max, pos, D, group, int(rotate), clip), "kv_append")
+    return qc, sc, zc
+
+
+def kv_attention(q: np.ndarray, k: tuple, v: tuple, seq_len: int, group: int = 128,
+                 sm_scale: float = None) -> np.ndarray:
+    """Decode attention of q [nq, D] over 4-bit caches k = (codes [nkv, s_max,
+    D/2], scale, zero [nkv, s_max, D/group]) and v alike; fp64 inside."""
+    q = _f16(q)
+    nq, D = q.shape
+    kc, ks, kz = (np.ascontiguousarray(k[0], dtype=np.uint8), _f16(k[1]), _f16(k[2]))
+    vc, vs, vz = (np.ascontiguousarray(v[0], dtype=np.uint8), _f16(v[1]), _f16(v[2]))
+    nkv, s_max = kc.shape[0], kc.shape[1]
+    if sm_scale is None:
+        sm_scale = 1.0 / np.sqrt(D)
+    out = np.empty((nq, D), np.uint16)
+    _check(lib().orc_kv_attention(_ptr(_u16(q)), _ptr(kc), _ptr(_u16(ks)), _ptr(_u16(kz)),
+                                  _ptr(vc), _ptr(_u16(vs)), _ptr(_u16(vz)), _ptr(out), nq, nkv,
+                                  s_max, seq_len, D, group, float(sm_scale)), "kv_attention")
     return out.view(np.float16)
 
 

@@ -853,6 +853,100 @@ int orc_kv_dequant(const uint8_t *q, const uint16_t *scale, const uint16_t *zero
     return err ? ORC_ERR_NOMEM : ORC_OK;
 }
 
+/* Append (App. A.10, decode): quantize rows new tokens' head vectors and
+ * store them at token position pos of a cache laid out [rows, s_max, ...]. */
+int orc_kv_append(const uint16_t *kv, uint8_t *qc, uint16_t *sc, uint16_t *zc, int64_t rows,
+                  int64_t s_max, int64_t pos, int64_t D, int64_t G, int rotate, float clip)
+{
+    if (rows < 0 || s_max <= 0 || pos < 0 || pos >= s_max)
+        return ORC_ERR_ARG;
+    uint8_t *q = (uint8_t *)malloc((size_t)(rows * D / 2) + 1);
+    uint16_t *s = (uint16_t *)malloc((size_t)(rows * (D / G)) * 2 + 2);
+    uint16_t *z = (uint16_t *)malloc((size_t)(rows * (D / G)) * 2 + 2);
+    int st = ORC_ERR_NOMEM;
+    if (q && s && z) {
+        st = orc_kv_quant(kv, q, s, z, rows, D, G, rotate, clip);
+        if (st == ORC_OK)
+            for (int64_t r = 0; r < rows; r++) {
+                memcpy(qc + (r * s_max + pos) * (D / 2), q + r * (D / 2), (size_t)(D / 2));
+                memcpy(sc + (r * s_max + pos) * (D / G), s + r * (D / G), (size_t)(D / G) * 2);
+                memcpy(zc + (r * s_max + pos) * (D / G), z + r * (D / G), (size_t)(D / G) * 2);
+            }
+    }
+    free(q);
+    free(s);
+    free(z);
+    return st;
+}
+
+/* Decode attention over the 4-bit cache (§4 Stage 2c, App. A.10): for query
+ * row i (its cache row is i / (nq / nkv)), with the dequantized cache
+ * khat[t][d] = code * scale + zero of the group of d (the rotated basis; the
+ * queries are rotated alike, so q . khat is the attention score):
+ *   score_t = sm_scale * sum_d q[d] khat[t][d],   t < seq_len
+ *   p = softmax(score),  out[d] = RN16(sum_t p_t vhat[t][d]).
+ * Everything is evaluated in fp64 (exact dequantization, plain softmax with
+ * the maximum subtracted). */
+int orc_kv_attention(const uint16_t *q, const uint8_t *kc, const uint16_t *ks,
+                     const uint16_t *kz, const uint8_t *vc, const uint16_t *vs,
+                     const uint16_t *vz, uint16_t *out, int64_t nq, int64_t nkv, int64_t s_max,
+                     int64_t seq_len, int64_t D, int64_t G, float sm_scale)
+{
+    if (nq < 0 || nkv <= 0 || (nq % nkv) || s_max <= 0 || seq_len <= 0 || seq_len > s_max ||
+        D <= 0 || (D & 1) || G <= 0 || D % G)
+        return ORC_ERR_ARG;
+    const int64_t rep = nq / nkv, ng = D / G;
+    int err = 0;
+#pragma omp parallel for schedule(static) reduction(| : err)
+    for (int64_t i = 0; i < nq; i++) {
+        const int64_t kv = i / rep;
+        double *sc = (double *)malloc((size_t)seq_len * sizeof(double));
+        double *o = (double *)malloc((size_t)D * sizeof(double));
+        if (!sc || !o) {
+            free(sc);
+            free(o);
+            err |= 1;
+            continue;
+        }
+        double mx = -INFINITY;
+        for (int64_t t = 0; t < seq_len; t++) {
+            const int64_t row = kv * s_max + t;
+            double acc = 0.0;
+            for (int64_t d = 0; d < D; d++) {
+                int c = (kc[row * (D / 2) + d / 2] >> ((d & 1) * 4)) & 0xF;
+                double kh = (double)c * orc_f16_to_f32(ks[row * ng + d / G]) +
+                            orc_f16_to_f32(kz[row * ng + d / G]);
+                acc += (double)orc_f16_to_f32(q[i * D + d]) * kh;
+            }
+            sc[t] = acc * (double)sm_scale;
+            if (sc[t] > mx)
+                mx = sc[t];
+        }
+        double l = 0.0;
+        for (int64_t t = 0; t < seq_len; t++) {
+            sc[t] = exp(sc[t] - mx);
+            l += sc[t];
+        }
+        for (int64_t d = 0; d < D; d++)
+            o[d] = 0.0;
+        for (int64_t t = 0; t < seq_len; t++) {
+            const int64_t row = kv * s_max + t;
+            const double p = sc[t] / l;
+            for (int64_t d = 0; d < D; d++) {
+                int c = (vc[row * (D / 2) + d / 2] >> ((d & 1) * 4)) & 0xF;
+                double vh = (double)c * orc_f16_to_f32(vs[row * ng + d / G]) +
+                            orc_f16_to_f32(vz[row * ng + d / G]);
+                o[d] += p * vh;
+            }
+        }
+        for (int64_t d = 0; d < D; d++)
+            out[i * D + d] = orc_f32_to_f16((float)o[d]);
+        free(sc);
+        free(o);
+    }
+    return err ? ORC_ERR_NOMEM : ORC_OK;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Threads (for timing the oracle as a CPU baseline).                       */
 /* ------------------------------------------------------------------------ */

@@ -54,6 +54,10 @@ SIGNATURES = {
     "quarot_hadamard_heads_quant_int4": (_I, [_P, _P, _P, _I64, _I64, _I64, _F, _P]),
     "quarot_kv_quant": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P]),
     "quarot_kv_dequant": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _P]),
+    "quarot_kv_append": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I64, _I64, _I, _F, _P]),
+    "quarot_kv_attention_workspace_size": (ctypes.c_size_t, [_I64, _I64, _I64]),
+    "quarot_kv_decode_attention": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64,
+                                        _I64, _I64, _F, _P, ctypes.c_size_t, _P]),
 }
 
 _lib = None
@@ -314,10 +318,60 @@ def quarot_kv_dequant(q: torch.Tensor, scale: torch.Tensor, zero: torch.Tensor,
     return out
 
 
+def quarot_kv_append(kv_new: torch.Tensor, q_cache: torch.Tensor, scale_cache: torch.Tensor,
+                     zero_cache: torch.Tensor, pos: int, group: int = 128, rotate: bool = True,
+                     clip_ratio: float = 0.95, stream: Optional[torch.cuda.Stream] = None):
+    """Quantize kv_new [rows, D] into token position pos of the caches
+    q_cache [rows, s_max, D/2], scale/zero_cache [rows, s_max, D/group]."""
+    D = kv_new.shape[-1]
+    rows = _rows(kv_new, D)
+    s_max = q_cache.shape[-2]
+    _check("quarot_kv_append", lib().quarot_kv_append(
+        _ptr(kv_new, torch.float16, "kv_new"), _ptr(q_cache, torch.uint8, "q_cache"),
+        _ptr(scale_cache, torch.float16, "scale_cache"),
+        _ptr(zero_cache, torch.float16, "zero_cache"), rows, s_max, pos, D, group,
+        int(bool(rotate)), float(clip_ratio), _stream(stream)))
+
+
+def quarot_kv_attention_workspace_size(nq: int, seq_len: int, head_dim: int) -> int:
+    return int(lib().quarot_kv_attention_workspace_size(nq, seq_len, head_dim))
+
+
+def quarot_kv_decode_attention(q: torch.Tensor, k_cache, v_cache, seq_len: int,
+                               group: int = 128, sm_scale: Optional[float] = None,
+                               out: Optional[torch.Tensor] = None,
+                               workspace: Optional[torch.Tensor] = None,
+                               stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """Decode attention of rotated queries q [nq, D] over 4-bit caches
+    k_cache = (codes [nkv, s_max, D/2], scale, zero [nkv, s_max, D/group]),
+    v_cache alike.  Returns fp16 [nq, D]."""
+    nq, D = q.shape
+    kc, ks, kz = k_cache
+    vc, vs, vz = v_cache
+    nkv, s_max = kc.shape[0], kc.shape[1]
+    if sm_scale is None:
+        sm_scale = D ** -0.5
+    if out is None:
+        out = torch.empty((nq, D), dtype=torch.float16, device=q.device)
+    need = quarot_kv_attention_workspace_size(nq, seq_len, D)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    _check("quarot_kv_decode_attention", lib().quarot_kv_decode_attention(
+        _ptr(q, torch.float16, "q"), _ptr(kc, torch.uint8, "k_codes"),
+        _ptr(ks, torch.float16, "k_scale"), _ptr(kz, torch.float16, "k_zero"),
+        _ptr(vc, torch.uint8, "v_codes"), _ptr(vs, torch.float16, "v_scale"),
+        _ptr(vz, torch.float16, "v_zero"), _ptr(out, torch.float16, "out"), nq, nkv, s_max,
+        seq_len, D, group, float(sm_scale),
+        _ptr(workspace, torch.uint8, "workspace") if workspace is not None else None,
+        workspace.numel() if workspace is not None else 0, _stream(stream)))
+    return out
+
+
 __all__ = [
     "QuarotError", "lib", "quarot_version", "quarot_hadamard_factor",
     "quarot_hadamard_factor_table", "quarot_linear_workspace_size", "quarot_hadamard",
     "quarot_quant_int4", "quarot_w4a4_gemm", "quarot_linear", "prepare_weight",
     "quarot_swiglu", "quarot_swiglu_quant_int4", "quarot_hadamard_heads", "quarot_hadamard_heads_quant_int4",
-    "quarot_kv_quant", "quarot_kv_dequant",
+    "quarot_kv_quant", "quarot_kv_dequant", "quarot_kv_append",
+    "quarot_kv_attention_workspace_size", "quarot_kv_decode_attention",
 ]

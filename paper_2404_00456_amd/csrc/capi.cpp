@@ -453,7 +453,110 @@ quarot_status quarot_kv_quant(const quarot_f16 *kv, uint8_t *q, quarot_f16 *scal
     a.group = (int)group;
     a.c = rotation_scale(head_dim);
     a.clip = clip_ratio;
+    a.ostride = 1;
     hipError_t e = launch_rotate(a, EPI_KV, rotate != 0, k, m, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+quarot_status quarot_kv_append(const quarot_f16 *kv_new, uint8_t *q_cache,
+                               quarot_f16 *scale_cache, quarot_f16 *zero_cache, int64_t rows,
+                               int64_t s_max, int64_t pos, int64_t head_dim, int64_t group,
+                               int rotate, float clip_ratio, void *stream)
+{
+    if (rows < 0 || s_max <= 0 || pos < 0 || pos >= s_max || !clip_ok(clip_ratio) ||
+        head_dim <= 0 || group <= 0)
+        return QUAROT_ERR_INVALID_ARG;
+    if (head_dim < 8 || head_dim > 512 || (head_dim & (head_dim - 1)) || group < 8 ||
+        group > head_dim || (group & (group - 1)))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    int k, m;
+    quarot_status st = check_rot_size(head_dim, rotate != 0, EPI_KV, &k, &m);
+    if (st)
+        return st;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!kv_new || !q_cache || !scale_cache || !zero_cache)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(kv_new) || !aligned16(q_cache) || !aligned16(scale_cache) ||
+        !aligned16(zero_cache))
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    RotArgs a{};
+    a.x = kv_new;
+    a.out = q_cache;
+    a.scale = scale_cache;
+    a.zero = zero_cache;
+    a.rows = rows;
+    a.n = (int)head_dim;
+    a.group = (int)group;
+    a.c = rotation_scale(head_dim);
+    a.clip = clip_ratio;
+    a.ostride = s_max;
+    a.ooff = pos;
+    hipError_t e = launch_rotate(a, EPI_KV, rotate != 0, k, m, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+size_t quarot_kv_attention_workspace_size(int64_t nq, int64_t seq_len, int64_t head_dim)
+{
+    if (nq <= 0 || seq_len <= 0 || head_dim <= 0)
+        return 0;
+    const int splits = kv_attn_splits(nq, seq_len);
+    return splits > 1 ? (size_t)nq * splits * (size_t)(head_dim + 2) * sizeof(float) : 0;
+}
+
+quarot_status quarot_kv_decode_attention(const quarot_f16 *q, const uint8_t *k_codes,
+                                         const quarot_f16 *k_scale, const quarot_f16 *k_zero,
+                                         const uint8_t *v_codes, const quarot_f16 *v_scale,
+                                         const quarot_f16 *v_zero, quarot_f16 *out, int64_t nq,
+                                         int64_t nkv, int64_t s_max, int64_t seq_len,
+                                         int64_t head_dim, int64_t group, float sm_scale,
+                                         void *workspace, size_t workspace_bytes, void *stream)
+{
+    if (nq < 0 || nkv <= 0 || s_max <= 0 || seq_len <= 0 || seq_len > s_max ||
+        head_dim <= 0 || group <= 0 || !(sm_scale > 0.0f) || !std::isfinite(sm_scale))
+        return QUAROT_ERR_INVALID_ARG;
+    if (nq % nkv)
+        return QUAROT_ERR_INVALID_ARG;
+    if ((head_dim != 64 && head_dim != 128 && head_dim != 256) || group < 32 ||
+        group > head_dim || (group & (group - 1)) || s_max > 0x7FFFFFFF || nq > 0x7FFFFFFF)
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (nq == 0)
+        return QUAROT_OK;
+    if (!q || !k_codes || !k_scale || !k_zero || !v_codes || !v_scale || !v_zero || !out)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k_codes) || !aligned16(k_scale) || !aligned16(k_zero) ||
+        !aligned16(v_codes) || !aligned16(v_scale) || !aligned16(v_zero) || !aligned16(out))
+        return QUAROT_ERR_ALIGNMENT;
+    const size_t need = quarot_kv_attention_workspace_size(nq, seq_len, head_dim);
+    if (need && (!workspace || workspace_bytes < need))
+        return QUAROT_ERR_WORKSPACE;
+    if (need && !aligned16(workspace))
+        return QUAROT_ERR_ALIGNMENT;
+    quarot_status st = check_device();
+    if (st)
+        return st;
+    KvAttnArgs a{};
+    a.q = q;
+    a.kc = k_codes;
+    a.ks = k_scale;
+    a.kz = k_zero;
+    a.vc = v_codes;
+    a.vs = v_scale;
+    a.vz = v_zero;
+    a.out = out;
+    a.part = static_cast<float *>(workspace);
+    a.nq = nq;
+    a.s_max = s_max;
+    a.rep = (int)(nq / nkv);
+    a.seq_len = (int)seq_len;
+    a.D = (int)head_dim;
+    a.G = (int)group;
+    a.splits = kv_attn_splits(nq, seq_len);
+    a.chunk = (int)(((seq_len + a.splits - 1) / a.splits + 63) / 64 * 64);
+    a.sm_scale = sm_scale;
+    hipError_t e = launch_kv_attention(a, (hipStream_t)stream);
     return e == hipSuccess ? QUAROT_OK : hip_fail(e);
 }
 

@@ -34,7 +34,31 @@ struct RotArgs {
     int s0;              // first butterfly bit (0; log2(head_dim) across heads)
     float c;             // RN32(1/sqrt(n)), or RN32(1/sqrt(heads)) across heads
     float clip;
+    int64_t ostride;     // EPI_KV: output row of input row r is r * ostride + ooff
+    int64_t ooff;
 };
+
+struct KvAttnArgs {
+    const uint16_t *q;  // [nq, D] rotated queries
+    const uint8_t *kc;  // [nkv, s_max, D/2] codes
+    const uint16_t *ks, *kz;  // [nkv, s_max, D/G]
+    const uint8_t *vc;
+    const uint16_t *vs, *vz;
+    uint16_t *out;      // [nq, D]
+    float *part;        // [nq, splits, D + 2] partial (max, sum, o) when splits > 1
+    int64_t nq;
+    int64_t s_max;
+    int rep;            // query rows per cache row
+    int seq_len;
+    int D, G;
+    int splits, chunk;  // sequence split: tokens [s * chunk, (s + 1) * chunk)
+    float sm_scale;
+};
+
+// Sequence splits of the decode attention for nq query rows (the workspace
+// holds nq * splits * (D + 2) floats when splits > 1).
+int kv_attn_splits(int64_t nq, int64_t seq_len);
+hipError_t launch_kv_attention(const KvAttnArgs &a, hipStream_t s);
 
 struct GemmArgs {
     const uint8_t *xq;

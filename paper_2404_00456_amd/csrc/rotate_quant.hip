@@ -355,10 +355,11 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
 #pragma unroll
         for (int e = 0; e < 8; ++e)
             pk |= asym_code(v[0][e], dv, zf) << (4 * e);
-        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (N / 2);
+        const int64_t orow = row * a.ostride + a.ooff;  // Append: a cache position
+        uint8_t *qr = static_cast<uint8_t *>(a.out) + orow * (N / 2);
         *reinterpret_cast<uint32_t *>(qr + pos * 4) = pk;
         if ((pos & (gl - 1)) == 0) {
-            const int64_t gi = row * (N / a.group) + pos / gl;
+            const int64_t gi = orow * (N / a.group) + pos / gl;
             a.scale[gi] = s16;
             a.zero[gi] = z16;
         }

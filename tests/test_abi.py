@@ -121,6 +121,27 @@ def test_invalid_arguments_rejected_before_device(L):
     assert L.quarot_kv_quant(P, P, P, None, 4, 128, 128, 1, 0.95, S) == INVALID
     assert L.quarot_kv_dequant(P, P, P, P, 4, 128, 0, 0, S) == INVALID
     assert L.quarot_kv_dequant(P, P, UNALIGNED, P, 4, 128, 128, 0, S) == ALIGN
+    # kv append / decode attention
+    assert L.quarot_kv_append(P, P, P, P, 4, 16, 16, 128, 128, 1, 0.95, S) == INVALID  # pos
+    assert L.quarot_kv_append(P, P, P, P, 4, 16, -1, 128, 128, 1, 0.95, S) == INVALID
+    assert L.quarot_kv_append(P, P, P, P, 4, 16, 3, 96, 32, 1, 0.95, S) == UNSUPPORTED
+    assert L.quarot_kv_append(P, None, P, P, 4, 16, 3, 128, 128, 1, 0.95, S) == INVALID
+    assert L.quarot_kv_append(None, None, None, None, 0, 16, 3, 128, 128, 1, 0.95, S) == OK
+    A = (P, P, P, P, P, P, P, P2)
+    assert L.quarot_kv_decode_attention(*A, 8, 3, 64, 64, 128, 128, 0.1, P, 1 << 20, S) == INVALID
+    assert L.quarot_kv_decode_attention(*A, 8, 8, 64, 65, 128, 128, 0.1, P, 1 << 20, S) == INVALID
+    assert L.quarot_kv_decode_attention(*A, 8, 8, 64, 0, 128, 128, 0.1, P, 1 << 20, S) == INVALID
+    assert L.quarot_kv_decode_attention(*A, 8, 8, 64, 64, 96, 32, 0.1, P, 1 << 20, S) == UNSUPPORTED
+    assert L.quarot_kv_decode_attention(*A, 8, 8, 64, 64, 128, 16, 0.1, P, 1 << 20, S) == UNSUPPORTED
+    assert L.quarot_kv_decode_attention(*A, 8, 8, 64, 64, 128, 128, 0.0, P, 1 << 20, S) == INVALID
+    assert L.quarot_kv_decode_attention(P, None, P, P, P, P, P, P2, 8, 8, 64, 64, 128, 128, 0.1,
+                                        P, 1 << 20, S) == INVALID
+    assert L.quarot_kv_decode_attention(*A, 0, 8, 64, 64, 128, 128, 0.1, None, 0, S) == OK
+    need = L.quarot_kv_attention_workspace_size(64, 4096, 128)
+    assert need == 64 * 16 * (128 + 2) * 4  # 16 chunks of 256 tokens per row
+    assert L.quarot_kv_decode_attention(*A, 64, 64, 4096, 4096, 128, 128, 0.1, P, need - 4,
+                                        S) == WORKSPACE
+    assert L.quarot_kv_attention_workspace_size(4096, 4096, 128) == 0  # one chunk per row
     # swiglu prologue
     assert L.quarot_swiglu(P, P2, P, 12, S) == UNSUPPORTED
     assert L.quarot_swiglu(P, P2, P, -8, S) == INVALID
