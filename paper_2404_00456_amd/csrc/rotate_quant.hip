@@ -207,9 +207,12 @@ __device__ __forceinline__ float row_absmax(float amax, int w, float *red)
 
 // ------------------------------------------------------------ m = 1 -----
 
-// Butterflies run over element bits >= a.s0 only (0: the whole
-// Walsh-Hadamard transform; log2(head_dim): across heads).
-template <int LOGL, int W, int C, int EPI, bool ROT, int PRO = PRO_PLAIN>
+// HEADS: the butterflies run over element bits >= a.s0 only (log2(head_dim):
+// across heads); otherwise over all bits (s0 = 0 at compile time, so that
+// no stage carries a branch).
+// KVROW (EPI_KV): the quantization group is the whole row.
+template <int LOGL, int W, int C, int EPI, bool ROT, int PRO = PRO_PLAIN, bool HEADS = false,
+          bool KVROW = false>
 __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
 {
     constexpr int L = 1 << LOGL;
@@ -238,7 +241,7 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
         load_row8<PRO>(a, row * N + ((cc * W + w) * L + pos) * 8, v[cc]);
 
     if constexpr (ROT) {
-        const int s0 = a.s0;
+        const int s0 = HEADS ? a.s0 : 0;
         // element bits 0..2: inside each chunk
 #pragma unroll
         for (int h = 1, bit = 0; h < 8; h <<= 1, ++bit)
@@ -329,39 +332,75 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
         }
         if (pos == 0 && w == 0)
             a.scale[row] = s16;
-    } else {  // EPI_KV: W == 1, C == 1, a group is G/8 consecutive positions
-        static_assert(W == 1 && C == 1, "KV rows fit one wave");
-        float mx = v[0][0], mn = v[0][0];
+    } else {  // EPI_KV: one wave per row; a group is G consecutive elements
+        static_assert(W == 1, "KV rows fit one wave");
+        // element i = (cc L + pos) 8 + e.  A group of G <= 8L elements is an
+        // aligned block of G/8 positions of one chunk (lane_pos maps aligned
+        // blocks of 2, 4, 8, 16 lanes onto themselves); a larger group takes
+        // all L positions of G/(8L) consecutive chunks.
+        const int gl = KVROW ? L * C : a.group >> 3;  // positions per group
+        float mx[C], mn[C];
 #pragma unroll
-        for (int e = 1; e < 8; ++e) {
-            mx = fmaxf(mx, v[0][e]);
-            mn = fminf(mn, v[0][e]);
-        }
-        // the lanes of one group are an aligned block of gl lanes (lane_pos
-        // maps aligned blocks of 2, 4, 8, 16 lanes onto themselves)
-        const int gl = a.group >> 3;  // lanes per group
-        static_for<LOGL>([&](auto J) {
-            if ((1 << J) < gl) {
-                mx = lane_max<J>(mx);
-                mn = lane_min<J>(mn);
+        for (int cc = 0; cc < C; ++cc) {
+            mx[cc] = v[cc][0];
+            mn[cc] = v[cc][0];
+#pragma unroll
+            for (int e = 1; e < 8; ++e) {
+                mx[cc] = fmaxf(mx[cc], v[cc][e]);
+                mn[cc] = fminf(mn[cc], v[cc][e]);
             }
-        });
-        const float mxc = mx * a.clip, mnc = mn * a.clip;
-        const float s32 = (mxc - mnc) / 15.0f;
-        const uint16_t s16 = f2h(s32), z16 = f2h(mnc);
-        const Divisor dv = make_divisor(h2f(s16));
-        const float zf = h2f(z16);
-        uint32_t pk = 0;
+        }
+        static_for<LOGL>([&](auto J) {
+            if ((1 << J) < gl)
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-            pk |= asym_code(v[0][e], dv, zf) << (4 * e);
+                for (int cc = 0; cc < C; ++cc) {
+                    mx[cc] = lane_max<J>(mx[cc]);
+                    mn[cc] = lane_min<J>(mn[cc]);
+                }
+        });
+#pragma unroll
+        for (int h = 1; h < C; h <<= 1)
+            if (h * L < gl) {
+                float tx[C], tn[C];
+#pragma unroll
+                for (int cc = 0; cc < C; ++cc) {
+                    tx[cc] = fmaxf(mx[cc], mx[cc ^ h]);
+                    tn[cc] = fminf(mn[cc], mn[cc ^ h]);
+                }
+#pragma unroll
+                for (int cc = 0; cc < C; ++cc) {
+                    mx[cc] = tx[cc];
+                    mn[cc] = tn[cc];
+                }
+            }
         const int64_t orow = row * a.ostride + a.ooff;  // Append: a cache position
         uint8_t *qr = static_cast<uint8_t *>(a.out) + orow * (N / 2);
-        *reinterpret_cast<uint32_t *>(qr + pos * 4) = pk;
-        if ((pos & (gl - 1)) == 0) {
-            const int64_t gi = orow * (N / a.group) + pos / gl;
-            a.scale[gi] = s16;
-            a.zero[gi] = z16;
+        uint16_t s16 = 0, z16 = 0;
+        Divisor dv{};
+        float zf = 0.0f;
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc) {
+            // the group's scale and zero, formed again only where a group
+            // starts (uniform across the wave)
+            if (cc == 0 || (!KVROW && (cc * L) % gl == 0)) {
+                const float mxc = mx[cc] * a.clip, mnc = mn[cc] * a.clip;
+                const float s32 = (mxc - mnc) / 15.0f;
+                s16 = f2h(s32);
+                z16 = f2h(mnc);
+                dv = make_divisor(h2f(s16));
+                zf = h2f(z16);
+            }
+            uint32_t pk = 0;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                pk |= asym_code(v[cc][e], dv, zf) << (4 * e);
+            const int p8 = (cc * L + pos) * 8;  // first element of this chunk
+            *reinterpret_cast<uint32_t *>(qr + p8 / 2) = pk;
+            if (KVROW ? p8 == 0 : p8 % a.group == 0) {
+                const int64_t gi = KVROW ? orow : orow * (N / a.group) + p8 / a.group;
+                a.scale[gi] = s16;
+                a.zero[gi] = z16;
+            }
         }
     }
 }
@@ -729,53 +768,75 @@ __global__ __launch_bounds__(256) void k_swiglu(const uint16_t *g, const uint16_
 
 // ------------------------------------------------------ KV dequant -------
 
-template <int LOGL, bool INV>
+template <int LOGL, int C, bool INV>
 __global__ __launch_bounds__(256) void k_kv_dequant(KvDeqArgs a)
 {
     constexpr int L = 1 << LOGL;
-    constexpr int RPW = 64 / L, RPB = 4 * RPW, N = 8 * L;
+    constexpr int RPW = 64 / L, RPB = 4 * RPW, N = 8 * L * C;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int pos = lane_pos(lane) & (L - 1);
     const int64_t row = (int64_t)blockIdx.x * RPB + wave * RPW + (lane >> LOGL);
     if (row >= a.rows)
         return;
-    const uint32_t pk = *reinterpret_cast<const uint32_t *>(a.q + row * (N / 2) + pos * 4);
-    const int64_t gi = row * (N / a.group) + (pos * 8) / a.group;
-    const float sf = h2f(a.scale[gi]), zf = h2f(a.zero[gi]);
-    float v[8];
+    float v[C][8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const float t = (float)((pk >> (4 * e)) & 0xFu) * sf;
-        v[e] = t + zf;
+    for (int cc = 0; cc < C; ++cc) {
+        const int p8 = (cc * L + pos) * 8;  // element index i = (cc L + pos) 8 + e
+        const uint32_t pk = *reinterpret_cast<const uint32_t *>(a.q + row * (N / 2) + p8 / 2);
+        const int64_t gi = row * (N / a.group) + p8 / a.group;
+        const float sf = h2f(a.scale[gi]), zf = h2f(a.zero[gi]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const float t = (float)((pk >> (4 * e)) & 0xFu) * sf;
+            v[cc][e] = t + zf;
+        }
     }
     if constexpr (INV) {
 #pragma unroll
         for (int h = 1; h < 8; h <<= 1)
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (!(e & h)) {
-                    float p = v[e], q = v[e + h];
-                    v[e] = p + q;
-                    v[e + h] = p - q;
-                }
-        const float sc = lane_stages<LOGL, 8>(v, lane, pos) * a.c;
+            for (int cc = 0; cc < C; ++cc)
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-            v[e] = __builtin_fmaf(v[e], sc, 0.0f);  // zeros +0, as in k_rot_pow2
+                for (int e = 0; e < 8; ++e)
+                    if (!(e & h)) {
+                        float p = v[cc][e], q = v[cc][e + h];
+                        v[cc][e] = p + q;
+                        v[cc][e + h] = p - q;
+                    }
+        const float sc = lane_stages<LOGL, 8 * C>(&v[0][0], lane, pos) * a.c;
+#pragma unroll
+        for (int h = 1; h < C; h <<= 1)
+#pragma unroll
+            for (int cc = 0; cc < C; ++cc)
+                if (!(cc & h)) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        float p = v[cc][e], q = v[cc + h][e];
+                        v[cc][e] = p + q;
+                        v[cc + h][e] = p - q;
+                    }
+                }
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc)
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                v[cc][e] = __builtin_fmaf(v[cc][e], sc, 0.0f);  // zeros +0, as in k_rot_pow2
     }
-    store8(a.out + row * N + pos * 8, v);
+#pragma unroll
+    for (int cc = 0; cc < C; ++cc)
+        store8(a.out + row * N + (cc * L + pos) * 8, v[cc]);
 }
 
 // ---------------------------------------------------------- dispatch -----
 
-template <int LOGL, int W, int C, int EPI, bool ROT, int PRO>
+template <int LOGL, int W, int C, int EPI, bool ROT, int PRO, bool HEADS, bool KVROW>
 hipError_t go_pow2(const RotArgs &a, hipStream_t s)
 {
     constexpr int L = 1 << LOGL;
     constexpr int RPB = (W == 1) ? 4 * (64 / L) : 1;
     const int64_t blocks = (a.rows + RPB - 1) / RPB;
-    hipLaunchKernelGGL((k_rot_pow2<LOGL, W, C, EPI, ROT, PRO>), dim3((unsigned)blocks),
-                       dim3(W == 1 ? 256 : 64 * W), 0, s, a);
+    hipLaunchKernelGGL((k_rot_pow2<LOGL, W, C, EPI, ROT, PRO, HEADS, KVROW>),
+                       dim3((unsigned)blocks), dim3(W == 1 ? 256 : 64 * W), 0, s, a);
     return hipGetLastError();
 }
 
@@ -799,26 +860,27 @@ hipError_t go_largem(const RotArgs &a, hipStream_t s)
     return hipGetLastError();
 }
 
-template <int EPI, bool ROT, int PRO>
+template <int EPI, bool ROT, int PRO, bool HEADS = false, bool KVROW = false>
 hipError_t dispatch_pow2(const RotArgs &a, int k, hipStream_t s)
 {
+    // short rows: up to 4 chunks (32 elements) per lane, D / 32 lanes per row
     switch (k) {
-    case 3: return go_pow2<0, 1, 1, EPI, ROT, PRO>(a, s);
-    case 4: return go_pow2<1, 1, 1, EPI, ROT, PRO>(a, s);
-    case 5: return go_pow2<2, 1, 1, EPI, ROT, PRO>(a, s);
-    case 6: return go_pow2<3, 1, 1, EPI, ROT, PRO>(a, s);
-    case 7: return go_pow2<4, 1, 1, EPI, ROT, PRO>(a, s);
-    case 8: return go_pow2<5, 1, 1, EPI, ROT, PRO>(a, s);
-    case 9: return go_pow2<6, 1, 1, EPI, ROT, PRO>(a, s);
+    case 3: return go_pow2<0, 1, 1, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+    case 4: return go_pow2<0, 1, 2, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+    case 5: return go_pow2<0, 1, 4, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+    case 6: return go_pow2<1, 1, 4, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+    case 7: return go_pow2<2, 1, 4, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+    case 8: return go_pow2<3, 1, 4, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+    case 9: return go_pow2<4, 1, 4, EPI, ROT, PRO, HEADS, KVROW>(a, s);
     }
     if constexpr (EPI != EPI_KV) {
         switch (k) {
-        case 10: return go_pow2<6, 1, 2, EPI, ROT, PRO>(a, s);
-        case 11: return go_pow2<6, 1, 4, EPI, ROT, PRO>(a, s);
-        case 12: return go_pow2<6, 1, 8, EPI, ROT, PRO>(a, s);
-        case 13: return go_pow2<6, 4, 4, EPI, ROT, PRO>(a, s);
-        case 14: return go_pow2<6, 4, 8, EPI, ROT, PRO>(a, s);
-        case 15: return go_pow2<6, 8, 8, EPI, ROT, PRO>(a, s);
+        case 10: return go_pow2<6, 1, 2, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+        case 11: return go_pow2<6, 1, 4, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+        case 12: return go_pow2<6, 1, 8, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+        case 13: return go_pow2<6, 4, 4, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+        case 14: return go_pow2<6, 4, 8, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+        case 15: return go_pow2<6, 8, 8, EPI, ROT, PRO, HEADS, KVROW>(a, s);
         }
     }
     return hipErrorInvalidValue;
@@ -862,15 +924,17 @@ hipError_t dispatch_rotated(const RotArgs &a, int k, int m, hipStream_t s)
     return hipErrorInvalidValue;
 }
 
-template <int LOGL>
+template <int LOGL, int C>
 hipError_t go_kvdeq(const KvDeqArgs &a, bool inv, hipStream_t s)
 {
     constexpr int RPB = 4 * (64 >> LOGL);
     const int64_t blocks = (a.rows + RPB - 1) / RPB;
     if (inv)
-        hipLaunchKernelGGL((k_kv_dequant<LOGL, true>), dim3((unsigned)blocks), dim3(256), 0, s, a);
+        hipLaunchKernelGGL((k_kv_dequant<LOGL, C, true>), dim3((unsigned)blocks), dim3(256), 0, s,
+                           a);
     else
-        hipLaunchKernelGGL((k_kv_dequant<LOGL, false>), dim3((unsigned)blocks), dim3(256), 0, s, a);
+        hipLaunchKernelGGL((k_kv_dequant<LOGL, C, false>), dim3((unsigned)blocks), dim3(256), 0,
+                           s, a);
     return hipGetLastError();
 }
 
@@ -911,13 +975,25 @@ hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, h
             return hipGetLastError();
         }
         if (epi == EPI_KV)
-            return dispatch_pow2<EPI_KV, false, PRO_PLAIN>(a, k, s);
+            return a.group == a.n ? dispatch_pow2<EPI_KV, false, PRO_PLAIN, false, true>(a, k, s)
+                                  : dispatch_pow2<EPI_KV, false, PRO_PLAIN>(a, k, s);
+        return hipErrorInvalidValue;
+    }
+    if (a.s0 > 0) {  // across heads: n a power of two
+        if (m != 1)
+            return hipErrorInvalidValue;
+        if (epi == EPI_F16)
+            return dispatch_pow2<EPI_F16, true, PRO_PLAIN, true>(a, k, s);
+        if (epi == EPI_SYM)
+            return dispatch_pow2<EPI_SYM, true, PRO_PLAIN, true>(a, k, s);
         return hipErrorInvalidValue;
     }
     switch (epi) {
     case EPI_F16: return dispatch_rotated<EPI_F16, PRO_PLAIN>(a, k, m, s);
     case EPI_SYM: return dispatch_rotated<EPI_SYM, PRO_PLAIN>(a, k, m, s);
-    case EPI_KV: return dispatch_pow2<EPI_KV, true, PRO_PLAIN>(a, k, s);
+    case EPI_KV:
+        return a.group == a.n ? dispatch_pow2<EPI_KV, true, PRO_PLAIN, false, true>(a, k, s)
+                              : dispatch_pow2<EPI_KV, true, PRO_PLAIN>(a, k, s);
     }
     return hipErrorInvalidValue;
 }
@@ -937,14 +1013,16 @@ hipError_t launch_kv_dequant(const KvDeqArgs &a, bool inverse_rotate, hipStream_
 {
     if (a.rows == 0)
         return hipSuccess;
+    // two chunks (16 elements) per lane: each store instruction then writes
+    // 128 contiguous bytes of a row (measured faster than 1 or 4 chunks)
     switch (a.n) {
-    case 8: return go_kvdeq<0>(a, inverse_rotate, s);
-    case 16: return go_kvdeq<1>(a, inverse_rotate, s);
-    case 32: return go_kvdeq<2>(a, inverse_rotate, s);
-    case 64: return go_kvdeq<3>(a, inverse_rotate, s);
-    case 128: return go_kvdeq<4>(a, inverse_rotate, s);
-    case 256: return go_kvdeq<5>(a, inverse_rotate, s);
-    case 512: return go_kvdeq<6>(a, inverse_rotate, s);
+    case 8: return go_kvdeq<0, 1>(a, inverse_rotate, s);
+    case 16: return go_kvdeq<0, 2>(a, inverse_rotate, s);
+    case 32: return go_kvdeq<1, 2>(a, inverse_rotate, s);
+    case 64: return go_kvdeq<2, 2>(a, inverse_rotate, s);
+    case 128: return go_kvdeq<3, 2>(a, inverse_rotate, s);
+    case 256: return go_kvdeq<4, 2>(a, inverse_rotate, s);
+    case 512: return go_kvdeq<5, 2>(a, inverse_rotate, s);
     }
     return hipErrorInvalidValue;
 }
