@@ -148,6 +148,45 @@ quarot_status quarot_linear(const quarot_f16 *x, const uint8_t *wq, const quarot
                             void *stream);
 
 /*
+ * 6- and 8-bit variants of the same scheme (§5.3 round-to-nearest ablation,
+ * App. A.6: per-token / per-channel symmetric quantization at more bits),
+ * one code per byte:
+ *   qmax = 2^(bits-1) - 1 (31 or 127), s = RN16(RN(RN(absmax * clip) / qmax)),
+ *   q = clamp(rint_even(RN(y / s)), -qmax - 1, qmax) as int8.
+ *   x fp16 [rows, n]; q int8 [rows, n]; scale fp16 [rows]; bits 6 or 8.
+ * rotate != 0 needs n supported by quarot_hadamard_factor; rotate == 0 needs
+ * n a positive multiple of 8.  Used offline for the weights as well.
+ */
+quarot_status quarot_quant_int8(const quarot_f16 *x, int8_t *q, quarot_f16 *scale, int64_t rows,
+                                int64_t n, int rotate, float clip_ratio, int bits, void *stream);
+
+/*
+ * W8A8 GEMM with fused dequant (6- or 8-bit codes, one per byte):
+ *   xq int8 [M, K], sx fp16 [M]; wq int8 [N, K], sw fp16 [N];
+ *   y fp16 [M, N] = RN16(RN(RN(float(acc) * sx[m]) * sw[n])), acc exact int32;
+ *   acc_out int32 [M, N] or NULL.
+ * M, N >= 0; K a positive multiple of 64, at most 65536.
+ */
+quarot_status quarot_w8a8_gemm(const int8_t *xq, const quarot_f16 *sx, const int8_t *wq,
+                               const quarot_f16 *sw, quarot_f16 *y, int32_t *acc_out,
+                               int64_t M, int64_t N, int64_t K, void *stream);
+
+/* Workspace of quarot_linear_w8a8: M*K code bytes and 2*M scale bytes, each
+ * rounded up to 256 bytes (0 for invalid sizes).  Host-only. */
+size_t quarot_linear_w8a8_workspace_size(int64_t M, int64_t K);
+
+/*
+ * The 6/8-bit linear layer: quarot_quant_int8(x, rotate, clip_ratio, bits)
+ * into the workspace, then quarot_w8a8_gemm into y (two launches).  The
+ * weights wq, sw come from quarot_quant_int8 of W [N, K] with the same
+ * rotate and bits.  Size and alignment rules of both calls apply.
+ */
+quarot_status quarot_linear_w8a8(const quarot_f16 *x, const int8_t *wq, const quarot_f16 *sw,
+                                 quarot_f16 *y, int64_t M, int64_t N, int64_t K, int rotate,
+                                 float clip_ratio, int bits, void *workspace,
+                                 size_t workspace_bytes, void *stream);
+
+/*
  * The elementwise SwiGLU product alone: h = RN16(RN(silu(gate) * up)) with
  * the binary32 silu recipe of quarot_swiglu_quant_int4 below.
  * gate, up, h fp16 [count]; count a multiple of 8 (0 is a no-op).

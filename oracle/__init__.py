@@ -66,6 +66,9 @@ _SIGS = {
     "orc_kv_append": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I64, _I64, _I, _F]),
     "orc_kv_attention": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _I64,
                               _I64, _F]),
+    "orc_quant_sym8_f32": (_I, [_P, _P, _P, _I64, _I64, _F, _I]),
+    "orc_quant_int8": (_I, [_P, _P, _P, _I64, _I64, _I, _F, _I]),
+    "orc_gemm_i8": (_I, [_P, _P, _P, _I64, _I64, _I64]),
     "orc_set_threads": (None, [_I]),
     "orc_max_threads": (_I, []),
 }
@@ -197,6 +200,39 @@ def quant_int4(x: np.ndarray, rotate: bool = True, clip: float = 1.0):
     _check(lib().orc_quant_int4(_ptr(_u16(x)), _ptr(q), _ptr(s), rows, n,
                                 int(rotate), clip), "quant_int4")
     return q, s.view(np.float16)
+
+
+def quant_sym8_f32(y: np.ndarray, clip: float = 1.0, bits: int = 8):
+    y = np.ascontiguousarray(y, dtype=np.float32)
+    rows, n = y.shape
+    q = np.empty((rows, n), np.int8)
+    s = np.empty(rows, np.uint16)
+    _check(lib().orc_quant_sym8_f32(_ptr(y), _ptr(q), _ptr(s), rows, n, clip, bits),
+           "quant_sym8_f32")
+    return q, s.view(np.float16)
+
+
+def quant_int8(x: np.ndarray, rotate: bool = True, clip: float = 1.0, bits: int = 8):
+    """fp16 rows -> (int8 codes [rows, n] with 2^(bits-1) - 1 levels a side,
+    fp16 scales [rows])."""
+    x = _f16(x)
+    rows, n = x.shape
+    q = np.empty((rows, n), np.int8)
+    s = np.empty(rows, np.uint16)
+    _check(lib().orc_quant_int8(_ptr(_u16(x)), _ptr(q), _ptr(s), rows, n, int(rotate), clip,
+                                bits), "quant_int8")
+    return q, s.view(np.float16)
+
+
+def gemm_i8(xq: np.ndarray, wq: np.ndarray) -> np.ndarray:
+    xq = np.ascontiguousarray(xq, dtype=np.int8)
+    wq = np.ascontiguousarray(wq, dtype=np.int8)
+    M, K = xq.shape
+    N, K2 = wq.shape
+    assert K == K2
+    acc = np.empty((M, N), np.int32)
+    _check(lib().orc_gemm_i8(_ptr(xq), _ptr(wq), _ptr(acc), M, N, K), "gemm_i8")
+    return acc
 
 
 def gemm_i32(xq: np.ndarray, wq: np.ndarray) -> np.ndarray:

@@ -664,6 +664,106 @@ int orc_heads_quant_int4(const uint16_t *z, uint8_t *q, uint16_t *s, int64_t row
 }
 
 /* ------------------------------------------------------------------------ */
+/* 6- and 8-bit variants (§5.3 RTN ablation, App. A.6: the same per-token / */
+/* per-channel symmetric scheme at more bits), one code per byte.           */
+/* ------------------------------------------------------------------------ */
+
+/* qmax = 2^(bits-1) - 1:  s16 = RN16(RN(RN(absmax * clip) / qmax)),
+ * q = clamp(rint_even(RN(y / f32(s16))), -qmax - 1, qmax); s16 == 0 gives
+ * codes 0. */
+static void quant_sym8_row(const float *y, int64_t n, float clip, int qmax, int8_t *q,
+                           uint16_t *s)
+{
+    float amax = 0.0f;
+    for (int64_t i = 0; i < n; i++) {
+        float a = fabsf(y[i]);
+        if (a > amax)
+            amax = a;
+    }
+    float s32 = (amax * clip) / (float)qmax;
+    uint16_t s16 = orc_f32_to_f16(s32);
+    float sf = orc_f16_to_f32(s16);
+    *s = s16;
+    for (int64_t i = 0; i < n; i++) {
+        int v = 0;
+        if (sf != 0.0f) {
+            float r = rintf(y[i] / sf);
+            if (r < (float)(-qmax - 1))
+                r = (float)(-qmax - 1);
+            if (r > (float)qmax)
+                r = (float)qmax;
+            v = (int)r;
+        }
+        q[i] = (int8_t)v;
+    }
+}
+
+int orc_quant_sym8_f32(const float *y, int8_t *q, uint16_t *s, int64_t rows, int64_t n,
+                       float clip, int bits)
+{
+    if (n <= 0 || rows < 0 || (bits != 6 && bits != 8))
+        return ORC_ERR_ARG;
+    const int qmax = (1 << (bits - 1)) - 1;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; r++)
+        quant_sym8_row(y + r * n, n, clip, qmax, q + r * n, s + r);
+    return ORC_OK;
+}
+
+/* fp16 rows -> (optional rotation, kept in fp32) -> int8 codes [rows, n]. */
+int orc_quant_int8(const uint16_t *x, int8_t *q, uint16_t *s, int64_t rows, int64_t n,
+                   int rotate, float clip, int bits)
+{
+    if (n <= 0 || rows < 0 || (bits != 6 && bits != 8))
+        return ORC_ERR_ARG;
+    const int qmax = (1 << (bits - 1)) - 1;
+    struct rot_plan pl = {0, 1, 1.0f, NULL};
+    if (rotate) {
+        int st = plan_init(&pl, n);
+        if (st)
+            return st;
+    }
+    int err = 0;
+#pragma omp parallel for schedule(static) reduction(| : err)
+    for (int64_t r = 0; r < rows; r++) {
+        float *t = (float *)malloc((size_t)n * 3 * sizeof(float));
+        if (!t) {
+            err |= 1;
+            continue;
+        }
+        for (int64_t i = 0; i < n; i++)
+            t[i] = orc_f16_to_f32(x[r * n + i]);
+        const float *y = t;
+        if (rotate) {
+            rotate_row(t, t + n, t + 2 * n, n, pl.k, pl.m, pl.Hm, pl.c);
+            y = t + n;
+        }
+        quant_sym8_row(y, n, clip, qmax, q + r * n, s + r);
+        free(t);
+    }
+    free(pl.Hm);
+    return err ? ORC_ERR_NOMEM : ORC_OK;
+}
+
+/* acc[M, N] = Xq[M, K] . Wq[N, K]^T over int8 codes, exact in int32
+ * (|acc| <= 128^2 K). */
+int orc_gemm_i8(const int8_t *xq, const int8_t *wq, int32_t *acc, int64_t M, int64_t N,
+                int64_t K)
+{
+    if (K <= 0 || M < 0 || N < 0)
+        return ORC_ERR_ARG;
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; m++)
+        for (int64_t n = 0; n < N; n++) {
+            int32_t s = 0;
+            for (int64_t k = 0; k < K; k++)
+                s += (int32_t)xq[m * K + k] * (int32_t)wq[n * K + k];
+            acc[m * N + n] = s;
+        }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Integer GEMM and dequantization (§4 Stage 2b, App. A.10).                */
 /* ------------------------------------------------------------------------ */
 

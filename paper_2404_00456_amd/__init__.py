@@ -48,6 +48,11 @@ SIGNATURES = {
     "quarot_w4a4_gemm": (_I, [_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P]),
     "quarot_linear_workspace_size": (ctypes.c_size_t, [_I64, _I64]),
     "quarot_linear": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P, ctypes.c_size_t, _P]),
+    "quarot_quant_int8": (_I, [_P, _P, _P, _I64, _I64, _I, _F, _I, _P]),
+    "quarot_w8a8_gemm": (_I, [_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P]),
+    "quarot_linear_w8a8_workspace_size": (ctypes.c_size_t, [_I64, _I64]),
+    "quarot_linear_w8a8": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _I, _P,
+                                ctypes.c_size_t, _P]),
     "quarot_swiglu": (_I, [_P, _P, _P, _I64, _P]),
     "quarot_swiglu_quant_int4": (_I, [_P, _P, _P, _P, _I64, _I64, _F, _P]),
     "quarot_hadamard_heads": (_I, [_P, _P, _I64, _I64, _I64, _P]),
@@ -217,6 +222,61 @@ def prepare_weight(w: torch.Tensor, rotate: bool = True, clip_ratio: float = 1.0
     return quarot_quant_int4(w, rotate=rotate, clip_ratio=clip_ratio, stream=stream)
 
 
+def quarot_quant_int8(x: torch.Tensor, rotate: bool = True, clip_ratio: float = 1.0,
+                      bits: int = 8, q: Optional[torch.Tensor] = None,
+                      scale: Optional[torch.Tensor] = None,
+                      stream: Optional[torch.cuda.Stream] = None):
+    """Per-row symmetric 6/8-bit codes, one int8 per element.
+    Returns (codes int8 [..., n], scale fp16 [...])."""
+    n = x.shape[-1]
+    rows = _rows(x, n)
+    if q is None:
+        q = torch.empty(x.shape, dtype=torch.int8, device=x.device)
+    if scale is None:
+        scale = torch.empty(x.shape[:-1], dtype=torch.float16, device=x.device)
+    _check("quarot_quant_int8", lib().quarot_quant_int8(
+        _ptr(x, torch.float16, "x"), _ptr(q, torch.int8, "q"),
+        _ptr(scale, torch.float16, "scale"), rows, n, int(bool(rotate)), float(clip_ratio),
+        int(bits), _stream(stream)))
+    return q, scale
+
+
+def quarot_w8a8_gemm(xq: torch.Tensor, sx: torch.Tensor, wq: torch.Tensor, sw: torch.Tensor,
+                     y: Optional[torch.Tensor] = None, acc_out: Optional[torch.Tensor] = None,
+                     want_acc: bool = False, stream: Optional[torch.cuda.Stream] = None):
+    """y = dequant(Xq Wq^T) over int8 codes; returns y, or (y, acc)."""
+    M, K = xq.shape
+    N = wq.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=xq.device)
+    if want_acc and acc_out is None:
+        acc_out = torch.empty((M, N), dtype=torch.int32, device=xq.device)
+    _check("quarot_w8a8_gemm", lib().quarot_w8a8_gemm(
+        _ptr(xq, torch.int8, "xq"), _ptr(sx, torch.float16, "sx"), _ptr(wq, torch.int8, "wq"),
+        _ptr(sw, torch.float16, "sw"), _ptr(y, torch.float16, "y"),
+        _ptr(acc_out, torch.int32, "acc_out"), M, N, K, _stream(stream)))
+    return (y, acc_out) if (want_acc or acc_out is not None) else y
+
+
+def quarot_linear_w8a8(x: torch.Tensor, wq: torch.Tensor, sw: torch.Tensor, rotate: bool = True,
+                       clip_ratio: float = 1.0, bits: int = 8,
+                       y: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None,
+                       stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    M, K = x.shape
+    N = wq.shape[0]
+    need = int(lib().quarot_linear_w8a8_workspace_size(M, K))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    _check("quarot_linear_w8a8", lib().quarot_linear_w8a8(
+        _ptr(x, torch.float16, "x"), _ptr(wq, torch.int8, "wq"), _ptr(sw, torch.float16, "sw"),
+        _ptr(y, torch.float16, "y"), M, N, K, int(bool(rotate)), float(clip_ratio), int(bits),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream)))
+    return y
+
+
 def quarot_swiglu(gate: torch.Tensor, up: torch.Tensor, h: Optional[torch.Tensor] = None,
                   stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """h = RN16(silu(gate) * up) elementwise (binary32 silu recipe)."""
@@ -371,6 +431,7 @@ __all__ = [
     "QuarotError", "lib", "quarot_version", "quarot_hadamard_factor",
     "quarot_hadamard_factor_table", "quarot_linear_workspace_size", "quarot_hadamard",
     "quarot_quant_int4", "quarot_w4a4_gemm", "quarot_linear", "prepare_weight",
+    "quarot_quant_int8", "quarot_w8a8_gemm", "quarot_linear_w8a8",
     "quarot_swiglu", "quarot_swiglu_quant_int4", "quarot_hadamard_heads", "quarot_hadamard_heads_quant_int4",
     "quarot_kv_quant", "quarot_kv_dequant", "quarot_kv_append",
     "quarot_kv_attention_workspace_size", "quarot_kv_decode_attention",

@@ -308,6 +308,107 @@ quarot_status quarot_linear(const quarot_f16 *x, const uint8_t *wq, const quarot
     return e == hipSuccess ? QUAROT_OK : hip_fail(e);
 }
 
+quarot_status quarot_quant_int8(const quarot_f16 *x, int8_t *q, quarot_f16 *scale, int64_t rows,
+                                int64_t n, int rotate, float clip_ratio, int bits, void *stream)
+{
+    if (rows < 0 || !clip_ok(clip_ratio) || (bits != 6 && bits != 8))
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;
+    quarot_status st = check_rot_size(n, rotate != 0, EPI_SYM8, &k, &m);
+    if (st)
+        return st;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!x || !q || !scale)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(q) || !aligned16(scale))
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    RotArgs a{};
+    a.x = x;
+    a.out = q;
+    a.scale = scale;
+    a.rows = rows;
+    a.n = (int)n;
+    a.c = rotation_scale(n);
+    a.clip = clip_ratio;
+    a.qmax = (1 << (bits - 1)) - 1;
+    hipError_t e = launch_rotate(a, EPI_SYM8, rotate != 0, k, m, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+quarot_status quarot_w8a8_gemm(const int8_t *xq, const quarot_f16 *sx, const int8_t *wq,
+                               const quarot_f16 *sw, quarot_f16 *y, int32_t *acc_out,
+                               int64_t M, int64_t N, int64_t K, void *stream)
+{
+    const uint8_t *xb = reinterpret_cast<const uint8_t *>(xq);
+    const uint8_t *wb = reinterpret_cast<const uint8_t *>(wq);
+    quarot_status st = check_gemm(xb, sx, wb, sw, y, acc_out, M, N, K);
+    if (st || M == 0 || N == 0)
+        return st;
+    if ((st = check_device()))
+        return st;
+    GemmArgs a{xb, sx, wb, sw, y, acc_out, (int)M, (int)N, (int)K};
+    hipError_t e = launch_gemm(a, (hipStream_t)stream, 8);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+size_t quarot_linear_w8a8_workspace_size(int64_t M, int64_t K)
+{
+    if (M < 0 || K <= 0)
+        return 0;
+    const size_t codes = ((size_t)M * (size_t)K + 255) & ~(size_t)255;
+    const size_t scales = ((size_t)M * 2 + 255) & ~(size_t)255;
+    return codes + scales;
+}
+
+quarot_status quarot_linear_w8a8(const quarot_f16 *x, const int8_t *wq, const quarot_f16 *sw,
+                                 quarot_f16 *y, int64_t M, int64_t N, int64_t K, int rotate,
+                                 float clip_ratio, int bits, void *workspace,
+                                 size_t workspace_bytes, void *stream)
+{
+    if (M < 0 || N < 0 || !clip_ok(clip_ratio) || (bits != 6 && bits != 8))
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;
+    quarot_status st = check_rot_size(K, rotate != 0, EPI_SYM8, &k, &m);
+    if (st)
+        return st;
+    if ((st = check_gemm_sizes(M, N, K)))
+        return st;
+    if (M == 0 || N == 0)
+        return QUAROT_OK;
+    if (!x || !wq || !sw || !y)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(wq) || !aligned16(sw) || !aligned16(y))
+        return QUAROT_ERR_ALIGNMENT;
+    if (!workspace || workspace_bytes < quarot_linear_w8a8_workspace_size(M, K))
+        return QUAROT_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    uint8_t *xq = static_cast<uint8_t *>(workspace);
+    quarot_f16 *sx =
+        reinterpret_cast<quarot_f16 *>(xq + (((size_t)M * (size_t)K + 255) & ~(size_t)255));
+    RotArgs ra{};
+    ra.x = x;
+    ra.out = xq;
+    ra.scale = sx;
+    ra.rows = M;
+    ra.n = (int)K;
+    ra.c = rotation_scale(K);
+    ra.clip = clip_ratio;
+    ra.qmax = (1 << (bits - 1)) - 1;
+    hipError_t e = launch_rotate(ra, EPI_SYM8, rotate != 0, k, m, (hipStream_t)stream);
+    if (e != hipSuccess)
+        return hip_fail(e);
+    GemmArgs ga{xq, sx, reinterpret_cast<const uint8_t *>(wq), sw, y, nullptr, (int)M, (int)N,
+                (int)K};
+    e = launch_gemm(ga, (hipStream_t)stream, 8);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
 quarot_status quarot_swiglu(const quarot_f16 *gate, const quarot_f16 *up, quarot_f16 *h,
                             int64_t count, void *stream)
 {

@@ -14,6 +14,7 @@ enum Epilogue : int {
     EPI_F16 = 0,  // store RN16(y)
     EPI_SYM = 1,  // per-row symmetric int4 codes + fp16 scale
     EPI_KV = 2,   // per-group asymmetric uint4 codes + fp16 scale, zero
+    EPI_SYM8 = 3, // per-row symmetric codes in [-qmax-1, qmax], one byte each
 };
 
 // Load stages of the rotate kernels.
@@ -36,6 +37,7 @@ struct RotArgs {
     float clip;
     int64_t ostride;     // EPI_KV: output row of input row r is r * ostride + ooff
     int64_t ooff;
+    int qmax;            // EPI_SYM8: 2^(bits-1) - 1 (127 or 31)
 };
 
 struct KvAttnArgs {
@@ -85,7 +87,8 @@ struct KvDeqArgs {
 // rotation; sizes have been validated by the caller.
 hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, hipStream_t s,
                          int pro = PRO_PLAIN);
-hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
+// bits = 4: packed int4 codes [rows, K/2]; bits = 8: one int8 code per byte.
+hipError_t launch_gemm(const GemmArgs &a, hipStream_t s, int bits = 4);
 hipError_t launch_kv_dequant(const KvDeqArgs &a, bool inverse_rotate, hipStream_t s);
 hipError_t launch_swiglu(const uint16_t *g, const uint16_t *u, uint16_t *h, int64_t count,
                          hipStream_t s);

@@ -280,17 +280,24 @@ constexpr int waitcnt_imm(int vm, int lgkm)
 // next tile's first S, which land during the epilogue.  That needs at least
 // S k-steps per tile; the launcher gives every block a single tile
 // otherwise.
-__global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
+//
+// BITS = 8 (codes of 6 or 8 bits, one byte each): the same ring, tiles and
+// epilogue, but a k-step is 64 k (64 bytes per row), each 16-byte LDS read
+// is one MFMA operand as it is (no widening), and the accumulators hold acc
+// itself (no factor 256).  The 32 MFMAs of a k-step split into two halves
+// around the barrier, as the two substeps of the 4-bit path do.
+template <int BITS>
+__device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
 {
-    extern __shared__ __align__(16) uint8_t lds[];
+    static_assert(BITS == 4 || BITS == 8, "int4 or int8 codes");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 2, wn = wave & 3;
     const int M = a.M, N = a.N, K = a.K;
     const int TM = (M + BM - 1) / BM, TN = (N + BN - 1) / BN;
     const int T = TM * TN;
     const int G = gridDim.x, b = blockIdx.x;
-    const int64_t ldk = K / 2;
-    const int KT = K / 128;
+    const int64_t ldk = BITS == 4 ? K / 2 : K;
+    const int KT = BITS == 4 ? K / 128 : K / 64;
 
     // this block's tiles: logical positions b, b + G, ... within a
     // per-XCD ordering when the grid and the tile count allow it
@@ -407,18 +414,32 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
                 ops[8 + i] = *reinterpret_cast<const uint4 *>(sb + arow + i * 16 * BKB);
         };
         auto substep = [&](const uint4 (&ops)[8 + NI], int h) {
-            v4i aq[NI];
-#pragma unroll
-            for (int i = 0; i < NI; ++i)
-                aq[i] = widen(h ? make_uint2(ops[8 + i].z, ops[8 + i].w)
-                                : make_uint2(ops[8 + i].x, ops[8 + i].y));
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const v4i bq =
-                    widen(h ? make_uint2(ops[j].z, ops[j].w) : make_uint2(ops[j].x, ops[j].y));
+            if constexpr (BITS == 4) {
+                v4i aq[NI];
 #pragma unroll
                 for (int i = 0; i < NI; ++i)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aq[i], bq, acc[i][j], 0, 0, 0);
+                    aq[i] = widen(h ? make_uint2(ops[8 + i].z, ops[8 + i].w)
+                                    : make_uint2(ops[8 + i].x, ops[8 + i].y));
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const v4i bq = widen(h ? make_uint2(ops[j].z, ops[j].w)
+                                           : make_uint2(ops[j].x, ops[j].y));
+#pragma unroll
+                    for (int i = 0; i < NI; ++i)
+                        acc[i][j] =
+                            __builtin_amdgcn_mfma_i32_16x16x64_i8(aq[i], bq, acc[i][j], 0, 0, 0);
+                }
+            } else {
+                // half h: the B slices j = 4h .. 4h+3 against every A slice
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int j = 4 * h + jj;
+                    const v4i bq = __builtin_bit_cast(v4i, ops[j]);
+#pragma unroll
+                    for (int i = 0; i < NI; ++i)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
+                            __builtin_bit_cast(v4i, ops[8 + i]), bq, acc[i][j], 0, 0, 0);
+                }
             }
         };
 
@@ -475,16 +496,17 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
             scale_dma(m1, n1, (it + 1) & 1);
 
         if (fast_tile(m0, n0)) {
-            // y = RN16(RN(RN(f32(acc) sx) sw)).  The accumulators hold 256 acc
-            // and f32(256 acc) = 256 f32(acc), so multiplying by sx / 256
-            // (exact) gives the same RN(f32(acc) sx) without the shift.
+            // y = RN16(RN(RN(f32(acc) sx) sw)).  With 4-bit codes the
+            // accumulators hold 256 acc and f32(256 acc) = 256 f32(acc), so
+            // multiplying by sx / 256 (exact) gives the same RN(f32(acc) sx)
+            // without the shift.
             const uint8_t *sc = lds + RING_BYTES + (it & 1) * (SCALE_BYTES / 2);
             const uint16_t *lsx = reinterpret_cast<const uint16_t *>(sc);
             const uint16_t *lsw = lsx + BM;
             float sxs[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                sxs[j] = h2f(lsx[wm * 128 + j * 16 + orow]) * 0x1p-8f;
+                sxs[j] = h2f(lsx[wm * 128 + j * 16 + orow]) * (BITS == 4 ? 0x1p-8f : 1.0f);
             float swf[NI][4];
 #pragma unroll
             for (int i = 0; i < NI; ++i) {
@@ -541,7 +563,7 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
                 uint16_t hv[4];
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    iv[r] = acc[i][j][r] >> 8;
+                    iv[r] = BITS == 4 ? acc[i][j][r] >> 8 : acc[i][j][r];
                     const float tt = (float)iv[r] * sxf[j];
                     hv[r] = f2h(tt * swf[r]);
                 }
@@ -578,15 +600,30 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));  // no DMA may outlive the block's LDS
 }
 
+__global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    gemm_main<4>(a, lds);
+}
+
+__global__ __launch_bounds__(THREADS, 1) void k_gemm_w8a8(GemmArgs a)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    gemm_main<8>(a, lds);
+}
+
 }  // namespace
 
-hipError_t launch_gemm(const GemmArgs &a, hipStream_t s)
+hipError_t launch_gemm(const GemmArgs &a, hipStream_t s, int bits)
 {
     if (a.M == 0 || a.N == 0)
         return hipSuccess;
     const int TM = (a.M + BM - 1) / BM, TN = (a.N + BN - 1) / BN;
-    const bool main = (a.K % 128) == 0;
-    const void *fn = main ? (const void *)k_gemm_w4a4 : (const void *)k_gemm_w4a4_k64;
+    const bool main = bits == 8 || (a.K % 128) == 0;
+    const int ksteps = bits == 8 ? a.K / 64 : a.K / 128;
+    const void *fn = bits == 8 ? (const void *)k_gemm_w8a8
+                     : main    ? (const void *)k_gemm_w4a4
+                               : (const void *)k_gemm_w4a4_k64;
     const int lds_bytes = main ? MAIN_LDS_BYTES : LDS_BYTES;
     // more than 64 KB of dynamic LDS: raise the kernel's limit (per call, so
     // that every device the caller uses gets it; the call is host-side only)
@@ -603,10 +640,13 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s)
             cus <= 0)
             cus = 256;
         const int tiles = TM * TN;
-        int grid = (tiles < cus || a.K / 128 < S) ? tiles : cus;
+        int grid = (tiles < cus || ksteps < S) ? tiles : cus;
         if (grid >= 8 && tiles % 8 == 0)
             grid -= grid % 8;
-        hipLaunchKernelGGL(k_gemm_w4a4, dim3((unsigned)grid), dim3(THREADS), lds_bytes, s, a);
+        if (bits == 8)
+            hipLaunchKernelGGL(k_gemm_w8a8, dim3((unsigned)grid), dim3(THREADS), lds_bytes, s, a);
+        else
+            hipLaunchKernelGGL(k_gemm_w4a4, dim3((unsigned)grid), dim3(THREADS), lds_bytes, s, a);
     }
     else
         hipLaunchKernelGGL(k_gemm_w4a4_k64, dim3((unsigned)(TM * TN)), dim3(THREADS), lds_bytes, s,

@@ -87,6 +87,67 @@ __device__ __forceinline__ uint32_t asym_code(float y, const Divisor &d, float z
     return d.ok ? (uint32_t)(int)c : 0u;
 }
 
+// Symmetric code with qmax levels a side, as a byte:
+// clamp(rint_even(RN(y / sf)), -qmax - 1, qmax).
+__device__ __forceinline__ uint32_t sym8_code(float y, const Divisor &d, float qmaxf)
+{
+    const float c = fminf(fmaxf(rintf(quotient(y, d)), -qmaxf - 1.0f), qmaxf);
+    return d.ok ? ((uint32_t)(int)c & 0xFFu) : 0u;
+}
+
+// The symmetric epilogues: scale divisor, row stride of the codes, and the
+// codes of 8 (or 4) consecutive elements starting at element i0 of a row:
+// EPI_SYM packs nibbles (4 bytes per 8), EPI_SYM8 one byte per code.
+template <int EPI>
+__device__ __forceinline__ float sym_divisor(const RotArgs &a)
+{
+    return EPI == EPI_SYM ? 7.0f : (float)a.qmax;
+}
+
+template <int EPI>
+__device__ __forceinline__ int64_t sym_row_bytes(int64_t n)
+{
+    return EPI == EPI_SYM ? n / 2 : n;
+}
+
+template <int EPI>
+__device__ __forceinline__ void store_codes8(uint8_t *qr, int64_t i0, const float *v,
+                                             const Divisor &d, float qmaxf)
+{
+    if constexpr (EPI == EPI_SYM) {
+        uint32_t pk = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            pk |= sym_code(v[e], d) << (4 * e);
+        *reinterpret_cast<uint32_t *>(qr + i0 / 2) = pk;
+    } else {
+        uint2 pk = make_uint2(0, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            pk.x |= sym8_code(v[e], d, qmaxf) << (8 * e);
+            pk.y |= sym8_code(v[4 + e], d, qmaxf) << (8 * e);
+        }
+        *reinterpret_cast<uint2 *>(qr + i0) = pk;
+    }
+}
+
+template <int EPI>
+__device__ __forceinline__ void store_codes4(uint8_t *qr, int64_t i0, const float *v,
+                                             const Divisor &d, float qmaxf)
+{
+    if constexpr (EPI == EPI_SYM) {
+        const uint32_t pk = sym_code(v[0], d) | (sym_code(v[1], d) << 4) |
+                            (sym_code(v[2], d) << 8) | (sym_code(v[3], d) << 12);
+        *reinterpret_cast<uint16_t *>(qr + i0 / 2) = (uint16_t)pk;
+    } else {
+        uint32_t pk = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            pk |= sym8_code(v[e], d, qmaxf) << (8 * e);
+        *reinterpret_cast<uint32_t *>(qr + i0) = pk;
+    }
+}
+
 __device__ __forceinline__ void load8(const uint16_t *p, float *v)
 {
     uint4 raw = *reinterpret_cast<const uint4 *>(p);
@@ -309,7 +370,7 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
 #pragma unroll
         for (int cc = 0; cc < C; ++cc)
             store8(yr + ((cc * W + w) * L + pos) * 8, v[cc]);
-    } else if constexpr (EPI == EPI_SYM) {
+    } else if constexpr (EPI == EPI_SYM || EPI == EPI_SYM8) {
         __shared__ float red[W > 1 ? W : 1];
         float amax = 0.0f;
 #pragma unroll
@@ -318,18 +379,14 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
             for (int e = 0; e < 8; ++e)
                 amax = fmaxf(amax, fabsf(v[cc][e]));
         amax = row_absmax<LOGL, W>(amax, w, red);
-        const float s32 = (amax * a.clip) / 7.0f;
+        const float qd = sym_divisor<EPI>(a);
+        const float s32 = (amax * a.clip) / qd;
         const uint16_t s16 = f2h(s32);
         const Divisor dv = make_divisor(h2f(s16));
-        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (N / 2);
+        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(N);
 #pragma unroll
-        for (int cc = 0; cc < C; ++cc) {
-            uint32_t pk = 0;
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-                pk |= sym_code(v[cc][e], dv) << (4 * e);
-            *reinterpret_cast<uint32_t *>(qr + ((cc * W + w) * L + pos) * 4) = pk;
-        }
+        for (int cc = 0; cc < C; ++cc)
+            store_codes8<EPI>(qr, ((cc * W + w) * L + pos) * 8, v[cc], dv, qd);
         if (pos == 0 && w == 0)
             a.scale[row] = s16;
     } else {  // EPI_KV: one wave per row; a group is G consecutive elements
@@ -533,7 +590,7 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
                 store4(yr + g * M + 4 * p, &v[cc][4 * p]);
         }
     } else {
-        static_assert(EPI == EPI_SYM, "small-m kernels serve activations");
+        static_assert(EPI == EPI_SYM || EPI == EPI_SYM8, "small-m kernels serve activations");
         __shared__ float red[W > 1 ? W : 1];
         float amax = 0.0f;
 #pragma unroll
@@ -542,20 +599,17 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
             for (int b = 0; b < M; ++b)
                 amax = fmaxf(amax, fabsf(v[cc][b]));
         amax = row_absmax<LOGL, W>(amax, w, red);
-        const float s32 = (amax * a.clip) / 7.0f;
+        const float qd = sym_divisor<EPI>(a);
+        const float s32 = (amax * a.clip) / qd;
         const uint16_t s16 = f2h(s32);
         const Divisor dv = make_divisor(h2f(s16));
-        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (N / 2);
+        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(N);
 #pragma unroll
         for (int cc = 0; cc < C; ++cc) {
             const int g = (cc * W + w) * L + pos;
 #pragma unroll
-            for (int p = 0; p < M / 4; ++p) {
-                uint32_t pk = sym_code(v[cc][4 * p], dv) | (sym_code(v[cc][4 * p + 1], dv) << 4) |
-                              (sym_code(v[cc][4 * p + 2], dv) << 8) |
-                              (sym_code(v[cc][4 * p + 3], dv) << 12);
-                *reinterpret_cast<uint16_t *>(qr + g * (M / 2) + 2 * p) = (uint16_t)pk;
-            }
+            for (int p = 0; p < M / 4; ++p)
+                store_codes4<EPI>(qr, g * M + 4 * p, &v[cc][4 * p], dv, qd);
         }
         if (pos == 0 && w == 0)
             a.scale[row] = s16;
@@ -676,7 +730,7 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
             store8(yr + ch * 8, y);
         }
     } else {
-        static_assert(EPI == EPI_SYM, "large-m kernels serve activations");
+        static_assert(EPI == EPI_SYM || EPI == EPI_SYM8, "large-m kernels serve activations");
         float amax = 0.0f;
         for (int ch = tid; ch < chunks; ch += 64 * W)
 #pragma unroll
@@ -692,18 +746,19 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
 #pragma unroll
         for (int i = 1; i < W; ++i)
             amax = fmaxf(amax, red[i]);
-        const float s32 = (amax * a.clip) / 7.0f;
+        const float qd = sym_divisor<EPI>(a);
+        const float s32 = (amax * a.clip) / qd;
         const uint16_t s16 = f2h(s32);
         const Divisor dv = make_divisor(h2f(s16));
-        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (n / 2);
+        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(n);
         for (int ch = tid; ch < chunks; ch += 64 * W) {
-            uint32_t pk = 0;
+            float y[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
-                pk |= sym_code(rowbuf[gi * LD + b] * c, dv) << (4 * e);
+                y[e] = rowbuf[gi * LD + b] * c;
             }
-            *reinterpret_cast<uint32_t *>(qr + ch * 4) = pk;
+            store_codes8<EPI>(qr, ch * 8, y, dv, qd);
         }
         if (tid == 0)
             a.scale[row] = s16;
@@ -712,6 +767,7 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
 
 // ------------------------------------------------- no rotation, any n -----
 
+template <int EPI>
 __global__ __launch_bounds__(256) void k_quant_plain(RotArgs a)
 {
     __shared__ float red[4];
@@ -732,18 +788,15 @@ __global__ __launch_bounds__(256) void k_quant_plain(RotArgs a)
         red[tid >> 6] = amax;
     __syncthreads();
     amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-    const float s32 = (amax * a.clip) / 7.0f;
+    const float qd = sym_divisor<EPI>(a);
+    const float s32 = (amax * a.clip) / qd;
     const uint16_t s16 = f2h(s32);
     const Divisor dv = make_divisor(h2f(s16));
-    uint8_t *qr = static_cast<uint8_t *>(a.out) + row * (n / 2);
+    uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(n);
     for (int ch = tid; ch < chunks; ch += 256) {
         float v[8];
         load8(xr + ch * 8, v);
-        uint32_t pk = 0;
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-            pk |= sym_code(v[e], dv) << (4 * e);
-        *reinterpret_cast<uint32_t *>(qr + ch * 4) = pk;
+        store_codes8<EPI>(qr, ch * 8, v, dv, qd);
     }
     if (tid == 0)
         a.scale[row] = s16;
@@ -947,7 +1000,7 @@ bool rotate_supported(int epi, bool rotate, int k, int m, int n, int pro)
     if (pro == PRO_SWIGLU && (epi != EPI_SYM || !rotate))
         return false;
     if (!rotate)
-        return epi == EPI_SYM || (epi == EPI_KV && m == 1 && k >= 3 && k <= 9);
+        return epi == EPI_SYM || epi == EPI_SYM8 || (epi == EPI_KV && m == 1 && k >= 3 && k <= 9);
     if (epi == EPI_KV)
         return m == 1 && k >= 3 && k <= 9;
     switch (m) {
@@ -970,8 +1023,13 @@ hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, h
         return (epi == EPI_SYM && rotate) ? dispatch_rotated<EPI_SYM, PRO_SWIGLU>(a, k, m, s)
                                           : hipErrorInvalidValue;
     if (!rotate) {
-        if (epi == EPI_SYM) {
-            hipLaunchKernelGGL(k_quant_plain, dim3((unsigned)a.rows), dim3(256), 0, s, a);
+        if (epi == EPI_SYM || epi == EPI_SYM8) {
+            if (epi == EPI_SYM)
+                hipLaunchKernelGGL(k_quant_plain<EPI_SYM>, dim3((unsigned)a.rows), dim3(256), 0,
+                                   s, a);
+            else
+                hipLaunchKernelGGL(k_quant_plain<EPI_SYM8>, dim3((unsigned)a.rows), dim3(256), 0,
+                                   s, a);
             return hipGetLastError();
         }
         if (epi == EPI_KV)
@@ -991,6 +1049,7 @@ hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, h
     switch (epi) {
     case EPI_F16: return dispatch_rotated<EPI_F16, PRO_PLAIN>(a, k, m, s);
     case EPI_SYM: return dispatch_rotated<EPI_SYM, PRO_PLAIN>(a, k, m, s);
+    case EPI_SYM8: return dispatch_rotated<EPI_SYM8, PRO_PLAIN>(a, k, m, s);
     case EPI_KV:
         return a.group == a.n ? dispatch_pow2<EPI_KV, true, PRO_PLAIN, false, true>(a, k, s)
                               : dispatch_pow2<EPI_KV, true, PRO_PLAIN>(a, k, s);

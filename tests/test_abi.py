@@ -121,6 +121,17 @@ def test_invalid_arguments_rejected_before_device(L):
     assert L.quarot_kv_quant(P, P, P, None, 4, 128, 128, 1, 0.95, S) == INVALID
     assert L.quarot_kv_dequant(P, P, P, P, 4, 128, 0, 0, S) == INVALID
     assert L.quarot_kv_dequant(P, P, UNALIGNED, P, 4, 128, 128, 0, S) == ALIGN
+    # 6/8-bit
+    assert L.quarot_quant_int8(P, P2, P2, 4, 128, 1, 1.0, 4, S) == INVALID   # bits
+    assert L.quarot_quant_int8(P, P2, P2, 4, 128, 1, 0.0, 8, S) == INVALID
+    assert L.quarot_quant_int8(P, P2, P2, 4, 100, 1, 1.0, 8, S) == UNSUPPORTED
+    assert L.quarot_quant_int8(P, UNALIGNED, P2, 4, 128, 1, 1.0, 8, S) == ALIGN
+    assert L.quarot_quant_int8(None, None, None, 0, 128, 1, 1.0, 6, S) == OK
+    assert L.quarot_w8a8_gemm(P, P, P, P, P, None, 4, 4, 96, S) == UNSUPPORTED
+    assert L.quarot_w8a8_gemm(P, None, P, P, P, None, 4, 4, 128, S) == INVALID
+    assert L.quarot_linear_w8a8_workspace_size(3, 128) == 512 + 256
+    assert L.quarot_linear_w8a8(P, P, P, P, 4, 4, 128, 1, 1.0, 8, P, 10, S) == WORKSPACE
+    assert L.quarot_linear_w8a8(P, P, P, P, 4, 4, 128, 1, 1.0, 5, P, 4096, S) == INVALID
     # kv append / decode attention
     assert L.quarot_kv_append(P, P, P, P, 4, 16, 16, 128, 128, 1, 0.95, S) == INVALID  # pos
     assert L.quarot_kv_append(P, P, P, P, 4, 16, -1, 128, 128, 1, 0.95, S) == INVALID
