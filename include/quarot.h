@@ -187,6 +187,30 @@ quarot_status quarot_linear_w8a8(const quarot_f16 *x, const int8_t *wq, const qu
                                  size_t workspace_bytes, void *stream);
 
 /*
+ * Offline weight quantization with a per-row (per output channel) clip
+ * search (§5 Setup: round-to-nearest weights with "the clipping ratio
+ * extracted by a linear search over the squared error"; App. A.2).  For
+ * each row y (w rotated like an activation row when rotate != 0) and each
+ * candidate c_j = RN32((100 - j) / 100), j < n_candidates: the symmetric
+ * quantizer of quarot_quant_int4 (bits = 4) or quarot_quant_int8 (6, 8)
+ * with clip c_j, and E_j = sum_i (y_i - q_i * s)^2 (fp64, each difference
+ * exact).  The row keeps the first j with the smallest E_j; the codes and
+ * scale are exactly those of the plain quantizer with clip c_best.
+ *   w fp16 [rows, n]; q: uint8 [rows, n/2] (bits 4) or int8 [rows, n];
+ *   scale fp16 [rows]; clip_out float32 [rows] (c_best);
+ *   workspace: quarot_quant_search_workspace_size(rows, n, rotate) bytes
+ *   (binary32 rotated rows; 0 without rotation), 16-byte aligned.
+ * 1 <= n_candidates <= 100.  Sums in a different order than a sequential
+ * loop, so a choice between two candidates whose errors agree to ~1e-15
+ * relative could differ from a CPU reference.
+ */
+size_t quarot_quant_search_workspace_size(int64_t rows, int64_t n, int rotate);
+quarot_status quarot_quant_search(const quarot_f16 *w, void *q, quarot_f16 *scale,
+                                  float *clip_out, int64_t rows, int64_t n, int rotate, int bits,
+                                  int n_candidates, void *workspace, size_t workspace_bytes,
+                                  void *stream);
+
+/*
  * The elementwise SwiGLU product alone: h = RN16(RN(silu(gate) * up)) with
  * the binary32 silu recipe of quarot_swiglu_quant_int4 below.
  * gate, up, h fp16 [count]; count a multiple of 8 (0 is a no-op).

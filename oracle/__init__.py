@@ -69,6 +69,7 @@ _SIGS = {
     "orc_quant_sym8_f32": (_I, [_P, _P, _P, _I64, _I64, _F, _I]),
     "orc_quant_int8": (_I, [_P, _P, _P, _I64, _I64, _I, _F, _I]),
     "orc_gemm_i8": (_I, [_P, _P, _P, _I64, _I64, _I64]),
+    "orc_quant_search": (_I, [_P, _P, _P, _P, _I64, _I64, _I, _I, _I]),
     "orc_set_threads": (None, [_I]),
     "orc_max_threads": (_I, []),
 }
@@ -222,6 +223,19 @@ def quant_int8(x: np.ndarray, rotate: bool = True, clip: float = 1.0, bits: int 
     _check(lib().orc_quant_int8(_ptr(_u16(x)), _ptr(q), _ptr(s), rows, n, int(rotate), clip,
                                 bits), "quant_int8")
     return q, s.view(np.float16)
+
+
+def quant_search(w: np.ndarray, rotate: bool = True, bits: int = 4, n_candidates: int = 20):
+    """Per-row clip search: (codes, scales, chosen clip per row).  Codes are
+    packed nibbles [rows, n/2] for bits = 4, int8 [rows, n] for 6 and 8."""
+    w = _f16(w)
+    rows, n = w.shape
+    q = np.empty((rows, n // 2), np.uint8) if bits == 4 else np.empty((rows, n), np.int8)
+    s = np.empty(rows, np.uint16)
+    c = np.empty(rows, np.float32)
+    _check(lib().orc_quant_search(_ptr(_u16(w)), _ptr(q), _ptr(s), _ptr(c), rows, n,
+                                  int(rotate), bits, n_candidates), "quant_search")
+    return q, s.view(np.float16), c
 
 
 def gemm_i8(xq: np.ndarray, wq: np.ndarray) -> np.ndarray:

@@ -745,6 +745,83 @@ int orc_quant_int8(const uint16_t *x, int8_t *q, uint16_t *s, int64_t rows, int6
     return err ? ORC_ERR_NOMEM : ORC_OK;
 }
 
+/* Weight quantization with a per-row clipping search (§5 Setup: RTN
+ * per-column symmetric quantization "where we extract the clipping ratio
+ * using a linear search over the squared error"; App. A.2).  For each row
+ * (output channel) y (rotated if asked), candidates c_j = RN32((100 - j) /
+ * 100), j < ncand; for each the scale and codes of the symmetric quantizer
+ * with that clip, and the error E_j = sum_i (y_i - q_i s16)^2, each term's
+ * difference exact in fp64 and the sum taken left to right in fp64.  The
+ * row keeps the first j with the smallest E_j.  bits = 4 packs nibbles,
+ * 6 or 8 stores one code per byte.  clip_out[r] = c_best. */
+int orc_quant_search(const uint16_t *x, void *q, uint16_t *s, float *clip_out, int64_t rows,
+                     int64_t n, int rotate, int bits, int ncand)
+{
+    if (n <= 0 || (n & 1) || rows < 0 || ncand < 1 || ncand > 100 ||
+        (bits != 4 && bits != 6 && bits != 8))
+        return ORC_ERR_ARG;
+    const int qmax = (1 << (bits - 1)) - 1;
+    struct rot_plan pl = {0, 1, 1.0f, NULL};
+    if (rotate) {
+        int st = plan_init(&pl, n);
+        if (st)
+            return st;
+    }
+    int err = 0;
+#pragma omp parallel for schedule(static) reduction(| : err)
+    for (int64_t r = 0; r < rows; r++) {
+        float *t = (float *)malloc((size_t)n * 3 * sizeof(float));
+        if (!t) {
+            err |= 1;
+            continue;
+        }
+        for (int64_t i = 0; i < n; i++)
+            t[i] = orc_f16_to_f32(x[r * n + i]);
+        const float *y = t;
+        if (rotate) {
+            rotate_row(t, t + n, t + 2 * n, n, pl.k, pl.m, pl.Hm, pl.c);
+            y = t + n;
+        }
+        float amax = 0.0f;
+        for (int64_t i = 0; i < n; i++)
+            if (fabsf(y[i]) > amax)
+                amax = fabsf(y[i]);
+        double best_e = INFINITY;
+        float best_c = 1.0f;
+        for (int j = 0; j < ncand; j++) {
+            const float c = (float)((double)(100 - j) / 100.0);
+            const uint16_t s16 = orc_f32_to_f16((amax * c) / (float)qmax);
+            const float sf = orc_f16_to_f32(s16);
+            double e = 0.0;
+            for (int64_t i = 0; i < n; i++) {
+                int v = 0;
+                if (sf != 0.0f) {
+                    float rr = rintf(y[i] / sf);
+                    if (rr < (float)(-qmax - 1))
+                        rr = (float)(-qmax - 1);
+                    if (rr > (float)qmax)
+                        rr = (float)qmax;
+                    v = (int)rr;
+                }
+                const double d = (double)y[i] - (double)v * (double)sf;
+                e += d * d;
+            }
+            if (e < best_e) {
+                best_e = e;
+                best_c = c;
+            }
+        }
+        clip_out[r] = best_c;
+        if (bits == 4)
+            quant_sym_row(y, n, best_c, (uint8_t *)q + r * (n / 2), s + r);
+        else
+            quant_sym8_row(y, n, best_c, qmax, (int8_t *)q + r * n, s + r);
+        free(t);
+    }
+    free(pl.Hm);
+    return err ? ORC_ERR_NOMEM : ORC_OK;
+}
+
 /* acc[M, N] = Xq[M, K] . Wq[N, K]^T over int8 codes, exact in int32
  * (|acc| <= 128^2 K). */
 int orc_gemm_i8(const int8_t *xq, const int8_t *wq, int32_t *acc, int64_t M, int64_t N,

@@ -53,6 +53,9 @@ SIGNATURES = {
     "quarot_linear_w8a8_workspace_size": (ctypes.c_size_t, [_I64, _I64]),
     "quarot_linear_w8a8": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _I, _P,
                                 ctypes.c_size_t, _P]),
+    "quarot_quant_search_workspace_size": (ctypes.c_size_t, [_I64, _I64, _I]),
+    "quarot_quant_search": (_I, [_P, _P, _P, _P, _I64, _I64, _I, _I, _I, _P, ctypes.c_size_t,
+                                 _P]),
     "quarot_swiglu": (_I, [_P, _P, _P, _I64, _P]),
     "quarot_swiglu_quant_int4": (_I, [_P, _P, _P, _P, _I64, _I64, _F, _P]),
     "quarot_hadamard_heads": (_I, [_P, _P, _I64, _I64, _I64, _P]),
@@ -277,6 +280,29 @@ def quarot_linear_w8a8(x: torch.Tensor, wq: torch.Tensor, sw: torch.Tensor, rota
     return y
 
 
+def quarot_quant_search(w: torch.Tensor, rotate: bool = True, bits: int = 4,
+                        n_candidates: int = 20, stream: Optional[torch.cuda.Stream] = None):
+    """Offline weight quantization with a per-row clip search.
+    Returns (codes, scale fp16 [rows], chosen clip float32 [rows]); codes are
+    packed nibbles uint8 [rows, n/2] for bits = 4, int8 [rows, n] otherwise."""
+    rows, n = w.shape
+    dev = w.device
+    if bits == 4:
+        q = torch.empty((rows, n // 2), dtype=torch.uint8, device=dev)
+    else:
+        q = torch.empty((rows, n), dtype=torch.int8, device=dev)
+    scale = torch.empty(rows, dtype=torch.float16, device=dev)
+    clip = torch.empty(rows, dtype=torch.float32, device=dev)
+    need = int(lib().quarot_quant_search_workspace_size(rows, n, int(bool(rotate))))
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _check("quarot_quant_search", lib().quarot_quant_search(
+        _ptr(w, torch.float16, "w"), ctypes.c_void_p(q.data_ptr()),
+        _ptr(scale, torch.float16, "scale"), _ptr(clip, torch.float32, "clip"), rows, n,
+        int(bool(rotate)), int(bits), int(n_candidates), _ptr(ws, torch.uint8, "workspace"),
+        ws.numel(), _stream(stream)))
+    return q, scale, clip
+
+
 def quarot_swiglu(gate: torch.Tensor, up: torch.Tensor, h: Optional[torch.Tensor] = None,
                   stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """h = RN16(silu(gate) * up) elementwise (binary32 silu recipe)."""
@@ -431,7 +457,7 @@ __all__ = [
     "QuarotError", "lib", "quarot_version", "quarot_hadamard_factor",
     "quarot_hadamard_factor_table", "quarot_linear_workspace_size", "quarot_hadamard",
     "quarot_quant_int4", "quarot_w4a4_gemm", "quarot_linear", "prepare_weight",
-    "quarot_quant_int8", "quarot_w8a8_gemm", "quarot_linear_w8a8",
+    "quarot_quant_int8", "quarot_w8a8_gemm", "quarot_linear_w8a8", "quarot_quant_search",
     "quarot_swiglu", "quarot_swiglu_quant_int4", "quarot_hadamard_heads", "quarot_hadamard_heads_quant_int4",
     "quarot_kv_quant", "quarot_kv_dequant", "quarot_kv_append",
     "quarot_kv_attention_workspace_size", "quarot_kv_decode_attention",

@@ -409,6 +409,62 @@ quarot_status quarot_linear_w8a8(const quarot_f16 *x, const int8_t *wq, const qu
     return e == hipSuccess ? QUAROT_OK : hip_fail(e);
 }
 
+size_t quarot_quant_search_workspace_size(int64_t rows, int64_t n, int rotate)
+{
+    if (rows < 0 || n <= 0 || !rotate)
+        return 0;
+    return ((size_t)rows * (size_t)n * sizeof(float) + 255) & ~(size_t)255;
+}
+
+quarot_status quarot_quant_search(const quarot_f16 *w, void *q, quarot_f16 *scale,
+                                  float *clip_out, int64_t rows, int64_t n, int rotate, int bits,
+                                  int n_candidates, void *workspace, size_t workspace_bytes,
+                                  void *stream)
+{
+    if (rows < 0 || (bits != 4 && bits != 6 && bits != 8) || n_candidates < 1 ||
+        n_candidates > 100)
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;  // without rotation the search reads the fp16 rows itself
+    quarot_status st = check_rot_size(n, rotate != 0, rotate ? EPI_F32 : EPI_SYM, &k, &m);
+    if (st)
+        return st;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!w || !q || !scale || !clip_out)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(w) || !aligned16(q) || !aligned16(scale) || !aligned16(clip_out))
+        return QUAROT_ERR_ALIGNMENT;
+    const size_t need = quarot_quant_search_workspace_size(rows, n, rotate);
+    if (need && (!workspace || workspace_bytes < need))
+        return QUAROT_ERR_WORKSPACE;
+    if (need && !aligned16(workspace))
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    if (rotate) {
+        RotArgs a{};
+        a.x = w;
+        a.out = workspace;
+        a.rows = rows;
+        a.n = (int)n;
+        a.c = rotation_scale(n);
+        a.clip = 1.0f;
+        hipError_t e = launch_rotate(a, EPI_F32, true, k, m, (hipStream_t)stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    SearchArgs sa{};
+    sa.y = rotate ? workspace : (const void *)w;
+    sa.q = q;
+    sa.scale = scale;
+    sa.clip = clip_out;
+    sa.rows = rows;
+    sa.n = (int)n;
+    sa.ncand = n_candidates;
+    hipError_t e = launch_quant_search(sa, bits, rotate != 0, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
 quarot_status quarot_swiglu(const quarot_f16 *gate, const quarot_f16 *up, quarot_f16 *h,
                             int64_t count, void *stream)
 {

@@ -15,6 +15,7 @@ enum Epilogue : int {
     EPI_SYM = 1,  // per-row symmetric int4 codes + fp16 scale
     EPI_KV = 2,   // per-group asymmetric uint4 codes + fp16 scale, zero
     EPI_SYM8 = 3, // per-row symmetric codes in [-qmax-1, qmax], one byte each
+    EPI_F32 = 4,  // store y in binary32 (input of the weights' clip search)
 };
 
 // Load stages of the rotate kernels.
@@ -56,6 +57,17 @@ struct KvAttnArgs {
     int splits, chunk;  // sequence split: tokens [s * chunk, (s + 1) * chunk)
     float sm_scale;
 };
+
+struct SearchArgs {
+    const void *y;       // binary32 rows (rotated) or fp16 rows [rows, n]
+    void *q;             // codes: packed nibbles (4 bits) or one byte each
+    uint16_t *scale;     // [rows]
+    float *clip;         // [rows] chosen clip
+    int64_t rows;
+    int n;
+    int ncand;           // candidates c_j = RN32((100 - j) / 100), j < ncand
+};
+hipError_t launch_quant_search(const SearchArgs &a, int bits, bool f32_in, hipStream_t s);
 
 // Sequence splits of the decode attention for nq query rows (the workspace
 // holds nq * splits * (D + 2) floats when splits > 1).

@@ -249,6 +249,30 @@ __device__ __forceinline__ void load_row4(const RotArgs &a, int64_t off, float *
     }
 }
 
+// 8 (4) values of y at element offset off of the output: fp16 (EPI_F16) or
+// binary32 (EPI_F32).
+template <int EPI>
+__device__ __forceinline__ void store_y8(void *out, int64_t off, const float *v)
+{
+    if constexpr (EPI == EPI_F16) {
+        store8(static_cast<uint16_t *>(out) + off, v);
+    } else {
+        float4 *p = reinterpret_cast<float4 *>(static_cast<float *>(out) + off);
+        p[0] = make_float4(v[0], v[1], v[2], v[3]);
+        p[1] = make_float4(v[4], v[5], v[6], v[7]);
+    }
+}
+
+template <int EPI>
+__device__ __forceinline__ void store_y4(void *out, int64_t off, const float *v)
+{
+    if constexpr (EPI == EPI_F16)
+        store4(static_cast<uint16_t *>(out) + off, v);
+    else
+        *reinterpret_cast<float4 *>(static_cast<float *>(out) + off) =
+            make_float4(v[0], v[1], v[2], v[3]);
+}
+
 // Max over the L-lane group (xor butterfly), then over the W waves.
 template <int LOGL, int W>
 __device__ __forceinline__ float row_absmax(float amax, int w, float *red)
@@ -365,11 +389,10 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
                 v[cc][e] = __builtin_fmaf(v[cc][e], sc, 0.0f);
     }
 
-    if constexpr (EPI == EPI_F16) {
-        uint16_t *yr = static_cast<uint16_t *>(a.out) + row * N;
+    if constexpr (EPI == EPI_F16 || EPI == EPI_F32) {
 #pragma unroll
         for (int cc = 0; cc < C; ++cc)
-            store8(yr + ((cc * W + w) * L + pos) * 8, v[cc]);
+            store_y8<EPI>(a.out, row * N + ((cc * W + w) * L + pos) * 8, v[cc]);
     } else if constexpr (EPI == EPI_SYM || EPI == EPI_SYM8) {
         __shared__ float red[W > 1 ? W : 1];
         float amax = 0.0f;
@@ -580,14 +603,13 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
         for (int b = 0; b < M; ++b)
             v[cc][b] = __builtin_fmaf(v[cc][b], sc, 0.0f);
 
-    if constexpr (EPI == EPI_F16) {
-        uint16_t *yr = static_cast<uint16_t *>(a.out) + row * N;
+    if constexpr (EPI == EPI_F16 || EPI == EPI_F32) {
 #pragma unroll
         for (int cc = 0; cc < C; ++cc) {
             const int g = (cc * W + w) * L + pos;
 #pragma unroll
             for (int p = 0; p < M / 4; ++p)
-                store4(yr + g * M + 4 * p, &v[cc][4 * p]);
+                store_y4<EPI>(a.out, row * N + g * M + 4 * p, &v[cc][4 * p]);
         }
     } else {
         static_assert(EPI == EPI_SYM || EPI == EPI_SYM8, "small-m kernels serve activations");
@@ -718,8 +740,7 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
     }
     const float c = a.c;
     const int chunks = n / 8;
-    if constexpr (EPI == EPI_F16) {
-        uint16_t *yr = static_cast<uint16_t *>(a.out) + row * n;
+    if constexpr (EPI == EPI_F16 || EPI == EPI_F32) {
         for (int ch = tid; ch < chunks; ch += 64 * W) {
             float y[8];
 #pragma unroll
@@ -727,7 +748,7 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
                 const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
                 y[e] = __builtin_fmaf(rowbuf[gi * LD + b], c, 0.0f);  // zeros +0
             }
-            store8(yr + ch * 8, y);
+            store_y8<EPI>(a.out, row * n + ch * 8, y);
         }
     } else {
         static_assert(EPI == EPI_SYM || EPI == EPI_SYM8, "large-m kernels serve activations");
@@ -816,6 +837,98 @@ __global__ __launch_bounds__(256) void k_swiglu(const uint16_t *g, const uint16_
         float v[8];
         load_row8<PRO_SWIGLU>(a, c * 8, v);
         store8(h + c * 8, v);  // exact: v holds fp16 values
+    }
+}
+
+// ------------------------------------------------ weights' clip search ---
+
+// Per-row clip search (§5 Setup: the weights' clipping ratio by a linear
+// search over the squared error; App. A.2).  One block per row.  For each
+// candidate c_j = RN32((100 - j) / 100) the symmetric quantizer's scale and
+// codes, and E_j = sum (y - q s16)^2 with each difference exact in fp64,
+// summed per thread over its chunks and then across the block in a fixed
+// order.  The row keeps the first j with the smallest E_j, then writes its
+// codes, scale and clip.
+template <int BITS, typename TIN>
+__global__ __launch_bounds__(256) void k_quant_search(SearchArgs a)
+{
+    constexpr int QMAX = BITS == 4 ? 7 : BITS == 6 ? 31 : 127;
+    constexpr float QF = (float)QMAX;
+    __shared__ float redf[4];
+    __shared__ double redd[4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t row = blockIdx.x;
+    const int n = a.n, chunks = n / 8;
+    const TIN *yr = static_cast<const TIN *>(a.y) + row * n;
+    auto load = [&](int ch, float *v) {
+        if constexpr (sizeof(TIN) == 4) {
+            const float4 p0 = reinterpret_cast<const float4 *>(yr + ch * 8)[0];
+            const float4 p1 = reinterpret_cast<const float4 *>(yr + ch * 8)[1];
+            v[0] = p0.x, v[1] = p0.y, v[2] = p0.z, v[3] = p0.w;
+            v[4] = p1.x, v[5] = p1.y, v[6] = p1.z, v[7] = p1.w;
+        } else {
+            load8(reinterpret_cast<const uint16_t *>(yr) + ch * 8, v);
+        }
+    };
+    float amax = 0.0f;
+    for (int ch = tid; ch < chunks; ch += 256) {
+        float v[8];
+        load(ch, v);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            amax = fmaxf(amax, fabsf(v[e]));
+    }
+    static_for<6>([&](auto J) { amax = lane_max<J>(amax); });
+    if (lane == 0)
+        redf[wave] = amax;
+    __syncthreads();
+    amax = fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3]));
+
+    double best_e = __builtin_inf();
+    float best_c = 1.0f;
+    for (int j = 0; j < a.ncand; ++j) {
+        const float c = (float)((double)(100 - j) / 100.0);
+        const float sf = h2f(f2h((amax * c) / QF));
+        const Divisor dv = make_divisor(sf);
+        double e = 0.0;
+        for (int ch = tid; ch < chunks; ch += 256) {
+            float v[8];
+            load(ch, v);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const float cq = dv.ok ? fminf(fmaxf(rintf(quotient(v[k], dv)), -QF - 1.0f), QF)
+                                       : 0.0f;
+                const double d = (double)v[k] - (double)cq * (double)sf;
+                e += d * d;  // two roundings, as the CPU reference
+            }
+        }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1)
+            e += __shfl_xor(e, o);
+        __syncthreads();  // redd of the previous candidate has been read
+        if (lane == 0)
+            redd[wave] = e;
+        __syncthreads();
+        e = ((redd[0] + redd[1]) + redd[2]) + redd[3];
+        if (e < best_e) {  // uniform across the block
+            best_e = e;
+            best_c = c;
+        }
+    }
+    const uint16_t s16 = f2h((amax * best_c) / QF);
+    const Divisor dv = make_divisor(h2f(s16));
+    uint8_t *qr = static_cast<uint8_t *>(a.q) + row * (BITS == 4 ? n / 2 : n);
+    for (int ch = tid; ch < chunks; ch += 256) {
+        float v[8];
+        load(ch, v);
+        if constexpr (BITS == 4)
+            store_codes8<EPI_SYM>(qr, ch * 8, v, dv, QF);
+        else
+            store_codes8<EPI_SYM8>(qr, ch * 8, v, dv, QF);
+    }
+    if (tid == 0) {
+        a.scale[row] = s16;
+        a.clip[row] = best_c;
     }
 }
 
@@ -1047,6 +1160,7 @@ hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, h
         return hipErrorInvalidValue;
     }
     switch (epi) {
+    case EPI_F32: return dispatch_rotated<EPI_F32, PRO_PLAIN>(a, k, m, s);
     case EPI_F16: return dispatch_rotated<EPI_F16, PRO_PLAIN>(a, k, m, s);
     case EPI_SYM: return dispatch_rotated<EPI_SYM, PRO_PLAIN>(a, k, m, s);
     case EPI_SYM8: return dispatch_rotated<EPI_SYM8, PRO_PLAIN>(a, k, m, s);
@@ -1055,6 +1169,29 @@ hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, h
                               : dispatch_pow2<EPI_KV, true, PRO_PLAIN>(a, k, s);
     }
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_quant_search(const SearchArgs &a, int bits, bool f32_in, hipStream_t s)
+{
+    if (a.rows == 0)
+        return hipSuccess;
+    const dim3 grid((unsigned)a.rows), block(256);
+    if (f32_in) {
+        if (bits == 4)
+            hipLaunchKernelGGL((k_quant_search<4, float>), grid, block, 0, s, a);
+        else if (bits == 6)
+            hipLaunchKernelGGL((k_quant_search<6, float>), grid, block, 0, s, a);
+        else
+            hipLaunchKernelGGL((k_quant_search<8, float>), grid, block, 0, s, a);
+    } else {
+        if (bits == 4)
+            hipLaunchKernelGGL((k_quant_search<4, uint16_t>), grid, block, 0, s, a);
+        else if (bits == 6)
+            hipLaunchKernelGGL((k_quant_search<6, uint16_t>), grid, block, 0, s, a);
+        else
+            hipLaunchKernelGGL((k_quant_search<8, uint16_t>), grid, block, 0, s, a);
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_swiglu(const uint16_t *g, const uint16_t *u, uint16_t *h, int64_t count,

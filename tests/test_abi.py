@@ -132,6 +132,15 @@ def test_invalid_arguments_rejected_before_device(L):
     assert L.quarot_linear_w8a8_workspace_size(3, 128) == 512 + 256
     assert L.quarot_linear_w8a8(P, P, P, P, 4, 4, 128, 1, 1.0, 8, P, 10, S) == WORKSPACE
     assert L.quarot_linear_w8a8(P, P, P, P, 4, 4, 128, 1, 1.0, 5, P, 4096, S) == INVALID
+    # clip search
+    assert L.quarot_quant_search(P, P, P, P, 4, 128, 1, 5, 20, P, 1 << 20, S) == INVALID
+    assert L.quarot_quant_search(P, P, P, P, 4, 128, 1, 4, 0, P, 1 << 20, S) == INVALID
+    assert L.quarot_quant_search(P, P, P, P, 4, 128, 1, 4, 101, P, 1 << 20, S) == INVALID
+    assert L.quarot_quant_search(P, P, P, P, 4, 100, 1, 4, 20, P, 1 << 20, S) == UNSUPPORTED
+    assert L.quarot_quant_search(P, P, P, P, 4, 128, 1, 4, 20, P, 100, S) == WORKSPACE
+    assert L.quarot_quant_search(P, P, P, None, 4, 128, 1, 4, 20, P, 1 << 20, S) == INVALID
+    assert L.quarot_quant_search_workspace_size(4, 128, 1) == 4 * 128 * 4
+    assert L.quarot_quant_search_workspace_size(4, 128, 0) == 0
     # kv append / decode attention
     assert L.quarot_kv_append(P, P, P, P, 4, 16, 16, 128, 128, 1, 0.95, S) == INVALID  # pos
     assert L.quarot_kv_append(P, P, P, P, 4, 16, -1, 128, 128, 1, 0.95, S) == INVALID
