@@ -159,6 +159,76 @@ def bench_kv(q, workloads, torch, np, dev, stream, iters):
     return res
 
 
+def time_us(torch, stream, fn, iters=10):
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(iters):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / iters * 1e3
+
+
+def bench_next(q, torch, dev, stream, layers):
+    """The built next rows on 70B shapes, timed in the same run:
+    - the down-projection input as silu(gate) * up -> H_1024 x H_28 -> int4
+      (fused, and unfused as quarot_swiglu then quarot_quant_int4);
+    - the out_proj input (64 heads x 128) through the head-wise Hadamard
+      -> int4;
+    - the 8-bit GEMM (W8A8) on both FFN shapes, its codes from
+      quarot_quant_int8 of the same activations and weights.
+    gate/up/attention-output rows are seeded torch.randn draws on the GPU."""
+    M = 16384
+    g = torch.Generator(device=dev)
+    g.manual_seed(1)
+    res = {}
+    n = 28672
+    gate = torch.randn((M, n), generator=g, device=dev).to(torch.float16)
+    up = torch.randn((M, n), generator=g, device=dev).to(torch.float16)
+    codes = torch.empty((M, n // 2), dtype=torch.uint8, device=dev)
+    sc = torch.empty(M, dtype=torch.float16, device=dev)
+    h = torch.empty_like(gate)
+    us = time_us(torch, stream, lambda: q.quarot_swiglu_quant_int4(gate, up, q=codes, scale=sc))
+    us_un = time_us(torch, stream, lambda: (q.quarot_swiglu(gate, up, h=h),
+                                            q.quarot_quant_int4(h, q=codes, scale=sc)))
+    nb = M * n * 4 + M * n // 2 + 2 * M
+    res["swiglu_quant_int4"] = {
+        "workload": f"gate, up fp16 [{M}, {n}] -> RN16(silu(gate) up) -> H_1024 x H_28 -> int4",
+        "us": round(us, 1), "GBps": round(nb / (us * 1e-6) / 1e9, 1),
+        "frac_hbm": round(nb / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+        "unfused_us": round(us_un, 1)}
+    del gate, up, h, codes
+    n = 8192
+    z = torch.randn((M, n), generator=g, device=dev).to(torch.float16)
+    codes = torch.empty((M, n // 2), dtype=torch.uint8, device=dev)
+    us = time_us(torch, stream,
+                 lambda: q.quarot_hadamard_heads_quant_int4(z, 64, q=codes, scale=sc))
+    nb = M * n * 2 + M * n // 2 + 2 * M
+    res["hadamard_heads_quant_int4"] = {
+        "workload": f"attention output fp16 [{M}, 64 heads x 128] -> H_64 x I_128 -> int4",
+        "us": round(us, 1), "GBps": round(nb / (us * 1e-6) / 1e9, 1),
+        "frac_hbm": round(nb / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    del z, codes
+    w8 = {}
+    for L in layers:
+        wl = L["wl"]
+        xq, sx = q.quarot_quant_int8(L["xd"], rotate=True, bits=8)
+        wd = torch.from_numpy(L["w"]).to(dev)
+        wq, sw = q.quarot_quant_int8(wd, rotate=True, bits=8)
+        del wd
+        y = L["y"]
+        us = time_us(torch, stream, lambda: q.quarot_w8a8_gemm(xq, sx, wq, sw, y=y))
+        ops = 2 * wl.M * wl.N * wl.K
+        w8[wl.name] = {"us": round(us, 1), "TOPS": round(ops / (us * 1e-6) / 1e12, 1),
+                       "frac_int8_peak": round(ops / (us * 1e-6) / 1e12 / PEAK_I8_TOPS, 4)}
+        del xq, wq
+    res["w8a8_gemm"] = w8
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -169,6 +239,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kv", action="store_true", help="skip the KV-cache leg")
     ap.add_argument("--kv-iters", type=int, default=5)
+    ap.add_argument("--no-next", action="store_true",
+                    help="skip the fused-prologue and 8-bit legs")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB once (a plain copy "
                          "kernel of known size, to scale hardware byte counters)")
@@ -259,6 +331,7 @@ def main():
         }
 
     kv = None if args.no_kv else bench_kv(q, workloads, torch, np, dev, stream, args.kv_iters)
+    nxt = None if args.no_next else bench_next(q, torch, dev, stream, layers)
 
     if args.copy_mib:
         src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
@@ -311,6 +384,7 @@ def main():
                      "frac": round(gemm_tops / PEAK_I8_TOPS, 4), "traffic": traffic},
         "kernels": kernels,
         "kv": kv,
+        "next": nxt,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
