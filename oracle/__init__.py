@@ -70,6 +70,8 @@ _SIGS = {
     "orc_quant_int8": (_I, [_P, _P, _P, _I64, _I64, _I, _F, _I]),
     "orc_gemm_i8": (_I, [_P, _P, _P, _I64, _I64, _I64]),
     "orc_quant_search": (_I, [_P, _P, _P, _P, _I64, _I64, _I, _I, _I]),
+    "orc_quant_int4_grouped": (_I, [_P, _P, _P, _I64, _I64, _I64, _I, _F]),
+    "orc_gemm_grouped": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I64]),
     "orc_set_threads": (None, [_I]),
     "orc_max_threads": (_I, []),
 }
@@ -236,6 +238,32 @@ def quant_search(w: np.ndarray, rotate: bool = True, bits: int = 4, n_candidates
     _check(lib().orc_quant_search(_ptr(_u16(w)), _ptr(q), _ptr(s), _ptr(c), rows, n,
                                   int(rotate), bits, n_candidates), "quant_search")
     return q, s.view(np.float16), c
+
+
+def quant_int4_grouped(x: np.ndarray, group: int = 128, rotate: bool = True, clip: float = 1.0):
+    """Group-wise int4: (codes [rows, n/2], scales fp16 group-major [n/group, rows])."""
+    x = _f16(x)
+    rows, n = x.shape
+    q = np.empty((rows, n // 2), np.uint8)
+    s = np.empty((n // group, rows), np.uint16)
+    _check(lib().orc_quant_int4_grouped(_ptr(_u16(x)), _ptr(q), _ptr(s), rows, n, group,
+                                        int(rotate), clip), "quant_int4_grouped")
+    return q, s.view(np.float16)
+
+
+def gemm_grouped(xq: np.ndarray, sx: np.ndarray, wq: np.ndarray, sw: np.ndarray,
+                 group: int = 128) -> np.ndarray:
+    """Group-wise W4A4 product with per-group dequant; sx [K/G, M], sw [K/G, N]."""
+    xq = np.ascontiguousarray(xq, dtype=np.uint8)
+    wq = np.ascontiguousarray(wq, dtype=np.uint8)
+    sx = _f16(sx)
+    sw = _f16(sw)
+    M, Kh = xq.shape
+    N = wq.shape[0]
+    y = np.empty((M, N), np.uint16)
+    _check(lib().orc_gemm_grouped(_ptr(xq), _ptr(_u16(sx)), _ptr(wq), _ptr(_u16(sw)), _ptr(y),
+                                  M, N, 2 * Kh, group), "gemm_grouped")
+    return y.view(np.float16)
 
 
 def gemm_i8(xq: np.ndarray, wq: np.ndarray) -> np.ndarray:

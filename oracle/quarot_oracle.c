@@ -840,15 +840,88 @@ int orc_gemm_i8(const int8_t *xq, const int8_t *wq, int32_t *acc, int64_t M, int
     return ORC_OK;
 }
 
-/* ------------------------------------------------------------------------ */
-/* Integer GEMM and dequantization (§4 Stage 2b, App. A.10).                */
-/* ------------------------------------------------------------------------ */
-
 static int nibble(const uint8_t *row, int64_t k)
 {
     int v = (row[k >> 1] >> ((k & 1) * 4)) & 0xF;
     return v >= 8 ? v - 16 : v;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Group-wise W4A4 (§5.3 group-wise ablation: a scale per group of G        */
+/* consecutive input channels, for the activations and the weights).        */
+/* ------------------------------------------------------------------------ */
+
+/* Each (rotated) row in groups of G consecutive elements, each group
+ * quantized exactly like a row of quant_sym_row (its own absmax and fp16
+ * scale).  Codes [rows, n/2] as usual; scales group-major: s[g * rows + r]. */
+int orc_quant_int4_grouped(const uint16_t *x, uint8_t *q, uint16_t *s, int64_t rows, int64_t n,
+                           int64_t G, int rotate, float clip)
+{
+    if (n <= 0 || rows < 0 || G <= 0 || (G & 1) || n % G)
+        return ORC_ERR_ARG;
+    struct rot_plan pl = {0, 1, 1.0f, NULL};
+    if (rotate) {
+        int st = plan_init(&pl, n);
+        if (st)
+            return st;
+    }
+    const int64_t ng = n / G;
+    int err = 0;
+#pragma omp parallel for schedule(static) reduction(| : err)
+    for (int64_t r = 0; r < rows; r++) {
+        float *t = (float *)malloc((size_t)n * 3 * sizeof(float));
+        if (!t) {
+            err |= 1;
+            continue;
+        }
+        for (int64_t i = 0; i < n; i++)
+            t[i] = orc_f16_to_f32(x[r * n + i]);
+        const float *y = t;
+        if (rotate) {
+            rotate_row(t, t + n, t + 2 * n, n, pl.k, pl.m, pl.Hm, pl.c);
+            y = t + n;
+        }
+        for (int64_t g = 0; g < ng; g++)
+            quant_sym_row(y + g * G, G, clip, q + r * (n / 2) + g * (G / 2), s + g * rows + r);
+        free(t);
+    }
+    free(pl.Hm);
+    return err ? ORC_ERR_NOMEM : ORC_OK;
+}
+
+/* The group-wise product: per group g of G columns of K, acc_g exact in
+ * int32 and t_g = RN(RN(f32(acc_g) * sx[g][m]) * sw[g][n]) (the per-token
+ * dequant of §4 Stage 2b, per group); Y = RN16 of the binary32 sum
+ * ((+0 + t_0) + t_1) + ..., in increasing g.  sx [K/G, M], sw [K/G, N]. */
+int orc_gemm_grouped(const uint8_t *xq, const uint16_t *sx, const uint8_t *wq, const uint16_t *sw,
+                     uint16_t *y, int64_t M, int64_t N, int64_t K, int64_t G)
+{
+    if (K <= 0 || (K & 1) || M < 0 || N < 0 || G <= 0 || K % G)
+        return ORC_ERR_ARG;
+    const int64_t ng = K / G;
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; m++) {
+        const uint8_t *xr = xq + m * (K / 2);
+        for (int64_t n = 0; n < N; n++) {
+            const uint8_t *wr = wq + n * (K / 2);
+            float sum = 0.0f;
+            for (int64_t g = 0; g < ng; g++) {
+                int32_t a = 0;
+                for (int64_t k = g * G; k < (g + 1) * G; k++)
+                    a += nibble(xr, k) * nibble(wr, k);
+                float t = (float)a * orc_f16_to_f32(sx[g * M + m]);
+                t = t * orc_f16_to_f32(sw[g * N + n]);
+                sum = sum + t;
+            }
+            y[m * N + n] = orc_f32_to_f16(sum);
+        }
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Integer GEMM and dequantization (§4 Stage 2b, App. A.10).                */
+/* ------------------------------------------------------------------------ */
 
 /* acc[M, N] = Xq[M, K] . Wq[N, K]^T, exact in int32 (|acc| <= 64 K). */
 int orc_gemm_i32(const uint8_t *xq, const uint8_t *wq, int32_t *acc, int64_t M, int64_t N,
