@@ -178,7 +178,9 @@ def bench_next(q, torch, dev, stream, layers):
     - the out_proj input (64 heads x 128) through the head-wise Hadamard
       -> int4;
     - the 8-bit GEMM (W8A8) on both FFN shapes, its codes from
-      quarot_quant_int8 of the same activations and weights.
+      quarot_quant_int8 of the same activations and weights;
+    - group-wise W4A4: the group quantizer (rotation to binary32, then
+      per-group scales) and the grouped GEMM on the FFN shapes.
     gate/up/attention-output rows are seeded torch.randn draws on the GPU."""
     M = 16384
     g = torch.Generator(device=dev)
@@ -225,6 +227,32 @@ def bench_next(q, torch, dev, stream, layers):
                        "frac_int8_peak": round(ops / (us * 1e-6) / 1e12 / PEAK_I8_TOPS, 4)}
         del xq, wq
     res["w8a8_gemm"] = w8
+    # group-wise W4A4 (G = 128 on both FFN shapes; 64 and 256 on the up
+    # shape): rotate to binary32 + group quantizer, and the grouped GEMM
+    gw = {}
+    for L in layers:
+        wl = L["wl"]
+        for G in ((64, 128, 256) if wl.name == "llama2_70b_up" else (128,)):
+            wd = torch.from_numpy(L["w"]).to(dev)
+            wq, sw = q.quarot_quant_int4_grouped(wd, group=G, rotate=True)
+            del wd
+            xq = torch.empty((wl.M, wl.K // 2), dtype=torch.uint8, device=dev)
+            sx = torch.empty((wl.K // G, wl.M), dtype=torch.float16, device=dev)
+            ws = torch.empty(q.lib().quarot_quant_int4_grouped_workspace_size(wl.M, wl.K, 1),
+                             dtype=torch.uint8, device=dev)
+            us_q = time_us(torch, stream, lambda: q.quarot_quant_int4_grouped(
+                L["xd"], group=G, rotate=True, q=xq, scale=sx, workspace=ws))
+            del ws
+            y = L["y"]
+            us_g = time_us(torch, stream,
+                           lambda: q.quarot_w4a4_gemm_grouped(xq, sx, wq, sw, group=G, y=y))
+            ops = 2 * wl.M * wl.N * wl.K
+            gw[f"{wl.name}_g{G}"] = {
+                "quant_us": round(us_q, 1), "gemm_us": round(us_g, 1),
+                "gemm_TOPS": round(ops / (us_g * 1e-6) / 1e12, 1),
+                "frac_int8_peak": round(ops / (us_g * 1e-6) / 1e12 / PEAK_I8_TOPS, 4)}
+            del xq, sx, wq, sw
+    res["w4a4_grouped"] = gw
     torch.cuda.empty_cache()
     return res
 

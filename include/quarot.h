@@ -211,6 +211,58 @@ quarot_status quarot_quant_search(const quarot_f16 *w, void *q, quarot_f16 *scal
                                   void *stream);
 
 /*
+ * Group-wise quantization (§5.3, the group-size ablation of W4A4: a scale
+ * per group of `group` consecutive input channels).  Each row (rotated by
+ * H_n first when rotate != 0, kept in binary32) is cut into n / group
+ * groups; each group is quantized exactly as quarot_quant_int4 quantizes a
+ * whole row (its own absmax, s16 = RN16(absmax * clip_ratio / 7), codes
+ * clamp(rint(y / s16), -8, 7)).
+ *   x fp16 [rows, n]; q uint8 [rows, n/2] (packed as quarot_quant_int4);
+ *   scale fp16 GROUP-MAJOR [n / group, rows]: scale[g * rows + r];
+ *   workspace: quarot_quant_int4_grouped_workspace_size(rows, n, rotate)
+ *   bytes (the binary32 rotated rows; 0 without rotation), 16-B aligned.
+ * group: a power of two in [8, 512] dividing n.  Two launches with
+ * rotation (rotate to binary32, then quantize), one without.
+ */
+size_t quarot_quant_int4_grouped_workspace_size(int64_t rows, int64_t n, int rotate);
+quarot_status quarot_quant_int4_grouped(const quarot_f16 *x, uint8_t *q, quarot_f16 *scale,
+                                        int64_t rows, int64_t n, int64_t group, int rotate,
+                                        float clip_ratio, void *workspace,
+                                        size_t workspace_bytes, void *stream);
+
+/*
+ * Group-wise W4A4 product (§5.3 group-size ablation; the per-token dequant
+ * of §4 Stage 2b applied per group).  For each group g of `group` columns
+ * of K: acc_g = exact int32 dot product of the codes,
+ * t_g = RN(RN(f32(acc_g) * sx[g][m]) * sw[g][n]), and
+ * y[m][n] = RN16(((+0 + t_0) + t_1) + ... ) in increasing g, in binary32.
+ *   xq uint8 [M, K/2], wq uint8 [N, K/2] (packed int4 codes);
+ *   sx fp16 [K/group, M], sw fp16 [K/group, N] (group-major, as written by
+ *   quarot_quant_int4_grouped); y fp16 [M, N].
+ * group: 64, 128 or 256; K a multiple of max(group, 128), K <= 65536.
+ * One launch.
+ */
+quarot_status quarot_w4a4_gemm_grouped(const uint8_t *xq, const quarot_f16 *sx,
+                                       const uint8_t *wq, const quarot_f16 *sw, quarot_f16 *y,
+                                       int64_t M, int64_t N, int64_t K, int64_t group,
+                                       void *stream);
+
+/*
+ * The group-wise linear layer: quarot_quant_int4_grouped of x [M, K] into
+ * the workspace, then quarot_w4a4_gemm_grouped.  wq, sw come from
+ * quarot_quant_int4_grouped of W [N, K] with the same group and rotate.
+ * workspace: quarot_linear_w4a4_grouped_workspace_size(M, K, group, rotate)
+ * bytes, 256-B aligned (codes, then scales, then binary32 rotated rows).
+ */
+size_t quarot_linear_w4a4_grouped_workspace_size(int64_t M, int64_t K, int64_t group,
+                                                 int rotate);
+quarot_status quarot_linear_w4a4_grouped(const quarot_f16 *x, const uint8_t *wq,
+                                         const quarot_f16 *sw, quarot_f16 *y, int64_t M,
+                                         int64_t N, int64_t K, int64_t group, int rotate,
+                                         float clip_ratio, void *workspace,
+                                         size_t workspace_bytes, void *stream);
+
+/*
  * The elementwise SwiGLU product alone: h = RN16(RN(silu(gate) * up)) with
  * the binary32 silu recipe of quarot_swiglu_quant_int4 below.
  * gate, up, h fp16 [count]; count a multiple of 8 (0 is a no-op).

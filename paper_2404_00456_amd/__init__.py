@@ -56,6 +56,13 @@ SIGNATURES = {
     "quarot_quant_search_workspace_size": (ctypes.c_size_t, [_I64, _I64, _I]),
     "quarot_quant_search": (_I, [_P, _P, _P, _P, _I64, _I64, _I, _I, _I, _P, ctypes.c_size_t,
                                  _P]),
+    "quarot_quant_int4_grouped_workspace_size": (ctypes.c_size_t, [_I64, _I64, _I]),
+    "quarot_quant_int4_grouped": (_I, [_P, _P, _P, _I64, _I64, _I64, _I, _F, _P,
+                                       ctypes.c_size_t, _P]),
+    "quarot_w4a4_gemm_grouped": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _P]),
+    "quarot_linear_w4a4_grouped_workspace_size": (ctypes.c_size_t, [_I64, _I64, _I64, _I]),
+    "quarot_linear_w4a4_grouped": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I64, _I, _F, _P,
+                                        ctypes.c_size_t, _P]),
     "quarot_swiglu": (_I, [_P, _P, _P, _I64, _P]),
     "quarot_swiglu_quant_int4": (_I, [_P, _P, _P, _P, _I64, _I64, _F, _P]),
     "quarot_hadamard_heads": (_I, [_P, _P, _I64, _I64, _I64, _P]),
@@ -303,6 +310,68 @@ def quarot_quant_search(w: torch.Tensor, rotate: bool = True, bits: int = 4,
     return q, scale, clip
 
 
+def quarot_quant_int4_grouped(x: torch.Tensor, group: int = 128, rotate: bool = True,
+                              clip_ratio: float = 1.0, q: Optional[torch.Tensor] = None,
+                              scale: Optional[torch.Tensor] = None,
+                              workspace: Optional[torch.Tensor] = None,
+                              stream: Optional[torch.cuda.Stream] = None):
+    """Group-wise symmetric int4 of x [rows, n] (optionally rotated first).
+    Returns (codes uint8 [rows, n/2], scale fp16 [n/group, rows])."""
+    rows, n = x.shape
+    dev = x.device
+    if q is None:
+        q = torch.empty((rows, n // 2), dtype=torch.uint8, device=dev)
+    if scale is None:
+        scale = torch.empty((n // group if group > 0 else 0, rows), dtype=torch.float16,
+                            device=dev)
+    need = int(lib().quarot_quant_int4_grouped_workspace_size(rows, n, int(bool(rotate))))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _check("quarot_quant_int4_grouped", lib().quarot_quant_int4_grouped(
+        _ptr(x, torch.float16, "x"), _ptr(q, torch.uint8, "q"),
+        _ptr(scale, torch.float16, "scale"), rows, n, int(group), int(bool(rotate)),
+        float(clip_ratio), _ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
+        _stream(stream)))
+    return q, scale
+
+
+def quarot_w4a4_gemm_grouped(xq: torch.Tensor, sx: torch.Tensor, wq: torch.Tensor,
+                             sw: torch.Tensor, group: int = 128,
+                             y: Optional[torch.Tensor] = None,
+                             stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """Group-wise W4A4 product; sx [K/group, M], sw [K/group, N] group-major."""
+    M, Kh = xq.shape
+    N = wq.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=xq.device)
+    _check("quarot_w4a4_gemm_grouped", lib().quarot_w4a4_gemm_grouped(
+        _ptr(xq, torch.uint8, "xq"), _ptr(sx, torch.float16, "sx"), _ptr(wq, torch.uint8, "wq"),
+        _ptr(sw, torch.float16, "sw"), _ptr(y, torch.float16, "y"), M, N, 2 * Kh, int(group),
+        _stream(stream)))
+    return y
+
+
+def quarot_linear_w4a4_grouped(x: torch.Tensor, wq: torch.Tensor, sw: torch.Tensor,
+                               group: int = 128, rotate: bool = True, clip_ratio: float = 1.0,
+                               y: Optional[torch.Tensor] = None,
+                               workspace: Optional[torch.Tensor] = None,
+                               stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """The group-wise 4-bit linear layer (quantize x per group, grouped GEMM)."""
+    M, K = x.shape
+    N = wq.shape[0]
+    need = int(lib().quarot_linear_w4a4_grouped_workspace_size(M, K, int(group),
+                                                               int(bool(rotate))))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    _check("quarot_linear_w4a4_grouped", lib().quarot_linear_w4a4_grouped(
+        _ptr(x, torch.float16, "x"), _ptr(wq, torch.uint8, "wq"), _ptr(sw, torch.float16, "sw"),
+        _ptr(y, torch.float16, "y"), M, N, K, int(group), int(bool(rotate)), float(clip_ratio),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream)))
+    return y
+
+
 def quarot_swiglu(gate: torch.Tensor, up: torch.Tensor, h: Optional[torch.Tensor] = None,
                   stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """h = RN16(silu(gate) * up) elementwise (binary32 silu recipe)."""
@@ -458,6 +527,7 @@ __all__ = [
     "quarot_hadamard_factor_table", "quarot_linear_workspace_size", "quarot_hadamard",
     "quarot_quant_int4", "quarot_w4a4_gemm", "quarot_linear", "prepare_weight",
     "quarot_quant_int8", "quarot_w8a8_gemm", "quarot_linear_w8a8", "quarot_quant_search",
+    "quarot_quant_int4_grouped", "quarot_w4a4_gemm_grouped", "quarot_linear_w4a4_grouped",
     "quarot_swiglu", "quarot_swiglu_quant_int4", "quarot_hadamard_heads", "quarot_hadamard_heads_quant_int4",
     "quarot_kv_quant", "quarot_kv_dequant", "quarot_kv_append",
     "quarot_kv_attention_workspace_size", "quarot_kv_decode_attention",

@@ -465,6 +465,173 @@ quarot_status quarot_quant_search(const quarot_f16 *w, void *q, quarot_f16 *scal
     return e == hipSuccess ? QUAROT_OK : hip_fail(e);
 }
 
+// ---------------------------------------------------------- group-wise ---
+
+namespace {
+
+quarot_status check_group(int64_t n, int64_t group)
+{
+    if (group <= 0)
+        return QUAROT_ERR_INVALID_ARG;
+    if (group < 8 || group > 512 || (group & (group - 1)) || n % group)
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    return QUAROT_OK;
+}
+
+quarot_status check_group_quant_grid(int64_t rows, int64_t n, int64_t group)
+{
+    const int64_t rpb = 256 / (group / 8);  // rows per block of the group quantizer
+    if ((rows + rpb - 1) / rpb * (n / group) > 0x7FFFFFFF)
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    return QUAROT_OK;
+}
+
+quarot_status check_gemm_grouped_sizes(int64_t M, int64_t N, int64_t K, int64_t group)
+{
+    quarot_status st = check_gemm_sizes(M, N, K);
+    if (st)
+        return st;
+    if (group != 64 && group != 128 && group != 256)
+        return group <= 0 ? QUAROT_ERR_INVALID_ARG : QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (K % (group < 128 ? 128 : group))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (M > 0 && N > 0 && (int64_t)((M + 255) / 256) * ((N + 127) / 128) > 0x7FFFFFFF)
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    return QUAROT_OK;
+}
+
+size_t f32_rows_bytes(int64_t rows, int64_t n)
+{
+    return ((size_t)rows * (size_t)n * sizeof(float) + 255) & ~(size_t)255;
+}
+
+// Rotation to binary32 (when asked) and the group quantizer.
+quarot_status group_quant(const quarot_f16 *x, uint8_t *q, quarot_f16 *scale, int64_t rows,
+                          int64_t n, int64_t group, bool rotate, int k, int m, float clip,
+                          void *f32_rows, hipStream_t s)
+{
+    if (rotate) {
+        RotArgs a{};
+        a.x = x;
+        a.out = f32_rows;
+        a.rows = rows;
+        a.n = (int)n;
+        a.c = rotation_scale(n);
+        a.clip = 1.0f;
+        hipError_t e = launch_rotate(a, EPI_F32, true, k, m, s);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    hipError_t e = launch_quant_grouped(rotate ? f32_rows : (const void *)x, rotate, q, scale,
+                                        rows, (int)n, (int)group, clip, s);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+}  // namespace
+
+size_t quarot_quant_int4_grouped_workspace_size(int64_t rows, int64_t n, int rotate)
+{
+    if (rows < 0 || n <= 0 || !rotate)
+        return 0;
+    return f32_rows_bytes(rows, n);
+}
+
+quarot_status quarot_quant_int4_grouped(const quarot_f16 *x, uint8_t *q, quarot_f16 *scale,
+                                        int64_t rows, int64_t n, int64_t group, int rotate,
+                                        float clip_ratio, void *workspace,
+                                        size_t workspace_bytes, void *stream)
+{
+    if (rows < 0 || !clip_ok(clip_ratio))
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;
+    quarot_status st = check_rot_size(n, rotate != 0, rotate ? EPI_F32 : EPI_SYM, &k, &m);
+    if (st)
+        return st;
+    if ((st = check_group(n, group)) || (st = check_group_quant_grid(rows, n, group)))
+        return st;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!x || !q || !scale)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(q) || !aligned16(scale))
+        return QUAROT_ERR_ALIGNMENT;
+    const size_t need = quarot_quant_int4_grouped_workspace_size(rows, n, rotate);
+    if (need && (!workspace || workspace_bytes < need))
+        return QUAROT_ERR_WORKSPACE;
+    if (need && !aligned16(workspace))
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    return group_quant(x, q, scale, rows, n, group, rotate != 0, k, m, clip_ratio, workspace,
+                       (hipStream_t)stream);
+}
+
+quarot_status quarot_w4a4_gemm_grouped(const uint8_t *xq, const quarot_f16 *sx,
+                                       const uint8_t *wq, const quarot_f16 *sw, quarot_f16 *y,
+                                       int64_t M, int64_t N, int64_t K, int64_t group,
+                                       void *stream)
+{
+    quarot_status st = check_gemm_grouped_sizes(M, N, K, group);
+    if (st || M == 0 || N == 0)
+        return st;
+    if ((st = check_gemm(xq, sx, wq, sw, y, nullptr, M, N, K)))
+        return st;
+    if ((st = check_device()))
+        return st;
+    GemmArgs a{xq, sx, wq, sw, y, nullptr, (int)M, (int)N, (int)K};
+    hipError_t e = launch_gemm_grouped(a, (int)group, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+size_t quarot_linear_w4a4_grouped_workspace_size(int64_t M, int64_t K, int64_t group,
+                                                 int rotate)
+{
+    if (M < 0 || K <= 0 || group <= 0 || K % group)
+        return 0;
+    const size_t scales = ((size_t)(K / group) * (size_t)M * 2 + 255) & ~(size_t)255;
+    return codes_bytes(M, K) + scales + (rotate ? f32_rows_bytes(M, K) : 0);
+}
+
+quarot_status quarot_linear_w4a4_grouped(const quarot_f16 *x, const uint8_t *wq,
+                                         const quarot_f16 *sw, quarot_f16 *y, int64_t M,
+                                         int64_t N, int64_t K, int64_t group, int rotate,
+                                         float clip_ratio, void *workspace,
+                                         size_t workspace_bytes, void *stream)
+{
+    if (M < 0 || N < 0 || !clip_ok(clip_ratio))
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;
+    quarot_status st = check_rot_size(K, rotate != 0, rotate ? EPI_F32 : EPI_SYM, &k, &m);
+    if (st)
+        return st;
+    if ((st = check_gemm_grouped_sizes(M, N, K, group)) ||
+        (st = check_group_quant_grid(M, K, group)))
+        return st;
+    if (M == 0 || N == 0)
+        return QUAROT_OK;
+    if (!x || !wq || !sw || !y)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(wq) || !aligned16(sw) || !aligned16(y))
+        return QUAROT_ERR_ALIGNMENT;
+    if (!workspace ||
+        workspace_bytes < quarot_linear_w4a4_grouped_workspace_size(M, K, group, rotate))
+        return QUAROT_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    uint8_t *xq = static_cast<uint8_t *>(workspace);
+    quarot_f16 *sx = reinterpret_cast<quarot_f16 *>(xq + codes_bytes(M, K));
+    void *f32_rows = reinterpret_cast<uint8_t *>(sx) +
+                     (((size_t)(K / group) * (size_t)M * 2 + 255) & ~(size_t)255);
+    if ((st = group_quant(x, xq, sx, M, K, group, rotate != 0, k, m, clip_ratio, f32_rows,
+                          (hipStream_t)stream)))
+        return st;
+    GemmArgs ga{xq, sx, wq, sw, y, nullptr, (int)M, (int)N, (int)K};
+    hipError_t e = launch_gemm_grouped(ga, (int)group, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
 quarot_status quarot_swiglu(const quarot_f16 *gate, const quarot_f16 *up, quarot_f16 *h,
                             int64_t count, void *stream)
 {

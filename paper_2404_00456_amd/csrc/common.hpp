@@ -101,6 +101,13 @@ hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, h
                          int pro = PRO_PLAIN);
 // bits = 4: packed int4 codes [rows, K/2]; bits = 8: one int8 code per byte.
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s, int bits = 4);
+// Group-wise W4A4, groups of `group` (64, 128, 256) along K, K a multiple of
+// max(group, 128); a.sx [K/group, M], a.sw [K/group, N].
+hipError_t launch_gemm_grouped(const GemmArgs &a, int group, hipStream_t s);
+// Group-wise symmetric int4 of binary32 (f32_in) or fp16 rows: codes
+// [rows, n/2], scales group-major [n/group, rows].
+hipError_t launch_quant_grouped(const void *y, bool f32_in, uint8_t *q, uint16_t *scale,
+                                int64_t rows, int n, int group, float clip, hipStream_t s);
 hipError_t launch_kv_dequant(const KvDeqArgs &a, bool inverse_rotate, hipStream_t s);
 hipError_t launch_swiglu(const uint16_t *g, const uint16_t *u, uint16_t *h, int64_t count,
                          hipStream_t s);

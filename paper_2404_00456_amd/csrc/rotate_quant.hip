@@ -932,6 +932,48 @@ __global__ __launch_bounds__(256) void k_quant_search(SearchArgs a)
     }
 }
 
+// --------------------------------------------- group-wise quantization ---
+
+// Group-wise symmetric int4 (§5.3 group-wise ablation): every G = 8 L
+// consecutive elements of a row get their own absmax, fp16 scale and codes,
+// exactly as a whole row does per token.  L lanes hold one group (8
+// elements each) and reduce its absmax among themselves; a block of 256
+// threads covers one group column g of 256 / L consecutive rows, so the
+// group-major scale writes s[g][r0 ..] are contiguous.
+template <int LOGL, typename TIN>
+__global__ __launch_bounds__(256) void k_quant_grouped(const void *y, uint8_t *q,
+                                                       uint16_t *scale, int64_t rows, int n,
+                                                       float clip)
+{
+    constexpr int L = 1 << LOGL, G = 8 * L, R = 256 / L;
+    const int ng = n / G;
+    const int g = (int)(blockIdx.x % (unsigned)ng);
+    const int64_t row = (int64_t)(blockIdx.x / (unsigned)ng) * R + (threadIdx.x >> LOGL);
+    const int li = threadIdx.x & (L - 1);
+    if (row >= rows)  // a whole group of lanes leaves together
+        return;
+    const int64_t e0 = row * n + (int64_t)g * G + li * 8;
+    float v[8];
+    if constexpr (sizeof(TIN) == 4) {
+        const float4 p0 = reinterpret_cast<const float4 *>(static_cast<const float *>(y) + e0)[0];
+        const float4 p1 = reinterpret_cast<const float4 *>(static_cast<const float *>(y) + e0)[1];
+        v[0] = p0.x, v[1] = p0.y, v[2] = p0.z, v[3] = p0.w;
+        v[4] = p1.x, v[5] = p1.y, v[6] = p1.z, v[7] = p1.w;
+    } else {
+        load8(static_cast<const uint16_t *>(y) + e0, v);
+    }
+    float amax = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        amax = fmaxf(amax, fabsf(v[e]));
+    static_for<LOGL>([&](auto J) { amax = lane_max<J>(amax); });
+    const uint16_t s16 = f2h((amax * clip) / 7.0f);
+    const Divisor dv = make_divisor(h2f(s16));
+    store_codes8<EPI_SYM>(q, e0, v, dv, 7.0f);
+    if (li == 0)
+        scale[(int64_t)g * rows + row] = s16;
+}
+
 // ------------------------------------------------------ KV dequant -------
 
 template <int LOGL, int C, bool INV>
@@ -1192,6 +1234,40 @@ hipError_t launch_quant_search(const SearchArgs &a, int bits, bool f32_in, hipSt
             hipLaunchKernelGGL((k_quant_search<8, uint16_t>), grid, block, 0, s, a);
     }
     return hipGetLastError();
+}
+
+template <typename TIN>
+static hipError_t quant_grouped_as(const void *y, uint8_t *q, uint16_t *scale, int64_t rows,
+                                   int n, int group, float clip, hipStream_t s)
+{
+    const int logl = ilog2(group / 8);
+    const int64_t rpb = 256 >> logl;  // rows per block
+    const int64_t blocks = (rows + rpb - 1) / rpb * (n / group);
+    if (blocks > 0x7FFFFFFF)
+        return hipErrorInvalidValue;
+    const dim3 grid((unsigned)blocks), block(256);
+    switch (logl) {
+    case 0: hipLaunchKernelGGL((k_quant_grouped<0, TIN>), grid, block, 0, s, y, q, scale, rows, n, clip); break;
+    case 1: hipLaunchKernelGGL((k_quant_grouped<1, TIN>), grid, block, 0, s, y, q, scale, rows, n, clip); break;
+    case 2: hipLaunchKernelGGL((k_quant_grouped<2, TIN>), grid, block, 0, s, y, q, scale, rows, n, clip); break;
+    case 3: hipLaunchKernelGGL((k_quant_grouped<3, TIN>), grid, block, 0, s, y, q, scale, rows, n, clip); break;
+    case 4: hipLaunchKernelGGL((k_quant_grouped<4, TIN>), grid, block, 0, s, y, q, scale, rows, n, clip); break;
+    case 5: hipLaunchKernelGGL((k_quant_grouped<5, TIN>), grid, block, 0, s, y, q, scale, rows, n, clip); break;
+    case 6: hipLaunchKernelGGL((k_quant_grouped<6, TIN>), grid, block, 0, s, y, q, scale, rows, n, clip); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_quant_grouped(const void *y, bool f32_in, uint8_t *q, uint16_t *scale,
+                                int64_t rows, int n, int group, float clip, hipStream_t s)
+{
+    if (group < 8 || group > 512 || (group & (group - 1)) || n % group)
+        return hipErrorInvalidValue;
+    if (rows == 0)
+        return hipSuccess;
+    return f32_in ? quant_grouped_as<float>(y, q, scale, rows, n, group, clip, s)
+                  : quant_grouped_as<uint16_t>(y, q, scale, rows, n, group, clip, s);
 }
 
 hipError_t launch_swiglu(const uint16_t *g, const uint16_t *u, uint16_t *h, int64_t count,

@@ -185,6 +185,41 @@ def test_invalid_arguments_rejected_before_device(L):
     assert L.quarot_hadamard_heads(None, None, 0, 64, 128, S) == OK
     assert L.quarot_hadamard_heads_quant_int4(P, P2, None, 4, 64, 128, 1.0, S) == INVALID
     assert L.quarot_hadamard_heads_quant_int4(P, P2, P, 4, 64, 128, 2.0, S) == INVALID
+    # group-wise
+    G = L.quarot_quant_int4_grouped
+    assert G(P, P2, P, 4, 128, 128, 1, 1.0, P, 1 << 20, S) != INVALID  # valid: device check
+    assert G(P, P2, P, 4, 128, 0, 1, 1.0, P, 1 << 20, S) == INVALID
+    assert G(P, P2, P, 4, 128, 48, 1, 1.0, P, 1 << 20, S) == UNSUPPORTED   # not a power of two
+    assert G(P, P2, P, 4, 128, 4, 1, 1.0, P, 1 << 20, S) == UNSUPPORTED    # below 8
+    assert G(P, P2, P, 4, 1024, 1024, 1, 1.0, P, 1 << 20, S) == UNSUPPORTED  # above 512
+    assert G(P, P2, P, 4, 384, 256, 0, 1.0, P, 1 << 20, S) == UNSUPPORTED  # does not divide n
+    assert G(P, P2, P, 4, 128, 64, 1, 0.0, P, 1 << 20, S) == INVALID
+    assert G(P, P2, P, 4, 128, 64, 1, 1.0, P, 100, S) == WORKSPACE
+    assert G(P, P2, P, 4, 128, 64, 1, 1.0, None, 0, S) == WORKSPACE
+    assert G(P, None, P, 4, 128, 64, 1, 1.0, P, 1 << 20, S) == INVALID
+    assert G(P, P2, UNALIGNED, 4, 128, 64, 1, 1.0, P, 1 << 20, S) == ALIGN
+    assert G(None, None, None, 0, 128, 64, 1, 1.0, None, 0, S) == OK
+    assert L.quarot_quant_int4_grouped_workspace_size(4, 128, 1) == 4 * 128 * 4
+    assert L.quarot_quant_int4_grouped_workspace_size(4, 128, 0) == 0
+    GG = L.quarot_w4a4_gemm_grouped
+    assert GG(P, P, P, P, P, 4, 4, 256, 32, S) == UNSUPPORTED
+    assert GG(P, P, P, P, P, 4, 4, 256, 512, S) == UNSUPPORTED
+    assert GG(P, P, P, P, P, 4, 4, 256, 0, S) == INVALID
+    assert GG(P, P, P, P, P, 4, 4, 192, 64, S) == UNSUPPORTED   # K not a multiple of 128
+    assert GG(P, P, P, P, P, 4, 4, 384, 256, S) == UNSUPPORTED  # K not a multiple of 256
+    assert GG(P, None, P, P, P, 4, 4, 256, 128, S) == INVALID
+    assert GG(P, P, P, P, UNALIGNED, 4, 4, 256, 128, S) == ALIGN
+    assert GG(None, None, None, None, None, 0, 4, 256, 128, S) == OK
+    LG = L.quarot_linear_w4a4_grouped
+    need = L.quarot_linear_w4a4_grouped_workspace_size(3, 256, 128, 1)
+    assert need == 512 + 256 + 3 * 256 * 4  # codes, scales, binary32 rows (256-B rounded)
+    assert L.quarot_linear_w4a4_grouped_workspace_size(3, 256, 128, 0) == 512 + 256
+    assert LG(P, P, P, P, 4, 4, 256, 128, 1, 1.0, P, 10, S) == WORKSPACE
+    assert LG(P, P, P, P, 4, 4, 256, 128, 1, 1.0, ctypes.c_void_p((1 << 20) + 16), 1 << 20,
+              S) == ALIGN
+    assert LG(P, P, P, P, 4, 4, 256, 96, 1, 1.0, P, 1 << 20, S) == UNSUPPORTED
+    assert LG(P, P, P, P, 4, 4, 256, 128, 1, 1.5, P, 1 << 20, S) == INVALID
+    assert LG(None, None, None, None, 0, 4, 256, 128, 1, 1.0, None, 0, S) == OK
 
 
 @pytest.mark.skipif(has_gpu(), reason="valid arguments would reach a real device")
@@ -195,6 +230,11 @@ def test_no_device_reported(L):
     assert L.quarot_w4a4_gemm(P, P, P, P, P, None, 4, 4, 128, None) == NODEV
     assert L.quarot_swiglu_quant_int4(P, P2, P, P2, 4, 28672, 1.0, None) == NODEV
     assert L.quarot_hadamard_heads_quant_int4(P, P2, P, 4, 64, 128, 1.0, None) == NODEV
+    assert L.quarot_quant_int4_grouped(P, P2, P, 4, 128, 128, 1, 1.0, P, 1 << 20,
+                                       None) == NODEV
+    assert L.quarot_w4a4_gemm_grouped(P, P, P, P, P, 4, 4, 256, 64, None) == NODEV
+    assert L.quarot_linear_w4a4_grouped(P, P, P, P, 4, 4, 256, 256, 1, 1.0, P, 1 << 20,
+                                        None) == NODEV
 
 
 def test_binding_rejects_host_tensors():
