@@ -54,7 +54,7 @@ GEMM_TRAFFIC = {"source_sha256_16": "7de0c60db672ea41", "bytes_per_launch": 3.45
 def gemm_source_hash() -> str:
     import hashlib
     h = hashlib.sha256()
-    for f in ("gemm_w4a4.hip", "common.hpp"):
+    for f in ("gemm_w4a4.hip", "gemm_common.hpp", "common.hpp"):
         with open(os.path.join(ROOT, "paper_2404_00456_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

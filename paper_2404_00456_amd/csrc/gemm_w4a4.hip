@@ -23,50 +23,12 @@
 // Blocks are numbered XCD by XCD (the dispatcher deals blocks to the eight
 // XCDs round-robin) and, within an XCD, in groups of 8 m-tiles, so blocks
 // that share an L2 also share operand panels.
-#include "common.hpp"
+#include "gemm_common.hpp"
 
 namespace quarot {
 namespace {
 
-typedef int v4i __attribute__((ext_vector_type(4)));
-typedef float f2 __attribute__((ext_vector_type(2)));
-typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-
-constexpr int BM = 256;   // X rows per block
-constexpr int BN = 256;   // W rows per block
-constexpr int BKB = 64;   // packed bytes per row per k-step
-constexpr int LDSR = 80;  // LDS row pitch (bytes)
-constexpr int GM = 8;     // m-tiles per group in the tile order
-constexpr int STAGE = (BM + BN) * LDSR;
-constexpr int LDS_BYTES = 2 * STAGE;
-
-__device__ __forceinline__ v4i widen(uint2 d)
-{
-    v4i r;
-    r[0] = (int)((d.x << 4) & 0xF0F0F0F0u);
-    r[1] = (int)(d.x & 0xF0F0F0F0u);
-    r[2] = (int)((d.y << 4) & 0xF0F0F0F0u);
-    r[3] = (int)(d.y & 0xF0F0F0F0u);
-    return r;
-}
-
-__device__ __forceinline__ void tile_of(int bid, int nblk, int TM, int TN, int &tm, int &tn)
-{
-    int t = bid;
-    if ((nblk & 7) == 0)
-        t = (bid & 7) * (nblk >> 3) + (bid >> 3);
-    const int gsize = GM * TN;
-    const int g = t / gsize;
-    const int first = g * GM;
-    const int gm = min(TM - first, GM);
-    const int r = t - g * gsize;
-    tm = first + r % gm;
-    tn = r / gm;
-}
-
-constexpr int THREADS = 512;
-constexpr int WN = 64;   // n per wave
-constexpr int NI = WN / 16;  // n slices per wave (MFMA A operands)
+using namespace gemm;
 
 __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_k64(GemmArgs a)
 {
@@ -215,274 +177,6 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_k64(GemmArgs a)
 
 
 // ------------------------------------------------------------------------
-// Group-wise W4A4 (a scale per group of GS = 64, 128 or 256 input channels
-// for activations and weights).  A k-step covers KS = max(GS, 128) k; the
-// MFMA substeps of one group accumulate its integer product in a temporary
-// (256 acc_g, exact), which is dequantized at once,
-// t = RN(RN(f32(acc_g) sx[g][m]) sw[g][n]), and added to binary32 output
-// accumulators in group order.  The binary32 accumulators live in VGPRs
-// next to the MFMA temporaries, so a wave covers 64 x 64 (block 256 x 128,
-// waves 4 x 2) instead of 128 x 64.  Scales are group-major
-// (sx [K/GS, M], sw [K/GS, N]); a lane's 4 row scales and four 4-column
-// scale quads of the next k-step's groups are fetched with its operands.
-constexpr int GBN = 128;  // W rows per block
-
-template <int GS>
-struct GroupTile {
-    static constexpr int KS = GS < 128 ? 128 : GS;  // k per k-step
-    static constexpr int SUB = KS / 64;             // MFMA substeps per k-step
-    static constexpr int GSUB = GS / 64;            // substeps per group
-    static constexpr int GPS = KS / GS;             // groups per k-step
-    static constexpr int ROWB = KS / 2;             // packed bytes per row per k-step
-    static constexpr int PITCH = ROWB + 16;         // LDS row pitch
-    static constexpr int TILE = (BM + GBN) * PITCH;
-    static constexpr int SCB = GPS * (BM + GBN) * 2;  // scale bytes: sx [GPS][BM], sw [GPS][GBN]
-    static constexpr int STAGE = TILE + SCB;
-    static constexpr int NSC = SCB / 16;              // 16-byte scale chunks per stage
-    static constexpr int LDS = 2 * STAGE;
-    static constexpr int CPR = ROWB / 16;           // 16-byte chunks per row
-    static constexpr int NLX = BM * CPR / THREADS;  // X chunks per thread
-    static constexpr int NLW = GBN * CPR / THREADS; // W chunks per thread
-    static constexpr bool CACHE_W = GS <= 128;      // W fragments kept across j
-    static constexpr bool FLOAT_SW = GPS == 1;      // sw held converted, else packed
-};
-
-template <int GS>
-__global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped(GemmArgs a)
-{
-    using T = GroupTile<GS>;
-    extern __shared__ __align__(16) uint8_t lds[];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;  // 64-row x 64-column wave tiles
-    const int M = a.M, N = a.N, K = a.K;
-    const int TM = (M + BM - 1) / BM, TN = (N + GBN - 1) / GBN;
-    int tm, tn;
-    tile_of(blockIdx.x, gridDim.x, TM, TN, tm, tn);
-    const int m0 = tm * BM, n0 = tn * GBN;
-    const int64_t ldk = K / 2;
-    const int KT = K / T::KS;
-
-    // global -> LDS: 16-byte chunk id = tid + 512 i, CPR chunks per row
-    const uint8_t *gx[T::NLX];
-    const uint8_t *gw[T::NLW];
-    int xrow[T::NLX], xcol[T::NLX], wrow[T::NLW], wcol[T::NLW];
-#pragma unroll
-    for (int i = 0; i < T::NLX; ++i) {
-        const int id = tid + THREADS * i;
-        xrow[i] = id / T::CPR;
-        xcol[i] = id % T::CPR;
-        gx[i] = a.xq + (int64_t)min(m0 + xrow[i], M - 1) * ldk + xcol[i] * 16;
-    }
-#pragma unroll
-    for (int i = 0; i < T::NLW; ++i) {
-        const int id = tid + THREADS * i;
-        wrow[i] = id / T::CPR;
-        wcol[i] = id % T::CPR;
-        gw[i] = a.wq + (int64_t)min(n0 + wrow[i], N - 1) * ldk + wcol[i] * 16;
-    }
-
-    const int orow = lane & 15;
-    const int obyte = (lane >> 4) * 8;
-    const bool nvec = (N & 3) == 0;
-
-    // scales: thread tid < NSC fetches 8 consecutive fp16 of one group's
-    // sx (chunks 0..32 GPS - 1) or sw (the rest) of the next k-step
-    constexpr int XCH = BM / 8, WCH = GBN / 8;  // chunks per group
-    const bool sc_ld = tid < T::NSC;
-    const int sc_g2 = tid < T::GPS * XCH ? tid / XCH : (tid - T::GPS * XCH) / WCH;
-    const bool sc_x = tid < T::GPS * XCH;
-    const int sc_c = sc_x ? tid % XCH : (tid - T::GPS * XCH) % WCH;
-    const int sc_lim = sc_x ? M : N;                    // rows of the scale vector
-    const int sc_e0 = (sc_x ? m0 : n0) + sc_c * 8;      // first element
-    const bool sc_vec = ((sc_x ? M : N) & 7) == 0 && sc_e0 + 7 < sc_lim;
-    const int sc_lds = T::TILE + (sc_x ? sc_g2 * BM + sc_c * 8
-                                       : T::GPS * BM + sc_g2 * GBN + sc_c * 8) * 2;
-
-    uint4 px[T::NLX], pw[T::NLW], psc;
-    auto gload = [&](int kt) {
-#pragma unroll
-        for (int i = 0; i < T::NLX; ++i)
-            px[i] = *reinterpret_cast<const uint4 *>(gx[i] + (int64_t)kt * T::ROWB);
-#pragma unroll
-        for (int i = 0; i < T::NLW; ++i)
-            pw[i] = *reinterpret_cast<const uint4 *>(gw[i] + (int64_t)kt * T::ROWB);
-        if (sc_ld) {
-            const int64_t g = (int64_t)kt * T::GPS + sc_g2;
-            const uint16_t *v = (sc_x ? a.sx : a.sw) + g * sc_lim;
-            if (sc_vec) {
-                psc = *reinterpret_cast<const uint4 *>(v + sc_e0);
-            } else {
-                uint32_t h[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    h[e] = v[min(sc_e0 + e, sc_lim - 1)];
-                psc = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                                 h[6] | (h[7] << 16));
-            }
-        }
-    };
-    auto lstore = [&](int stage) {
-        uint8_t *base = lds + stage * T::STAGE;
-#pragma unroll
-        for (int i = 0; i < T::NLX; ++i)
-            *reinterpret_cast<uint4 *>(base + xrow[i] * T::PITCH + xcol[i] * 16) = px[i];
-#pragma unroll
-        for (int i = 0; i < T::NLW; ++i)
-            *reinterpret_cast<uint4 *>(base + (BM + wrow[i]) * T::PITCH + wcol[i] * 16) = pw[i];
-        if (sc_ld)
-            *reinterpret_cast<uint4 *>(base + sc_lds) = psc;
-    };
-    // this k-step's scales from LDS: sx divided by 256; sw converted (one
-    // group per k-step) or kept packed and converted at use (two groups)
-    float sxc[T::GPS][4], swc[T::FLOAT_SW ? 4 : 1][4];
-    uint2 swp[T::FLOAT_SW ? 1 : T::GPS][4];
-    auto scales = [&](const uint8_t *sb) {
-        const uint16_t *lsx = reinterpret_cast<const uint16_t *>(sb + T::TILE);
-        const uint16_t *lsw = lsx + T::GPS * BM;
-#pragma unroll
-        for (int g2 = 0; g2 < T::GPS; ++g2) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                sxc[g2][j] = h2f(lsx[g2 * BM + wm * 64 + j * 16 + orow]) * 0x1p-8f;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint2 w2 = *reinterpret_cast<const uint2 *>(
-                    lsw + g2 * GBN + wn * 64 + i * 16 + (lane >> 4) * 4);
-                if constexpr (T::FLOAT_SW) {
-                    swc[i][0] = h2f((uint16_t)w2.x);
-                    swc[i][1] = h2f((uint16_t)(w2.x >> 16));
-                    swc[i][2] = h2f((uint16_t)w2.y);
-                    swc[i][3] = h2f((uint16_t)(w2.y >> 16));
-                } else {
-                    swp[g2][i] = w2;
-                }
-            }
-        }
-    };
-    auto swv = [&](int g2, int i, int r) {
-        if constexpr (T::FLOAT_SW)
-            return swc[i][r];
-        else {
-            const uint32_t w = r < 2 ? swp[g2][i].x : swp[g2][i].y;
-            return h2f((uint16_t)(w >> (16 * (r & 1))));
-        }
-    };
-
-    float yacc[4][4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                yacc[i][j][r] = 0.0f;
-
-    gload(0);
-    lstore(0);
-    __syncthreads();
-
-    for (int kt = 0; kt < KT; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < KT)
-            gload(kt + 1);
-        const uint8_t *sb = lds + cur * T::STAGE;
-        scales(sb);
-        auto wfrag = [&](int kk, int i) {
-            return widen(*reinterpret_cast<const uint2 *>(
-                sb + (BM + wn * 64 + i * 16 + orow) * T::PITCH + kk * 32 + obyte));
-        };
-        v4i aq[T::CACHE_W ? T::SUB : 1][4];
-        if constexpr (T::CACHE_W) {
-#pragma unroll
-            for (int kk = 0; kk < T::SUB; ++kk)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    aq[kk][i] = wfrag(kk, i);
-        }
-        // units u = (j, g2): the MFMAs of unit u + 1 are issued before the
-        // dequant of unit u, and nothing moves across units, so two sets of
-        // temporaries are live at a time
-        constexpr int U = 4 * T::GPS;
-        auto mfma_unit = [&](auto UI, v4i(&t)[4]) {
-            constexpr int j = decltype(UI)::value / T::GPS, g2 = decltype(UI)::value % T::GPS;
-            if constexpr (!T::CACHE_W)  // W fragments are read again per unit, not kept
-                __asm__ volatile("" ::: "memory");
-            const uint8_t *p = sb + (wm * 64 + j * 16 + orow) * T::PITCH + obyte;
-#pragma unroll
-            for (int s2 = 0; s2 < T::GSUB; ++s2) {
-                const int kk = g2 * T::GSUB + s2;
-                const v4i bq = widen(*reinterpret_cast<const uint2 *>(p + kk * 32));
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    v4i w;
-                    if constexpr (T::CACHE_W)
-                        w = aq[kk][i];
-                    else
-                        w = wfrag(kk, i);
-                    t[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
-                        w, bq, s2 == 0 ? v4i{0, 0, 0, 0} : t[i], 0, 0, 0);
-                }
-            }
-        };
-        // f32(256 acc_g) (sx / 256) is RN(f32(acc_g) sx): the same real, no
-        // overflow or underflow; then * sw, then the add
-        auto dequant_unit = [&](auto UI, const v4i(&t)[4]) {
-            constexpr int j = decltype(UI)::value / T::GPS, g2 = decltype(UI)::value % T::GPS;
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float u = ((float)t[i][r] * sxc[g2][j]) * swv(g2, i, r);
-                    yacc[i][j][r] = yacc[i][j][r] + u;
-                    // pinned here: otherwise the dequant sinks below the
-                    // later units' MFMAs and all their temporaries stay live
-                    __asm__ volatile("" : "+v"(yacc[i][j][r]));
-                }
-        };
-        v4i ta[4], tb[4];
-        mfma_unit(std::integral_constant<int, 0>{}, ta);
-        static_for<U>([&](auto UI) {
-            constexpr int u = decltype(UI)::value;
-            if constexpr (u + 1 < U)
-                mfma_unit(std::integral_constant<int, u + 1>{}, (u & 1) ? ta : tb);
-            __builtin_amdgcn_sched_barrier(0);
-            dequant_unit(UI, (u & 1) ? tb : ta);
-            __builtin_amdgcn_sched_barrier(0);
-        });
-        if (kt + 1 < KT)
-            lstore(cur ^ 1);
-        __syncthreads();
-    }
-
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int nb = n0 + wn * 64 + i * 16 + (lane >> 4) * 4;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int m = m0 + wm * 64 + j * 16 + orow;
-            if (m >= M)
-                continue;
-            uint16_t hv[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                hv[r] = f2h(yacc[i][j][r]);
-            uint16_t *yrow = a.y + (int64_t)m * N;
-            if (nvec && nb + 3 < N) {
-                uint2 pk;
-                pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
-                pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
-                *reinterpret_cast<uint2 *>(yrow + nb) = pk;
-            } else {
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    if (nb + r < N)
-                        yrow[nb + r] = hv[r];
-            }
-        }
-    }
-}
-
-// ------------------------------------------------------------------------
 // Main kernel (K a multiple of 128).  Same block tile, waves and epilogue as
 // the fallback above; the operand path differs:
 //
@@ -507,38 +201,6 @@ constexpr int DPW = RING_STAGE / 1024 / (THREADS / 64);  // DMAs per wave per k-
 constexpr int SCALE_BYTES = 2 * (BM + BN) * 2;
 constexpr int MAIN_LDS_BYTES = RING_BYTES + SCALE_BYTES;
 
-typedef __attribute__((address_space(3))) void lds_void;
-
-// 16 bytes per lane from global memory straight into LDS at
-// lds_base + 16 * lane.  Issued as inline asm on purpose: for the compiler's
-// own LDS-DMA builtin the waitcnt pass cannot tell the DMA target from the
-// stage being read and waits for every DMA before each LDS read, which
-// serializes the ring.  Here only the explicit s_waitcnt below orders it.
-// The kernel uses M0 for nothing else (checked in its ISA); the s_nop is
-// the wait state the ISA asks for between an SALU write of M0 and a VMEM
-// instruction with LDS destination.
-__device__ __forceinline__ void dma16(const void *g, uint32_t lds_base)
-{
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-                 :
-                 : "v"(g), "s"(lds_base)
-                 : "memory");
-}
-
-// 4 bytes per lane into LDS at lds_base + 4 * lane (same rules as dma16).
-__device__ __forceinline__ void dma4(const void *g, uint32_t lds_base)
-{
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
-                 :
-                 : "v"(g), "s"(lds_base)
-                 : "memory");
-}
-
-// s_waitcnt immediate: vmcnt(vm) expcnt(7) lgkmcnt(lgkm) in the gfx9 layout
-constexpr int waitcnt_imm(int vm, int lgkm)
-{
-    return (vm & 15) | (((vm >> 4) & 3) << 14) | (7 << 4) | ((lgkm & 15) << 8);
-}
 
 // Persistent: each block walks a range of tiles.  Block b sits on XCD b % 8
 // (the dispatcher deals blocks round-robin), so the 8 XCDs own contiguous
@@ -881,36 +543,6 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w8a8(GemmArgs a)
 }
 
 }  // namespace
-
-namespace {
-template <int GS>
-hipError_t gemm_grouped_as(const GemmArgs &a, hipStream_t s)
-{
-    using T = GroupTile<GS>;
-    if (a.K % T::KS)
-        return hipErrorInvalidValue;
-    const int TM = (a.M + BM - 1) / BM, TN = (a.N + GBN - 1) / GBN;
-    hipError_t e = hipFuncSetAttribute((const void *)k_gemm_w4a4_grouped<GS>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, T::LDS);
-    if (e != hipSuccess)
-        return e;
-    hipLaunchKernelGGL(k_gemm_w4a4_grouped<GS>, dim3((unsigned)(TM * TN)), dim3(THREADS), T::LDS,
-                       s, a);
-    return hipGetLastError();
-}
-}  // namespace
-
-hipError_t launch_gemm_grouped(const GemmArgs &a, int group, hipStream_t s)
-{
-    if (a.M == 0 || a.N == 0)
-        return hipSuccess;
-    switch (group) {
-    case 64: return gemm_grouped_as<64>(a, s);
-    case 128: return gemm_grouped_as<128>(a, s);
-    case 256: return gemm_grouped_as<256>(a, s);
-    }
-    return hipErrorInvalidValue;
-}
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s, int bits)
 {

@@ -51,7 +51,11 @@ def rand_group_case(seed, M, N, K, group):
 @pytest.mark.parametrize("M,N,K,group", [
     (1, 1, 128, 128), (16, 256, 128, 64), (255, 257, 256, 128), (300, 520, 1024, 256),
     (513, 100, 4096, 128), (64, 1000, 11008, 64), (64, 1000, 11008, 128),
-    (40, 300, 11008, 256), (2, 3, 65536, 64), (7, 129, 65536, 256)])
+    (40, 300, 11008, 256), (2, 3, 65536, 64), (7, 129, 65536, 256),
+    # M, N multiples of 8 (the persistent ring kernel): ragged tiles, fewer
+    # k-steps than ring stages (one tile per block), a single k-step
+    (8, 8, 256, 256), (264, 136, 2048, 128), (1024, 1024, 256, 128), (520, 392, 128, 64),
+    (24, 8192, 65536, 128)])
 def test_gemm_grouped(dev, orc, M, N, K, group):
     import paper_2404_00456_amd as q
     say(f"grouped gemm M={M} N={N} K={K} group={group}")
