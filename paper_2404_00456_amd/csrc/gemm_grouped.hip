@@ -27,6 +27,16 @@ using namespace gemm;
 // below takes M and N multiples of 8.
 constexpr int GBN = 128;  // W rows per block
 
+// Integer to binary32 without a conversion instruction: an MFMA temporary
+// started at kMagic (the bits of M = 1.5 * 2^23) instead of 0 ends as the
+// bits of M + 256 acc_g, since |256 acc_g| <= 2^22 keeps the sum in
+// [2^23, 2^24], where the float spacing is 1.  Hence (bits as float) - M is
+// f32(256 acc_g) exactly, and with sxc = sx / 256 (an fp16 significand, 11
+// bits) the product M * sxc has at most 12 significant bits and is exact,
+// so fma(bits as float, sxc, -M * sxc) = RN(f32(acc_g) sx) in one step.
+constexpr int kMagic = 0x4B400000;
+constexpr float kMagicF = 0x1.8p23f;
+
 template <int GS>
 struct GroupTile {
     static constexpr int KS = GS < 128 ? 128 : GS;  // k per k-step
@@ -510,14 +520,16 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_ring(GemmArgs 
             // this step's scales: sx / 256, sw converted (one group per
             // step) or packed and converted at use (two groups)
             const uint16_t *lsc = reinterpret_cast<const uint16_t *>(sb + C::OPB);
-            float sxc[C::GPS][4];
+            float sxc[C::GPS][4], nsxc[C::GPS][4];
             float swc[C::GPS == 1 ? 4 : 1][4];
             uint2 swp[C::GPS == 1 ? 1 : C::GPS][4];
 #pragma unroll
             for (int g2 = 0; g2 < C::GPS; ++g2) {
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+                for (int j = 0; j < 4; ++j) {
                     sxc[g2][j] = h2f(lsc[256 * g2 + wm * 64 + j * 16 + orow]) * 0x1p-8f;
+                    nsxc[g2][j] = -(kMagicF * sxc[g2][j]);  // exact: 12 significant bits
+                }
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const uint2 w2 = *reinterpret_cast<const uint2 *>(
@@ -559,17 +571,22 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_ring(GemmArgs 
                         else
                             w8 = half8(wr[i], sub);
                         tt[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
-                            widen(w8), bq, s2 == 0 ? v4i{0, 0, 0, 0} : tt[i], 0, 0, 0);
+                            widen(w8), bq, s2 == 0 ? v4i{kMagic, kMagic, kMagic, kMagic} : tt[i],
+                            0, 0, 0);
                     }
                 }
             };
+            // the temporaries hold M + 256 acc_g as binary32 bits (see
+            // kMagic): fma(that, sx / 256, -M sx / 256) = RN(f32(acc_g) sx)
             auto dequant_unit = [&](auto UI, const v4i(&tt)[4]) {
                 constexpr int j = decltype(UI)::value / C::GPS, g2 = decltype(UI)::value % C::GPS;
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        const float u = ((float)tt[i][r] * sxc[g2][j]) * swv(g2, i, r);
+                        const int bits = tt[i][r];  // (a vector element is not bit_cast directly)
+                        const float v = __int_as_float(bits);
+                        const float u = __builtin_fmaf(v, sxc[g2][j], nsxc[g2][j]) * swv(g2, i, r);
                         yacc[i][j][r] = yacc[i][j][r] + u;
                         __asm__ volatile("" : "+v"(yacc[i][j][r]));
                     }
@@ -580,8 +597,17 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_ring(GemmArgs 
                 constexpr int u = decltype(UI)::value;
                 if constexpr (u + 1 < U)
                     mfma_unit(std::integral_constant<int, u + 1>{}, (u & 1) ? ta : tb);
-                __builtin_amdgcn_sched_barrier(0);
                 dequant_unit(UI, (u & 1) ? tb : ta);
+                // the next unit's MFMAs spread among this unit's dequant, so
+                // the matrix core works while the VALU does
+                if constexpr (u + 1 < U) {
+                    constexpr int NM = 4 * C::GSUB;
+#pragma unroll
+                    for (int k = 0; k < NM; ++k) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x002, 56 / NM, 0);
+                    }
+                }
                 __builtin_amdgcn_sched_barrier(0);
             });
 
