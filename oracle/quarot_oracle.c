@@ -48,6 +48,29 @@
  *      dequant yhat = RN(RN(f32(q) * f32(s16)) + f32(z16)), optionally
  *      rotated back (H/sqrt(n) is an involution for symmetric Sylvester H),
  *      then RN16.
+ *  - 6/8-bit variants (§5.3 RTN rows, App. A.6): the symmetric quantizer with
+ *    qmax = 2^(bits-1) - 1 in place of 7, codes clamped to [-qmax-1, qmax],
+ *    one signed byte each; int8 x int8 -> int32, dequant as above.
+ *  - Weight clip search (§5 Setup, App. A.2): candidates
+ *    c_j = RN32((100 - j) / 100), the error sum_i (y_i - q_i s16)^2 in fp64
+ *    with each difference exact, the first j of least error.
+ *  - Group-wise (§5.3 group-size ablation): each group of G channels of a
+ *    (rotated) row quantized like a whole row, scales group-major [n/G, rows];
+ *    the product sums t_g = RN(RN(f32(acc_g) sx_g) sw_g) over g in increasing
+ *    order from +0 in binary32.
+ *  - SwiGLU input (§4 Stage 1b): h = RN16(RN(silu(g) u)) with a fixed binary32
+ *    silu (Cody-Waite reduction, degree-7 Taylor exp; see orc_silu_f32).
+ *  - Decode attention (§4 Stage 2c): fp64 scores and softmax over the exactly
+ *    dequantized cache, the output rounded once to fp16.
+ *
+ * Pins: every function here is checked by tests/test_oracle_*.py against
+ * something other than itself (paper values, closed forms, brute force,
+ * numpy/scipy/torch references, exact-rational searches).  Parity unpinned
+ * (conventions with no external definition, fixed here and shared by the
+ * GPU side): the binary32 order of the butterfly stages (checked exactly only
+ * where no rounding occurs), which Hadamard matrix of each order m is used,
+ * the silu recipe's exp (pinned to 4 ulps of the true exp), and the order of
+ * the group-wise sum (pinned within its rounding bound).
  */
 #include <math.h>
 #include <stdint.h>

@@ -88,6 +88,19 @@ def test_hadamard_fp16(dev, orc, n):
     assert_fp16_close(y, orc.hadamard(x), f"hadamard n={n}")
 
 
+@pytest.mark.parametrize("n", [8, 128, 1024, 8192, 32768, 24, 3072, 5120, 28672, 216, 11008])
+def test_hadamard_in_place(dev, orc, n):
+    """x == y is allowed: every kernel family (power of two, exact small m,
+    fp64 large m) reads a row whole before writing it."""
+    import paper_2404_00456_amd as q
+    rows = 261 if n <= 1024 else 7
+    say(f"hadamard in place n={n} rows={rows}")
+    x = workloads.random_rows(n + 5, rows, n, "normal")
+    xd = T(x, dev)
+    q.quarot_hadamard(xd, y=xd)
+    assert_fp16_close(H(xd), orc.hadamard(x), f"hadamard in place n={n}")
+
+
 @pytest.mark.parametrize("n", ROT_SIZES)
 def test_quant_int4_rotated(dev, orc, n):
     import paper_2404_00456_amd as q
