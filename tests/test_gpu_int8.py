@@ -96,3 +96,25 @@ def test_linear_w8a8_layer(dev, orc, name, rows, bits):
     rxq, rsx = orc.quant_int8(x[sel], rotate=True, clip=1.0, bits=bits)
     ry = orc.dequant(orc.gemm_i8(rxq, rwq), rsx, rsw)
     assert_fp16_close(y[sel], ry, f"{name} int{bits} y")
+
+
+@pytest.mark.parametrize("name", ["llama2_70b_up", "llama2_70b_down"])
+def test_linear_w8a8_full_size(dev, orc, name):
+    """The benchmarked W8A8 shapes (M = 16384), outputs sampled by row: a
+    row of y depends on its own codes and scale only."""
+    import paper_2404_00456_amd as q
+    wl = workloads.LINEAR[name]
+    say(f"linear w8a8 full size {name}: inputs M={wl.M} K={wl.K} N={wl.N}")
+    x, w, _ = workloads.linear_inputs(wl)
+    wq_d, sw_d = q.quarot_quant_int8(T(w, dev), rotate=True, bits=8)
+    rwq, rsw = orc.quant_int8(w, rotate=True, clip=1.0, bits=8)
+    assert_same(H(wq_d), rwq, f"{name} int8 weight codes")
+    assert_same(H(sw_d).view(np.uint16), rsw.view(np.uint16), f"{name} int8 weight scales")
+    del w
+    y = H(q.quarot_linear_w8a8(T(x, dev), wq_d, sw_d, rotate=True, bits=8))
+    rows = np.sort(np.random.default_rng(4).choice(wl.M, 12, replace=False))
+    rows[0], rows[-1] = 0, wl.M - 1
+    say(f"linear w8a8 full size {name}: oracle on {len(rows)} rows")
+    rxq, rsx = orc.quant_int8(x[rows], rotate=True, clip=1.0, bits=8)
+    ry = orc.dequant(orc.gemm_i8(rxq, rwq), rsx, rsw)
+    assert_fp16_close(y[rows], ry, f"{name} int8 y rows")

@@ -48,7 +48,9 @@ def check_attention(dev, orc, q, k, v, seq, G, what):
 @pytest.mark.parametrize("nkv,rep,s_max,seq,D,G", [
     (1, 1, 1, 1, 128, 128), (3, 1, 40, 17, 128, 128), (16, 1, 300, 300, 128, 64),
     (4, 8, 512, 511, 128, 128), (8, 1, 2048, 1500, 64, 32), (2, 2, 1000, 999, 256, 128),
-    (64, 1, 4096, 4096, 128, 128), (1, 1, 9000, 8191, 128, 128)])
+    (64, 1, 4096, 4096, 128, 128), (1, 1, 9000, 8191, 128, 128),
+    # the benchmarked decode step: 16 x 64 query rows over 4096 cached tokens
+    (1024, 1, 4096, 4096, 128, 128)])
 def test_decode_attention_random_cache(dev, orc, nkv, rep, s_max, seq, D, G):
     rng = np.random.default_rng(nkv * 7 + s_max + D + G)
     k = rand_cache(rng, nkv, s_max, D, G)
