@@ -36,6 +36,7 @@ if ROOT not in sys.path:
 
 # MI355X published peaks
 PEAK_I8_TOPS = 5000.0   # dense int8 MFMA, TOP/s
+PEAK_F32_ADDS = 78.6e12  # fp32 vector adds per second (157.3 TFLOP/s counts an FMA as 2)
 PEAK_HBM_GBS = 8000.0   # HBM3E, GB/s
 
 
@@ -349,14 +350,45 @@ def main():
     rbytes = [rotate_bytes(L["wl"].M, L["wl"].K) for L in layers]
     kernels = {}
     for li, L in enumerate(layers):
-        nm = L["wl"].name
+        wl = L["wl"]
+        nm = wl.name
+        k2, m = q.quarot_hadamard_factor(wl.K)
+        # VALU floor of the rotation: log2(2^k) butterfly adds and m - 1
+        # m-factor adds per element at the fp32 vector add rate
+        valu_us = wl.M * wl.K * (k2 + m - 1) / PEAK_F32_ADDS * 1e6
+        hbm_us = rbytes[li] / (PEAK_HBM_GBS * 1e9) * 1e6
+        pct = lambda a, p_: [round(float(np.percentile(a, p_)) * 1e3, 1) for p_ in p_]
         kernels[nm] = {
             "rotate_quant_us": round(rot_ms[li] * 1e3, 2),
+            "rotate_quant_us_p10_p50_p90": pct(rot[li], (10, 50, 90)),
             "rotate_quant_GBps": round(rbytes[li] / (rot_ms[li] * 1e-3) / 1e9, 1),
+            "rotate_quant_frac_hbm": round(hbm_us / (rot_ms[li] * 1e3), 4),
+            "rotate_quant_frac_valu_bound": round(valu_us / (rot_ms[li] * 1e3), 4),
             "gemm_us": round(gemm_ms[li] * 1e3, 2),
+            "gemm_us_p10_p50_p90": pct(gem[li], (10, 50, 90)),
             "gemm_TOPS": round(ops[li] / (gemm_ms[li] * 1e-3) / 1e12, 1),
             "linear_TOPS": round(ops[li] / ((gemm_ms[li] + rot_ms[li]) * 1e-3) / 1e12, 1),
         }
+
+    # the int8 MFMA peak re-derived from the device (CUs x peak clock x 8192
+    # ops per clock per CU) and an MFMA-only probe's attainable rate
+    cus, clk_khz = q.quarot_device_peaks()
+    probe_out = torch.empty(cus * 512, dtype=torch.int32, device=dev)
+    probe_ops = q.quarot_mfma_probe(probe_out, cus, 2000)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(10):
+        q.quarot_mfma_probe(probe_out, cus, 2000)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    probe_tops = probe_ops * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    del probe_out
+    peak_i8 = {"cus": cus, "peak_sclk_mhz": clk_khz / 1000,
+               "derived_TOPS": round(cus * clk_khz * 1e3 * 8192 / 1e12, 1),
+               "published_TOPS": PEAK_I8_TOPS,
+               "mfma_probe_TOPS": round(probe_tops, 1),
+               "gemm_frac_of_probe": round(gemm_tops / probe_tops, 4)}
 
     kv = None if args.no_kv else bench_kv(q, workloads, torch, np, dev, stream, args.kv_iters)
     nxt = None if args.no_next else bench_next(q, torch, dev, stream, layers)
@@ -411,6 +443,7 @@ def main():
                      "achieved": round(gemm_tops, 1), "peak": PEAK_I8_TOPS, "unit": "TOP/s",
                      "frac": round(gemm_tops / PEAK_I8_TOPS, 4), "traffic": traffic},
         "kernels": kernels,
+        "peak_i8": peak_i8,
         "kv": kv,
         "next": nxt,
         "cpu_baseline": cpu,

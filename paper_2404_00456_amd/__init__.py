@@ -41,6 +41,8 @@ SIGNATURES = {
     "quarot_status_string": (ctypes.c_char_p, [_I]),
     "quarot_last_hip_error": (_I, []),
     "quarot_version": (_I, []),
+    "quarot_device_peaks": (_I, [_P, _P]),
+    "quarot_mfma_probe": (_I, [_P, _I64, _I, _P]),
     "quarot_hadamard_factor": (_I, [_I64, _P, _P]),
     "quarot_hadamard_factor_table": (_I, [_I, _P]),
     "quarot_hadamard": (_I, [_P, _P, _I64, _I64, _P]),
@@ -143,6 +145,25 @@ def quarot_hadamard_factor(n: int) -> Optional[Tuple[int, int]]:
     m = ctypes.c_int()
     st = lib().quarot_hadamard_factor(n, ctypes.byref(k), ctypes.byref(m))
     return None if st else (k.value, m.value)
+
+
+def quarot_device_peaks() -> Tuple[int, int]:
+    """(compute units, peak shader clock in kHz) of the current device."""
+    cus = ctypes.c_int()
+    clk = ctypes.c_int()
+    _check("quarot_device_peaks", lib().quarot_device_peaks(ctypes.byref(cus), ctypes.byref(clk)))
+    return cus.value, clk.value
+
+
+def quarot_mfma_probe(out: torch.Tensor, blocks: int, iters: int,
+                      stream: Optional[torch.cuda.Stream] = None) -> int:
+    """Enqueue the int8-MFMA-only probe; returns its number of int ops
+    (2 per multiply-add).  out: int32 device tensor of blocks * 512."""
+    if out.numel() < blocks * 512:
+        raise ValueError("out must hold blocks * 512 int32")
+    _check("quarot_mfma_probe", lib().quarot_mfma_probe(
+        _ptr(out, torch.int32, "out"), int(blocks), int(iters), _stream(stream)))
+    return blocks * 8 * iters * 32 * 16384 * 2  # waves x MFMAs x multiply-adds x 2
 
 
 def quarot_hadamard_factor_table(m: int):
@@ -523,7 +544,8 @@ def quarot_kv_decode_attention(q: torch.Tensor, k_cache, v_cache, seq_len: int,
 
 
 __all__ = [
-    "QuarotError", "lib", "quarot_version", "quarot_hadamard_factor",
+    "QuarotError", "lib", "quarot_version", "quarot_device_peaks", "quarot_mfma_probe",
+    "quarot_hadamard_factor",
     "quarot_hadamard_factor_table", "quarot_linear_workspace_size", "quarot_hadamard",
     "quarot_quant_int4", "quarot_w4a4_gemm", "quarot_linear", "prepare_weight",
     "quarot_quant_int8", "quarot_w8a8_gemm", "quarot_linear_w8a8", "quarot_quant_search",

@@ -81,6 +81,10 @@ def test_workspace_size(L):
 
 
 def test_invalid_arguments_rejected_before_device(L):
+    # Every call here must be invalid: the pointers are fake, and a call
+    # with valid arguments would launch a kernel on them where a device is
+    # present.  Valid arguments are exercised only without a device
+    # (test_no_device_reported) and with real buffers in the GPU tests.
     S = None  # null stream
     # hadamard
     assert L.quarot_hadamard(P, P2, -1, 128, S) == INVALID
@@ -185,9 +189,14 @@ def test_invalid_arguments_rejected_before_device(L):
     assert L.quarot_hadamard_heads(None, None, 0, 64, 128, S) == OK
     assert L.quarot_hadamard_heads_quant_int4(P, P2, None, 4, 64, 128, 1.0, S) == INVALID
     assert L.quarot_hadamard_heads_quant_int4(P, P2, P, 4, 64, 128, 2.0, S) == INVALID
+    # measurement utilities
+    assert L.quarot_device_peaks(None, None) == INVALID
+    assert L.quarot_mfma_probe(P, 0, 10, S) == INVALID
+    assert L.quarot_mfma_probe(P, 4, 0, S) == INVALID
+    assert L.quarot_mfma_probe(None, 4, 10, S) == INVALID
+    assert L.quarot_mfma_probe(UNALIGNED, 4, 10, S) == ALIGN
     # group-wise
     G = L.quarot_quant_int4_grouped
-    assert G(P, P2, P, 4, 128, 128, 1, 1.0, P, 1 << 20, S) != INVALID  # valid: device check
     assert G(P, P2, P, 4, 128, 0, 1, 1.0, P, 1 << 20, S) == INVALID
     assert G(P, P2, P, 4, 128, 48, 1, 1.0, P, 1 << 20, S) == UNSUPPORTED   # not a power of two
     assert G(P, P2, P, 4, 128, 4, 1, 1.0, P, 1 << 20, S) == UNSUPPORTED    # below 8
@@ -233,6 +242,9 @@ def test_no_device_reported(L):
     assert L.quarot_quant_int4_grouped(P, P2, P, 4, 128, 128, 1, 1.0, P, 1 << 20,
                                        None) == NODEV
     assert L.quarot_w4a4_gemm_grouped(P, P, P, P, P, 4, 4, 256, 64, None) == NODEV
+    cus, clk = ctypes.c_int(), ctypes.c_int()
+    assert L.quarot_device_peaks(ctypes.byref(cus), ctypes.byref(clk)) == NODEV
+    assert L.quarot_mfma_probe(P, 4, 10, None) == NODEV
     assert L.quarot_linear_w4a4_grouped(P, P, P, P, 4, 4, 256, 256, 1, 1.0, P, 1 << 20,
                                         None) == NODEV
 
