@@ -32,6 +32,26 @@ def hipcc() -> str:
     return p if os.path.exists(p) else "hipcc"
 
 
+ISA_SHA = os.path.join(HERE, "gemm_isa.sha")
+
+
+def kernel_isa_sha(src: str, symbol: str) -> str:
+    """sha256[:16] of one kernel's gfx950 assembly (comments and directives
+    dropped): it changes exactly when that kernel's machine code does."""
+    cmd = [hipcc(), *[f for f in FLAGS if f not in ("-fPIC", "-shared")], "-I",
+           os.path.join(ROOT, "include"), "-S", "--cuda-device-only", src, "-o", "-"]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("hipcc -S failed for " + src)
+    asm = res.stdout
+    start = asm.index(symbol + ":")
+    body = asm[start:asm.index(".Lfunc_end", start)]
+    lines = [ln.split(";")[0].strip() for ln in body.splitlines()]
+    text = "\n".join(ln for ln in lines if ln and not ln.startswith("."))
+    import hashlib
+    return hashlib.sha256(text.encode()).hexdigest()[:16]
+
+
 def build(verbose: bool = False) -> str:
     srcs = [os.path.join(CSRC, s) for s in SOURCES]
     tmp = LIB + ".tmp"
@@ -44,6 +64,12 @@ def build(verbose: bool = False) -> str:
         sys.stderr.write(res.stdout + res.stderr)
         raise RuntimeError("hipcc failed building libquarot.so")
     os.replace(tmp, LIB)
+    # fingerprint of the per-token GEMM's machine code, which the bench's
+    # stored hardware byte counts refer to
+    sha = kernel_isa_sha(os.path.join(CSRC, "gemm_w4a4.hip"),
+                         "_ZN6quarot12_GLOBAL__N_111k_gemm_w4a4ENS_8GemmArgsE")
+    with open(ISA_SHA, "w") as f:
+        f.write(sha + "\n")
     return LIB
 
 
