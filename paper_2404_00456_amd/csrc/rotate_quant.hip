@@ -73,26 +73,38 @@ __device__ __forceinline__ float quotient(float y, const Divisor &d)
     return __builtin_fmaf(e, d.r, q0);
 }
 
+// Rounding to an integer code without conversion instructions: for t
+// clamped to the code range (|t| < 2^22), t + 1.5 * 2^23 lies in
+// [2^23, 2^24), where floats are spaced by 1, so the add rounds t to the
+// nearest integer, ties to even, and the low bits of the sum's encoding are
+// that integer in two's complement.  Clamping before rounding equals
+// rounding before clamping, as the bounds are integers.
+__device__ __forceinline__ uint32_t round_bits(float t)
+{
+    return __float_as_uint(t + 0x1.8p23f);
+}
+
 // Symmetric int4 code (§4 Stage 2b): clamp(rint_even(RN(y / sf)), -8, 7).
 __device__ __forceinline__ uint32_t sym_code(float y, const Divisor &d)
 {
-    const float c = fminf(fmaxf(rintf(quotient(y, d)), -8.0f), 7.0f);
-    return d.ok ? ((uint32_t)(int)c & 0xFu) : 0u;
+    const uint32_t c = round_bits(fminf(fmaxf(quotient(y, d), -8.0f), 7.0f)) & 0xFu;
+    return d.ok ? c : 0u;
 }
 
 // Asymmetric uint4 code: clamp(rint_even(RN(RN(y - zf) / sf)), 0, 15).
 __device__ __forceinline__ uint32_t asym_code(float y, const Divisor &d, float zf)
 {
-    const float c = fminf(fmaxf(rintf(quotient(y - zf, d)), 0.0f), 15.0f);
-    return d.ok ? (uint32_t)(int)c : 0u;
+    const uint32_t c = round_bits(fminf(fmaxf(quotient(y - zf, d), 0.0f), 15.0f)) & 0xFu;
+    return d.ok ? c : 0u;
 }
 
 // Symmetric code with qmax levels a side, as a byte:
 // clamp(rint_even(RN(y / sf)), -qmax - 1, qmax).
 __device__ __forceinline__ uint32_t sym8_code(float y, const Divisor &d, float qmaxf)
 {
-    const float c = fminf(fmaxf(rintf(quotient(y, d)), -qmaxf - 1.0f), qmaxf);
-    return d.ok ? ((uint32_t)(int)c & 0xFFu) : 0u;
+    const uint32_t c =
+        round_bits(fminf(fmaxf(quotient(y, d), -qmaxf - 1.0f), qmaxf)) & 0xFFu;
+    return d.ok ? c : 0u;
 }
 
 // The symmetric epilogues: scale divisor, row stride of the codes, and the
@@ -156,6 +168,29 @@ __device__ __forceinline__ void load8(const uint16_t *p, float *v)
     for (int i = 0; i < 4; ++i) {
         v[2 * i] = h2f((uint16_t)(w[i] & 0xFFFFu));
         v[2 * i + 1] = h2f((uint16_t)(w[i] >> 16));
+    }
+}
+
+// load8 followed by the butterfly on element bit 0, (t_2i, t_2i+1) ->
+// (RN(t_2i + t_2i+1), RN(t_2i - t_2i+1)) with t = f32(x): each output is one
+// v_fma_mix_f32 on the two fp16 halves of the dword, f32(a) * (+-1) + f32(b)
+// rounded once, so no conversion instruction is needed.  (Written as asm:
+// the compiler turns an fma by +-1 into an add of converted values.)
+__device__ __forceinline__ void load8_bit0(const uint16_t *p, float *v)
+{
+    uint4 raw = *reinterpret_cast<const uint4 *>(p);
+    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        float sum, dif;
+        // src0 = low half (sum) / high half (dif), src1 = +-1.0 as f32,
+        // src2 = high half (sum) / low half (dif)
+        __asm__("v_fma_mix_f32 %0, %1, 1.0, %1 op_sel:[0,0,1] op_sel_hi:[1,0,1]"
+                : "=v"(sum) : "v"(w[i]));
+        __asm__("v_fma_mix_f32 %0, %1, -1.0, %1 op_sel:[1,0,0] op_sel_hi:[1,0,1]"
+                : "=v"(dif) : "v"(w[i]));
+        v[2 * i] = sum;
+        v[2 * i + 1] = dif;
     }
 }
 
@@ -320,16 +355,22 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
         w = wave;
     }
 
+    // plain fp16 rows rotated from bit 0 take that butterfly in the load
+    constexpr bool BIT0 = ROT && PRO == PRO_PLAIN && !HEADS;
     float v[C][8];
 #pragma unroll
-    for (int cc = 0; cc < C; ++cc)
-        load_row8<PRO>(a, row * N + ((cc * W + w) * L + pos) * 8, v[cc]);
+    for (int cc = 0; cc < C; ++cc) {
+        if constexpr (BIT0)
+            load8_bit0(a.x + row * N + ((cc * W + w) * L + pos) * 8, v[cc]);
+        else
+            load_row8<PRO>(a, row * N + ((cc * W + w) * L + pos) * 8, v[cc]);
+    }
 
     if constexpr (ROT) {
         const int s0 = HEADS ? a.s0 : 0;
         // element bits 0..2: inside each chunk
 #pragma unroll
-        for (int h = 1, bit = 0; h < 8; h <<= 1, ++bit)
+        for (int h = BIT0 ? 2 : 1, bit = BIT0 ? 1 : 0; h < 8; h <<= 1, ++bit)
             if (bit >= s0)
 #pragma unroll
                 for (int cc = 0; cc < C; ++cc)
@@ -379,14 +420,21 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
                             v[cc + h][e] = p - q;
                         }
                     }
-        // y = u * c: sigma * c is exact and RN(sigma u * sigma c) = RN(u c);
-        // the fma with +0 makes a zero +0 (the sign folding can leave -0)
+        // y = u * c: sigma * c is exact and RN(sigma u * sigma c) = RN(u c).
+        // The sign folding can leave -0 where the result is +0: the fp16 /
+        // fp32 outputs take an fma with +0, which makes a zero +0; the
+        // quantizers do not see the sign of a zero (|y|, y / s), except the
+        // KV group bounds, which are made +0 once per group below.
         const float sc = sigma * a.c;
 #pragma unroll
         for (int cc = 0; cc < C; ++cc)
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                v[cc][e] = __builtin_fmaf(v[cc][e], sc, 0.0f);
+            for (int e = 0; e < 8; ++e) {
+                if constexpr (EPI == EPI_F16 || EPI == EPI_F32)
+                    v[cc][e] = __builtin_fmaf(v[cc][e], sc, 0.0f);
+                else
+                    v[cc][e] = v[cc][e] * sc;
+            }
     }
 
     if constexpr (EPI == EPI_F16 || EPI == EPI_F32) {
@@ -463,7 +511,8 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
             // the group's scale and zero, formed again only where a group
             // starts (uniform across the wave)
             if (cc == 0 || (!KVROW && (cc * L) % gl == 0)) {
-                const float mxc = mx[cc] * a.clip, mnc = mn[cc] * a.clip;
+                // + 0: a bound that is a zero is +0 (see the rotation above)
+                const float mxc = (mx[cc] + 0.0f) * a.clip, mnc = (mn[cc] + 0.0f) * a.clip;
                 const float s32 = (mxc - mnc) / 15.0f;
                 s16 = f2h(s32);
                 z16 = f2h(mnc);
@@ -596,12 +645,16 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
                     v[cc + h][b] = p - q;
                 }
             }
-    const float sc = sigma * a.c;  // as in k_rot_pow2: zeros come out +0
+    const float sc = sigma * a.c;  // as in k_rot_pow2: +0 zeros where the sign shows
 #pragma unroll
     for (int cc = 0; cc < C; ++cc)
 #pragma unroll
-        for (int b = 0; b < M; ++b)
-            v[cc][b] = __builtin_fmaf(v[cc][b], sc, 0.0f);
+        for (int b = 0; b < M; ++b) {
+            if constexpr (EPI == EPI_F16 || EPI == EPI_F32)
+                v[cc][b] = __builtin_fmaf(v[cc][b], sc, 0.0f);
+            else
+                v[cc][b] = v[cc][b] * sc;
+        }
 
     if constexpr (EPI == EPI_F16 || EPI == EPI_F32) {
 #pragma unroll
