@@ -239,6 +239,32 @@ __device__ __forceinline__ void dpp_fmac4(float &a, float &b, float &c, float &d
 }
 #undef QUAROT_DPP_FMAC4
 
+// Four lane-pair maxima (or minima) across position bit J = 0 or 1, each
+// one DPP-sourced v_max_f32 / v_min_f32 (the compiler's fmaxf of a DPP move
+// adds a canonicalizing max of its own); same hazard rule as above.
+#define QUAROT_DPP_MINMAX4(OP, CTL)                                                        \
+    asm volatile("s_nop 1\n\t"                                                             \
+                 OP "_dpp %0, %0, %0 " CTL " row_mask:0xf bank_mask:0xf\n\t"               \
+                 OP "_dpp %1, %1, %1 " CTL " row_mask:0xf bank_mask:0xf\n\t"               \
+                 OP "_dpp %2, %2, %2 " CTL " row_mask:0xf bank_mask:0xf\n\t"               \
+                 OP "_dpp %3, %3, %3 " CTL " row_mask:0xf bank_mask:0xf"                     \
+                 : "+v"(a), "+v"(b), "+v"(c), "+v"(d))
+
+template <int J, bool MAX>
+__device__ __forceinline__ void dpp_minmax4(float &a, float &b, float &c, float &d)
+{
+    static_assert(J == 0 || J == 1, "quad permutations only");
+    if constexpr (MAX && J == 0)
+        QUAROT_DPP_MINMAX4("v_max_f32", "quad_perm:[1,0,3,2]");
+    else if constexpr (MAX)
+        QUAROT_DPP_MINMAX4("v_max_f32", "quad_perm:[2,3,0,1]");
+    else if constexpr (J == 0)
+        QUAROT_DPP_MINMAX4("v_min_f32", "quad_perm:[1,0,3,2]");
+    else
+        QUAROT_DPP_MINMAX4("v_min_f32", "quad_perm:[2,3,0,1]");
+}
+#undef QUAROT_DPP_MINMAX4
+
 // One Walsh-Hadamard stage across position bit J on R registers (R a
 // multiple of 4), s = pos_sign(pos, J).  J < 4: DPP as above (flips the
 // sign of the lanes with the bit set).  J = 4, 5 (lane ^ 16 by ds_swizzle,

@@ -467,24 +467,30 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
         // blocks of 2, 4, 8, 16 lanes onto themselves); a larger group takes
         // all L positions of G/(8L) consecutive chunks.
         const int gl = KVROW ? L * C : a.group >> 3;  // positions per group
+        // chunk max and min as three-input max / min (v_max3 / v_min3: one
+        // instruction per two values)
         float mx[C], mn[C];
 #pragma unroll
         for (int cc = 0; cc < C; ++cc) {
-            mx[cc] = v[cc][0];
-            mn[cc] = v[cc][0];
-#pragma unroll
-            for (int e = 1; e < 8; ++e) {
-                mx[cc] = fmaxf(mx[cc], v[cc][e]);
-                mn[cc] = fminf(mn[cc], v[cc][e]);
-            }
+            const float *u = v[cc];
+            mx[cc] = fmaxf(fmaxf(fmaxf(fmaxf(u[0], u[1]), u[2]), fmaxf(u[3], u[4])),
+                           fmaxf(fmaxf(u[5], u[6]), u[7]));
+            mn[cc] = fminf(fminf(fminf(fminf(u[0], u[1]), u[2]), fminf(u[3], u[4])),
+                           fminf(fminf(u[5], u[6]), u[7]));
         }
         static_for<LOGL>([&](auto J) {
-            if ((1 << J) < gl)
+            if ((1 << J) < gl) {
+                if constexpr (C == 4 && J <= 1) {
+                    dpp_minmax4<J, true>(mx[0], mx[1], mx[2], mx[3]);
+                    dpp_minmax4<J, false>(mn[0], mn[1], mn[2], mn[3]);
+                } else {
 #pragma unroll
-                for (int cc = 0; cc < C; ++cc) {
-                    mx[cc] = lane_max<J>(mx[cc]);
-                    mn[cc] = lane_min<J>(mn[cc]);
+                    for (int cc = 0; cc < C; ++cc) {
+                        mx[cc] = lane_max<J>(mx[cc]);
+                        mn[cc] = lane_min<J>(mn[cc]);
+                    }
                 }
+            }
         });
 #pragma unroll
         for (int h = 1; h < C; h <<= 1)
