@@ -44,6 +44,17 @@ __device__ __forceinline__ float ubyte(uint32_t w)
     return (float)((w >> (8 * I)) & 0xFFu);
 }
 
+// The low and high nibbles of each byte of w, as bytes.  The values pass
+// through an empty asm: knowing the masks, the compiler would otherwise
+// split each into four byte extractions (v_bfe / v_and) before converting,
+// instead of one v_cvt_f32_ubyte0..3 per byte.
+__device__ __forceinline__ void nibble_bytes(uint32_t w, uint32_t &lo, uint32_t &hi)
+{
+    lo = w & 0x0F0F0F0Fu;
+    hi = (w >> 4) & 0x0F0F0F0Fu;
+    __asm__("" : "+v"(lo), "+v"(hi));
+}
+
 // sum over e of x[e] * code_e for the 32 codes of one 16-byte slice
 // (element 2j in the low nibble of byte j)
 __device__ __forceinline__ float dot_codes(const uint4 &c, const float *x)
@@ -52,7 +63,8 @@ __device__ __forceinline__ float dot_codes(const uint4 &c, const float *x)
     float acc = 0.0f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const uint32_t lo = w[i] & 0x0F0F0F0Fu, hi = (w[i] >> 4) & 0x0F0F0F0Fu;
+        uint32_t lo, hi;
+        nibble_bytes(w[i], lo, hi);
         acc = __builtin_fmaf(x[8 * i + 0], ubyte<0>(lo), acc);
         acc = __builtin_fmaf(x[8 * i + 1], ubyte<0>(hi), acc);
         acc = __builtin_fmaf(x[8 * i + 2], ubyte<1>(lo), acc);
@@ -71,7 +83,8 @@ __device__ __forceinline__ void axpy_codes(const uint4 &c, float w, float *o)
     const uint32_t v[4] = {c.x, c.y, c.z, c.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const uint32_t lo = v[i] & 0x0F0F0F0Fu, hi = (v[i] >> 4) & 0x0F0F0F0Fu;
+        uint32_t lo, hi;
+        nibble_bytes(v[i], lo, hi);
         o[8 * i + 0] = __builtin_fmaf(w, ubyte<0>(lo), o[8 * i + 0]);
         o[8 * i + 1] = __builtin_fmaf(w, ubyte<0>(hi), o[8 * i + 1]);
         o[8 * i + 2] = __builtin_fmaf(w, ubyte<1>(lo), o[8 * i + 2]);
