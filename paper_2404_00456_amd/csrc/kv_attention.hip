@@ -167,7 +167,12 @@ __global__ __launch_bounds__(64 * ATT_WAVES) void k_kv_attn(KvAttnArgs a)
             sc[u] = ok[u] ? s * a.sm_scale : -inf;
             tmax = fmaxf(tmax, sc[u]);
         }
-        static_for<6>([&](auto J) { tmax = lane_max<J>(tmax); });
+        // the LPT lanes of a token hold the same score (their butterfly sums
+        // add the same pairs), so the maximum runs over the other lane bits
+        static_for<6>([&](auto J) {
+            if constexpr (J >= LOGLPT)
+                tmax = lane_max<J>(tmax);
+        });
         const float mn = fmaxf(m, tmax);  // finite: every iteration has a token
         if (mn > m) {                     // uniform across the wave
             const float alpha = __expf(m - mn);
