@@ -144,6 +144,43 @@ quarot_status quarot_w4a4_gemm(const uint8_t *xq, const quarot_f16 *sx, const ui
                                int64_t M, int64_t N, int64_t K, void *stream);
 
 /*
+ * int4 codes in the tiled e3m2 operand layout.  gfx950 has no int4 matrix
+ * instruction; its fp6 one (v_mfma_f32_16x16x128_f8f6f4) takes 128-deep
+ * slices at twice the int8 rate.  Every code q in -8..8 is exact as an e3m2
+ * number (sign, 3 exponent bits of bias 3, 2 mantissa bits), so the
+ * products and the binary32 sums of them (integers below 2^24 for
+ * K <= 65536) are the exact integer dot products of §4 Stage 2b.
+ * Layout of a [rows, K] code matrix, 6 bits per code (1.5 times the int4
+ * bytes): K/128 blocks of rows * 96 bytes.  In block b, unit u = 0..3 of
+ * row r holds the codes of k = 128 b + 32 u + e (e = 0..31) as the 192-bit
+ * word sum_e e3m2(q_e) << 6e.  Its dwords 0-3 (the head) sit at byte
+ * r * 64 + 16 (u ^ ((r >> 1) & 3)) of the block; its dwords 4-5 (the tail)
+ * at byte rows * 64 + r * 32 + 8 (u ^ ((r >> 2) & 3)).  A 256-row tile's
+ * k-block is then two runs of consecutive bytes, and the slot swizzles
+ * spread the GEMM's LDS reads over all banks.
+ *
+ * quarot_pack_e3m2: q4 uint8 [rows, k/2] int4 codes (low nibble first, as
+ * quarot_quant_int4 writes them) -> q6 (rows * k * 3/4 bytes, layout above).
+ * rows >= 0 (0 is a no-op); k a positive multiple of 128, at most 65536;
+ * q4 and q6 16-byte aligned and not overlapping.  Meant for the weights,
+ * once per matrix.
+ */
+quarot_status quarot_pack_e3m2(const uint8_t *q4, uint8_t *q6, int64_t rows, int64_t k,
+                               void *stream);
+
+/*
+ * quarot_w4a4_gemm with both operands in the tiled e3m2 layout: the same y
+ * and acc_out, bit for bit.
+ *   xq6 M * K * 3/4 bytes, sx fp16 [M]
+ *   wq6 N * K * 3/4 bytes, sw fp16 [N]
+ * M, N >= 0 (0 is a no-op); K a positive multiple of 128, at most 65536.
+ */
+quarot_status quarot_w4a4_gemm_e3m2(const uint8_t *xq6, const quarot_f16 *sx,
+                                    const uint8_t *wq6, const quarot_f16 *sw, quarot_f16 *y,
+                                    int32_t *acc_out, int64_t M, int64_t N, int64_t K,
+                                    void *stream);
+
+/*
  * Bytes of device workspace quarot_linear needs for M rows of width K:
  * the packed codes (M*K/2) and scales (2*M), each rounded up to 256 bytes.
  * Host-only; returns 0 for invalid sizes.

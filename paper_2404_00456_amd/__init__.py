@@ -48,6 +48,8 @@ SIGNATURES = {
     "quarot_hadamard": (_I, [_P, _P, _I64, _I64, _P]),
     "quarot_quant_int4": (_I, [_P, _P, _P, _I64, _I64, _I, _F, _P]),
     "quarot_w4a4_gemm": (_I, [_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P]),
+    "quarot_pack_e3m2": (_I, [_P, _P, _I64, _I64, _P]),
+    "quarot_w4a4_gemm_e3m2": (_I, [_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P]),
     "quarot_linear_workspace_size": (ctypes.c_size_t, [_I64, _I64]),
     "quarot_linear": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P, ctypes.c_size_t, _P]),
     "quarot_quant_int8": (_I, [_P, _P, _P, _I64, _I64, _I, _F, _I, _P]),
@@ -224,6 +226,41 @@ def quarot_w4a4_gemm(xq: torch.Tensor, sx: torch.Tensor, wq: torch.Tensor, sw: t
         _ptr(xq, torch.uint8, "xq"), _ptr(sx, torch.float16, "sx"), _ptr(wq, torch.uint8, "wq"),
         _ptr(sw, torch.float16, "sw"), _ptr(y, torch.float16, "y"),
         _ptr(acc_out, torch.int32, "acc_out"), M, N, 2 * Kh, _stream(stream)))
+    return (y, acc_out) if (want_acc or acc_out is not None) else y
+
+
+def quarot_pack_e3m2(q4: torch.Tensor, out: Optional[torch.Tensor] = None,
+                     stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """int4 codes [rows, k/2] -> the tiled e3m2 operand layout, as uint8
+    [k/128, rows*96] (one row per 128-wide k block)."""
+    rows, kh = q4.shape
+    k = 2 * kh
+    if out is None:
+        out = torch.empty((k // 128 if k % 128 == 0 else 0, rows * 96), dtype=torch.uint8,
+                          device=q4.device)
+    _check("quarot_pack_e3m2", lib().quarot_pack_e3m2(
+        _ptr(q4, torch.uint8, "q4"), _ptr(out, torch.uint8, "out"), rows, k, _stream(stream)))
+    return out
+
+
+def quarot_w4a4_gemm_e3m2(xq6: torch.Tensor, sx: torch.Tensor, wq6: torch.Tensor,
+                          sw: torch.Tensor, y: Optional[torch.Tensor] = None,
+                          acc_out: Optional[torch.Tensor] = None, want_acc: bool = False,
+                          stream: Optional[torch.cuda.Stream] = None):
+    """quarot_w4a4_gemm on operands in the tiled e3m2 layout
+    (xq6 [K/128, M*96], wq6 [K/128, N*96])."""
+    M, N = sx.shape[0], sw.shape[0]
+    K = 128 * xq6.shape[0]
+    if xq6.shape[1] != M * 96 or wq6.shape != (xq6.shape[0], N * 96):
+        raise ValueError("quarot_w4a4_gemm_e3m2: operand shapes do not match sx, sw")
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=xq6.device)
+    if want_acc and acc_out is None:
+        acc_out = torch.empty((M, N), dtype=torch.int32, device=xq6.device)
+    _check("quarot_w4a4_gemm_e3m2", lib().quarot_w4a4_gemm_e3m2(
+        _ptr(xq6, torch.uint8, "xq6"), _ptr(sx, torch.float16, "sx"),
+        _ptr(wq6, torch.uint8, "wq6"), _ptr(sw, torch.float16, "sw"), _ptr(y, torch.float16, "y"),
+        _ptr(acc_out, torch.int32, "acc_out"), M, N, K, _stream(stream)))
     return (y, acc_out) if (want_acc or acc_out is not None) else y
 
 

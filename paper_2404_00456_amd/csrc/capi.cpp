@@ -292,6 +292,45 @@ quarot_status quarot_w4a4_gemm(const uint8_t *xq, const quarot_f16 *sx, const ui
     return e == hipSuccess ? QUAROT_OK : hip_fail(e);
 }
 
+quarot_status quarot_pack_e3m2(const uint8_t *q4, uint8_t *q6, int64_t rows, int64_t k,
+                               void *stream)
+{
+    if (rows < 0 || k <= 0)
+        return QUAROT_ERR_INVALID_ARG;
+    if (k % 128 || k > 65536 || rows > (int64_t(1) << 30))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!q4 || !q6)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(q4) || !aligned16(q6))
+        return QUAROT_ERR_ALIGNMENT;
+    quarot_status st = check_device();
+    if (st)
+        return st;
+    hipError_t e = launch_pack_e3m2(q4, q6, rows, (int)k, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+quarot_status quarot_w4a4_gemm_e3m2(const uint8_t *xq6, const quarot_f16 *sx,
+                                    const uint8_t *wq6, const quarot_f16 *sw, quarot_f16 *y,
+                                    int32_t *acc_out, int64_t M, int64_t N, int64_t K,
+                                    void *stream)
+{
+    quarot_status st = check_gemm(xq6, sx, wq6, sw, y, acc_out, M, N, K);
+    if (st)
+        return st;
+    if (K % 128)
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (M == 0 || N == 0)
+        return QUAROT_OK;
+    if ((st = check_device()))
+        return st;
+    GemmArgs a{xq6, sx, wq6, sw, y, acc_out, (int)M, (int)N, (int)K};
+    hipError_t e = launch_gemm(a, (hipStream_t)stream, 6);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
 size_t quarot_linear_workspace_size(int64_t M, int64_t K)
 {
     if (M < 0 || K <= 0 || (K & 1))

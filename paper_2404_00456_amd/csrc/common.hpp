@@ -100,7 +100,11 @@ struct KvDeqArgs {
 hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, hipStream_t s,
                          int pro = PRO_PLAIN);
 // bits = 4: packed int4 codes [rows, K/2]; bits = 8: one int8 code per byte.
+// bits: 4 (int4 codes), 8 (one code per byte) or 6 (int4 codes in the e3m2
+// layout written by launch_pack_e3m2; K a multiple of 128).
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s, int bits = 4);
+// int4 codes [rows, k/2] -> e3m2 layout [rows, k/128 * 96]; k % 128 == 0.
+hipError_t launch_pack_e3m2(const uint8_t *q4, uint8_t *q6, int64_t rows, int k, hipStream_t s);
 // Group-wise W4A4, groups of `group` (64, 128, 256) along K, K a multiple of
 // max(group, 128); a.sx [K/group, M], a.sw [K/group, N].
 hipError_t launch_gemm_grouped(const GemmArgs &a, int group, hipStream_t s);

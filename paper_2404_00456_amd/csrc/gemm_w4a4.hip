@@ -192,14 +192,65 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_k64(GemmArgs a)
 //    1 KB = 16 rows x 64 B); unit c of row r sits at unit c ^ ((r >> 1) & 3),
 //    which makes the 16-byte reads of 8 consecutive rows hit 8 distinct bank
 //    groups.
-constexpr int S = 3;                         // LDS ring stages
-constexpr int RING_STAGE = (BM + BN) * BKB;  // 32 KB: X rows then W rows
-constexpr int RING_BYTES = S * RING_STAGE;
-constexpr int DPW = RING_STAGE / 1024 / (THREADS / 64);  // DMAs per wave per k-step
+constexpr int S = 3;  // LDS ring stages
 // Scales of a tile (256 sx then 256 sw, fp16) live in LDS after the ring,
 // double buffered by tile parity.
 constexpr int SCALE_BYTES = 2 * (BM + BN) * 2;
-constexpr int MAIN_LDS_BYTES = RING_BYTES + SCALE_BYTES;
+
+// Per code format: bytes per row per k-step, stage and ring sizes, DMAs per
+// wave per k-step.  4- and 8-bit codes: 64 bytes per row (32 KB stages).
+// e3m2 codes (BITS = 6): 96 bytes per row; a stage holds the 64-byte heads
+// of all 512 rows (X then W, laid out as the 4-bit stages), then their
+// 32-byte tails (X then W).
+template <int BITS>
+struct Ring {
+    static constexpr int KB = BITS == 6 ? 96 : 64;
+    static constexpr int STAGE = (BM + BN) * KB;
+    static constexpr int BYTES = S * STAGE;
+    static constexpr int DPW = STAGE / 1024 / (THREADS / 64);
+    static constexpr int LDS = BYTES + SCALE_BYTES;
+};
+constexpr int HEADS = (BM + BN) * 64;  // e3m2 stage: offset of the tails
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// One e3m2 operand slice of a lane: 32 codes, six dwords (head, tail).
+struct Op6 {
+    uint4 h;
+    uint2 t;
+};
+
+// v_mfma_f32_16x16x128_f8f6f4 with both operands e3m2 (format 3), no scale.
+// Every product of two codes is an integer of magnitude <= 64 and every
+// partial sum an integer below 2^24, so the binary32 accumulation is exact.
+__device__ __forceinline__ v4f mfma6(const Op6 &a, const Op6 &b, v4f c)
+{
+    const v8i av = {(int)a.h.x, (int)a.h.y, (int)a.h.z, (int)a.h.w, (int)a.t.x, (int)a.t.y, 0, 0};
+    const v8i bv = {(int)b.h.x, (int)b.h.y, (int)b.h.z, (int)b.h.w, (int)b.t.x, (int)b.t.y, 0, 0};
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(av, bv, c, 3, 3, 0, 0, 0, 0);
+}
+
+template <int BITS>
+struct AccOf {
+    typedef v4i type;
+};
+template <>
+struct AccOf<6> {
+    typedef v4f type;
+};
+
+// acc as int32 (4-bit codes: the accumulators hold 256 acc)
+template <int BITS, typename T>
+__device__ __forceinline__ int acc_int(T v)
+{
+    if constexpr (BITS == 4)
+        return v >> 8;
+    else if constexpr (BITS == 6)
+        return (int)v;
+    else
+        return v;
+}
 
 
 // Persistent: each block walks a range of tiles.  Block b sits on XCD b % 8
@@ -216,18 +267,30 @@ constexpr int MAIN_LDS_BYTES = RING_BYTES + SCALE_BYTES;
 // is one MFMA operand as it is (no widening), and the accumulators hold acc
 // itself (no factor 256).  The 32 MFMAs of a k-step split into two halves
 // around the barrier, as the two substeps of the 4-bit path do.
+//
+// BITS = 6 (int4 codes stored as e3m2, see k_pack_e3m2): a k-step is 128 k
+// (96 bytes per row), one v_mfma_f32_16x16x128_f8f6f4 per 16x16 slice pair
+// (half the MFMA count of the 4-bit path, no widening), binary32
+// accumulators holding acc exactly.  Lane group g of an operand takes unit
+// g (its 16-byte head and 8-byte tail), the same k in A and B.
 template <int BITS>
 __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
 {
-    static_assert(BITS == 4 || BITS == 8, "int4 or int8 codes");
+    static_assert(BITS == 4 || BITS == 6 || BITS == 8, "int4, e3m2 or int8 codes");
+    typedef Ring<BITS> R;
+    constexpr int KB = R::KB;
+    constexpr int DPW = R::DPW;
+    constexpr int RING_STAGE = R::STAGE;
+    constexpr int RING_BYTES = R::BYTES;
+    typedef typename AccOf<BITS>::type Acc;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 2, wn = wave & 3;
     const int M = a.M, N = a.N, K = a.K;
     const int TM = (M + BM - 1) / BM, TN = (N + BN - 1) / BN;
     const int T = TM * TN;
     const int G = gridDim.x, b = blockIdx.x;
-    const int64_t ldk = BITS == 4 ? K / 2 : K;
-    const int KT = BITS == 4 ? K / 128 : K / 64;
+    const int64_t ldk = BITS == 4 ? K / 2 : K;  // row pitch (4- and 8-bit codes)
+    const int KT = BITS == 8 ? K / 64 : K / 128;
 
     // this block's tiles: logical positions b, b + G, ... within a
     // per-XCD ordering when the grid and the tile count allow it
@@ -254,13 +317,33 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     // DMA sources: instruction i of wave w moves 16 rows of X (i < 2) or W
     // (i >= 2): rows 16*(w + 8*(i&1)) + lane/4 land at unit lane%4 of their
     // LDS row, so they fetch global unit (lane%4) ^ swizzle(row)
+    //
+    // e3m2 operands (tiled layout, see k_pack_e3m2): the same instructions
+    // i < 4 move heads, 64 bytes per row, already swizzled in memory, so
+    // lane l fetches unit l % 4 of its row; i = 4 (X) and 5 (W) move tails:
+    // wave w, rows 32 w + lane/2, 16 bytes each.  Every instruction reads
+    // 1 KB of consecutive bytes (rows past the matrix edge are clamped).
     const int rsub = lane >> 2;
     const int cunit = (lane & 3) ^ ((lane >> 3) & 3);
-    static_assert(DPW == 4, "two X and two W chunks per wave");
+    static_assert(DPW == (BITS == 6 ? 6 : 4), "two X and two W chunks per wave (+ tails)");
     int dst[DPW];
 #pragma unroll
     for (int i = 0; i < DPW; ++i)
-        dst[i] = (i < 2 ? 0 : BM * BKB) + (wave + 8 * (i & 1)) * 1024;
+        dst[i] = i < 4 ? (i < 2 ? 0 : BM * BKB) + (wave + 8 * (i & 1)) * 1024
+                       : HEADS + (i == 4 ? 0 : BM * 32) + wave * 1024;
+    // e3m2: source of DMA i for k-step sk of the tile at (m0, n0)
+    auto src6 = [&](int i, int m0, int n0, int sk) -> const uint8_t * {
+        const bool xop = i < 2 || i == 4;
+        const int64_t rows = xop ? M : N;
+        const uint8_t *blk = (xop ? a.xq : a.wq) + (int64_t)sk * (rows * 96);
+        const int org = xop ? m0 : n0;
+        if (i < 4) {
+            const int r = 16 * (wave + 8 * (i & 1)) + rsub;
+            return blk + (int64_t)min(org + r, (int)rows - 1) * 64 + (lane & 3) * 16;
+        }
+        const int r = 32 * wave + (lane >> 1);
+        return blk + rows * 64 + (int64_t)min(org + r, (int)rows - 1) * 32 + (lane & 1) * 16;
+    };
     auto sources = [&](int m0, int n0, const uint8_t *(&src)[DPW]) {
 #pragma unroll
         for (int i = 0; i < DPW; ++i) {
@@ -276,11 +359,22 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
         for (int i = 0; i < DPW; ++i)
             dma16(src[i] + (int64_t)kt * BKB, __builtin_amdgcn_readfirstlane(sbase + dst[i]));
     };
+    auto issue6 = [&](int m0, int n0, int sk, int stage) {
+        const uint32_t sbase = lds_base + stage * RING_STAGE;
+#pragma unroll
+        for (int i = 0; i < DPW; ++i)
+            dma16(src6(i, m0, n0, sk), __builtin_amdgcn_readfirstlane(sbase + dst[i]));
+    };
 
     const int orow = lane & 15;
     const int ounit = ((lane >> 4) ^ ((orow >> 1) & 3)) << 4;
     const int brow = (wm * 128 + orow) * BKB + ounit;        // X slice rows (B operand)
     const int arow = (BM + wn * WN + orow) * BKB + ounit;    // W slice rows (A operand)
+    // e3m2 tails: the 8 bytes of unit g of row r sit at slot g ^ ((r >> 2) & 3)
+    // of the row's 32-byte tail (16-row slices start at multiples of 16)
+    const int toff = 8 * ((lane >> 4) ^ ((orow >> 2) & 3));
+    const int btail = HEADS + (wm * 128 + orow) * 32 + toff;
+    const int atail = HEADS + BM * 32 + (wn * WN + orow) * 32 + toff;
 
     // Tiles wholly inside the matrices (and no int32 output) take the fast
     // epilogue, with the scales staged in LDS: one 4-byte DMA per wave
@@ -305,14 +399,19 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     int m0, n0;
     tile_mn(t, m0, n0);
     const uint8_t *src[DPW];
-    sources(m0, n0, src);
+    if constexpr (BITS != 6)
+        sources(m0, n0, src);
     if (fast_tile(m0, n0))
         scale_dma(m0, n0, 0);
     // ring position: global step g of this block lives in stage g % S
     int g = 0;
 #pragma unroll
-    for (int i = 0; i < S; ++i)
-        issue(src, min(i, KT - 1), i);
+    for (int i = 0; i < S; ++i) {
+        if constexpr (BITS == 6)
+            issue6(m0, n0, min(i, KT - 1), i);
+        else
+            issue(src, min(i, KT - 1), i);
+    }
 
     for (int it = 0; t >= 0; ++it) {
         const int tn_ = tile_pos(it + 1);
@@ -320,19 +419,20 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
         const uint8_t *nsrc[DPW];
         if (tn_ >= 0) {
             tile_mn(tn_, m1, n1);
-            sources(m1, n1, nsrc);
-        } else {
+            if constexpr (BITS != 6)
+                sources(m1, n1, nsrc);
+        } else if constexpr (BITS != 6) {
 #pragma unroll
             for (int i = 0; i < DPW; ++i)
                 nsrc[i] = src[i];
         }
 
-        v4i acc[NI][8];
+        Acc acc[NI][8];
 #pragma unroll
         for (int i = 0; i < NI; ++i)
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                acc[i][j] = v4i{0, 0, 0, 0};
+                acc[i][j] = Acc{0, 0, 0, 0};
 
         auto read_step = [&](uint4 (&ops)[8 + NI], int stage) {
             const uint8_t *sb = lds + stage * RING_STAGE;
@@ -359,7 +459,7 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
                         acc[i][j] =
                             __builtin_amdgcn_mfma_i32_16x16x64_i8(aq[i], bq, acc[i][j], 0, 0, 0);
                 }
-            } else {
+            } else if constexpr (BITS == 8) {
                 // half h: the B slices j = 4h .. 4h+3 against every A slice
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) {
@@ -385,6 +485,81 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
             __builtin_amdgcn_s_barrier();
             __asm__ volatile("" ::: "memory");
         }
+        if constexpr (BITS == 6) {
+            // A k-step is four quarters of 8 MFMAs over the slice pairs
+            // A[0..1] x B[0..3], A[0..1] x B[4..7], A[2..3] x B[0..3],
+            // A[2..3] x B[4..7].  Every read lands in registers a quarter
+            // has just freed, at least one quarter before its first use, so
+            // the operands are not double buffered (200 live VGPRs):
+            //   quarter 1: read B[4..7], A[2..3] of this step
+            //   barrier after quarter 2 (every read of this stage done)
+            //   quarter 3: read A[0..1] of the next step
+            //   quarter 4: read B[0..3] of the next step
+            // sched_barrier(0) fences keep that order: left to itself the
+            // scheduler sinks each read to just before its first MFMA.
+            Op6 A[NI], B[8];
+            auto rdA = [&](int i, int stage) {
+                const uint8_t *sb = lds + stage * RING_STAGE;
+                A[i].h = *reinterpret_cast<const uint4 *>(sb + arow + i * 16 * 64);
+                A[i].t = *reinterpret_cast<const uint2 *>(sb + atail + i * 16 * 32);
+            };
+            auto rdB = [&](int j, int stage) {
+                const uint8_t *sb = lds + stage * RING_STAGE;
+                B[j].h = *reinterpret_cast<const uint4 *>(sb + brow + j * 16 * 64);
+                B[j].t = *reinterpret_cast<const uint2 *>(sb + btail + j * 16 * 32);
+            };
+            auto quarter = [&](int i0, int j0) {
+#pragma unroll
+                for (int i = i0; i < i0 + 2; ++i)
+#pragma unroll
+                    for (int j = j0; j < j0 + 4; ++j)
+                        acc[i][j] = mfma6(A[i], B[j], acc[i][j]);
+            };
+            rdA(0, g % S);
+            rdA(1, g % S);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                rdB(j, g % S);
+            for (int kt = 0; kt < KT; ++kt, ++g) {
+                const int cs = g % S, nx = (g + 1) % S;
+#pragma unroll
+                for (int j = 4; j < 8; ++j)
+                    rdB(j, cs);
+                rdA(2, cs);
+                rdA(3, cs);
+                __builtin_amdgcn_sched_barrier(0);
+                quarter(0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+                quarter(0, 4);
+                __builtin_amdgcn_sched_barrier(0);
+                __asm__ volatile("" ::: "memory");
+                __builtin_amdgcn_s_waitcnt(waitcnt_imm((S - 2) * DPW, 0));
+                __builtin_amdgcn_s_barrier();
+                __asm__ volatile("" ::: "memory");
+                {
+                    // addresses recomputed from the (wave-uniform) tile
+                    // origin each step rather than kept in 24 VGPRs; the
+                    // empty asm keeps the compiler from hoisting them
+                    const bool here = kt + S < KT;
+                    const bool cur = here || tn_ < 0;
+                    int sk = here ? kt + S : (tn_ >= 0 ? kt + S - KT : KT - 1);
+                    int me = cur ? m0 : m1, ne = cur ? n0 : n1;
+                    __asm__ volatile("" : "+s"(me), "+s"(ne), "+s"(sk));
+                    issue6(me, ne, sk, g % S);
+                }
+                rdA(0, nx);
+                rdA(1, nx);
+                __builtin_amdgcn_sched_barrier(0);
+                quarter(2, 0);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    rdB(j, nx);
+                __builtin_amdgcn_sched_barrier(0);
+                quarter(2, 4);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
         uint4 R[8 + NI], Rn[8 + NI];
         read_step(R, g % S);
         for (int kt = 0; kt < KT; ++kt, ++g) {
@@ -415,6 +590,7 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
 #pragma unroll
             for (int o = 0; o < 8 + NI; ++o)
                 R[o] = Rn[o];
+        }
         }
         // the extra read after the last step touched stage g % S (the next
         // tile's step 0, landed) and is discarded
@@ -493,7 +669,7 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
                 uint16_t hv[4];
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    iv[r] = BITS == 4 ? acc[i][j][r] >> 8 : acc[i][j][r];
+                    iv[r] = acc_int<BITS>(acc[i][j][r]);
                     const float tt = (float)iv[r] * sxf[j];
                     hv[r] = f2h(tt * swf[r]);
                 }
@@ -522,9 +698,11 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
         t = tn_;
         m0 = m1;
         n0 = n1;
+        if constexpr (BITS != 6) {
 #pragma unroll
-        for (int i = 0; i < DPW; ++i)
-            src[i] = nsrc[i];
+            for (int i = 0; i < DPW; ++i)
+                src[i] = nsrc[i];
+        }
     }
     __asm__ volatile("" ::: "memory");
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));  // no DMA may outlive the block's LDS
@@ -542,6 +720,63 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w8a8(GemmArgs a)
     gemm_main<8>(a, lds);
 }
 
+__global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_e3m2(GemmArgs a)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    gemm_main<6>(a, lds);
+}
+
+// e3m2 code of an integer q in -8..8, from the bits of the binary32 q: the
+// exponent field e and the top two mantissa bits m give 4 e + m, which is
+// 4 (E + 124) + M for the e3m2 exponent field E and mantissa M (1 <= |q|:
+// E = e - 124 for bias 3 against 127); q = 0 gives 0 after the clamp.  The
+// sign moves from bit 31 to bit 5.
+__device__ __forceinline__ uint32_t e3m2_of_int(int q)
+{
+    const uint32_t b = __float_as_uint((float)q);
+    const int mag = (int)((b >> 21) & 0x3FFu) - 4 * 124;
+    return (uint32_t)max(mag, 0) | ((b >> 26) & 0x20u);
+}
+
+// int4 codes (two per byte, low nibble first) -> the tiled e3m2 layout.
+// The 32 codes of unit u (k = 128 b + 32 u + e, e = 0..31) of row r form the
+// 192-bit word sum_e code(q_e) << 6e, code(q) being q in e3m2 (sign, 3
+// exponent bits of bias 3, 2 mantissa bits; every integer in -8..8 is exact).
+// K-block b takes rows * 96 bytes at b * rows * 96: first the 64-byte heads
+// of all rows (dwords 0-3 of unit u at 16-byte slot u ^ ((r >> 1) & 3) of the
+// row's head), then the 32-byte tails (dwords 4-5 of unit u at 8-byte slot
+// u ^ ((r >> 2) & 3)).  The GEMM moves a tile's k-step as consecutive
+// kilobytes, and the slot swizzles make its LDS reads conflict-free.
+// One thread per (b, r, u), u fastest.
+__global__ __launch_bounds__(256) void k_pack_e3m2(const uint8_t *__restrict__ q4,
+                                                   uint8_t *__restrict__ q6, int64_t rows,
+                                                   int kb)
+{
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= rows * kb * 4)
+        return;
+    const int u = (int)(t & 3);
+    const int64_t rb = t >> 2;
+    const int64_t r = rb % rows;
+    const int b = (int)(rb / rows);
+    const uint4 in = *reinterpret_cast<const uint4 *>(q4 + r * ((int64_t)kb * 64) + (4 * b + u) * 16);
+    const uint32_t w[4] = {in.x, in.y, in.z, in.w};
+    uint32_t o[6] = {0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int e = 0; e < 32; ++e) {
+        const uint32_t n = (w[e >> 3] >> (4 * (e & 7))) & 15u;
+        const uint32_t code = e3m2_of_int(((int)n ^ 8) - 8);
+        const int bit = 6 * e;
+        o[bit >> 5] |= code << (bit & 31);
+        if ((bit & 31) > 26)
+            o[(bit >> 5) + 1] |= code >> (32 - (bit & 31));
+    }
+    uint8_t *blk = q6 + (int64_t)b * rows * 96;
+    const int hs = u ^ (int)((r >> 1) & 3), ts = u ^ (int)((r >> 2) & 3);
+    *reinterpret_cast<uint4 *>(blk + r * 64 + 16 * hs) = make_uint4(o[0], o[1], o[2], o[3]);
+    *reinterpret_cast<uint2 *>(blk + rows * 64 + r * 32 + 8 * ts) = make_uint2(o[4], o[5]);
+}
+
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s, int bits)
@@ -549,12 +784,13 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s, int bits)
     if (a.M == 0 || a.N == 0)
         return hipSuccess;
     const int TM = (a.M + BM - 1) / BM, TN = (a.N + BN - 1) / BN;
-    const bool main = bits == 8 || (a.K % 128) == 0;
+    const bool main = bits != 4 || (a.K % 128) == 0;
     const int ksteps = bits == 8 ? a.K / 64 : a.K / 128;
-    const void *fn = bits == 8 ? (const void *)k_gemm_w8a8
-                     : main    ? (const void *)k_gemm_w4a4
-                               : (const void *)k_gemm_w4a4_k64;
-    const int lds_bytes = main ? MAIN_LDS_BYTES : LDS_BYTES;
+    const void *fn = bits == 8   ? (const void *)k_gemm_w8a8
+                     : bits == 6 ? (const void *)k_gemm_w4a4_e3m2
+                     : main      ? (const void *)k_gemm_w4a4
+                                 : (const void *)k_gemm_w4a4_k64;
+    const int lds_bytes = bits == 6 ? Ring<6>::LDS : main ? Ring<4>::LDS : LDS_BYTES;
     // more than 64 KB of dynamic LDS: raise the kernel's limit (per call, so
     // that every device the caller uses gets it; the call is host-side only)
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
@@ -575,12 +811,26 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s, int bits)
             grid -= grid % 8;
         if (bits == 8)
             hipLaunchKernelGGL(k_gemm_w8a8, dim3((unsigned)grid), dim3(THREADS), lds_bytes, s, a);
+        else if (bits == 6)
+            hipLaunchKernelGGL(k_gemm_w4a4_e3m2, dim3((unsigned)grid), dim3(THREADS), lds_bytes,
+                               s, a);
         else
             hipLaunchKernelGGL(k_gemm_w4a4, dim3((unsigned)grid), dim3(THREADS), lds_bytes, s, a);
     }
     else
         hipLaunchKernelGGL(k_gemm_w4a4_k64, dim3((unsigned)(TM * TN)), dim3(THREADS), lds_bytes, s,
                            a);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_e3m2(const uint8_t *q4, uint8_t *q6, int64_t rows, int k, hipStream_t s)
+{
+    const int kb = k / 128;
+    const int64_t threads = rows * kb * 4;
+    if (threads == 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(k_pack_e3m2, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, q4,
+                       q6, rows, kb);
     return hipGetLastError();
 }
 

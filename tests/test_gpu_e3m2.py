@@ -1,0 +1,161 @@
+"""GPU parity of the e3m2 operand path of the W4A4 GEMM (§4 Stage 2b,
+App. A.10): int4 codes stored as e3m2 numbers and multiplied by gfx950's
+fp6 matrix instruction.  The packed bytes are decoded on the host from the
+layout's definition and must give back every code; the GEMM's int32
+accumulators and fp16 outputs must equal the oracle's bit for bit, and the
+int4 path's on the full-size shapes."""
+import numpy as np
+import pytest
+
+from test_gpu_parity import H, T, assert_fp16_close, assert_same, rand_codes, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2404_00456_amd as q
+    q.lib()
+    return torch.device("cuda:0")
+
+
+def e3m2_value(c: int) -> float:
+    """Value of a 6-bit e3m2 code: sign, 3 exponent bits (bias 3), 2 mantissa
+    bits, subnormals at exponent field 0, no infinities or NaNs."""
+    s = -1.0 if c & 0x20 else 1.0
+    e, m = (c >> 2) & 7, c & 3
+    if e == 0:
+        return s * 2.0 ** -2 * (m / 4)
+    return s * 2.0 ** (e - 3) * (1 + m / 4)
+
+
+E3M2 = np.array([e3m2_value(c) for c in range(64)])
+
+
+def decode_e3m2_layout(q6: np.ndarray, rows: int, k: int) -> np.ndarray:
+    """Tiled e3m2 layout [k/128, rows*96] -> code values [rows, k].  In block
+    b, row r's unit u is the 192-bit little-endian word made of the 16-byte
+    head at slot u ^ ((r >> 1) & 3) of the row's 64 bytes (heads of all rows
+    first) and the 8-byte tail at slot u ^ ((r >> 2) & 3) of its 32 bytes
+    (after the heads); code e sits at bits 6e..6e+5."""
+    kb = k // 128
+    buf = np.asarray(q6, np.uint8).reshape(kb, rows * 96)
+    heads = buf[:, :rows * 64].reshape(kb, rows, 4, 16)
+    tails = buf[:, rows * 64:].reshape(kb, rows, 4, 8)
+    r = np.arange(rows)
+    out = np.empty((rows, kb, 4, 32))
+    for u in range(4):
+        h = heads[:, r, u ^ ((r >> 1) & 3), :]
+        t = tails[:, r, u ^ ((r >> 2) & 3), :]
+        word = np.concatenate([h, t], axis=2)
+        bits = np.unpackbits(word, axis=2, bitorder="little").reshape(kb, rows, 32, 6)
+        codes = bits.astype(np.int64) @ (1 << np.arange(6))
+        out[:, :, u, :] = E3M2[codes].transpose(1, 0, 2)
+    return out.reshape(rows, k)
+
+
+def test_e3m2_table_holds_int4():
+    """Every int4 code is an e3m2 number (exactly one 6-bit code each, up to
+    the sign of zero)."""
+    for qv in range(-8, 8):
+        hits = [c for c in range(64) if E3M2[c] == qv and not (qv == 0 and c & 0x20)]
+        assert len(hits) == 1, qv
+
+
+@pytest.mark.parametrize("rows,k", [(1, 128), (37, 384), (300, 8192), (5, 65536)])
+def test_pack_e3m2_layout(dev, orc, rows, k):
+    import paper_2404_00456_amd as q
+    say(f"pack e3m2 rows={rows} k={k}")
+    rng = np.random.default_rng(rows * 3 + k)
+    q4 = rand_codes(rng, rows, k)
+    q4[0, : min(8, k // 2)] = np.arange(0, 256, 32, dtype=np.uint8)[: min(8, k // 2)] | 0x08
+    q6 = H(q.quarot_pack_e3m2(T(q4, dev)))
+    assert q6.shape == (k // 128, rows * 96)
+    assert_same(decode_e3m2_layout(q6, rows, k), orc.unpack_int4(q4).astype(np.float64),
+                f"e3m2 layout rows={rows} k={k}")
+
+
+def _gemm_case(dev, orc, M, N, K, xq, wq, sx, sw):
+    import paper_2404_00456_amd as q
+    x6 = q.quarot_pack_e3m2(T(xq, dev))
+    w6 = q.quarot_pack_e3m2(T(wq, dev))
+    y, acc = q.quarot_w4a4_gemm_e3m2(x6, T(sx, dev), w6, T(sw, dev), want_acc=True)
+    y_only = q.quarot_w4a4_gemm_e3m2(x6, T(sx, dev), w6, T(sw, dev))
+    racc = orc.gemm_i32(xq, wq)
+    assert_same(H(acc), racc, f"e3m2 acc M={M} N={N} K={K}")
+    ry = orc.dequant(racc, sx, sw)
+    assert_fp16_close(H(y), ry, f"e3m2 y M={M} N={N} K={K}")
+    assert_fp16_close(H(y_only), ry, f"e3m2 y (no acc) M={M} N={N} K={K}")
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 1, 128), (16, 256, 128), (255, 257, 384),
+                                   (300, 520, 1024), (513, 100, 4096), (64, 1000, 11008),
+                                   (256, 256, 28672), (2, 3, 65536),
+                                   (2048, 8448, 128), (2048, 8448, 256), (2048, 8448, 384),
+                                   (2304, 8448, 512), (2200, 8400, 1024)])
+def test_gemm_e3m2_exact(dev, orc, M, N, K):
+    """Ragged edges, k-step counts below, at and above the LDS ring depth,
+    blocks that walk several tiles, the largest K."""
+    say(f"e3m2 gemm M={M} N={N} K={K}")
+    rng = np.random.default_rng(M * 7 + N * 3 + K + 1)
+    xq = rand_codes(rng, M, K)
+    wq = rand_codes(rng, N, K)
+    sx = rng.uniform(0.01, 2.0, M).astype(np.float16)
+    sw = rng.uniform(0.0005, 0.05, N).astype(np.float16)
+    _gemm_case(dev, orc, M, N, K, xq, wq, sx, sw)
+
+
+def test_gemm_e3m2_extreme_codes(dev, orc):
+    """All -8 codes at K = 65536: acc = 2^22, the largest magnitude, still an
+    exact binary32 integer."""
+    M, N, K = 40, 300, 65536
+    xq = np.full((M, K // 2), 0x88, np.uint8)
+    wq = np.full((N, K // 2), 0x88, np.uint8)
+    sx = np.full(M, 0.001, np.float16)
+    sw = np.full(N, 0.002, np.float16)
+    _gemm_case(dev, orc, M, N, K, xq, wq, sx, sw)
+
+
+def test_gemm_e3m2_tiny_scales(dev, orc):
+    """Outputs across the fp16 subnormal range and underflow."""
+    M, N, K = 512, 768, 2048
+    rng = np.random.default_rng(12)
+    xq = rand_codes(rng, M, K)
+    wq = rand_codes(rng, N, K)
+    sx = (2.0 ** rng.uniform(-24, -10, M)).astype(np.float16)
+    sw = (2.0 ** rng.uniform(-14, -6, N)).astype(np.float16)
+    _gemm_case(dev, orc, M, N, K, xq, wq, sx, sw)
+
+
+@pytest.mark.parametrize("M,N,K", [(16384, 28672, 8192), (16384, 8192, 28672)])
+def test_gemm_e3m2_full_size(dev, orc, M, N, K):
+    """Llama-2-70B FFN shapes at prefill (16384 tokens), in the launch
+    configuration the benchmark times: every output equal to the int4
+    path's, and sampled rows equal to the oracle's."""
+    import torch
+    import paper_2404_00456_amd as q
+    say(f"e3m2 gemm full size M={M} N={N} K={K}")
+    g = torch.Generator(device=dev).manual_seed(M + N + K)
+    xq = torch.randint(0, 256, (M, K // 2), generator=g, device=dev, dtype=torch.uint8)
+    wq = torch.randint(0, 256, (N, K // 2), generator=g, device=dev, dtype=torch.uint8)
+    sx = (torch.rand(M, generator=g, device=dev) * 0.05 + 0.01).half()
+    sw = (torch.rand(N, generator=g, device=dev) * 0.002 + 0.0005).half()
+    x6, w6 = q.quarot_pack_e3m2(xq), q.quarot_pack_e3m2(wq)
+    for name, a4, a6 in (("X", xq, x6), ("W", wq, w6)):
+        h4, h6 = H(a4), H(a6)
+        assert_same(decode_e3m2_layout(h6, h4.shape[0], K), orc.unpack_int4(h4).astype(np.float64),
+                    f"full size e3m2 layout {name}")
+    y4 = q.quarot_w4a4_gemm(xq, sx, wq, sw)
+    y6 = q.quarot_w4a4_gemm_e3m2(x6, sx, w6, sw)
+    torch.cuda.synchronize()
+    nd = int((y4.view(torch.int16) != y6.view(torch.int16)).sum().item())
+    say(f"full size e3m2 vs int4: {nd} differing of {M * N}")
+    assert nd == 0
+    rows = np.array([0, 1, 255, 256, 8191, M - 1])
+    xs, ss = H(xq[rows]), H(sx[rows])
+    racc = orc.gemm_i32(xs, H(wq))
+    ry = orc.dequant(racc, ss, H(sw))
+    assert_same(H(y6[rows]).view(np.uint16), ry.view(np.uint16), "full size sampled rows")
