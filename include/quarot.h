@@ -181,6 +181,32 @@ quarot_status quarot_w4a4_gemm_e3m2(const uint8_t *xq6, const quarot_f16 *sx,
                                     void *stream);
 
 /*
+ * quarot_quant_int4 with the codes written in the tiled e3m2 layout above:
+ * the same codes and scales (§4 Stage 2b), for quarot_w4a4_gemm_e3m2.
+ *   x fp16 [rows, n], q6 rows * n * 3/4 bytes, scale fp16 [rows]
+ * n a multiple of 128 and, with rotate != 0, n = 2^k (k <= 15) or
+ * n = 12 * 2^10, 12 * 2^11, 20 * 2^9, 20 * 2^10, 28 * 2^9, 28 * 2^10;
+ * rows <= 2^30.  Other n: quarot_quant_int4 then quarot_pack_e3m2.
+ */
+quarot_status quarot_quant_int4_e3m2(const quarot_f16 *x, uint8_t *q6, quarot_f16 *scale,
+                                     int64_t rows, int64_t n, int rotate, float clip_ratio,
+                                     void *stream);
+
+/*
+ * The 4-bit linear layer on the e3m2 path: quarot_quant_int4_e3m2 of x into
+ * the workspace, then quarot_w4a4_gemm_e3m2 into y (two launches).  The
+ * weights come from quarot_quant_int4 of W [N, K] then quarot_pack_e3m2.
+ * y equals quarot_linear's bit for bit.  Workspace: at least
+ * quarot_linear_e3m2_workspace_size(M, K) bytes, 256-byte aligned (0 for
+ * invalid sizes).  Size rules of both calls apply.
+ */
+size_t quarot_linear_e3m2_workspace_size(int64_t M, int64_t K);
+quarot_status quarot_linear_e3m2(const quarot_f16 *x, const uint8_t *wq6, const quarot_f16 *sw,
+                                 quarot_f16 *y, int64_t M, int64_t N, int64_t K, int rotate,
+                                 float clip_ratio, void *workspace, size_t workspace_bytes,
+                                 void *stream);
+
+/*
  * Bytes of device workspace quarot_linear needs for M rows of width K:
  * the packed codes (M*K/2) and scales (2*M), each rounded up to 256 bytes.
  * Host-only; returns 0 for invalid sizes.
@@ -342,6 +368,14 @@ quarot_status quarot_swiglu(const quarot_f16 *gate, const quarot_f16 *up, quarot
  *   n supported by quarot_hadamard_factor; clip_ratio in (0, 1].
  */
 quarot_status quarot_swiglu_quant_int4(const quarot_f16 *gate, const quarot_f16 *up, uint8_t *q,
+                                       quarot_f16 *scale, int64_t rows, int64_t n,
+                                       float clip_ratio, void *stream);
+
+/*
+ * quarot_swiglu_quant_int4 with the codes in the tiled e3m2 layout (for
+ * quarot_w4a4_gemm_e3m2); n as for quarot_quant_int4_e3m2 with rotation.
+ */
+quarot_status quarot_swiglu_quant_e3m2(const quarot_f16 *gate, const quarot_f16 *up, uint8_t *q6,
                                        quarot_f16 *scale, int64_t rows, int64_t n,
                                        float clip_ratio, void *stream);
 

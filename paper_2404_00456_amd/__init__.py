@@ -50,6 +50,11 @@ SIGNATURES = {
     "quarot_w4a4_gemm": (_I, [_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P]),
     "quarot_pack_e3m2": (_I, [_P, _P, _I64, _I64, _P]),
     "quarot_w4a4_gemm_e3m2": (_I, [_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P]),
+    "quarot_quant_int4_e3m2": (_I, [_P, _P, _P, _I64, _I64, _I, _F, _P]),
+    "quarot_linear_e3m2_workspace_size": (ctypes.c_size_t, [_I64, _I64]),
+    "quarot_linear_e3m2": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P, ctypes.c_size_t,
+                                _P]),
+    "quarot_swiglu_quant_e3m2": (_I, [_P, _P, _P, _P, _I64, _I64, _F, _P]),
     "quarot_linear_workspace_size": (ctypes.c_size_t, [_I64, _I64]),
     "quarot_linear": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P, ctypes.c_size_t, _P]),
     "quarot_quant_int8": (_I, [_P, _P, _P, _I64, _I64, _I, _F, _I, _P]),
@@ -262,6 +267,71 @@ def quarot_w4a4_gemm_e3m2(xq6: torch.Tensor, sx: torch.Tensor, wq6: torch.Tensor
         _ptr(wq6, torch.uint8, "wq6"), _ptr(sw, torch.float16, "sw"), _ptr(y, torch.float16, "y"),
         _ptr(acc_out, torch.int32, "acc_out"), M, N, K, _stream(stream)))
     return (y, acc_out) if (want_acc or acc_out is not None) else y
+
+
+def quarot_quant_int4_e3m2(x: torch.Tensor, rotate: bool = True, clip_ratio: float = 1.0,
+                           q6: Optional[torch.Tensor] = None,
+                           scale: Optional[torch.Tensor] = None,
+                           stream: Optional[torch.cuda.Stream] = None):
+    """quarot_quant_int4 with the codes in the tiled e3m2 layout
+    ([n/128, rows*96] uint8); returns (q6, scale)."""
+    rows, n = x.shape
+    if q6 is None:
+        q6 = torch.empty((n // 128 if n % 128 == 0 else 0, rows * 96), dtype=torch.uint8,
+                         device=x.device)
+    if scale is None:
+        scale = torch.empty((rows,), dtype=torch.float16, device=x.device)
+    _check("quarot_quant_int4_e3m2", lib().quarot_quant_int4_e3m2(
+        _ptr(x, torch.float16, "x"), _ptr(q6, torch.uint8, "q6"),
+        _ptr(scale, torch.float16, "scale"), rows, n, int(bool(rotate)), float(clip_ratio),
+        _stream(stream)))
+    return q6, scale
+
+
+def quarot_linear_e3m2_workspace_size(M: int, K: int) -> int:
+    return int(lib().quarot_linear_e3m2_workspace_size(M, K))
+
+
+def quarot_linear_e3m2(x: torch.Tensor, wq6: torch.Tensor, sw: torch.Tensor,
+                       rotate: bool = True, clip_ratio: float = 1.0,
+                       y: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None,
+                       stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """The 4-bit linear layer on the e3m2 path (weights from
+    prepare_weight_e3m2); y equals quarot_linear's bit for bit."""
+    M, K = x.shape
+    N = sw.shape[0]
+    need = quarot_linear_e3m2_workspace_size(M, K)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    _check("quarot_linear_e3m2", lib().quarot_linear_e3m2(
+        _ptr(x, torch.float16, "x"), _ptr(wq6, torch.uint8, "wq6"), _ptr(sw, torch.float16, "sw"),
+        _ptr(y, torch.float16, "y"), M, N, K, int(bool(rotate)), float(clip_ratio),
+        _ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream)))
+    return y
+
+
+def quarot_swiglu_quant_e3m2(gate: torch.Tensor, up: torch.Tensor, clip_ratio: float = 1.0,
+                             stream: Optional[torch.cuda.Stream] = None):
+    """quarot_swiglu_quant_int4 with the codes in the tiled e3m2 layout."""
+    rows, n = gate.shape
+    q6 = torch.empty((n // 128 if n % 128 == 0 else 0, rows * 96), dtype=torch.uint8,
+                     device=gate.device)
+    scale = torch.empty((rows,), dtype=torch.float16, device=gate.device)
+    _check("quarot_swiglu_quant_e3m2", lib().quarot_swiglu_quant_e3m2(
+        _ptr(gate, torch.float16, "gate"), _ptr(up, torch.float16, "up"),
+        _ptr(q6, torch.uint8, "q6"), _ptr(scale, torch.float16, "scale"), rows, n,
+        float(clip_ratio), _stream(stream)))
+    return q6, scale
+
+
+def prepare_weight_e3m2(w: torch.Tensor, rotate: bool = True, clip_ratio: float = 1.0,
+                        stream: Optional[torch.cuda.Stream] = None):
+    """prepare_weight, then the codes repacked into the tiled e3m2 layout."""
+    wq, sw = quarot_quant_int4(w, rotate=rotate, clip_ratio=clip_ratio, stream=stream)
+    return quarot_pack_e3m2(wq, stream=stream), sw
 
 
 def quarot_linear(x: torch.Tensor, wq: torch.Tensor, sw: torch.Tensor, rotate: bool = True,

@@ -382,6 +382,91 @@ quarot_status quarot_linear(const quarot_f16 *x, const uint8_t *wq, const quarot
     return e == hipSuccess ? QUAROT_OK : hip_fail(e);
 }
 
+quarot_status quarot_quant_int4_e3m2(const quarot_f16 *x, uint8_t *q6, quarot_f16 *scale,
+                                     int64_t rows, int64_t n, int rotate, float clip_ratio,
+                                     void *stream)
+{
+    if (rows < 0 || !clip_ok(clip_ratio))
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;
+    quarot_status st = check_rot_size(n, rotate != 0, EPI_E3M2, &k, &m);
+    if (st)
+        return st;
+    if (rows > (int64_t(1) << 30))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!x || !q6 || !scale)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(q6) || !aligned16(scale))
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    RotArgs a{};
+    a.x = x;
+    a.out = q6;
+    a.scale = scale;
+    a.rows = rows;
+    a.n = (int)n;
+    a.c = rotation_scale(n);
+    a.clip = clip_ratio;
+    hipError_t e = launch_rotate(a, EPI_E3M2, rotate != 0, k, m, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+size_t quarot_linear_e3m2_workspace_size(int64_t M, int64_t K)
+{
+    if (M < 0 || K <= 0 || (K % 128))
+        return 0;
+    const size_t codes = ((size_t)M * (size_t)(K / 4 * 3) + 255) & ~(size_t)255;
+    const size_t scales = ((size_t)M * 2 + 255) & ~(size_t)255;
+    return codes + scales;
+}
+
+quarot_status quarot_linear_e3m2(const quarot_f16 *x, const uint8_t *wq6, const quarot_f16 *sw,
+                                 quarot_f16 *y, int64_t M, int64_t N, int64_t K, int rotate,
+                                 float clip_ratio, void *workspace, size_t workspace_bytes,
+                                 void *stream)
+{
+    if (M < 0 || N < 0 || !clip_ok(clip_ratio))
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;
+    quarot_status st = check_rot_size(K, rotate != 0, EPI_E3M2, &k, &m);
+    if (st)
+        return st;
+    if ((st = check_gemm_sizes(M, N, K)))
+        return st;
+    if (M == 0 || N == 0)
+        return QUAROT_OK;
+    if (!x || !wq6 || !sw || !y)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(wq6) || !aligned16(sw) || !aligned16(y))
+        return QUAROT_ERR_ALIGNMENT;
+    if (!workspace || workspace_bytes < quarot_linear_e3m2_workspace_size(M, K))
+        return QUAROT_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    uint8_t *xq6 = static_cast<uint8_t *>(workspace);
+    const size_t codes = ((size_t)M * (size_t)(K / 4 * 3) + 255) & ~(size_t)255;
+    quarot_f16 *sx = reinterpret_cast<quarot_f16 *>(xq6 + codes);
+    RotArgs ra{};
+    ra.x = x;
+    ra.out = xq6;
+    ra.scale = sx;
+    ra.rows = M;
+    ra.n = (int)K;
+    ra.c = rotation_scale(K);
+    ra.clip = clip_ratio;
+    hipError_t e = launch_rotate(ra, EPI_E3M2, rotate != 0, k, m, (hipStream_t)stream);
+    if (e != hipSuccess)
+        return hip_fail(e);
+    GemmArgs ga{xq6, sx, wq6, sw, y, nullptr, (int)M, (int)N, (int)K};
+    e = launch_gemm(ga, (hipStream_t)stream, 6);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
 quarot_status quarot_quant_int8(const quarot_f16 *x, int8_t *q, quarot_f16 *scale, int64_t rows,
                                 int64_t n, int rotate, float clip_ratio, int bits, void *stream)
 {
@@ -756,6 +841,41 @@ quarot_status quarot_swiglu_quant_int4(const quarot_f16 *gate, const quarot_f16 
     a.c = rotation_scale(n);
     a.clip = clip_ratio;
     hipError_t e = launch_rotate(a, EPI_SYM, true, k, m, (hipStream_t)stream, PRO_SWIGLU);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+quarot_status quarot_swiglu_quant_e3m2(const quarot_f16 *gate, const quarot_f16 *up, uint8_t *q6,
+                                       quarot_f16 *scale, int64_t rows, int64_t n,
+                                       float clip_ratio, void *stream)
+{
+    if (rows < 0 || !clip_ok(clip_ratio))
+        return QUAROT_ERR_INVALID_ARG;
+    int k, m;
+    quarot_status st = check_rot_size(n, true, EPI_E3M2, &k, &m);
+    if (st)
+        return st;
+    if (!rotate_supported(EPI_E3M2, true, k, m, (int)n, PRO_SWIGLU))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (rows > (int64_t(1) << 30))
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (rows == 0)
+        return QUAROT_OK;
+    if (!gate || !up || !q6 || !scale)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(gate) || !aligned16(up) || !aligned16(q6) || !aligned16(scale))
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device()))
+        return st;
+    RotArgs a{};
+    a.x = gate;
+    a.x2 = up;
+    a.out = q6;
+    a.scale = scale;
+    a.rows = rows;
+    a.n = (int)n;
+    a.c = rotation_scale(n);
+    a.clip = clip_ratio;
+    hipError_t e = launch_rotate(a, EPI_E3M2, true, k, m, (hipStream_t)stream, PRO_SWIGLU);
     return e == hipSuccess ? QUAROT_OK : hip_fail(e);
 }
 

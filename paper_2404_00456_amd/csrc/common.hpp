@@ -16,6 +16,7 @@ enum Epilogue : int {
     EPI_KV = 2,   // per-group asymmetric uint4 codes + fp16 scale, zero
     EPI_SYM8 = 3, // per-row symmetric codes in [-qmax-1, qmax], one byte each
     EPI_F32 = 4,  // store y in binary32 (input of the weights' clip search)
+    EPI_E3M2 = 5, // EPI_SYM's codes as e3m2 numbers, tiled layout (see e3m2_head)
 };
 
 // Load stages of the rotate kernels.
@@ -23,6 +24,56 @@ enum Prologue : int {
     PRO_PLAIN = 0,   // x is the row
     PRO_SWIGLU = 1,  // the row is RN16(silu(x) * x2) (gate x, up x2)
 };
+
+// ---- int4 codes as e3m2 numbers (the operand format of the fp6 GEMM) ----
+//
+// e3m2: sign, 3 exponent bits (bias 3), 2 mantissa bits; every integer in
+// -8..8 is exact.  For such an integer q, the binary32 encoding b of q has
+// exponent field e and top mantissa bits m with 4 e + m = 4 (E + 124) + M
+// for q's e3m2 exponent field E and mantissa M (|q| >= 1), so the code is
+// (b >> 21 & 0x3FF) - 496, clamped at 0 for q = 0, plus the sign at bit 5.
+__device__ __forceinline__ uint32_t e3m2_of_bits(uint32_t b)
+{
+    const int mag = (int)((b >> 21) & 0x3FFu) - 4 * 124;
+    return (uint32_t)(mag > 0 ? mag : 0) | ((b >> 26) & 0x20u);
+}
+
+__device__ __forceinline__ uint32_t e3m2_of_int(int q)
+{
+    return e3m2_of_bits(__float_as_uint((float)q));
+}
+
+// 32 int4 codes (two's complement nibbles, low nibble first) -> the 192-bit
+// unit sum_e e3m2(q_e) << 6e as six dwords.
+__device__ __forceinline__ void e3m2_unit(const uint32_t (&w)[4], uint32_t (&o)[6])
+{
+#pragma unroll
+    for (int d = 0; d < 6; ++d)
+        o[d] = 0;
+#pragma unroll
+    for (int e = 0; e < 32; ++e) {
+        const uint32_t n = (w[e >> 3] >> (4 * (e & 7))) & 15u;
+        const uint32_t code = e3m2_of_int(((int)n ^ 8) - 8);
+        const int bit = 6 * e;
+        o[bit >> 5] |= code << (bit & 31);
+        if ((bit & 31) > 26)
+            o[(bit >> 5) + 1] |= code >> (32 - (bit & 31));
+    }
+}
+
+// Tiled e3m2 layout of a [rows, K] code matrix: K/128 blocks of rows * 96
+// bytes.  Unit u (k = 128 b + 32 u .. + 31) of row r: dwords 0-3 (head) at
+// e3m2_head, dwords 4-5 (tail) at e3m2_tail.  The row-dependent slot
+// swizzles make the GEMM's LDS reads of 16 rows hit distinct banks.
+__device__ __forceinline__ int64_t e3m2_head(int64_t rows, int64_t r, int b, int u)
+{
+    return (int64_t)b * rows * 96 + r * 64 + 16 * (u ^ (int)((r >> 1) & 3));
+}
+
+__device__ __forceinline__ int64_t e3m2_tail(int64_t rows, int64_t r, int b, int u)
+{
+    return (int64_t)b * rows * 96 + rows * 64 + r * 32 + 8 * (u ^ (int)((r >> 2) & 3));
+}
 
 struct RotArgs {
     const uint16_t *x;   // fp16 [rows, n]

@@ -726,18 +726,6 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_e3m2(GemmArgs a)
     gemm_main<6>(a, lds);
 }
 
-// e3m2 code of an integer q in -8..8, from the bits of the binary32 q: the
-// exponent field e and the top two mantissa bits m give 4 e + m, which is
-// 4 (E + 124) + M for the e3m2 exponent field E and mantissa M (1 <= |q|:
-// E = e - 124 for bias 3 against 127); q = 0 gives 0 after the clamp.  The
-// sign moves from bit 31 to bit 5.
-__device__ __forceinline__ uint32_t e3m2_of_int(int q)
-{
-    const uint32_t b = __float_as_uint((float)q);
-    const int mag = (int)((b >> 21) & 0x3FFu) - 4 * 124;
-    return (uint32_t)max(mag, 0) | ((b >> 26) & 0x20u);
-}
-
 // int4 codes (two per byte, low nibble first) -> the tiled e3m2 layout.
 // The 32 codes of unit u (k = 128 b + 32 u + e, e = 0..31) of row r form the
 // 192-bit word sum_e code(q_e) << 6e, code(q) being q in e3m2 (sign, 3
@@ -761,20 +749,10 @@ __global__ __launch_bounds__(256) void k_pack_e3m2(const uint8_t *__restrict__ q
     const int b = (int)(rb / rows);
     const uint4 in = *reinterpret_cast<const uint4 *>(q4 + r * ((int64_t)kb * 64) + (4 * b + u) * 16);
     const uint32_t w[4] = {in.x, in.y, in.z, in.w};
-    uint32_t o[6] = {0, 0, 0, 0, 0, 0};
-#pragma unroll
-    for (int e = 0; e < 32; ++e) {
-        const uint32_t n = (w[e >> 3] >> (4 * (e & 7))) & 15u;
-        const uint32_t code = e3m2_of_int(((int)n ^ 8) - 8);
-        const int bit = 6 * e;
-        o[bit >> 5] |= code << (bit & 31);
-        if ((bit & 31) > 26)
-            o[(bit >> 5) + 1] |= code >> (32 - (bit & 31));
-    }
-    uint8_t *blk = q6 + (int64_t)b * rows * 96;
-    const int hs = u ^ (int)((r >> 1) & 3), ts = u ^ (int)((r >> 2) & 3);
-    *reinterpret_cast<uint4 *>(blk + r * 64 + 16 * hs) = make_uint4(o[0], o[1], o[2], o[3]);
-    *reinterpret_cast<uint2 *>(blk + rows * 64 + r * 32 + 8 * ts) = make_uint2(o[4], o[5]);
+    uint32_t o[6];
+    e3m2_unit(w, o);
+    *reinterpret_cast<uint4 *>(q6 + e3m2_head(rows, r, b, u)) = make_uint4(o[0], o[1], o[2], o[3]);
+    *reinterpret_cast<uint2 *>(q6 + e3m2_tail(rows, r, b, u)) = make_uint2(o[4], o[5]);
 }
 
 }  // namespace

@@ -116,19 +116,53 @@ __device__ __forceinline__ uint32_t sym8_code(float y, const Divisor &d, float q
     return d.ok ? c : 0u;
 }
 
+// The EPI_SYM code of y as an e3m2 number: the same clamp and rounding, with
+// the rounded value kept as a binary32 integer (t + 1.5 * 2^23 rounds t to
+// an integer; subtracting 1.5 * 2^23 again is exact).
+__device__ __forceinline__ uint32_t e3m2_code(float y, const Divisor &d)
+{
+    const float t = fminf(fmaxf(quotient(y, d), -8.0f), 7.0f);
+    const float r = (t + 0x1.8p23f) - 0x1.8p23f;
+    return d.ok ? e3m2_of_bits(__float_as_uint(r)) : 0u;
+}
+
+// Codes of the 8 elements i0 .. i0+7 (i0 a multiple of 8) of row r into the
+// tiled e3m2 layout: their 48 bits are bytes 6p .. 6p+5 of the 24 of unit u
+// (i0 = 128 b + 32 u + 8 p), whose bytes 0-15 are the head and 16-23 the
+// tail; each lane writes one dword and one short.
+__device__ __forceinline__ void store_e3m2_8(uint8_t *q, int64_t rows, int64_t r, int64_t i0,
+                                             const float *v, const Divisor &d)
+{
+    uint32_t c[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        c[e] = e3m2_code(v[e], d);
+    const uint32_t lo = c[0] | (c[1] << 6) | (c[2] << 12) | (c[3] << 18) | (c[4] << 24) | (c[5] << 30);
+    const uint32_t hi = (c[5] >> 2) | (c[6] << 4) | (c[7] << 10);
+    const int p = (int)(i0 >> 3) & 3, u = (int)(i0 >> 5) & 3, b = (int)(i0 >> 7);
+    const int64_t h = e3m2_head(rows, r, b, u), t = e3m2_tail(rows, r, b, u);
+    const bool odd = (p & 1) != 0;
+    const uint32_t dw = odd ? (lo >> 16) | (hi << 16) : lo;
+    const uint16_t sh = (uint16_t)(odd ? lo : hi);
+    const int64_t da = p == 0 ? h : p == 1 ? h + 8 : p == 2 ? h + 12 : t + 4;
+    const int64_t sa = p == 0 ? h + 4 : p == 1 ? h + 6 : p == 2 ? t : t + 2;
+    *reinterpret_cast<uint32_t *>(q + da) = dw;
+    *reinterpret_cast<uint16_t *>(q + sa) = sh;
+}
+
 // The symmetric epilogues: scale divisor, row stride of the codes, and the
 // codes of 8 (or 4) consecutive elements starting at element i0 of a row:
 // EPI_SYM packs nibbles (4 bytes per 8), EPI_SYM8 one byte per code.
 template <int EPI>
 __device__ __forceinline__ float sym_divisor(const RotArgs &a)
 {
-    return EPI == EPI_SYM ? 7.0f : (float)a.qmax;
+    return (EPI == EPI_SYM || EPI == EPI_E3M2) ? 7.0f : (float)a.qmax;
 }
 
 template <int EPI>
 __device__ __forceinline__ int64_t sym_row_bytes(int64_t n)
 {
-    return EPI == EPI_SYM ? n / 2 : n;
+    return (EPI == EPI_SYM || EPI == EPI_E3M2) ? n / 2 : n;
 }
 
 template <int EPI>
@@ -450,7 +484,7 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
 #pragma unroll
         for (int cc = 0; cc < C; ++cc)
             store_y8<EPI>(a.out, row * N + ((cc * W + w) * L + pos) * 8, v[cc]);
-    } else if constexpr (EPI == EPI_SYM || EPI == EPI_SYM8) {
+    } else if constexpr (EPI == EPI_SYM || EPI == EPI_SYM8 || EPI == EPI_E3M2) {
         __shared__ float red[W > 1 ? W : 1];
         float amax = 0.0f;
 #pragma unroll
@@ -463,10 +497,17 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
         const float s32 = (amax * a.clip) / qd;
         const uint16_t s16 = f2h(s32);
         const Divisor dv = make_divisor(h2f(s16));
-        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(N);
+        if constexpr (EPI == EPI_E3M2) {
 #pragma unroll
-        for (int cc = 0; cc < C; ++cc)
-            store_codes8<EPI>(qr, ((cc * W + w) * L + pos) * 8, v[cc], dv, qd);
+            for (int cc = 0; cc < C; ++cc)
+                store_e3m2_8(static_cast<uint8_t *>(a.out), a.rows, row,
+                             ((cc * W + w) * L + pos) * 8, v[cc], dv);
+        } else {
+            uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(N);
+#pragma unroll
+            for (int cc = 0; cc < C; ++cc)
+                store_codes8<EPI>(qr, ((cc * W + w) * L + pos) * 8, v[cc], dv, qd);
+        }
         if (pos == 0 && w == 0)
             a.scale[row] = s16;
     } else {  // EPI_KV: one wave per row; a group is G consecutive elements
@@ -680,7 +721,9 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
                 store_y4<EPI>(a.out, row * N + g * M + 4 * p, &v[cc][4 * p]);
         }
     } else {
-        static_assert(EPI == EPI_SYM || EPI == EPI_SYM8, "small-m kernels serve activations");
+        static_assert(EPI == EPI_SYM || EPI == EPI_SYM8 || EPI == EPI_E3M2,
+                      "small-m kernels serve activations");
+        static_assert(EPI != EPI_E3M2 || W > 1, "e3m2 rows stage in LDS: one row per block");
         __shared__ float red[W > 1 ? W : 1];
         float amax = 0.0f;
 #pragma unroll
@@ -693,13 +736,39 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
         const float s32 = (amax * a.clip) / qd;
         const uint16_t s16 = f2h(s32);
         const Divisor dv = make_divisor(h2f(s16));
-        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(N);
+        if constexpr (EPI == EPI_E3M2) {
+            // a lane's M codes do not fill whole 32-code units: the row's int4
+            // codes go through LDS, then each thread packs whole units
+            __shared__ uint4 stage[N / 32];
+            uint8_t *st = reinterpret_cast<uint8_t *>(stage);
 #pragma unroll
-        for (int cc = 0; cc < C; ++cc) {
-            const int g = (cc * W + w) * L + pos;
+            for (int cc = 0; cc < C; ++cc) {
+                const int g = (cc * W + w) * L + pos;
 #pragma unroll
-            for (int p = 0; p < M / 4; ++p)
-                store_codes4<EPI>(qr, g * M + 4 * p, &v[cc][4 * p], dv, qd);
+                for (int p = 0; p < M / 4; ++p)
+                    store_codes4<EPI_SYM>(st, g * M + 4 * p, &v[cc][4 * p], dv, qd);
+            }
+            __syncthreads();
+            uint8_t *q = static_cast<uint8_t *>(a.out);
+            for (int u = tid; u < N / 32; u += 64 * W) {
+                const uint4 in = stage[u];
+                const uint32_t wd[4] = {in.x, in.y, in.z, in.w};
+                uint32_t o[6];
+                e3m2_unit(wd, o);
+                *reinterpret_cast<uint4 *>(q + e3m2_head(a.rows, row, u >> 2, u & 3)) =
+                    make_uint4(o[0], o[1], o[2], o[3]);
+                *reinterpret_cast<uint2 *>(q + e3m2_tail(a.rows, row, u >> 2, u & 3)) =
+                    make_uint2(o[4], o[5]);
+            }
+        } else {
+            uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(N);
+#pragma unroll
+            for (int cc = 0; cc < C; ++cc) {
+                const int g = (cc * W + w) * L + pos;
+#pragma unroll
+                for (int p = 0; p < M / 4; ++p)
+                    store_codes4<EPI>(qr, g * M + 4 * p, &v[cc][4 * p], dv, qd);
+            }
         }
         if (pos == 0 && w == 0)
             a.scale[row] = s16;
@@ -885,7 +954,10 @@ __global__ __launch_bounds__(256) void k_quant_plain(RotArgs a)
     for (int ch = tid; ch < chunks; ch += 256) {
         float v[8];
         load8(xr + ch * 8, v);
-        store_codes8<EPI>(qr, ch * 8, v, dv, qd);
+        if constexpr (EPI == EPI_E3M2)
+            store_e3m2_8(static_cast<uint8_t *>(a.out), a.rows, row, ch * 8, v, dv);
+        else
+            store_codes8<EPI>(qr, ch * 8, v, dv, qd);
     }
     if (tid == 0)
         a.scale[row] = s16;
@@ -1186,16 +1258,45 @@ hipError_t dispatch_smallm(const RotArgs &a, int k, hipStream_t s)
     return hipErrorInvalidValue;
 }
 
+// e3m2 output from the small-m kernels: the configurations with one row per
+// block (the row is staged in LDS)
+template <int M, int PRO>
+hipError_t dispatch_smallm_e3m2(const RotArgs &a, int k, hipStream_t s)
+{
+    if constexpr (M == 12) {
+        if (k == 10)
+            return go_smallm<12, 6, 2, 8, EPI_E3M2, PRO>(a, s);
+        if (k == 11)
+            return go_smallm<12, 6, 4, 8, EPI_E3M2, PRO>(a, s);
+    } else {
+        if (k == 9)
+            return go_smallm<M, 6, 2, 4, EPI_E3M2, PRO>(a, s);
+        if (k == 10)
+            return go_smallm<M, 6, 4, 4, EPI_E3M2, PRO>(a, s);
+    }
+    return hipErrorInvalidValue;
+}
+
 template <int EPI, int PRO>
 hipError_t dispatch_rotated(const RotArgs &a, int k, int m, hipStream_t s)
 {
-    switch (m) {
-    case 1: return dispatch_pow2<EPI, true, PRO>(a, k, s);
-    case 12: return dispatch_smallm<12, 8, EPI, PRO>(a, k, s);
-    case 20: return dispatch_smallm<20, 4, EPI, PRO>(a, k, s);
-    case 28: return dispatch_smallm<28, 4, EPI, PRO>(a, k, s);
-    case 108: return (k <= 6) ? go_largem<108, 1, EPI, PRO>(a, s) : go_largem<108, 2, EPI, PRO>(a, s);
-    case 172: return go_largem<172, 1, EPI, PRO>(a, s);
+    if constexpr (EPI == EPI_E3M2) {
+        switch (m) {
+        case 1: return k >= 7 ? dispatch_pow2<EPI_E3M2, true, PRO>(a, k, s) : hipErrorInvalidValue;
+        case 12: return dispatch_smallm_e3m2<12, PRO>(a, k, s);
+        case 20: return dispatch_smallm_e3m2<20, PRO>(a, k, s);
+        case 28: return dispatch_smallm_e3m2<28, PRO>(a, k, s);
+        }
+        return hipErrorInvalidValue;
+    } else {
+        switch (m) {
+        case 1: return dispatch_pow2<EPI, true, PRO>(a, k, s);
+        case 12: return dispatch_smallm<12, 8, EPI, PRO>(a, k, s);
+        case 20: return dispatch_smallm<20, 4, EPI, PRO>(a, k, s);
+        case 28: return dispatch_smallm<28, 4, EPI, PRO>(a, k, s);
+        case 108: return (k <= 6) ? go_largem<108, 1, EPI, PRO>(a, s) : go_largem<108, 2, EPI, PRO>(a, s);
+        case 172: return go_largem<172, 1, EPI, PRO>(a, s);
+        }
     }
     return hipErrorInvalidValue;
 }
@@ -1220,8 +1321,21 @@ bool rotate_supported(int epi, bool rotate, int k, int m, int n, int pro)
 {
     if (n <= 0 || n % 8 != 0 || n > 32768)
         return false;
-    if (pro == PRO_SWIGLU && (epi != EPI_SYM || !rotate))
+    if (pro == PRO_SWIGLU && ((epi != EPI_SYM && epi != EPI_E3M2) || !rotate))
         return false;
+    if (epi == EPI_E3M2) {
+        if (n % 128)
+            return false;
+        if (!rotate)
+            return true;
+        switch (m) {
+        case 1: return k >= 7 && k <= 15;
+        case 12: return k == 10 || k == 11;
+        case 20:
+        case 28: return k == 9 || k == 10;
+        }
+        return false;
+    }
     if (!rotate)
         return epi == EPI_SYM || epi == EPI_SYM8 || (epi == EPI_KV && m == 1 && k >= 3 && k <= 9);
     if (epi == EPI_KV)
@@ -1242,13 +1356,22 @@ hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, h
 {
     if (a.rows == 0)
         return hipSuccess;
-    if (pro == PRO_SWIGLU)
-        return (epi == EPI_SYM && rotate) ? dispatch_rotated<EPI_SYM, PRO_SWIGLU>(a, k, m, s)
-                                          : hipErrorInvalidValue;
+    if (pro == PRO_SWIGLU) {
+        if (!rotate)
+            return hipErrorInvalidValue;
+        if (epi == EPI_SYM)
+            return dispatch_rotated<EPI_SYM, PRO_SWIGLU>(a, k, m, s);
+        if (epi == EPI_E3M2)
+            return dispatch_rotated<EPI_E3M2, PRO_SWIGLU>(a, k, m, s);
+        return hipErrorInvalidValue;
+    }
     if (!rotate) {
-        if (epi == EPI_SYM || epi == EPI_SYM8) {
+        if (epi == EPI_SYM || epi == EPI_SYM8 || epi == EPI_E3M2) {
             if (epi == EPI_SYM)
                 hipLaunchKernelGGL(k_quant_plain<EPI_SYM>, dim3((unsigned)a.rows), dim3(256), 0,
+                                   s, a);
+            else if (epi == EPI_E3M2)
+                hipLaunchKernelGGL(k_quant_plain<EPI_E3M2>, dim3((unsigned)a.rows), dim3(256), 0,
                                    s, a);
             else
                 hipLaunchKernelGGL(k_quant_plain<EPI_SYM8>, dim3((unsigned)a.rows), dim3(256), 0,
@@ -1274,6 +1397,7 @@ hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, h
     case EPI_F16: return dispatch_rotated<EPI_F16, PRO_PLAIN>(a, k, m, s);
     case EPI_SYM: return dispatch_rotated<EPI_SYM, PRO_PLAIN>(a, k, m, s);
     case EPI_SYM8: return dispatch_rotated<EPI_SYM8, PRO_PLAIN>(a, k, m, s);
+    case EPI_E3M2: return dispatch_rotated<EPI_E3M2, PRO_PLAIN>(a, k, m, s);
     case EPI_KV:
         return a.group == a.n ? dispatch_pow2<EPI_KV, true, PRO_PLAIN, false, true>(a, k, s)
                               : dispatch_pow2<EPI_KV, true, PRO_PLAIN>(a, k, s);

@@ -159,3 +159,96 @@ def test_gemm_e3m2_full_size(dev, orc, M, N, K):
     racc = orc.gemm_i32(xs, H(wq))
     ry = orc.dequant(racc, ss, H(sw))
     assert_same(H(y6[rows]).view(np.uint16), ry.view(np.uint16), "full size sampled rows")
+
+
+# ------------------------------------------- quantizer writing e3m2 ---
+
+E3M2_ROTATED_N = [128, 256, 1024, 4096, 8192, 16384, 32768, 12288, 24576, 10240, 20480, 14336,
+                  28672]
+
+
+@pytest.mark.parametrize("n", E3M2_ROTATED_N)
+def test_quant_int4_e3m2_rotated(dev, orc, n):
+    """Rotated rows quantized straight into the tiled e3m2 layout: every
+    code (decoded on the host) and every scale equal to the oracle's, with
+    clipping (the code -8 appears), an all-zero row and a spike."""
+    import paper_2404_00456_amd as q
+    import workloads
+    rows = 37 if n <= 8192 else 9
+    say(f"quant e3m2 rotate n={n} rows={rows}")
+    x = workloads.random_rows(n + 5, rows, n, "student_t3", 2.0)
+    x[0] = 0
+    x[1, 0] = 100.0
+    for clip in (1.0, 0.9):
+        q6, s6 = q.quarot_quant_int4_e3m2(T(x, dev), rotate=True, clip_ratio=clip)
+        rq, rs = orc.quant_int4(x, rotate=True, clip=clip)
+        assert_same(decode_e3m2_layout(H(q6), rows, n), orc.unpack_int4(rq).astype(np.float64),
+                    f"e3m2 codes n={n} clip={clip}")
+        assert_same(H(s6).view(np.uint16), rs.view(np.uint16), f"e3m2 scales n={n} clip={clip}")
+
+
+@pytest.mark.parametrize("n", [128, 384, 4096, 28672])
+def test_quant_int4_e3m2_plain(dev, orc, n):
+    import paper_2404_00456_amd as q
+    import workloads
+    rows = 13
+    x = workloads.random_rows(3 * n + 1, rows, n, "student_t3")
+    q6, s6 = q.quarot_quant_int4_e3m2(T(x, dev), rotate=False, clip_ratio=0.9)
+    rq, rs = orc.quant_int4(x, rotate=False, clip=0.9)
+    assert_same(decode_e3m2_layout(H(q6), rows, n), orc.unpack_int4(rq).astype(np.float64),
+                f"e3m2 plain codes n={n}")
+    assert_same(H(s6).view(np.uint16), rs.view(np.uint16), f"e3m2 plain scales n={n}")
+
+
+@pytest.mark.parametrize("rows", [1, 3, 255, 257])
+def test_quant_int4_e3m2_ragged_rows(dev, orc, rows):
+    """Row counts across the 4-rows-per-block kernels (n = 128, 1024) and the
+    row-per-block ones (n = 8192, 28672): the layout's row terms use the
+    total row count."""
+    import paper_2404_00456_amd as q
+    import workloads
+    for n in (128, 1024, 8192, 28672):
+        x = workloads.random_rows(rows * 7 + n, rows, n)
+        q6, s6 = q.quarot_quant_int4_e3m2(T(x, dev), rotate=True)
+        rq, rs = orc.quant_int4(x, rotate=True)
+        assert_same(decode_e3m2_layout(H(q6), rows, n), orc.unpack_int4(rq).astype(np.float64),
+                    f"e3m2 codes n={n} rows={rows}")
+        assert_same(H(s6).view(np.uint16), rs.view(np.uint16), f"e3m2 scales n={n} rows={rows}")
+
+
+@pytest.mark.parametrize("n", [14336, 28672])
+def test_swiglu_quant_e3m2(dev, orc, n):
+    import paper_2404_00456_amd as q
+    import workloads
+    rows = 9
+    g = workloads.random_rows(2 * n, rows, n, "normal", 3.0)
+    u = workloads.random_rows(2 * n + 1, rows, n, "student_t3", 1.0)
+    g[0] = -100.0
+    for clip in (1.0, 0.9):
+        q6, s6 = q.quarot_swiglu_quant_e3m2(T(g, dev), T(u, dev), clip_ratio=clip)
+        rq, rs = orc.swiglu_quant_int4(g, u, rotate=True, clip=clip)
+        assert_same(decode_e3m2_layout(H(q6), rows, n), orc.unpack_int4(rq).astype(np.float64),
+                    f"swiglu e3m2 codes n={n} clip={clip}")
+        assert_same(H(s6).view(np.uint16), rs.view(np.uint16), f"swiglu e3m2 scales n={n}")
+
+
+@pytest.mark.parametrize("M,N,K", [(37, 300, 1024), (300, 520, 8192), (257, 264, 28672)])
+def test_linear_e3m2(dev, orc, M, N, K):
+    """The e3m2 linear layer equals quarot_linear bit for bit, and the
+    oracle's layer within its defined arithmetic."""
+    import paper_2404_00456_amd as q
+    import workloads
+    say(f"linear e3m2 M={M} N={N} K={K}")
+    x = workloads.random_rows(M + K, M, K, "student_t3", 2.0)
+    w = workloads.random_rows(N + 2 * K, N, K, "normal", 0.05)
+    xd, wd = T(x, dev), T(w, dev)
+    wq, sw = q.prepare_weight(wd, rotate=True)
+    w6, sw6 = q.prepare_weight_e3m2(wd, rotate=True)
+    assert_same(H(sw6).view(np.uint16), H(sw).view(np.uint16), "e3m2 weight scales")
+    y4 = q.quarot_linear(xd, wq, sw, rotate=True, clip_ratio=0.9)
+    y6 = q.quarot_linear_e3m2(xd, w6, sw6, rotate=True, clip_ratio=0.9)
+    assert_same(H(y6).view(np.uint16), H(y4).view(np.uint16), "e3m2 linear == int4 linear")
+    rq, rs = orc.quant_int4(x, rotate=True, clip=0.9)
+    racc = orc.gemm_i32(rq, H(wq))
+    ry = orc.dequant(racc, rs, H(sw))
+    assert_fp16_close(H(y6), ry, f"e3m2 linear M={M} N={N} K={K}")
