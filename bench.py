@@ -7,11 +7,16 @@ Hadamard n = 8192) and down-projection shape K = 28672 -> N = 8192
 (n = 1024 * 28).  Synthetic inputs (seeded normals with 0.5% outlier
 channels x100, weights N(0, 0.02^2)), prepared weights resident in HBM.
 
-One step = both layers, each as the two launches quarot_linear makes:
-rotate+quantize the activations (quarot_quant_int4), then the W4A4 GEMM
-with fused dequant (quarot_w4a4_gemm).  HIP events on the launch stream
-bracket every kernel, so the per-kernel averages over the timed steps give
-the roofline figures.  value = 2*M*N*K summed over both layers / step time.
+One step = both layers, each as the two launches quarot_linear_e3m2 makes:
+rotate+quantize the activations straight into the e3m2 operand layout
+(quarot_quant_int4_e3m2), then the W4A4 GEMM on gfx950's fp6 matrix
+instruction with fused dequant (quarot_w4a4_gemm_e3m2; weights prepared
+and repacked once, untimed).  Its outputs equal the int4-operand path's
+(quarot_quant_int4 + quarot_w4a4_gemm) bit for bit; that path is timed
+beside it under kernels/<layer>/int4_operands.  HIP events on the launch
+stream bracket every kernel, so the per-kernel averages over the timed
+steps give the roofline figures.  value = 2*M*N*K summed over both layers
+/ step time.
 
 The same run then times the 4-bit KV cache path on its own workload (K and V
 fp16 [batch 16, 64 heads, 4096 tokens, head_dim 128], 1 GiB each):
@@ -36,6 +41,7 @@ if ROOT not in sys.path:
 
 # MI355X published peaks
 PEAK_I8_TOPS = 5000.0   # dense int8 MFMA, TOP/s
+PEAK_FP6_TOPS = 10100.0  # dense fp6 / fp4 MFMA, TFLOP/s (ops on exact integers here)
 PEAK_F32_ADDS = 78.6e12  # fp32 vector adds per second (157.3 TFLOP/s counts an FMA as 2)
 PEAK_HBM_GBS = 8000.0   # HBM3E, GB/s
 
@@ -44,28 +50,41 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-# HBM-side bytes per k_gemm_w4a4 launch on this workload, averaged over the
-# up and down launches: FETCH_SIZE x 2 + WRITE_SIZE x 1 (KiB, scaled by what
-# the counters read for a plain 1 GiB copy), from the two rocprofv3 --pmc runs
-# summarized in profiles/.  Valid only for the kernel source they were taken
-# with; after any change to it the figure is reported as null.
-GEMM_TRAFFIC = {"isa_sha256_16": "63759d8bd4b5d4a3", "bytes_per_launch": 3.458e+09}
+# HBM-side bytes per launch of each per-token GEMM on this workload,
+# averaged over the up and down launches: FETCH_SIZE x 2 + WRITE_SIZE x 1
+# (KiB, scaled by what the counters read for a plain 1 GiB copy), from the
+# two rocprofv3 --pmc runs summarized in profiles/.  Valid only for the
+# kernel machine code they were taken with (its fingerprint); after any
+# change to it the figure is reported as null.
+GEMM_TRAFFIC = {
+    "k_gemm_w4a4": {"isa_sha256_16": "63759d8bd4b5d4a3", "bytes_per_launch": 3.458e+09},
+    "k_gemm_w4a4_e3m2": {"isa_sha256_16": "", "bytes_per_launch": None},
+}
 
 
-def gemm_isa_hash() -> str:
-    """The per-token GEMM kernel's machine-code fingerprint written by the
+def gemm_isa_hash(kernel: str) -> str:
+    """A per-token GEMM kernel's machine-code fingerprint written by the
     build (empty if absent)."""
     try:
         with open(os.path.join(ROOT, "paper_2404_00456_amd", "gemm_isa.sha")) as f:
-            return f.read().strip()
+            for line in f:
+                parts = line.split()
+                if len(parts) == 2 and parts[0] == kernel:
+                    return parts[1]
     except OSError:
-        return ""
+        pass
+    return ""
 
 
-def rotate_bytes(M, K):
-    """Algorithmic HBM bytes of rotate+quantize: read fp16 x, write packed
-    int4 codes and one fp16 scale per row."""
-    return M * K * 2 + M * K // 2 + M * 2
+def gemm_traffic(kernel: str):
+    t = GEMM_TRAFFIC[kernel]
+    return t["bytes_per_launch"] if gemm_isa_hash(kernel) == t["isa_sha256_16"] else None
+
+
+def rotate_bytes(M, K, code_bits=4):
+    """Algorithmic HBM bytes of rotate+quantize: read fp16 x, write the codes
+    (4 bits each packed, or 6 in the e3m2 layout) and one fp16 scale per row."""
+    return M * K * 2 + M * K * code_bits // 8 + M * 2
 
 
 def kv_bytes(rows, D, group):
@@ -297,18 +316,34 @@ def main():
         wd = torch.from_numpy(w).to(dev)
         wq, sw = q.prepare_weight(wd, rotate=True)  # offline step, untimed
         del wd
+        w6 = q.quarot_pack_e3m2(wq)  # offline repack, untimed
         ws = torch.empty(q.quarot_linear_workspace_size(wl.M, wl.K), dtype=torch.uint8,
                          device=dev)
         xq = ws[: wl.M * wl.K // 2].view(wl.M, wl.K // 2)
         off = (wl.M * wl.K // 2 + 255) // 256 * 256
         sx = ws[off: off + 2 * wl.M].view(torch.float16)
+        x6 = torch.empty((wl.K // 128, wl.M * 96), dtype=torch.uint8, device=dev)
+        sx6 = torch.empty((wl.M,), dtype=torch.float16, device=dev)
         y = torch.empty((wl.M, wl.N), dtype=torch.float16, device=dev)
-        layers.append(dict(wl=wl, x=x, w=w, xd=xd, wq=wq, sw=sw, xq=xq, sx=sx, y=y))
+        layers.append(dict(wl=wl, x=x, w=w, xd=xd, wq=wq, sw=sw, w6=w6, xq=xq, sx=sx, x6=x6,
+                           sx6=sx6, y=y))
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
+        for li, L in enumerate(layers):
+            if ev is not None:
+                ev[2 * li].record(stream)
+            q.quarot_quant_int4_e3m2(L["xd"], rotate=True, clip_ratio=1.0, q6=L["x6"],
+                                     scale=L["sx6"])
+            if ev is not None:
+                ev[2 * li + 1].record(stream)
+            q.quarot_w4a4_gemm_e3m2(L["x6"], L["sx6"], L["w6"], L["sw"], y=L["y"])
+        if ev is not None:
+            ev[4].record(stream)
+
+    def step_int4(ev=None):
         for li, L in enumerate(layers):
             if ev is not None:
                 ev[2 * li].record(stream)
@@ -318,6 +353,17 @@ def main():
             q.quarot_w4a4_gemm(L["xq"], L["sx"], L["wq"], L["sw"], y=L["y"])
         if ev is not None:
             ev[4].record(stream)
+
+    def split(events):
+        """per-kernel durations from a step's events (ms)"""
+        rot = [[], []]
+        gem = [[], []]
+        for ev in events:
+            for li in range(2):
+                rot[li].append(ev[2 * li].elapsed_time(ev[2 * li + 1]))
+                end = ev[2 * li + 2] if li == 0 else ev[4]
+                gem[li].append(ev[2 * li + 1].elapsed_time(end))
+        return rot, gem
 
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
@@ -333,22 +379,30 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
+    rot, gem = split(events)
 
-    # per-kernel durations from the events (ms)
-    rot = [[], []]
-    gem = [[], []]
-    for ev in events:
-        for li in range(2):
-            rot[li].append(ev[2 * li].elapsed_time(ev[2 * li + 1]))
-            end = ev[2 * li + 2] if li == 0 else ev[4]
-            gem[li].append(ev[2 * li + 1].elapsed_time(end))
+    # the int4-operand path on the same inputs, for comparison (same outputs)
+    for _ in range(args.warmup):
+        step_int4()
+    ev4 = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step_int4(ev4[s])
+    torch.cuda.synchronize()
+    ms_step4 = (time.perf_counter() - t0) * 1e3 / args.steps
+    rot4, gem4 = split(ev4)
     ops = [2 * L["wl"].M * L["wl"].N * L["wl"].K for L in layers]
     total_ops = sum(ops)
     value = total_ops / (ms_step * 1e-3) / 1e12
     gemm_ms = [float(np.mean(g)) for g in gem]
     rot_ms = [float(np.mean(r)) for r in rot]
     gemm_tops = sum(ops) / (sum(gemm_ms) * 1e-3) / 1e12
-    rbytes = [rotate_bytes(L["wl"].M, L["wl"].K) for L in layers]
+    gemm4_ms = [float(np.mean(g)) for g in gem4]
+    rot4_ms = [float(np.mean(r)) for r in rot4]
+    gemm4_tops = sum(ops) / (sum(gemm4_ms) * 1e-3) / 1e12
+    rbytes = [rotate_bytes(L["wl"].M, L["wl"].K, 6) for L in layers]
+    rbytes4 = [rotate_bytes(L["wl"].M, L["wl"].K, 4) for L in layers]
     kernels = {}
     for li, L in enumerate(layers):
         wl = L["wl"]
@@ -369,6 +423,14 @@ def main():
             "gemm_us_p10_p50_p90": pct(gem[li], (10, 50, 90)),
             "gemm_TOPS": round(ops[li] / (gemm_ms[li] * 1e-3) / 1e12, 1),
             "linear_TOPS": round(ops[li] / ((gemm_ms[li] + rot_ms[li]) * 1e-3) / 1e12, 1),
+            "int4_operands": {
+                "rotate_quant_us": round(rot4_ms[li] * 1e3, 2),
+                "rotate_quant_GBps": round(rbytes4[li] / (rot4_ms[li] * 1e-3) / 1e9, 1),
+                "gemm_us": round(gemm4_ms[li] * 1e3, 2),
+                "gemm_us_p10_p50_p90": pct(gem4[li], (10, 50, 90)),
+                "gemm_TOPS": round(ops[li] / (gemm4_ms[li] * 1e-3) / 1e12, 1),
+                "linear_TOPS": round(ops[li] / ((gemm4_ms[li] + rot4_ms[li]) * 1e-3) / 1e12, 1),
+            },
         }
 
     # the int8 MFMA peak re-derived from the device (CUs x peak clock x 8192
@@ -384,12 +446,26 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     probe_tops = probe_ops * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    probe6_ops = q.quarot_mfma_probe_fp6(probe_out, cus, 2000)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(10):
+        q.quarot_mfma_probe_fp6(probe_out, cus, 2000)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    probe6_tops = probe6_ops * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e12
     del probe_out
     peak_i8 = {"cus": cus, "peak_sclk_mhz": clk_khz / 1000,
                "derived_TOPS": round(cus * clk_khz * 1e3 * 8192 / 1e12, 1),
                "published_TOPS": PEAK_I8_TOPS,
                "mfma_probe_TOPS": round(probe_tops, 1),
-               "gemm_frac_of_probe": round(gemm_tops / probe_tops, 4)}
+               "int4_operand_gemm_frac_of_probe": round(gemm4_tops / probe_tops, 4)}
+    # fp6: v_mfma_f32_16x16x128_f8f6f4 does 16 x 16 x 128 multiply-adds in 16
+    # cycles per SIMD, 16384 ops per clock per CU
+    peak_fp6 = {"derived_TOPS": round(cus * clk_khz * 1e3 * 16384 / 1e12, 1),
+                "published_TOPS": PEAK_FP6_TOPS,
+                "mfma_probe_TOPS": round(probe6_tops, 1),
+                "gemm_frac_of_probe": round(gemm_tops / probe6_tops, 4)}
 
     kv = None if args.no_kv else bench_kv(q, workloads, torch, np, dev, stream, args.kv_iters)
     nxt = None if args.no_next else bench_next(q, torch, dev, stream, layers)
@@ -419,8 +495,7 @@ def main():
                "sample": f"first {R} of {layers[0]['wl'].M} token rows of each layer "
                          f"(rotate+quantize+GEMM+dequant), {dt:.1f} s"}
 
-    traffic = (GEMM_TRAFFIC["bytes_per_launch"]
-               if gemm_isa_hash() == GEMM_TRAFFIC["isa_sha256_16"] else None)
+    traffic = gemm_traffic("k_gemm_w4a4_e3m2")
     out = {
         "metric": "W4A4 rotated-linear TOPS + % int8-MFMA peak; Hadamard/quant GB/s "
                   "(Llama2 shapes)",
@@ -433,18 +508,24 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "int4",
+        "dtype": "int4 codes as e3m2 (fp6 MFMA, exact fp32 sums)",
         "data": "synthetic",
         "config": {"workload": "llama2_70b_ffn_prefill: M=16384 tokens (batch 8 x seq 2048); "
                                "up K=8192->N=28672 (H_8192), down K=28672->N=8192 "
                                "(H_1024 x H_28)",
                    "global_batch": 8, "seq_len": 2048, "parallelism": "none"},
         "pct_int8_peak": round(100 * value / PEAK_I8_TOPS, 2),
-        "roofline": {"bound": "mfma", "kernel": "k_gemm_w4a4",
-                     "achieved": round(gemm_tops, 1), "peak": PEAK_I8_TOPS, "unit": "TOP/s",
-                     "frac": round(gemm_tops / PEAK_I8_TOPS, 4), "traffic": traffic},
+        "roofline": {"bound": "mfma", "kernel": "k_gemm_w4a4_e3m2",
+                     "achieved": round(gemm_tops, 1), "peak": PEAK_FP6_TOPS, "unit": "TOP/s",
+                     "frac": round(gemm_tops / PEAK_FP6_TOPS, 4), "traffic": traffic},
+        "int4_operand_path": {"ms_per_step": round(ms_step4, 4),
+                              "value": round(sum(ops) / (ms_step4 * 1e-3) / 1e12, 2),
+                              "gemm_kernel": "k_gemm_w4a4", "gemm_TOPS": round(gemm4_tops, 1),
+                              "gemm_frac_int8_peak": round(gemm4_tops / PEAK_I8_TOPS, 4),
+                              "traffic": gemm_traffic("k_gemm_w4a4")},
         "kernels": kernels,
         "peak_i8": peak_i8,
+        "peak_fp6": peak_fp6,
         "kv": kv,
         "next": nxt,
         "cpu_baseline": cpu,

@@ -42,6 +42,7 @@ SIGNATURES = {
     "quarot_last_hip_error": (_I, []),
     "quarot_version": (_I, []),
     "quarot_device_peaks": (_I, [_P, _P]),
+    "quarot_mfma_probe_fp6": (_I, [_P, _I64, _I, _P]),
     "quarot_mfma_probe": (_I, [_P, _I64, _I, _P]),
     "quarot_hadamard_factor": (_I, [_I64, _P, _P]),
     "quarot_hadamard_factor_table": (_I, [_I, _P]),
@@ -171,6 +172,17 @@ def quarot_mfma_probe(out: torch.Tensor, blocks: int, iters: int,
     _check("quarot_mfma_probe", lib().quarot_mfma_probe(
         _ptr(out, torch.int32, "out"), int(blocks), int(iters), _stream(stream)))
     return blocks * 8 * iters * 32 * 16384 * 2  # waves x MFMAs x multiply-adds x 2
+
+
+def quarot_mfma_probe_fp6(out: torch.Tensor, blocks: int, iters: int,
+                          stream: Optional[torch.cuda.Stream] = None) -> int:
+    """Enqueue the e3m2 fp6-MFMA-only probe; returns its number of ops (2
+    per multiply-add).  out: int32 device tensor of blocks * 512."""
+    if out.numel() < blocks * 512:
+        raise ValueError("out must hold blocks * 512 int32")
+    _check("quarot_mfma_probe_fp6", lib().quarot_mfma_probe_fp6(
+        _ptr(out, torch.int32, "out"), int(blocks), int(iters), _stream(stream)))
+    return blocks * 8 * iters * 32 * 32768 * 2
 
 
 def quarot_hadamard_factor_table(m: int):
@@ -660,4 +672,7 @@ __all__ = [
     "quarot_swiglu", "quarot_swiglu_quant_int4", "quarot_hadamard_heads", "quarot_hadamard_heads_quant_int4",
     "quarot_kv_quant", "quarot_kv_dequant", "quarot_kv_append",
     "quarot_kv_attention_workspace_size", "quarot_kv_decode_attention",
+    "quarot_mfma_probe_fp6", "quarot_pack_e3m2", "quarot_w4a4_gemm_e3m2",
+    "quarot_quant_int4_e3m2", "quarot_linear_e3m2_workspace_size", "quarot_linear_e3m2",
+    "quarot_swiglu_quant_e3m2", "prepare_weight_e3m2",
 ]

@@ -33,6 +33,10 @@ def hipcc() -> str:
 
 
 ISA_SHA = os.path.join(HERE, "gemm_isa.sha")
+GEMM_KERNELS = {
+    "k_gemm_w4a4": "_ZN6quarot12_GLOBAL__N_111k_gemm_w4a4ENS_8GemmArgsE",
+    "k_gemm_w4a4_e3m2": "_ZN6quarot12_GLOBAL__N_116k_gemm_w4a4_e3m2ENS_8GemmArgsE",
+}
 
 
 def kernel_isa_sha(src: str, symbol: str) -> str:
@@ -64,12 +68,13 @@ def build(verbose: bool = False) -> str:
         sys.stderr.write(res.stdout + res.stderr)
         raise RuntimeError("hipcc failed building libquarot.so")
     os.replace(tmp, LIB)
-    # fingerprint of the per-token GEMM's machine code, which the bench's
-    # stored hardware byte counts refer to
-    sha = kernel_isa_sha(os.path.join(CSRC, "gemm_w4a4.hip"),
-                         "_ZN6quarot12_GLOBAL__N_111k_gemm_w4a4ENS_8GemmArgsE")
+    # fingerprints of the per-token GEMMs' machine code, which the bench's
+    # stored hardware byte counts refer to: one "name sha" line per kernel
+    lines = []
+    for name, sym in GEMM_KERNELS.items():
+        lines.append(f"{name} {kernel_isa_sha(os.path.join(CSRC, 'gemm_w4a4.hip'), sym)}\n")
     with open(ISA_SHA, "w") as f:
-        f.write(sha + "\n")
+        f.writelines(lines)
     return LIB
 
 

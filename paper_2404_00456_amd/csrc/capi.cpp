@@ -195,6 +195,21 @@ quarot_status quarot_mfma_probe(int32_t *out, int64_t blocks, int iters, void *s
     return e == hipSuccess ? QUAROT_OK : hip_fail(e);
 }
 
+quarot_status quarot_mfma_probe_fp6(int32_t *out, int64_t blocks, int iters, void *stream)
+{
+    if (blocks <= 0 || blocks > (1 << 20) || iters <= 0 || iters > (1 << 20))
+        return QUAROT_ERR_INVALID_ARG;
+    if (!out)
+        return QUAROT_ERR_INVALID_ARG;
+    if (!aligned16(out))
+        return QUAROT_ERR_ALIGNMENT;
+    quarot_status st = check_device();
+    if (st)
+        return st;
+    hipError_t e = launch_mfma_probe_fp6(out, (int)blocks, iters, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
 quarot_status quarot_hadamard_factor(int64_t n, int *log2_pow2, int *m)
 {
     if (!log2_pow2 || !m || n <= 0)
