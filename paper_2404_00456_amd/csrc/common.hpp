@@ -43,22 +43,46 @@ __device__ __forceinline__ uint32_t e3m2_of_int(int q)
     return e3m2_of_bits(__float_as_uint((float)q));
 }
 
-// 32 int4 codes (two's complement nibbles, low nibble first) -> the 192-bit
-// unit sum_e e3m2(q_e) << 6e as six dwords.
+// 8 int4 codes (a dword of two's complement nibbles, low nibble first) ->
+// their e3m2 codes as 48 bits (code e at bit 6e): lo = bits 0-31, hi =
+// bits 32-47.  Byte lookups: v_perm_b32 picks, per byte, one of 8 table
+// bytes (the codes of q = 0..7, or of q = -8..-1), and the nibble's sign bit
+// chooses between the two lookups.
+__device__ __forceinline__ uint32_t e3m2_lut4(uint32_t x)  // 4 nibbles, one per byte
+{
+    const uint32_t sel = x & 0x07070707u;
+    const uint32_t pos = __builtin_amdgcn_perm(0x17161514u, 0x12100C00u, sel);  // q = 0..7
+    const uint32_t neg = __builtin_amdgcn_perm(0x2C303234u, 0x35363738u, sel);  // q = -8..-1
+    const uint32_t m = x & 0x08080808u;
+    const uint32_t mask = (m << 3) - (m >> 3);  // 0x3F in the bytes whose q < 0
+    return (neg & mask) | (pos & ~mask);
+}
+
+__device__ __forceinline__ void e3m2_of_nibbles8(uint32_t w, uint32_t &lo, uint32_t &hi)
+{
+    const uint32_t a = e3m2_lut4(w & 0x0F0F0F0Fu);         // codes 0, 2, 4, 6
+    const uint32_t b = e3m2_lut4((w >> 4) & 0x0F0F0F0Fu);  // codes 1, 3, 5, 7
+    // 12-bit pairs (c_2i | c_2i+1 << 6): pairs 0, 2 and pairs 1, 3 at bits 0, 16
+    const uint32_t p02 = (a & 0x00FF00FFu) | ((b & 0x00FF00FFu) << 6);
+    const uint32_t p13 = ((a >> 8) & 0x00FF00FFu) | (((b >> 8) & 0x00FF00FFu) << 6);
+    lo = (p02 & 0xFFFu) | ((p13 & 0xFFFu) << 12) | (p02 << 8 & 0xFF000000u);
+    hi = ((p02 >> 24) & 0xFu) | ((p13 >> 16) << 4);
+}
+
+// 32 int4 codes (four nibble dwords) -> the 192-bit unit sum_e e3m2(q_e) << 6e
+// as six dwords.
 __device__ __forceinline__ void e3m2_unit(const uint32_t (&w)[4], uint32_t (&o)[6])
 {
+    uint32_t lo[4], hi[4];
 #pragma unroll
-    for (int d = 0; d < 6; ++d)
-        o[d] = 0;
-#pragma unroll
-    for (int e = 0; e < 32; ++e) {
-        const uint32_t n = (w[e >> 3] >> (4 * (e & 7))) & 15u;
-        const uint32_t code = e3m2_of_int(((int)n ^ 8) - 8);
-        const int bit = 6 * e;
-        o[bit >> 5] |= code << (bit & 31);
-        if ((bit & 31) > 26)
-            o[(bit >> 5) + 1] |= code >> (32 - (bit & 31));
-    }
+    for (int k = 0; k < 4; ++k)
+        e3m2_of_nibbles8(w[k], lo[k], hi[k]);
+    o[0] = lo[0];
+    o[1] = hi[0] | (lo[1] << 16);
+    o[2] = (lo[1] >> 16) | (hi[1] << 16);
+    o[3] = lo[2];
+    o[4] = hi[2] | (lo[3] << 16);
+    o[5] = (lo[3] >> 16) | (hi[3] << 16);
 }
 
 // Tiled e3m2 layout of a [rows, K] code matrix: K/128 blocks of rows * 96

@@ -486,6 +486,11 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
             __asm__ volatile("" ::: "memory");
         }
         if constexpr (BITS == 6) {
+            // (A 4-wave variant, one wave per SIMD with 128 x 128 wave tiles
+            // and the accumulators in AGPRs, reads a third less from LDS per
+            // MFMA but measured ~5% slower on the Llama-2-70B FFN shapes:
+            // one wave per SIMD exposes the latencies the second one hides.)
+            //
             // A k-step is four quarters of 8 MFMAs over the slice pairs
             // A[0..1] x B[0..3], A[0..1] x B[4..7], A[2..3] x B[0..3],
             // A[2..3] x B[4..7].  Every read lands in registers a quarter
