@@ -66,6 +66,17 @@ __device__ __forceinline__ void dma16(const void *g, uint32_t lds_base)
                  : "memory");
 }
 
+// dma16 in the SGPR-base form: lane l reads base + voff[l] (a wave-uniform
+// 64-bit base, a 32-bit per-lane offset), so the per-step address update
+// is scalar work.
+__device__ __forceinline__ void dma16s(uint32_t voff, const void *base, uint32_t lds_base)
+{
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(voff), "s"(base), "s"(lds_base)
+                 : "memory");
+}
+
 // 4 bytes per lane into LDS at lds_base + 4 * lane (same rules as dma16).
 __device__ __forceinline__ void dma4(const void *g, uint32_t lds_base)
 {

@@ -213,6 +213,7 @@ struct Ring {
 constexpr int HEADS = (BM + BN) * 64;  // e3m2 stage: offset of the tails
 
 typedef int v8i __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) uint64_t lds_u64;
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 // One e3m2 operand slice of a lane: 32 codes, six dwords (head, tail).
@@ -331,18 +332,25 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     for (int i = 0; i < DPW; ++i)
         dst[i] = i < 4 ? (i < 2 ? 0 : BM * BKB) + (wave + 8 * (i & 1)) * 1024
                        : HEADS + (i == 4 ? 0 : BM * 32) + wave * 1024;
-    // e3m2: source of DMA i for k-step sk of the tile at (m0, n0)
-    auto src6 = [&](int i, int m0, int n0, int sk) -> const uint8_t * {
+    // e3m2 DMAs in the SGPR-base form.  voff6: lane offset of DMA i inside
+    // the tile's run of heads (or tails), rows past the matrix edge clamped;
+    // base6: the run's wave-uniform start for k-step sk.
+    auto voff6 = [&](int i, int m0, int n0) -> uint32_t {
         const bool xop = i < 2 || i == 4;
-        const int64_t rows = xop ? M : N;
-        const uint8_t *blk = (xop ? a.xq : a.wq) + (int64_t)sk * (rows * 96);
-        const int org = xop ? m0 : n0;
+        const int lim = (xop ? M - m0 : N - n0) - 1;
         if (i < 4) {
             const int r = 16 * (wave + 8 * (i & 1)) + rsub;
-            return blk + (int64_t)min(org + r, (int)rows - 1) * 64 + (lane & 3) * 16;
+            return (uint32_t)(min(r, lim) * 64 + (lane & 3) * 16);
         }
         const int r = 32 * wave + (lane >> 1);
-        return blk + rows * 64 + (int64_t)min(org + r, (int)rows - 1) * 32 + (lane & 1) * 16;
+        return (uint32_t)(min(r, lim) * 32 + (lane & 1) * 16);
+    };
+    auto base6 = [&](int i, int m0, int n0, int sk) -> const uint8_t * {
+        const bool xop = i < 2 || i == 4;
+        const int64_t rows = xop ? M : N;
+        const int64_t org = xop ? m0 : n0;
+        const uint8_t *blk = (xop ? a.xq : a.wq) + (int64_t)sk * (rows * 96);
+        return i < 4 ? blk + org * 64 : blk + rows * 64 + org * 32;
     };
     auto sources = [&](int m0, int n0, const uint8_t *(&src)[DPW]) {
 #pragma unroll
@@ -359,11 +367,16 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
         for (int i = 0; i < DPW; ++i)
             dma16(src[i] + (int64_t)kt * BKB, __builtin_amdgcn_readfirstlane(sbase + dst[i]));
     };
+    int dsts[DPW];  // LDS targets, wave-uniform (scalar registers)
+#pragma unroll
+    for (int i = 0; i < DPW; ++i)
+        dsts[i] = __builtin_amdgcn_readfirstlane(dst[i]);
+    uint32_t vo[DPW];
     auto issue6 = [&](int m0, int n0, int sk, int stage) {
         const uint32_t sbase = lds_base + stage * RING_STAGE;
 #pragma unroll
         for (int i = 0; i < DPW; ++i)
-            dma16(src6(i, m0, n0, sk), __builtin_amdgcn_readfirstlane(sbase + dst[i]));
+            dma16s(vo[i], base6(i, m0, n0, sk), sbase + dsts[i]);
     };
 
     const int orow = lane & 15;
@@ -399,8 +412,13 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     int m0, n0;
     tile_mn(t, m0, n0);
     const uint8_t *src[DPW];
-    if constexpr (BITS != 6)
+    if constexpr (BITS != 6) {
         sources(m0, n0, src);
+    } else {
+#pragma unroll
+        for (int i = 0; i < DPW; ++i)
+            vo[i] = voff6(i, m0, n0);
+    }
     if (fast_tile(m0, n0))
         scale_dma(m0, n0, 0);
     // ring position: global step g of this block lives in stage g % S
@@ -503,15 +521,20 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
             // sched_barrier(0) fences keep that order: left to itself the
             // scheduler sinks each read to just before its first MFMA.
             Op6 A[NI], B[8];
+            // tails read as volatile: the compiler would pair two slices'
+            // tails into one ds_read2st64_b64 and then copy each next to its
+            // head (the MFMA takes the six dwords as one register tuple)
             auto rdA = [&](int i, int stage) {
                 const uint8_t *sb = lds + stage * RING_STAGE;
                 A[i].h = *reinterpret_cast<const uint4 *>(sb + arow + i * 16 * 64);
-                A[i].t = *reinterpret_cast<const uint2 *>(sb + atail + i * 16 * 32);
+                const uint64_t t = *(const volatile lds_u64 *)(lds_void *)(sb + atail + i * 16 * 32);
+                A[i].t = make_uint2((uint32_t)t, (uint32_t)(t >> 32));
             };
             auto rdB = [&](int j, int stage) {
                 const uint8_t *sb = lds + stage * RING_STAGE;
                 B[j].h = *reinterpret_cast<const uint4 *>(sb + brow + j * 16 * 64);
-                B[j].t = *reinterpret_cast<const uint2 *>(sb + btail + j * 16 * 32);
+                const uint64_t t = *(const volatile lds_u64 *)(lds_void *)(sb + btail + j * 16 * 32);
+                B[j].t = make_uint2((uint32_t)t, (uint32_t)(t >> 32));
             };
             auto quarter = [&](int i0, int j0) {
 #pragma unroll
@@ -542,14 +565,19 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
                 __builtin_amdgcn_s_barrier();
                 __asm__ volatile("" ::: "memory");
                 {
-                    // addresses recomputed from the (wave-uniform) tile
-                    // origin each step rather than kept in 24 VGPRs; the
-                    // empty asm keeps the compiler from hoisting them
+                    // DMA of global step g+S: this tile's step kt+S, else the
+                    // next tile's step kt+S-KT (its lane offsets replace this
+                    // tile's once, when the first of them is issued), else a
+                    // harmless re-fetch
                     const bool here = kt + S < KT;
                     const bool cur = here || tn_ < 0;
-                    int sk = here ? kt + S : (tn_ >= 0 ? kt + S - KT : KT - 1);
-                    int me = cur ? m0 : m1, ne = cur ? n0 : n1;
-                    __asm__ volatile("" : "+s"(me), "+s"(ne), "+s"(sk));
+                    const int sk = here ? kt + S : (tn_ >= 0 ? kt + S - KT : KT - 1);
+                    const int me = cur ? m0 : m1, ne = cur ? n0 : n1;
+                    if (kt + S == KT && tn_ >= 0) {
+#pragma unroll
+                        for (int i = 0; i < DPW; ++i)
+                            vo[i] = voff6(i, m1, n1);
+                    }
                     issue6(me, ne, sk, g % S);
                 }
                 rdA(0, nx);
