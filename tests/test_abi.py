@@ -229,6 +229,43 @@ def test_invalid_arguments_rejected_before_device(L):
     assert LG(P, P, P, P, 4, 4, 256, 96, 1, 1.0, P, 1 << 20, S) == UNSUPPORTED
     assert LG(P, P, P, P, 4, 4, 256, 128, 1, 1.5, P, 1 << 20, S) == INVALID
     assert LG(None, None, None, None, 0, 4, 256, 128, 1, 1.0, None, 0, S) == OK
+    # e3m2 operand path
+    assert L.quarot_pack_e3m2(P, P2, -1, 128, S) == INVALID
+    assert L.quarot_pack_e3m2(P, P2, 4, 0, S) == INVALID
+    assert L.quarot_pack_e3m2(P, P2, 4, 192, S) == UNSUPPORTED      # not a multiple of 128
+    assert L.quarot_pack_e3m2(P, P2, 4, 65536 + 128, S) == UNSUPPORTED
+    assert L.quarot_pack_e3m2(None, P2, 4, 128, S) == INVALID
+    assert L.quarot_pack_e3m2(P, UNALIGNED, 4, 128, S) == ALIGN
+    assert L.quarot_pack_e3m2(None, None, 0, 128, S) == OK
+    E = L.quarot_w4a4_gemm_e3m2
+    assert E(P, P, P, P, P, None, 4, 4, 192, S) == UNSUPPORTED       # K not a multiple of 128
+    assert E(P, P, P, P, P, None, -1, 4, 128, S) == INVALID
+    assert E(P, P, P, P, P, None, 4, 4, 0, S) == INVALID
+    assert E(P, None, P, P, P, None, 4, 4, 128, S) == INVALID
+    assert E(P, P, P, P, P, UNALIGNED, 4, 4, 128, S) == ALIGN
+    assert E(None, None, None, None, None, None, 0, 4, 128, S) == OK
+    QE = L.quarot_quant_int4_e3m2
+    assert QE(P, P2, P2, 4, 128, 1, 0.0, S) == INVALID
+    assert QE(P, P2, P2, 4, 64, 1, 1.0, S) == UNSUPPORTED           # not a multiple of 128
+    assert QE(P, P2, P2, 4, 28 * 256, 1, 1.0, S) == UNSUPPORTED      # m = 28 needs 2^9 or 2^10
+    assert QE(P, P2, P2, 4, 108 * 128, 1, 1.0, S) == UNSUPPORTED     # m = 108: int4 + repack
+    assert QE(P, None, P2, 4, 128, 1, 1.0, S) == INVALID
+    assert QE(P, P2, UNALIGNED, 4, 128, 1, 1.0, S) == ALIGN
+    assert QE(None, None, None, 0, 128, 1, 1.0, S) == OK
+    LE = L.quarot_linear_e3m2
+    assert L.quarot_linear_e3m2_workspace_size(3, 256) == 768 + 256
+    assert L.quarot_linear_e3m2_workspace_size(3, 192) == 0
+    assert LE(P, P, P, P, 4, 4, 128, 1, 1.0, P, 10, S) == WORKSPACE
+    assert LE(P, P, P, P, 4, 4, 128, 1, 1.0, ctypes.c_void_p((1 << 20) + 16), 1 << 20,
+              S) == ALIGN
+    assert LE(P, P, P, P, 4, 4, 192, 1, 1.0, P, 1 << 20, S) == UNSUPPORTED
+    assert LE(P, P, P, P, 4, 4, 128, 1, 1.5, P, 1 << 20, S) == INVALID
+    assert LE(None, None, None, None, 0, 4, 128, 1, 1.0, None, 0, S) == OK
+    SE = L.quarot_swiglu_quant_e3m2
+    assert SE(P, P2, P, P2, 4, 8192 + 128, 1.0, S) == UNSUPPORTED
+    assert SE(P, P2, P, P2, 4, 28672, 0.0, S) == INVALID
+    assert SE(P, None, P, P2, 4, 28672, 1.0, S) == INVALID
+    assert L.quarot_mfma_probe_fp6(P, 0, 10, S) == INVALID
 
 
 @pytest.mark.skipif(has_gpu(), reason="valid arguments would reach a real device")
@@ -247,6 +284,12 @@ def test_no_device_reported(L):
     assert L.quarot_mfma_probe(P, 4, 10, None) == NODEV
     assert L.quarot_linear_w4a4_grouped(P, P, P, P, 4, 4, 256, 256, 1, 1.0, P, 1 << 20,
                                         None) == NODEV
+    assert L.quarot_pack_e3m2(P, P2, 4, 128, None) == NODEV
+    assert L.quarot_w4a4_gemm_e3m2(P, P, P, P, P, None, 4, 4, 128, None) == NODEV
+    assert L.quarot_quant_int4_e3m2(P, P2, P2, 4, 28672, 1, 1.0, None) == NODEV
+    assert L.quarot_linear_e3m2(P, P, P, P, 4, 4, 8192, 1, 1.0, P, 1 << 20, None) == NODEV
+    assert L.quarot_swiglu_quant_e3m2(P, P2, P, P2, 4, 28672, 1.0, None) == NODEV
+    assert L.quarot_mfma_probe_fp6(P, 4, 10, None) == NODEV
 
 
 def test_binding_rejects_host_tensors():
