@@ -378,6 +378,10 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
         for (int i = 0; i < DPW; ++i)
             dma16s(vo[i], base6(i, m0, n0, sk), sbase + dsts[i]);
     };
+    // running bases of the next DMA step (wave-uniform), advanced by one
+    // k-block per step: scalar adds instead of per-step products
+    const uint8_t *bcur[DPW];
+    auto stride6 = [&](int i) -> int64_t { return (int64_t)(i < 2 || i == 4 ? M : N) * 96; };
 
     const int orow = lane & 15;
     const int ounit = ((lane >> 4) ^ ((orow >> 1) & 3)) << 4;
@@ -429,6 +433,11 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
             issue6(m0, n0, min(i, KT - 1), i);
         else
             issue(src, min(i, KT - 1), i);
+    }
+    if constexpr (BITS == 6) {
+#pragma unroll
+        for (int i = 0; i < DPW; ++i)
+            bcur[i] = base6(i, m0, n0, S);
     }
 
     for (int it = 0; t >= 0; ++it) {
@@ -566,19 +575,26 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
                 __asm__ volatile("" ::: "memory");
                 {
                     // DMA of global step g+S: this tile's step kt+S, else the
-                    // next tile's step kt+S-KT (its lane offsets replace this
-                    // tile's once, when the first of them is issued), else a
-                    // harmless re-fetch
-                    const bool here = kt + S < KT;
-                    const bool cur = here || tn_ < 0;
-                    const int sk = here ? kt + S : (tn_ >= 0 ? kt + S - KT : KT - 1);
-                    const int me = cur ? m0 : m1, ne = cur ? n0 : n1;
-                    if (kt + S == KT && tn_ >= 0) {
+                    // next tile's step kt+S-KT (its bases and lane offsets
+                    // replace this tile's when the first of them is issued),
+                    // else a harmless re-fetch (keeps the wait counts exact)
+                    const uint32_t sbase = lds_base + (g % S) * RING_STAGE;
+                    if (kt + S < KT || tn_ >= 0) {
+                        if (kt + S == KT) {
 #pragma unroll
-                        for (int i = 0; i < DPW; ++i)
-                            vo[i] = voff6(i, m1, n1);
+                            for (int i = 0; i < DPW; ++i) {
+                                vo[i] = voff6(i, m1, n1);
+                                bcur[i] = base6(i, m1, n1, 0);
+                            }
+                        }
+#pragma unroll
+                        for (int i = 0; i < DPW; ++i) {
+                            dma16s(vo[i], bcur[i], sbase + dsts[i]);
+                            bcur[i] += stride6(i);
+                        }
+                    } else {
+                        issue6(m0, n0, KT - 1, g % S);
                     }
-                    issue6(me, ne, sk, g % S);
                 }
                 rdA(0, nx);
                 rdA(1, nx);
