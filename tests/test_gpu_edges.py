@@ -107,3 +107,54 @@ def test_side_stream_matches_default_stream(dev, orc):
     assert_same(H(scale1).view(np.uint16), H(scale0).view(np.uint16), "scales on a side stream")
     rq, _ = orc.quant_int4(x, rotate=True)
     assert_same(H(codes1), rq, "side-stream codes vs oracle")
+
+
+def test_e3m2_entry_points_edges(dev, orc):
+    """The e3m2 operand path: empty inputs are no-ops, rejected arguments
+    leave the outputs untouched, misaligned buffers are refused, and a side
+    stream gives the default stream's bits."""
+    import torch
+    import paper_2404_00456_amd as q
+    say("e3m2 edges")
+    e16 = torch.empty((0, 8192), dtype=torch.float16, device=dev)
+    q6, s6 = q.quarot_quant_int4_e3m2(e16, rotate=True)
+    assert q6.shape == (64, 0) and s6.shape == (0,)
+    assert q.quarot_pack_e3m2(torch.empty((0, 4096), dtype=torch.uint8, device=dev)).shape == (64, 0)
+    w6 = torch.zeros((64, 256 * 96), dtype=torch.uint8, device=dev)
+    sw = torch.ones(256, dtype=torch.float16, device=dev)
+    x6 = torch.zeros((64, 0), dtype=torch.uint8, device=dev)
+    assert q.quarot_w4a4_gemm_e3m2(x6, torch.ones(0, dtype=torch.float16, device=dev), w6,
+                                   sw).shape == (0, 256)
+    assert q.quarot_linear_e3m2(e16, w6, sw).shape == (0, 256)
+    # rejected: clip out of range, width without an e3m2 epilogue
+    x = T(workloads.random_rows(21, 32, 8192), dev)
+    qbuf = torch.full((64, 32 * 96), 0xAB, dtype=torch.uint8, device=dev)
+    sbuf = torch.full((32,), 7.0, dtype=torch.float16, device=dev)
+    for clip in (0.0, 1.5):
+        with pytest.raises(q.QuarotError):
+            q.quarot_quant_int4_e3m2(x, rotate=True, clip_ratio=clip, q6=qbuf, scale=sbuf)
+    with pytest.raises(q.QuarotError):  # 13824 = 2^7 * 108: refused, int4 + repack instead
+        q.quarot_quant_int4_e3m2(torch.zeros((32, 13824), dtype=torch.float16, device=dev),
+                                 rotate=True, q6=qbuf, scale=sbuf)
+    y = torch.full((32, 256), 3.0, dtype=torch.float16, device=dev)
+    with pytest.raises(q.QuarotError):  # clip out of range
+        q.quarot_linear_e3m2(x, w6, sw, clip_ratio=2.0, y=y)
+    torch.cuda.synchronize()
+    assert bool((qbuf == 0xAB).all()) and bool((sbuf == 7.0).all()) and bool((y == 3.0).all())
+    # misaligned code buffer
+    raw = torch.zeros(64 * 32 * 96 + 16, dtype=torch.uint8, device=dev)
+    with pytest.raises(q.QuarotError) as ei:
+        q.quarot_quant_int4_e3m2(x, rotate=True, q6=raw[8:8 + 64 * 32 * 96].view(64, 32 * 96),
+                                 scale=sbuf)
+    assert ei.value.status == 3
+    # side stream
+    xs = workloads.random_rows(23, 300, 8192)
+    xd = T(xs, dev)
+    a6, a_s = q.quarot_quant_int4_e3m2(xd, rotate=True)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        b6, b_s = q.quarot_quant_int4_e3m2(xd, rotate=True, stream=side)
+    torch.cuda.current_stream().wait_stream(side)
+    assert_same(H(b6), H(a6), "e3m2 codes on a side stream")
+    assert_same(H(b_s).view(np.uint16), H(a_s).view(np.uint16), "e3m2 scales on a side stream")
