@@ -523,7 +523,8 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
             // A[2..3] x B[4..7].  Every read lands in registers a quarter
             // has just freed, at least one quarter before its first use, so
             // the operands are not double buffered (200 live VGPRs):
-            //   quarter 1: read B[4..7], A[2..3] of this step
+            //   quarter 1: read B[4..7] of this step
+            //   quarter 2: read A[2..3] of this step
             //   barrier after quarter 2 (every read of this stage done)
             //   quarter 3: read A[0..1] of the next step
             //   quarter 4: read B[0..3] of the next step
@@ -564,17 +565,22 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
 #pragma unroll
                 for (int j = 4; j < 8; ++j)
                     rdB(j, cs);
-                rdA(2, cs);
-                rdA(3, cs);
                 quarter(0, 0);
 #pragma unroll
-                for (int k = 0; k < 6; ++k) {
-                    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                for (int k = 0; k < 8; ++k) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                 }
-                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
                 __builtin_amdgcn_sched_barrier(0);
+                rdA(2, cs);
+                rdA(3, cs);
                 quarter(0, 4);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 3);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 3);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, 4, 3);
                 __builtin_amdgcn_sched_barrier(0);
                 __asm__ volatile("" ::: "memory");
                 __builtin_amdgcn_s_waitcnt(waitcnt_imm((S - 2) * DPW, 0));
