@@ -335,11 +335,16 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     // e3m2 DMAs in the SGPR-base form.  voff6: lane offset of DMA i inside
     // the tile's run of heads (or tails), rows past the matrix edge clamped;
     // base6: the run's wave-uniform start for k-step sk.
+    //
+    // 4- and 8-bit codes (row-major, pitch ldk) use the same form: lane
+    // offset r * ldk + unit (rows clamped), base x + m0 * ldk + sk * 64.
     auto voff6 = [&](int i, int m0, int n0) -> uint32_t {
         const bool xop = i < 2 || i == 4;
         const int lim = (xop ? M - m0 : N - n0) - 1;
         if (i < 4) {
             const int r = 16 * (wave + 8 * (i & 1)) + rsub;
+            if constexpr (BITS != 6)
+                return (uint32_t)(min(r, lim) * (int)ldk + cunit * 16);
             return (uint32_t)(min(r, lim) * 64 + (lane & 3) * 16);
         }
         const int r = 32 * wave + (lane >> 1);
@@ -347,26 +352,14 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     };
     auto base6 = [&](int i, int m0, int n0, int sk) -> const uint8_t * {
         const bool xop = i < 2 || i == 4;
-        const int64_t rows = xop ? M : N;
         const int64_t org = xop ? m0 : n0;
+        if constexpr (BITS != 6)
+            return (xop ? a.xq : a.wq) + org * ldk + (int64_t)sk * BKB;
+        const int64_t rows = xop ? M : N;
         const uint8_t *blk = (xop ? a.xq : a.wq) + (int64_t)sk * (rows * 96);
         return i < 4 ? blk + org * 64 : blk + rows * 64 + org * 32;
     };
-    auto sources = [&](int m0, int n0, const uint8_t *(&src)[DPW]) {
-#pragma unroll
-        for (int i = 0; i < DPW; ++i) {
-            const int r = 16 * (wave + 8 * (i & 1)) + rsub;
-            src[i] = (i < 2) ? a.xq + (int64_t)min(m0 + r, M - 1) * ldk + cunit * 16
-                             : a.wq + (int64_t)min(n0 + r, N - 1) * ldk + cunit * 16;
-        }
-    };
     const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void *)lds;
-    auto issue = [&](const uint8_t *const (&src)[DPW], int kt, int stage) {
-        const uint32_t sbase = lds_base + stage * RING_STAGE;
-#pragma unroll
-        for (int i = 0; i < DPW; ++i)
-            dma16(src[i] + (int64_t)kt * BKB, __builtin_amdgcn_readfirstlane(sbase + dst[i]));
-    };
     int dsts[DPW];  // LDS targets, wave-uniform (scalar registers)
 #pragma unroll
     for (int i = 0; i < DPW; ++i)
@@ -381,7 +374,9 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     // running bases of the next DMA step (wave-uniform), advanced by one
     // k-block per step: scalar adds instead of per-step products
     const uint8_t *bcur[DPW];
-    auto stride6 = [&](int i) -> int64_t { return (int64_t)(i < 2 || i == 4 ? M : N) * 96; };
+    auto stride6 = [&](int i) -> int64_t {
+        return BITS == 6 ? (int64_t)(i < 2 || i == 4 ? M : N) * 96 : (int64_t)BKB;
+    };
 
     const int orow = lane & 15;
     const int ounit = ((lane >> 4) ^ ((orow >> 1) & 3)) << 4;
@@ -415,44 +410,25 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
         return;
     int m0, n0;
     tile_mn(t, m0, n0);
-    const uint8_t *src[DPW];
-    if constexpr (BITS != 6) {
-        sources(m0, n0, src);
-    } else {
 #pragma unroll
-        for (int i = 0; i < DPW; ++i)
-            vo[i] = voff6(i, m0, n0);
-    }
+    for (int i = 0; i < DPW; ++i)
+        vo[i] = voff6(i, m0, n0);
     if (fast_tile(m0, n0))
         scale_dma(m0, n0, 0);
     // ring position: global step g of this block lives in stage g % S
     int g = 0;
 #pragma unroll
-    for (int i = 0; i < S; ++i) {
-        if constexpr (BITS == 6)
-            issue6(m0, n0, min(i, KT - 1), i);
-        else
-            issue(src, min(i, KT - 1), i);
-    }
-    if constexpr (BITS == 6) {
+    for (int i = 0; i < S; ++i)
+        issue6(m0, n0, min(i, KT - 1), i);
 #pragma unroll
-        for (int i = 0; i < DPW; ++i)
-            bcur[i] = base6(i, m0, n0, S);
-    }
+    for (int i = 0; i < DPW; ++i)
+        bcur[i] = base6(i, m0, n0, S);
 
     for (int it = 0; t >= 0; ++it) {
         const int tn_ = tile_pos(it + 1);
         int m1 = 0, n1 = 0;
-        const uint8_t *nsrc[DPW];
-        if (tn_ >= 0) {
+        if (tn_ >= 0)
             tile_mn(tn_, m1, n1);
-            if constexpr (BITS != 6)
-                sources(m1, n1, nsrc);
-        } else if constexpr (BITS != 6) {
-#pragma unroll
-            for (int i = 0; i < DPW; ++i)
-                nsrc[i] = src[i];
-        }
 
         Acc acc[NI][8];
 #pragma unroll
@@ -644,17 +620,27 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
             __builtin_amdgcn_s_barrier();
             __asm__ volatile("" ::: "memory");
             // DMA of global step g+S: this tile's step kt+S, else the next
-            // tile's step kt+S-KT, else (no next tile) a harmless re-fetch.
-            // Selected without a branch, which would split the scheduling
-            // region of the loop body.
+            // tile's step kt+S-KT (its bases and lane offsets replace this
+            // tile's when the first of them is issued), else a harmless
+            // re-fetch (keeps the wait counts exact)
             {
-                const bool here = kt + S < KT;
-                const int sk = here ? kt + S : (tn_ >= 0 ? kt + S - KT : KT - 1);
                 const uint32_t sbase = lds_base + (g % S) * RING_STAGE;
+                if (kt + S < KT || tn_ >= 0) {
+                    if (kt + S == KT) {
 #pragma unroll
-                for (int i = 0; i < DPW; ++i)
-                    dma16((here ? src[i] : nsrc[i]) + (int64_t)sk * BKB,
-                          __builtin_amdgcn_readfirstlane(sbase + dst[i]));
+                        for (int i = 0; i < DPW; ++i) {
+                            vo[i] = voff6(i, m1, n1);
+                            bcur[i] = base6(i, m1, n1, 0);
+                        }
+                    }
+#pragma unroll
+                    for (int i = 0; i < DPW; ++i) {
+                        dma16s(vo[i], bcur[i], sbase + dsts[i]);
+                        bcur[i] += stride6(i);
+                    }
+                } else {
+                    issue6(m0, n0, KT - 1, g % S);
+                }
             }
             read_step(Rn, (g + 1) % S);
             substep(R, 1);
@@ -769,11 +755,6 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
         t = tn_;
         m0 = m1;
         n0 = n1;
-        if constexpr (BITS != 6) {
-#pragma unroll
-            for (int i = 0; i < DPW; ++i)
-                src[i] = nsrc[i];
-        }
     }
     __asm__ volatile("" ::: "memory");
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));  // no DMA may outlive the block's LDS
