@@ -382,13 +382,24 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_ring(GemmArgs 
         drow[i] = r;
         dunit[i] = (lane % C::UNITS) ^ ring_swz<C::ROWB>(r);
     }
-    auto sources = [&](int m0, int n0, const uint8_t *(&src)[C::DPW]) {
+    // SGPR-base form: a per-lane 32-bit offset inside the tile's rows (rows
+    // past the matrix edge clamped), fixed per tile, and a wave-uniform base
+    // advanced by one k-step per issue.  Whether DMA i moves X or W rows is
+    // uniform per wave (a chunk never straddles row BM).
+    bool dx[C::DPW];
+    int dsts[C::DPW];
 #pragma unroll
-        for (int i = 0; i < C::DPW; ++i) {
-            const int r = drow[i];
-            src[i] = r < BM ? a.xq + (int64_t)min(m0 + r, M - 1) * ldk + dunit[i] * 16
-                            : a.wq + (int64_t)min(n0 + r - BM, N - 1) * ldk + dunit[i] * 16;
-        }
+    for (int i = 0; i < C::DPW; ++i) {
+        dx[i] = __builtin_amdgcn_readfirstlane((wave + 8 * i) * C::RPC) < BM;
+        dsts[i] = __builtin_amdgcn_readfirstlane((wave + 8 * i) * 1024);
+    }
+    auto voffG = [&](int i, int m0, int n0) -> uint32_t {
+        const int r = dx[i] ? min(drow[i], M - 1 - m0) : min(drow[i] - BM, N - 1 - n0);
+        return (uint32_t)(r * (int)ldk + dunit[i] * 16);
+    };
+    auto baseG = [&](int i, int m0, int n0, int sk) -> const uint8_t * {
+        return (dx[i] ? a.xq + (int64_t)m0 * ldk : a.wq + (int64_t)n0 * ldk) +
+               (int64_t)sk * C::ROWB;
     };
     // scale DMA of wave w: slot w of the stage's scale area.  Slots 0..2GPS-1
     // hold sx of group g2 = w / 2 (128 rows each), slots 2GPS..3GPS-1 sw of
@@ -407,13 +418,13 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_ring(GemmArgs 
     };
 
     const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void *)lds;
-    auto issue = [&](const uint8_t *const (&src)[C::DPW], const uint16_t *ssrc, int kt,
-                     int stage) {
+    uint32_t vo[C::DPW];
+    const uint8_t *bcur[C::DPW];
+    auto issue = [&](const uint8_t *const (&base)[C::DPW], const uint16_t *ssrc, int stage) {
         const uint32_t sbase = lds_base + stage * C::STAGE;
 #pragma unroll
         for (int i = 0; i < C::DPW; ++i)
-            dma16(src[i] + (int64_t)kt * C::ROWB,
-                  __builtin_amdgcn_readfirstlane(sbase + (wave + 8 * i) * 1024));
+            dma16s(vo[i], base[i], sbase + dsts[i]);
         dma4(ssrc, __builtin_amdgcn_readfirstlane(sbase + C::OPB + wave * 256));
     };
 
@@ -440,13 +451,22 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_ring(GemmArgs 
         return;
     int m0, n0;
     tile_mn(t, m0, n0);
-    const uint8_t *src[C::DPW];
-    sources(m0, n0, src);
+#pragma unroll
+    for (int i = 0; i < C::DPW; ++i)
+        vo[i] = voffG(i, m0, n0);
     // global step g of this block lives in stage g % RS
     int g = 0;
 #pragma unroll
-    for (int i = 0; i < C::RS - 1; ++i)
-        issue(src, scale_src(m0, n0, min(i, KT - 1)), min(i, KT - 1), i);
+    for (int s = 0; s < C::RS - 1; ++s) {
+        const uint8_t *b0[C::DPW];
+#pragma unroll
+        for (int i = 0; i < C::DPW; ++i)
+            b0[i] = baseG(i, m0, n0, min(s, KT - 1));
+        issue(b0, scale_src(m0, n0, min(s, KT - 1)), s);
+    }
+#pragma unroll
+    for (int i = 0; i < C::DPW; ++i)
+        bcur[i] = baseG(i, m0, n0, C::RS - 1);
     __asm__ volatile("" ::: "memory");
     __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::RS - 2) * C::D, 15));
     __builtin_amdgcn_s_barrier();
@@ -455,15 +475,8 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_ring(GemmArgs 
     for (int it = 0; t >= 0; ++it) {
         const int tn_ = tile_pos(it + 1);
         int m1 = 0, n1 = 0;
-        const uint8_t *nsrc[C::DPW];
-        if (tn_ >= 0) {
+        if (tn_ >= 0)
             tile_mn(tn_, m1, n1);
-            sources(m1, n1, nsrc);
-        } else {
-#pragma unroll
-            for (int i = 0; i < C::DPW; ++i)
-                nsrc[i] = src[i];
-        }
 
         float yacc[4][4][4];
 #pragma unroll
@@ -483,12 +496,28 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_ring(GemmArgs 
                 const bool here = kt + C::RS - 1 < KT;
                 const bool cur = here || tn_ < 0;
                 const int sk = here ? kt + C::RS - 1 : (tn_ >= 0 ? kt + C::RS - 1 - KT : KT - 1);
-                const uint8_t *sel[C::DPW];
+                const int stage = (g + C::RS - 1) % C::RS;
+                if (here || tn_ >= 0) {
+                    // the next tile's bases and lane offsets replace this
+                    // tile's when the first of its DMAs is issued
+                    if (kt + C::RS - 1 == KT) {
 #pragma unroll
-                for (int i = 0; i < C::DPW; ++i)
-                    sel[i] = cur ? src[i] : nsrc[i];
-                issue(sel, scale_src(cur ? m0 : m1, cur ? n0 : n1, sk), sk,
-                      (g + C::RS - 1) % C::RS);
+                        for (int i = 0; i < C::DPW; ++i) {
+                            vo[i] = voffG(i, m1, n1);
+                            bcur[i] = baseG(i, m1, n1, 0);
+                        }
+                    }
+                    issue(bcur, scale_src(cur ? m0 : m1, cur ? n0 : n1, sk), stage);
+#pragma unroll
+                    for (int i = 0; i < C::DPW; ++i)
+                        bcur[i] += C::ROWB;
+                } else {
+                    const uint8_t *b0[C::DPW];
+#pragma unroll
+                    for (int i = 0; i < C::DPW; ++i)
+                        b0[i] = baseG(i, m0, n0, KT - 1);
+                    issue(b0, scale_src(m0, n0, KT - 1), stage);
+                }
             }
             const uint8_t *sb = lds + (g % C::RS) * C::STAGE;
             // operands of this step
@@ -645,9 +674,6 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_ring(GemmArgs 
         t = tn_;
         m0 = m1;
         n0 = n1;
-#pragma unroll
-        for (int i = 0; i < C::DPW; ++i)
-            src[i] = nsrc[i];
     }
     __asm__ volatile("" ::: "memory");
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));  // no DMA may outlive the block's LDS
