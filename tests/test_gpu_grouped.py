@@ -55,7 +55,7 @@ def rand_group_case(seed, M, N, K, group):
     # M, N multiples of 8 (the persistent ring kernel): ragged tiles, fewer
     # k-steps than ring stages (one tile per block), a single k-step
     (8, 8, 256, 256), (264, 136, 2048, 128), (1024, 1024, 256, 128), (520, 392, 128, 64),
-    (24, 8192, 65536, 128)])
+    (24, 8192, 65536, 128), (16, 264, 65536, 256), (8, 136, 65536, 64)])
 def test_gemm_grouped(dev, orc, M, N, K, group):
     import paper_2404_00456_amd as q
     say(f"grouped gemm M={M} N={N} K={K} group={group}")
