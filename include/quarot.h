@@ -41,6 +41,13 @@
  *    hipError_t is available from quarot_last_hip_error() on that thread.
  *    Faults inside a kernel surface at the caller's next synchronization.
  *  - Inputs must be finite; results for inf/nan inputs are unspecified.
+ *  - Failure injection (for tests of callers' error paths): while the
+ *    environment variable QUAROT_FAKE_HIP_ERROR holds the name of an entry
+ *    point (e.g. "quarot_linear"), that entry point validates its arguments
+ *    as usual and then returns QUAROT_ERR_HIP as if its first HIP runtime
+ *    call had failed with hipErrorLaunchFailure, before any device work;
+ *    quarot_last_hip_error() then returns that code.  The variable is read
+ *    on every call.
  */
 #ifndef QUAROT_H
 #define QUAROT_H
@@ -190,8 +197,9 @@ quarot_status quarot_w4a4_gemm_e3m2(const uint8_t *xq6, const quarot_f16 *sx,
  * the same codes and scales (§4 Stage 2b), for quarot_w4a4_gemm_e3m2.
  *   x fp16 [rows, n], q6 rows * n * 3/4 bytes, scale fp16 [rows]
  * n a multiple of 128 and, with rotate != 0, n = 2^k (k <= 15) or
- * n = 12 * 2^10, 12 * 2^11, 20 * 2^9, 20 * 2^10, 28 * 2^9, 28 * 2^10;
- * rows <= 2^30.  Other n: quarot_quant_int4 then quarot_pack_e3m2.
+ * n = 12 * 2^10, 12 * 2^11, 20 * 2^9, 20 * 2^10, 28 * 2^9, 28 * 2^10,
+ * 108 * 2^k (5 <= k <= 7), 172 * 2^k (k = 5, 6); rows <= 2^30.  Other n:
+ * quarot_quant_int4 then quarot_pack_e3m2.
  */
 quarot_status quarot_quant_int4_e3m2(const quarot_f16 *x, uint8_t *q6, quarot_f16 *scale,
                                      int64_t rows, int64_t n, int rotate, float clip_ratio,
@@ -273,21 +281,22 @@ quarot_status quarot_linear_w8a8(const quarot_f16 *x, const int8_t *wq, const qu
 
 /*
  * Offline weight quantization with a per-row (per output channel) clip
- * search (§5 Setup: round-to-nearest weights with "the clipping ratio
- * extracted by a linear search over the squared error"; App. A.2).  For
+ * search (§5 Setup: per-channel round-to-nearest weights whose clipping
+ * ratio is picked by a linear search on the squared error; App. A.2).  For
  * each row y (w rotated like an activation row when rotate != 0) and each
  * candidate c_j = RN32((100 - j) / 100), j < n_candidates: the symmetric
  * quantizer of quarot_quant_int4 (bits = 4) or quarot_quant_int8 (6, 8)
- * with clip c_j, and E_j = sum_i (y_i - q_i * s)^2 (fp64, each difference
- * exact).  The row keeps the first j with the smallest E_j; the codes and
- * scale are exactly those of the plain quantizer with clip c_best.
+ * with clip c_j, the terms e_i = RN64((y_i - q_i * s)^2) (the difference
+ * exact in binary64), and E_j = their sum in this fixed binary64 order:
+ * 256 interleaved partial sums P_t = e_t + e_{t+256} + ... (from +0, in
+ * increasing i), then P_t += P_{t+h} for h = 128, 64, ..., 1; E_j = P_0.
+ * The row keeps the first j with the smallest E_j; the codes and scale are
+ * exactly those of the plain quantizer with clip c_best.
  *   w fp16 [rows, n]; q: uint8 [rows, n/2] (bits 4) or int8 [rows, n];
  *   scale fp16 [rows]; clip_out float32 [rows] (c_best);
  *   workspace: quarot_quant_search_workspace_size(rows, n, rotate) bytes
  *   (binary32 rotated rows; 0 without rotation), 16-byte aligned.
- * 1 <= n_candidates <= 100.  Sums in a different order than a sequential
- * loop, so a choice between two candidates whose errors agree to ~1e-15
- * relative could differ from a CPU reference.
+ * 1 <= n_candidates <= 100.
  */
 size_t quarot_quant_search_workspace_size(int64_t rows, int64_t n, int rotate);
 quarot_status quarot_quant_search(const quarot_f16 *w, void *q, quarot_f16 *scale,

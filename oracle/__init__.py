@@ -44,6 +44,7 @@ _F = ctypes.c_float
 _SIGS = {
     "orc_f16_to_f32_array": (None, [_P, _P, _I64]),
     "orc_f32_to_f16_array": (None, [_P, _P, _I64]),
+    "orc_f64_to_f16_array": (None, [_P, _P, _I64]),
     "orc_sylvester_entry": (_I, [_I64, _I64]),
     "orc_hm_table": (_I, [_I, _P]),
     "orc_hadamard_factor": (_I, [_I64, _P, _P]),
@@ -128,6 +129,14 @@ def f32_to_f16(f: np.ndarray) -> np.ndarray:
     f = np.ascontiguousarray(np.asarray(f, dtype=np.float32))
     out = np.empty(f.shape, np.uint16)
     lib().orc_f32_to_f16_array(_ptr(f), _ptr(out), f.size)
+    return out.view(np.float16)
+
+
+def f64_to_f16(d: np.ndarray) -> np.ndarray:
+    """binary64 -> binary16 rounded once (nearest even)."""
+    d = np.ascontiguousarray(np.asarray(d, dtype=np.float64))
+    out = np.empty(d.shape, np.uint16)
+    lib().orc_f64_to_f16_array(_ptr(d), _ptr(out), d.size)
     return out.view(np.float16)
 
 

@@ -52,8 +52,9 @@
  *    qmax = 2^(bits-1) - 1 in place of 7, codes clamped to [-qmax-1, qmax],
  *    one signed byte each; int8 x int8 -> int32, dequant as above.
  *  - Weight clip search (§5 Setup, App. A.2): candidates
- *    c_j = RN32((100 - j) / 100), the error sum_i (y_i - q_i s16)^2 in fp64
- *    with each difference exact, the first j of least error.
+ *    c_j = RN32((100 - j) / 100), the error sum_i RN64((y_i - q_i s16)^2)
+ *    with each difference exact, summed in a fixed order (256 interleaved
+ *    partial sums, then a halving tree), the first j of least error.
  *  - Group-wise (§5.3 group-size ablation): each group of G channels of a
  *    (rotated) row quantized like a whole row, scales group-major [n/G, rows];
  *    the product sums t_g = RN(RN(f32(acc_g) sx_g) sw_g) over g in increasing
@@ -136,6 +137,50 @@ uint16_t orc_f32_to_f16(float f)
     if (rem > 0x1000u || (rem == 0x1000u && (r & 1u)))
         r++; /* a carry may reach the exponent, up to 0x7C00 = inf */
     return (uint16_t)(sign | r);
+}
+
+/* binary64 -> binary16, round to nearest even, straight from the binary64
+ * encoding (one rounding; going through binary32 first could round twice). */
+uint16_t orc_f64_to_f16(double d)
+{
+    uint64_t u;
+    memcpy(&u, &d, 8);
+    uint16_t sign = (uint16_t)((u >> 48) & 0x8000u);
+    int exp11 = (int)((u >> 52) & 0x7FFu);
+    uint64_t man = u & 0xFFFFFFFFFFFFFull;
+    if (exp11 == 0x7FF) /* inf or nan */
+        return (uint16_t)(sign | 0x7C00u | (man ? 0x200u : 0u));
+    int e = exp11 - 1023 + 15; /* binary16 biased exponent */
+    if (e >= 31)
+        return (uint16_t)(sign | 0x7C00u);
+    /* significand with the implicit bit: 53 bits (binary64 subnormals are
+     * far below the binary16 range and go to zero with the e < -10 rule) */
+    uint64_t mant = man | (exp11 ? (1ull << 52) : 0ull);
+    int shift; /* bits dropped to reach the binary16 significand */
+    uint32_t base;
+    if (e <= 0) {
+        if (e < -10)
+            return sign;
+        shift = 42 + (1 - e); /* subnormal: units of 2^-24 */
+        base = 0;
+    } else {
+        shift = 42;
+        base = (uint32_t)e << 10;
+        mant &= (1ull << 52) - 1ull; /* the exponent field carries the implicit bit */
+    }
+    uint64_t kept = mant >> shift;
+    uint64_t rem = mant & ((1ull << shift) - 1ull);
+    uint64_t half = 1ull << (shift - 1);
+    uint32_t r = base + (uint32_t)kept;
+    if (rem > half || (rem == half && (r & 1u)))
+        r++; /* a carry may reach the exponent, up to 0x7C00 = inf */
+    return (uint16_t)(sign | r);
+}
+
+void orc_f64_to_f16_array(const double *d, uint16_t *h, int64_t n)
+{
+    for (int64_t i = 0; i < n; i++)
+        h[i] = orc_f64_to_f16(d[i]);
 }
 
 void orc_f16_to_f32_array(const uint16_t *h, float *f, int64_t n)
@@ -768,15 +813,33 @@ int orc_quant_int8(const uint16_t *x, int8_t *q, uint16_t *s, int64_t rows, int6
     return err ? ORC_ERR_NOMEM : ORC_OK;
 }
 
-/* Weight quantization with a per-row clipping search (§5 Setup: RTN
- * per-column symmetric quantization "where we extract the clipping ratio
- * using a linear search over the squared error"; App. A.2).  For each row
- * (output channel) y (rotated if asked), candidates c_j = RN32((100 - j) /
- * 100), j < ncand; for each the scale and codes of the symmetric quantizer
- * with that clip, and the error E_j = sum_i (y_i - q_i s16)^2, each term's
- * difference exact in fp64 and the sum taken left to right in fp64.  The
- * row keeps the first j with the smallest E_j.  bits = 4 packs nibbles,
- * 6 or 8 stores one code per byte.  clip_out[r] = c_best. */
+/* Sum of e[0..n) in the fixed binary64 order that defines the clip
+ * search's error (the paper gives no order, and binary64 addition is not
+ * associative): 256 interleaved partial sums P_t = e_t + e_{t+256} + ...,
+ * each from +0 in increasing index, then halved pairwise,
+ * P_t <- P_t + P_{t+h} for h = 128, 64, ..., 1; the result is P_0. */
+static double search_err_sum(const double *e, int64_t n)
+{
+    double P[256];
+    for (int t = 0; t < 256; t++)
+        P[t] = 0.0;
+    for (int64_t i = 0; i < n; i++)
+        P[i % 256] = P[i % 256] + e[i];
+    for (int h = 128; h >= 1; h /= 2)
+        for (int t = 0; t < h; t++)
+            P[t] = P[t] + P[t + h];
+    return P[0];
+}
+
+/* Weight quantization with a per-row clipping search (§5 Setup: per-channel
+ * round-to-nearest weights whose clipping ratio is picked by a linear search
+ * on the squared error; App. A.2).  For each row (output channel) y
+ * (rotated if asked), candidates c_j = RN32((100 - j) / 100), j < ncand; for
+ * each the scale and codes of the symmetric quantizer with that clip, the
+ * terms e_i = RN64(d_i^2) with d_i = y_i - q_i s16 (exact in binary64), and
+ * E_j = search_err_sum(e).  The row keeps the first j with the smallest E_j.
+ * bits = 4 packs nibbles, 6 or 8 stores one code per byte.
+ * clip_out[r] = c_best. */
 int orc_quant_search(const uint16_t *x, void *q, uint16_t *s, float *clip_out, int64_t rows,
                      int64_t n, int rotate, int bits, int ncand)
 {
@@ -794,7 +857,10 @@ int orc_quant_search(const uint16_t *x, void *q, uint16_t *s, float *clip_out, i
 #pragma omp parallel for schedule(static) reduction(| : err)
     for (int64_t r = 0; r < rows; r++) {
         float *t = (float *)malloc((size_t)n * 3 * sizeof(float));
-        if (!t) {
+        double *et = (double *)malloc((size_t)n * sizeof(double));
+        if (!t || !et) {
+            free(t);
+            free(et);
             err |= 1;
             continue;
         }
@@ -815,7 +881,6 @@ int orc_quant_search(const uint16_t *x, void *q, uint16_t *s, float *clip_out, i
             const float c = (float)((double)(100 - j) / 100.0);
             const uint16_t s16 = orc_f32_to_f16((amax * c) / (float)qmax);
             const float sf = orc_f16_to_f32(s16);
-            double e = 0.0;
             for (int64_t i = 0; i < n; i++) {
                 int v = 0;
                 if (sf != 0.0f) {
@@ -827,8 +892,9 @@ int orc_quant_search(const uint16_t *x, void *q, uint16_t *s, float *clip_out, i
                     v = (int)rr;
                 }
                 const double d = (double)y[i] - (double)v * (double)sf;
-                e += d * d;
+                et[i] = d * d;
             }
+            const double e = search_err_sum(et, n);
             if (e < best_e) {
                 best_e = e;
                 best_c = c;
@@ -840,6 +906,7 @@ int orc_quant_search(const uint16_t *x, void *q, uint16_t *s, float *clip_out, i
         else
             quant_sym8_row(y, n, best_c, qmax, (int8_t *)q + r * n, s + r);
         free(t);
+        free(et);
     }
     free(pl.Hm);
     return err ? ORC_ERR_NOMEM : ORC_OK;
@@ -1213,7 +1280,7 @@ int orc_kv_attention(const uint16_t *q, const uint8_t *kc, const uint16_t *ks,
             }
         }
         for (int64_t d = 0; d < D; d++)
-            out[i * D + d] = orc_f32_to_f16((float)o[d]);
+            out[i * D + d] = orc_f64_to_f16(o[d]);
         free(sc);
         free(o);
     }

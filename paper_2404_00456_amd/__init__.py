@@ -142,6 +142,30 @@ def _rows(t: torch.Tensor, n: int) -> int:
     return t.numel() // n if n else 0
 
 
+# Shape checks against the sizes a call is given: the library trusts its
+# pointers, so a tensor smaller than the sizes say would be read or written
+# past its end.  They raise before anything is launched.
+
+def _shape(t: Optional[torch.Tensor], shape, name: str):
+    if t is not None and tuple(t.shape) != tuple(int(d) for d in shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _numel(t: Optional[torch.Tensor], n: int, name: str):
+    if t is not None and t.numel() != n:
+        raise ValueError(f"{name} must hold {n} elements, got {t.numel()}")
+
+
+def _ndim(t: torch.Tensor, d: int, name: str):
+    if t.dim() != d:
+        raise ValueError(f"{name} must be {d}-D, got shape {tuple(t.shape)}")
+
+
+def _group(group: int, D: int, name: str = "group"):
+    if group <= 0 or D % group:
+        raise ValueError(f"{name} must be a positive divisor of {D}, got {group}")
+
+
 # -- host-side queries ------------------------------------------------------
 
 def quarot_version() -> int:
@@ -203,6 +227,7 @@ def quarot_hadamard(x: torch.Tensor, y: Optional[torch.Tensor] = None,
                     stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """y = RN16(x . H_n / sqrt(n)) row by row; x fp16 [..., n]."""
     n = x.shape[-1]
+    _shape(y, x.shape, "y")
     if y is None:
         y = torch.empty_like(x)
     _check("quarot_hadamard", lib().quarot_hadamard(
@@ -218,6 +243,8 @@ def quarot_quant_int4(x: torch.Tensor, rotate: bool = True, clip_ratio: float = 
     Returns (codes uint8 [..., n/2], scale fp16 [...])."""
     n = x.shape[-1]
     rows = _rows(x, n)
+    _numel(q, rows * (n // 2), "q")
+    _numel(scale, rows, "scale")
     if q is None:
         q = torch.empty(x.shape[:-1] + (n // 2,), dtype=torch.uint8, device=x.device)
     if scale is None:
@@ -233,8 +260,15 @@ def quarot_w4a4_gemm(xq: torch.Tensor, sx: torch.Tensor, wq: torch.Tensor, sw: t
                      y: Optional[torch.Tensor] = None, acc_out: Optional[torch.Tensor] = None,
                      want_acc: bool = False, stream: Optional[torch.cuda.Stream] = None):
     """y = dequant(Xq Wq^T); returns y, or (y, acc) with want_acc."""
+    _ndim(xq, 2, "xq")
+    _ndim(wq, 2, "wq")
     M, Kh = xq.shape
     N = wq.shape[0]
+    _shape(wq, (N, Kh), "wq")
+    _numel(sx, M, "sx")
+    _numel(sw, N, "sw")
+    _shape(y, (M, N), "y")
+    _shape(acc_out, (M, N), "acc_out")
     if y is None:
         y = torch.empty((M, N), dtype=torch.float16, device=xq.device)
     if want_acc and acc_out is None:
@@ -250,8 +284,10 @@ def quarot_pack_e3m2(q4: torch.Tensor, out: Optional[torch.Tensor] = None,
                      stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """int4 codes [rows, k/2] -> the tiled e3m2 operand layout, as uint8
     [k/128, rows*96] (one row per 128-wide k block)."""
+    _ndim(q4, 2, "q4")
     rows, kh = q4.shape
     k = 2 * kh
+    _numel(out, rows * k * 3 // 4, "out")
     if out is None:
         out = torch.empty((k // 128 if k % 128 == 0 else 0, rows * 96), dtype=torch.uint8,
                           device=q4.device)
@@ -268,8 +304,11 @@ def quarot_w4a4_gemm_e3m2(xq6: torch.Tensor, sx: torch.Tensor, wq6: torch.Tensor
     (xq6 [K/128, M*96], wq6 [K/128, N*96])."""
     M, N = sx.shape[0], sw.shape[0]
     K = 128 * xq6.shape[0]
-    if xq6.shape[1] != M * 96 or wq6.shape != (xq6.shape[0], N * 96):
+    _ndim(xq6, 2, "xq6")
+    if xq6.shape[1] != M * 96 or tuple(wq6.shape) != (xq6.shape[0], N * 96):
         raise ValueError("quarot_w4a4_gemm_e3m2: operand shapes do not match sx, sw")
+    _shape(y, (M, N), "y")
+    _shape(acc_out, (M, N), "acc_out")
     if y is None:
         y = torch.empty((M, N), dtype=torch.float16, device=xq6.device)
     if want_acc and acc_out is None:
@@ -287,7 +326,10 @@ def quarot_quant_int4_e3m2(x: torch.Tensor, rotate: bool = True, clip_ratio: flo
                            stream: Optional[torch.cuda.Stream] = None):
     """quarot_quant_int4 with the codes in the tiled e3m2 layout
     ([n/128, rows*96] uint8); returns (q6, scale)."""
+    _ndim(x, 2, "x")
     rows, n = x.shape
+    _numel(q6, rows * n * 3 // 4, "q6")
+    _numel(scale, rows, "scale")
     if q6 is None:
         q6 = torch.empty((n // 128 if n % 128 == 0 else 0, rows * 96), dtype=torch.uint8,
                          device=x.device)
@@ -311,8 +353,11 @@ def quarot_linear_e3m2(x: torch.Tensor, wq6: torch.Tensor, sw: torch.Tensor,
                        stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """The 4-bit linear layer on the e3m2 path (weights from
     prepare_weight_e3m2); y equals quarot_linear's bit for bit."""
+    _ndim(x, 2, "x")
     M, K = x.shape
-    N = sw.shape[0]
+    N = sw.numel()
+    _numel(wq6, N * K * 3 // 4, "wq6")
+    _shape(y, (M, N), "y")
     need = quarot_linear_e3m2_workspace_size(M, K)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
@@ -328,6 +373,8 @@ def quarot_linear_e3m2(x: torch.Tensor, wq6: torch.Tensor, sw: torch.Tensor,
 def quarot_swiglu_quant_e3m2(gate: torch.Tensor, up: torch.Tensor, clip_ratio: float = 1.0,
                              stream: Optional[torch.cuda.Stream] = None):
     """quarot_swiglu_quant_int4 with the codes in the tiled e3m2 layout."""
+    _ndim(gate, 2, "gate")
+    _shape(up, gate.shape, "up")
     rows, n = gate.shape
     q6 = torch.empty((n // 128 if n % 128 == 0 else 0, rows * 96), dtype=torch.uint8,
                      device=gate.device)
@@ -351,8 +398,13 @@ def quarot_linear(x: torch.Tensor, wq: torch.Tensor, sw: torch.Tensor, rotate: b
                   workspace: Optional[torch.Tensor] = None,
                   stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """The 4-bit linear layer: rotate+quantize x, W4A4 GEMM, dequant."""
+    _ndim(x, 2, "x")
+    _ndim(wq, 2, "wq")
     M, K = x.shape
     N = wq.shape[0]
+    _shape(wq, (N, K // 2), "wq")
+    _numel(sw, N, "sw")
+    _shape(y, (M, N), "y")
     need = quarot_linear_workspace_size(M, K)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
@@ -380,6 +432,8 @@ def quarot_quant_int8(x: torch.Tensor, rotate: bool = True, clip_ratio: float = 
     Returns (codes int8 [..., n], scale fp16 [...])."""
     n = x.shape[-1]
     rows = _rows(x, n)
+    _numel(q, rows * n, "q")
+    _numel(scale, rows, "scale")
     if q is None:
         q = torch.empty(x.shape, dtype=torch.int8, device=x.device)
     if scale is None:
@@ -395,8 +449,15 @@ def quarot_w8a8_gemm(xq: torch.Tensor, sx: torch.Tensor, wq: torch.Tensor, sw: t
                      y: Optional[torch.Tensor] = None, acc_out: Optional[torch.Tensor] = None,
                      want_acc: bool = False, stream: Optional[torch.cuda.Stream] = None):
     """y = dequant(Xq Wq^T) over int8 codes; returns y, or (y, acc)."""
+    _ndim(xq, 2, "xq")
+    _ndim(wq, 2, "wq")
     M, K = xq.shape
     N = wq.shape[0]
+    _shape(wq, (N, K), "wq")
+    _numel(sx, M, "sx")
+    _numel(sw, N, "sw")
+    _shape(y, (M, N), "y")
+    _shape(acc_out, (M, N), "acc_out")
     if y is None:
         y = torch.empty((M, N), dtype=torch.float16, device=xq.device)
     if want_acc and acc_out is None:
@@ -413,8 +474,13 @@ def quarot_linear_w8a8(x: torch.Tensor, wq: torch.Tensor, sw: torch.Tensor, rota
                        y: Optional[torch.Tensor] = None,
                        workspace: Optional[torch.Tensor] = None,
                        stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    _ndim(x, 2, "x")
+    _ndim(wq, 2, "wq")
     M, K = x.shape
     N = wq.shape[0]
+    _shape(wq, (N, K), "wq")
+    _numel(sw, N, "sw")
+    _shape(y, (M, N), "y")
     need = int(lib().quarot_linear_w8a8_workspace_size(M, K))
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
@@ -432,6 +498,7 @@ def quarot_quant_search(w: torch.Tensor, rotate: bool = True, bits: int = 4,
     """Offline weight quantization with a per-row clip search.
     Returns (codes, scale fp16 [rows], chosen clip float32 [rows]); codes are
     packed nibbles uint8 [rows, n/2] for bits = 4, int8 [rows, n] otherwise."""
+    _ndim(w, 2, "w")
     rows, n = w.shape
     dev = w.device
     if bits == 4:
@@ -457,8 +524,12 @@ def quarot_quant_int4_grouped(x: torch.Tensor, group: int = 128, rotate: bool = 
                               stream: Optional[torch.cuda.Stream] = None):
     """Group-wise symmetric int4 of x [rows, n] (optionally rotated first).
     Returns (codes uint8 [rows, n/2], scale fp16 [n/group, rows])."""
+    _ndim(x, 2, "x")
     rows, n = x.shape
     dev = x.device
+    _group(group, n)
+    _shape(q, (rows, n // 2), "q")
+    _shape(scale, (n // group, rows), "scale")
     if q is None:
         q = torch.empty((rows, n // 2), dtype=torch.uint8, device=dev)
     if scale is None:
@@ -480,8 +551,15 @@ def quarot_w4a4_gemm_grouped(xq: torch.Tensor, sx: torch.Tensor, wq: torch.Tenso
                              y: Optional[torch.Tensor] = None,
                              stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """Group-wise W4A4 product; sx [K/group, M], sw [K/group, N] group-major."""
+    _ndim(xq, 2, "xq")
+    _ndim(wq, 2, "wq")
     M, Kh = xq.shape
     N = wq.shape[0]
+    _group(group, 2 * Kh)
+    _shape(wq, (N, Kh), "wq")
+    _shape(sx, (2 * Kh // group, M), "sx")
+    _shape(sw, (2 * Kh // group, N), "sw")
+    _shape(y, (M, N), "y")
     if y is None:
         y = torch.empty((M, N), dtype=torch.float16, device=xq.device)
     _check("quarot_w4a4_gemm_grouped", lib().quarot_w4a4_gemm_grouped(
@@ -497,8 +575,14 @@ def quarot_linear_w4a4_grouped(x: torch.Tensor, wq: torch.Tensor, sw: torch.Tens
                                workspace: Optional[torch.Tensor] = None,
                                stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """The group-wise 4-bit linear layer (quantize x per group, grouped GEMM)."""
+    _ndim(x, 2, "x")
+    _ndim(wq, 2, "wq")
     M, K = x.shape
     N = wq.shape[0]
+    _group(group, K)
+    _shape(wq, (N, K // 2), "wq")
+    _shape(sw, (K // group, N), "sw")
+    _shape(y, (M, N), "y")
     need = int(lib().quarot_linear_w4a4_grouped_workspace_size(M, K, int(group),
                                                                int(bool(rotate))))
     if workspace is None:
@@ -517,6 +601,7 @@ def quarot_swiglu(gate: torch.Tensor, up: torch.Tensor, h: Optional[torch.Tensor
     """h = RN16(silu(gate) * up) elementwise (binary32 silu recipe)."""
     if tuple(up.shape) != tuple(gate.shape):
         raise ValueError("gate and up must have the same shape")
+    _shape(h, gate.shape, "h")
     if h is None:
         h = torch.empty_like(gate)
     _check("quarot_swiglu", lib().quarot_swiglu(
@@ -535,6 +620,8 @@ def quarot_swiglu_quant_int4(gate: torch.Tensor, up: torch.Tensor, clip_ratio: f
     if tuple(up.shape) != tuple(gate.shape):
         raise ValueError("gate and up must have the same shape")
     rows = _rows(gate, n)
+    _numel(q, rows * (n // 2), "q")
+    _numel(scale, rows, "scale")
     if q is None:
         q = torch.empty(gate.shape[:-1] + (n // 2,), dtype=torch.uint8, device=gate.device)
     if scale is None:
@@ -550,6 +637,8 @@ def quarot_hadamard_heads(z: torch.Tensor, n_heads: int, y: Optional[torch.Tenso
                           stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """y = RN16(z (H_nh (x) I_dh) / sqrt(nh)); z fp16 [..., n_heads * head_dim]."""
     n = z.shape[-1]
+    _group(n_heads, n, "n_heads")
+    _shape(y, z.shape, "y")
     if y is None:
         y = torch.empty_like(z)
     _check("quarot_hadamard_heads", lib().quarot_hadamard_heads(
@@ -565,6 +654,9 @@ def quarot_hadamard_heads_quant_int4(z: torch.Tensor, n_heads: int, clip_ratio: 
     """out_proj input: per-token int4 codes of the head-wise rotation."""
     n = z.shape[-1]
     rows = _rows(z, n)
+    _group(n_heads, n, "n_heads")
+    _numel(q, rows * (n // 2), "q")
+    _numel(scale, rows, "scale")
     if q is None:
         q = torch.empty(z.shape[:-1] + (n // 2,), dtype=torch.uint8, device=z.device)
     if scale is None:
@@ -585,6 +677,10 @@ def quarot_kv_quant(kv: torch.Tensor, group: int = 128, rotate: bool = True,
     D = kv.shape[-1]
     rows = _rows(kv, D)
     lead = kv.shape[:-1]
+    _group(group, D)
+    _numel(q, rows * (D // 2), "q")
+    _numel(scale, rows * (D // group), "scale")
+    _numel(zero, rows * (D // group), "zero")
     if q is None:
         q = torch.empty(lead + (D // 2,), dtype=torch.uint8, device=kv.device)
     if scale is None:
@@ -604,6 +700,10 @@ def quarot_kv_dequant(q: torch.Tensor, scale: torch.Tensor, zero: torch.Tensor,
                       stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     D = 2 * q.shape[-1]
     rows = _rows(q, D // 2)
+    _group(group, D)
+    _numel(scale, rows * (D // group), "scale")
+    _numel(zero, rows * (D // group), "zero")
+    _numel(out, rows * D, "out")
     if out is None:
         out = torch.empty(q.shape[:-1] + (D,), dtype=torch.float16, device=q.device)
     _check("quarot_kv_dequant", lib().quarot_kv_dequant(
@@ -620,7 +720,15 @@ def quarot_kv_append(kv_new: torch.Tensor, q_cache: torch.Tensor, scale_cache: t
     q_cache [rows, s_max, D/2], scale/zero_cache [rows, s_max, D/group]."""
     D = kv_new.shape[-1]
     rows = _rows(kv_new, D)
+    _group(group, D)
+    if q_cache.dim() < 2:
+        raise ValueError("q_cache must be [rows, s_max, head_dim/2]")
     s_max = q_cache.shape[-2]
+    _numel(q_cache, rows * s_max * (D // 2), "q_cache")
+    if q_cache.shape[-1] != D // 2:
+        raise ValueError(f"q_cache rows must hold {D // 2} bytes, got {q_cache.shape[-1]}")
+    _numel(scale_cache, rows * s_max * (D // group), "scale_cache")
+    _numel(zero_cache, rows * s_max * (D // group), "zero_cache")
     _check("quarot_kv_append", lib().quarot_kv_append(
         _ptr(kv_new, torch.float16, "kv_new"), _ptr(q_cache, torch.uint8, "q_cache"),
         _ptr(scale_cache, torch.float16, "scale_cache"),
@@ -640,10 +748,18 @@ def quarot_kv_decode_attention(q: torch.Tensor, k_cache, v_cache, seq_len: int,
     """Decode attention of rotated queries q [nq, D] over 4-bit caches
     k_cache = (codes [nkv, s_max, D/2], scale, zero [nkv, s_max, D/group]),
     v_cache alike.  Returns fp16 [nq, D]."""
+    _ndim(q, 2, "q")
     nq, D = q.shape
     kc, ks, kz = k_cache
     vc, vs, vz = v_cache
+    _ndim(kc, 3, "k_codes")
     nkv, s_max = kc.shape[0], kc.shape[1]
+    _group(group, D)
+    for t, nm in ((kc, "k_codes"), (vc, "v_codes")):
+        _shape(t, (nkv, s_max, D // 2), nm)
+    for t, nm in ((ks, "k_scale"), (kz, "k_zero"), (vs, "v_scale"), (vz, "v_zero")):
+        _shape(t, (nkv, s_max, D // group), nm)
+    _shape(out, (nq, D), "out")
     if sm_scale is None:
         sm_scale = D ** -0.5
     if out is None:

@@ -4,6 +4,7 @@
 #include "../../include/quarot.h"
 
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 
 #include "common.hpp"
@@ -61,10 +62,26 @@ quarot_status hip_fail(hipError_t e)
     return QUAROT_ERR_HIP;
 }
 
-// The device of the calling thread must be a gfx950.  Cached per thread
-// and device (a host-side query, no device work).
-quarot_status check_device()
+// Failure injection for tests of the error path: when the environment
+// variable QUAROT_FAKE_HIP_ERROR holds the name of an entry point, that
+// entry point behaves as if its first HIP runtime call had failed with
+// hipErrorLaunchFailure.  It validates its arguments as usual, then returns
+// QUAROT_ERR_HIP before any device work (every output untouched), and
+// quarot_last_hip_error() reports the code.  Read on every call, so a
+// process can set and clear it.
+bool fake_hip_error(const char *call)
 {
+    const char *v = std::getenv("QUAROT_FAKE_HIP_ERROR");
+    return v && call && std::strcmp(v, call) == 0;
+}
+
+// The device of the calling thread must be a gfx950.  Cached per thread
+// and device (a host-side query, no device work).  `call` names the entry
+// point (for the failure injection above).
+quarot_status check_device(const char *call)
+{
+    if (fake_hip_error(call))
+        return hip_fail(hipErrorLaunchFailure);
     int dev = -1;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) {
@@ -164,7 +181,7 @@ quarot_status quarot_device_peaks(int *cu_count, int *max_clock_khz)
 {
     if (!cu_count || !max_clock_khz)
         return QUAROT_ERR_INVALID_ARG;
-    quarot_status st = check_device();
+    quarot_status st = check_device(__func__);
     if (st)
         return st;
     int dev = 0, cus = 0, clk = 0;
@@ -188,7 +205,7 @@ quarot_status quarot_mfma_probe(int32_t *out, int64_t blocks, int iters, void *s
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(out))
         return QUAROT_ERR_ALIGNMENT;
-    quarot_status st = check_device();
+    quarot_status st = check_device(__func__);
     if (st)
         return st;
     hipError_t e = launch_mfma_probe(out, (int)blocks, iters, (hipStream_t)stream);
@@ -203,7 +220,7 @@ quarot_status quarot_mfma_probe_fp6(int32_t *out, int64_t blocks, int iters, voi
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(out))
         return QUAROT_ERR_ALIGNMENT;
-    quarot_status st = check_device();
+    quarot_status st = check_device(__func__);
     if (st)
         return st;
     hipError_t e = launch_mfma_probe_fp6(out, (int)blocks, iters, (hipStream_t)stream);
@@ -250,7 +267,7 @@ quarot_status quarot_hadamard(const quarot_f16 *x, quarot_f16 *y, int64_t rows, 
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(x) || !aligned16(y))
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     RotArgs a{};
     a.x = x;
@@ -279,7 +296,7 @@ quarot_status quarot_quant_int4(const quarot_f16 *x, uint8_t *q, quarot_f16 *sca
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(x) || !aligned16(q) || !aligned16(scale))
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     RotArgs a{};
     a.x = x;
@@ -300,7 +317,7 @@ quarot_status quarot_w4a4_gemm(const uint8_t *xq, const quarot_f16 *sx, const ui
     quarot_status st = check_gemm(xq, sx, wq, sw, y, acc_out, M, N, K);
     if (st || M == 0 || N == 0)
         return st;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     GemmArgs a{xq, sx, wq, sw, y, acc_out, (int)M, (int)N, (int)K};
     hipError_t e = launch_gemm(a, (hipStream_t)stream);
@@ -320,7 +337,7 @@ quarot_status quarot_pack_e3m2(const uint8_t *q4, uint8_t *q6, int64_t rows, int
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(q4) || !aligned16(q6))
         return QUAROT_ERR_ALIGNMENT;
-    quarot_status st = check_device();
+    quarot_status st = check_device(__func__);
     if (st)
         return st;
     hipError_t e = launch_pack_e3m2(q4, q6, rows, (int)k, (hipStream_t)stream);
@@ -339,7 +356,7 @@ quarot_status quarot_w4a4_gemm_e3m2(const uint8_t *xq6, const quarot_f16 *sx,
         return QUAROT_ERR_UNSUPPORTED_SIZE;
     if (M == 0 || N == 0)
         return QUAROT_OK;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     GemmArgs a{xq6, sx, wq6, sw, y, acc_out, (int)M, (int)N, (int)K};
     hipError_t e = launch_gemm(a, (hipStream_t)stream, 6);
@@ -377,7 +394,7 @@ quarot_status quarot_linear(const quarot_f16 *x, const uint8_t *wq, const quarot
         return QUAROT_ERR_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     uint8_t *xq = static_cast<uint8_t *>(workspace);
     quarot_f16 *sx = reinterpret_cast<quarot_f16 *>(xq + codes_bytes(M, K));
@@ -415,7 +432,7 @@ quarot_status quarot_quant_int4_e3m2(const quarot_f16 *x, uint8_t *q6, quarot_f1
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(x) || !aligned16(q6) || !aligned16(scale))
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     RotArgs a{};
     a.x = x;
@@ -461,7 +478,7 @@ quarot_status quarot_linear_e3m2(const quarot_f16 *x, const uint8_t *wq6, const 
         return QUAROT_ERR_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     uint8_t *xq6 = static_cast<uint8_t *>(workspace);
     const size_t codes = ((size_t)M * (size_t)(K / 4 * 3) + 255) & ~(size_t)255;
@@ -497,7 +514,7 @@ quarot_status quarot_quant_int8(const quarot_f16 *x, int8_t *q, quarot_f16 *scal
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(x) || !aligned16(q) || !aligned16(scale))
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     RotArgs a{};
     a.x = x;
@@ -521,7 +538,7 @@ quarot_status quarot_w8a8_gemm(const int8_t *xq, const quarot_f16 *sx, const int
     quarot_status st = check_gemm(xb, sx, wb, sw, y, acc_out, M, N, K);
     if (st || M == 0 || N == 0)
         return st;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     GemmArgs a{xb, sx, wb, sw, y, acc_out, (int)M, (int)N, (int)K};
     hipError_t e = launch_gemm(a, (hipStream_t)stream, 8);
@@ -560,7 +577,7 @@ quarot_status quarot_linear_w8a8(const quarot_f16 *x, const int8_t *wq, const qu
         return QUAROT_ERR_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     uint8_t *xq = static_cast<uint8_t *>(workspace);
     quarot_f16 *sx =
@@ -613,7 +630,7 @@ quarot_status quarot_quant_search(const quarot_f16 *w, void *q, quarot_f16 *scal
         return QUAROT_ERR_WORKSPACE;
     if (need && !aligned16(workspace))
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     if (rotate) {
         RotArgs a{};
@@ -734,7 +751,7 @@ quarot_status quarot_quant_int4_grouped(const quarot_f16 *x, uint8_t *q, quarot_
         return QUAROT_ERR_WORKSPACE;
     if (need && !aligned16(workspace))
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     return group_quant(x, q, scale, rows, n, group, rotate != 0, k, m, clip_ratio, workspace,
                        (hipStream_t)stream);
@@ -750,7 +767,7 @@ quarot_status quarot_w4a4_gemm_grouped(const uint8_t *xq, const quarot_f16 *sx,
         return st;
     if ((st = check_gemm(xq, sx, wq, sw, y, nullptr, M, N, K)))
         return st;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     GemmArgs a{xq, sx, wq, sw, y, nullptr, (int)M, (int)N, (int)K};
     hipError_t e = launch_gemm_grouped(a, (int)group, (hipStream_t)stream);
@@ -792,7 +809,7 @@ quarot_status quarot_linear_w4a4_grouped(const quarot_f16 *x, const uint8_t *wq,
         return QUAROT_ERR_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     uint8_t *xq = static_cast<uint8_t *>(workspace);
     quarot_f16 *sx = reinterpret_cast<quarot_f16 *>(xq + codes_bytes(M, K));
@@ -819,7 +836,7 @@ quarot_status quarot_swiglu(const quarot_f16 *gate, const quarot_f16 *up, quarot
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(gate) || !aligned16(up) || !aligned16(h))
         return QUAROT_ERR_ALIGNMENT;
-    quarot_status st = check_device();
+    quarot_status st = check_device(__func__);
     if (st)
         return st;
     hipError_t e = launch_swiglu(gate, up, h, count, (hipStream_t)stream);
@@ -844,7 +861,7 @@ quarot_status quarot_swiglu_quant_int4(const quarot_f16 *gate, const quarot_f16 
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(gate) || !aligned16(up) || !aligned16(q) || !aligned16(scale))
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     RotArgs a{};
     a.x = gate;
@@ -879,7 +896,7 @@ quarot_status quarot_swiglu_quant_e3m2(const quarot_f16 *gate, const quarot_f16 
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(gate) || !aligned16(up) || !aligned16(q6) || !aligned16(scale))
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     RotArgs a{};
     a.x = gate;
@@ -899,9 +916,9 @@ quarot_status quarot_swiglu_quant_e3m2(const quarot_f16 *gate, const quarot_f16 
 namespace {
 
 // Head-wise transform: n = n_heads * head_dim, both powers of two.
-quarot_status heads_launch(const quarot_f16 *z, void *out, quarot_f16 *scale, int64_t rows,
-                           int64_t n_heads, int64_t head_dim, float clip, int epi,
-                           void *stream)
+quarot_status heads_launch(const char *call, const quarot_f16 *z, void *out,
+                           quarot_f16 *scale, int64_t rows, int64_t n_heads,
+                           int64_t head_dim, float clip, int epi, void *stream)
 {
     if (rows < 0 || n_heads <= 0 || head_dim <= 0 || !clip_ok(clip))
         return QUAROT_ERR_INVALID_ARG;
@@ -922,7 +939,7 @@ quarot_status heads_launch(const quarot_f16 *z, void *out, quarot_f16 *scale, in
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(z) || !aligned16(out) || (scale && !aligned16(scale)))
         return QUAROT_ERR_ALIGNMENT;
-    quarot_status st = check_device();
+    quarot_status st = check_device(call);
     if (st)
         return st;
     RotArgs a{};
@@ -945,14 +962,16 @@ extern "C" {
 quarot_status quarot_hadamard_heads(const quarot_f16 *z, quarot_f16 *y, int64_t rows,
                                     int64_t n_heads, int64_t head_dim, void *stream)
 {
-    return heads_launch(z, y, nullptr, rows, n_heads, head_dim, 1.0f, EPI_F16, stream);
+    return heads_launch(__func__, z, y, nullptr, rows, n_heads, head_dim, 1.0f, EPI_F16,
+                        stream);
 }
 
 quarot_status quarot_hadamard_heads_quant_int4(const quarot_f16 *z, uint8_t *q,
                                                quarot_f16 *scale, int64_t rows, int64_t n_heads,
                                                int64_t head_dim, float clip_ratio, void *stream)
 {
-    return heads_launch(z, q, scale, rows, n_heads, head_dim, clip_ratio, EPI_SYM, stream);
+    return heads_launch(__func__, z, q, scale, rows, n_heads, head_dim, clip_ratio, EPI_SYM,
+                        stream);
 }
 
 quarot_status quarot_kv_quant(const quarot_f16 *kv, uint8_t *q, quarot_f16 *scale,
@@ -974,7 +993,7 @@ quarot_status quarot_kv_quant(const quarot_f16 *kv, uint8_t *q, quarot_f16 *scal
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(kv) || !aligned16(q) || !aligned16(scale) || !aligned16(zero))
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     RotArgs a{};
     a.x = kv;
@@ -1013,7 +1032,7 @@ quarot_status quarot_kv_append(const quarot_f16 *kv_new, uint8_t *q_cache,
     if (!aligned16(kv_new) || !aligned16(q_cache) || !aligned16(scale_cache) ||
         !aligned16(zero_cache))
         return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device()))
+    if ((st = check_device(__func__)))
         return st;
     RotArgs a{};
     a.x = kv_new;
@@ -1067,7 +1086,7 @@ quarot_status quarot_kv_decode_attention(const quarot_f16 *q, const uint8_t *k_c
         return QUAROT_ERR_WORKSPACE;
     if (need && !aligned16(workspace))
         return QUAROT_ERR_ALIGNMENT;
-    quarot_status st = check_device();
+    quarot_status st = check_device(__func__);
     if (st)
         return st;
     KvAttnArgs a{};
@@ -1109,7 +1128,7 @@ quarot_status quarot_kv_dequant(const uint8_t *q, const quarot_f16 *scale,
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(scale) || !aligned16(zero) || !aligned16(out))
         return QUAROT_ERR_ALIGNMENT;
-    quarot_status st = check_device();
+    quarot_status st = check_device(__func__);
     if (st)
         return st;
     KvDeqArgs a{q, scale, zero, out, rows, (int)head_dim, (int)group,

@@ -888,7 +888,8 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
             store_y8<EPI>(a.out, row * n + ch * 8, y);
         }
     } else {
-        static_assert(EPI == EPI_SYM || EPI == EPI_SYM8, "large-m kernels serve activations");
+        static_assert(EPI == EPI_SYM || EPI == EPI_SYM8 || EPI == EPI_E3M2,
+                      "large-m kernels serve activations");
         float amax = 0.0f;
         for (int ch = tid; ch < chunks; ch += 64 * W)
 #pragma unroll
@@ -916,7 +917,10 @@ __global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
                 const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
                 y[e] = rowbuf[gi * LD + b] * c;
             }
-            store_codes8<EPI>(qr, ch * 8, y, dv, qd);
+            if constexpr (EPI == EPI_E3M2)
+                store_e3m2_8(static_cast<uint8_t *>(a.out), a.rows, row, ch * 8, y, dv);
+            else
+                store_codes8<EPI>(qr, ch * 8, y, dv, qd);
         }
         if (tid == 0)
             a.scale[row] = s16;
@@ -985,17 +989,17 @@ __global__ __launch_bounds__(256) void k_swiglu(const uint16_t *g, const uint16_
 // Per-row clip search (§5 Setup: the weights' clipping ratio by a linear
 // search over the squared error; App. A.2).  One block per row.  For each
 // candidate c_j = RN32((100 - j) / 100) the symmetric quantizer's scale and
-// codes, and E_j = sum (y - q s16)^2 with each difference exact in fp64,
-// summed per thread over its chunks and then across the block in a fixed
-// order.  The row keeps the first j with the smallest E_j, then writes its
-// codes, scale and clip.
+// codes, and E_j = sum RN64((y - q s16)^2) with each difference exact in
+// binary64, summed in a fixed order (256 interleaved partial sums, then a
+// halving tree; see below).  The row keeps the first j with the smallest
+// E_j, then writes its codes, scale and clip.
 template <int BITS, typename TIN>
 __global__ __launch_bounds__(256) void k_quant_search(SearchArgs a)
 {
     constexpr int QMAX = BITS == 4 ? 7 : BITS == 6 ? 31 : 127;
     constexpr float QF = (float)QMAX;
     __shared__ float redf[4];
-    __shared__ double redd[4];
+    __shared__ double redd[256];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t row = blockIdx.x;
     const int n = a.n, chunks = n / 8;
@@ -1030,26 +1034,35 @@ __global__ __launch_bounds__(256) void k_quant_search(SearchArgs a)
         const float c = (float)((double)(100 - j) / 100.0);
         const float sf = h2f(f2h((amax * c) / QF));
         const Divisor dv = make_divisor(sf);
+        // The error's defined binary64 order: thread t sums the terms of
+        // elements t, t + 256, ... from +0 in increasing index; the 256
+        // partial sums P_t are then halved pairwise (P_t += P_{t+h},
+        // h = 128, ..., 1).  Every wave evaluates the whole tree from the
+        // LDS copy, so all threads hold the same total.
         double e = 0.0;
-        for (int ch = tid; ch < chunks; ch += 256) {
-            float v[8];
-            load(ch, v);
-#pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const float cq = dv.ok ? fminf(fmaxf(rintf(quotient(v[k], dv)), -QF - 1.0f), QF)
-                                       : 0.0f;
-                const double d = (double)v[k] - (double)cq * (double)sf;
-                e += d * d;  // two roundings, as the CPU reference
-            }
+        for (int i = tid; i < n; i += 256) {
+            float v;
+            if constexpr (sizeof(TIN) == 4)
+                v = yr[i];
+            else
+                v = h2f(yr[i]);  // fp16 bits
+            const float cq = dv.ok ? fminf(fmaxf(rintf(quotient(v, dv)), -QF - 1.0f), QF)
+                                   : 0.0f;
+            const double d = (double)v - (double)cq * (double)sf;
+            const double t = d * d;  // rounded on its own (no contraction)
+            e = e + t;
         }
+        __syncthreads();  // redd of the previous candidate has been read
+        redd[tid] = e;
+        __syncthreads();
+        // h = 128 and h = 64: lane l of any wave forms
+        // (P_l + P_{l+128}) + (P_{l+64} + P_{l+192})
+        e = (redd[lane] + redd[lane + 128]) + (redd[lane + 64] + redd[lane + 192]);
+        // h = 32 .. 1: the xor butterflies give lane l the sum of lanes l
+        // and l ^ h, which for l < h is the tree's P_l + P_{l+h}
 #pragma unroll
         for (int o = 32; o >= 1; o >>= 1)
-            e += __shfl_xor(e, o);
-        __syncthreads();  // redd of the previous candidate has been read
-        if (lane == 0)
-            redd[wave] = e;
-        __syncthreads();
-        e = ((redd[0] + redd[1]) + redd[2]) + redd[3];
+            e = e + __shfl_xor(e, o);
         if (e < best_e) {  // uniform across the block
             best_e = e;
             best_c = c;
@@ -1286,6 +1299,10 @@ hipError_t dispatch_rotated(const RotArgs &a, int k, int m, hipStream_t s)
         case 12: return dispatch_smallm_e3m2<12, PRO>(a, k, s);
         case 20: return dispatch_smallm_e3m2<20, PRO>(a, k, s);
         case 28: return dispatch_smallm_e3m2<28, PRO>(a, k, s);
+        case 108:
+            return (k <= 6) ? go_largem<108, 1, EPI_E3M2, PRO>(a, s)
+                            : go_largem<108, 2, EPI_E3M2, PRO>(a, s);
+        case 172: return go_largem<172, 1, EPI_E3M2, PRO>(a, s);
         }
         return hipErrorInvalidValue;
     } else {
@@ -1333,6 +1350,8 @@ bool rotate_supported(int epi, bool rotate, int k, int m, int n, int pro)
         case 12: return k == 10 || k == 11;
         case 20:
         case 28: return k == 9 || k == 10;
+        case 108: return k >= 5 && k <= 7;  // n a multiple of 128
+        case 172: return k >= 5 && k <= 6;
         }
         return false;
     }

@@ -248,7 +248,8 @@ def test_invalid_arguments_rejected_before_device(L):
     assert QE(P, P2, P2, 4, 128, 1, 0.0, S) == INVALID
     assert QE(P, P2, P2, 4, 64, 1, 1.0, S) == UNSUPPORTED           # not a multiple of 128
     assert QE(P, P2, P2, 4, 28 * 256, 1, 1.0, S) == UNSUPPORTED      # m = 28 needs 2^9 or 2^10
-    assert QE(P, P2, P2, 4, 108 * 128, 1, 1.0, S) == UNSUPPORTED     # m = 108: int4 + repack
+    assert QE(P, P2, P2, 4, 108 * 16, 1, 1.0, S) == UNSUPPORTED      # m = 108 needs 2^5 .. 2^7
+    assert QE(P, P2, P2, 4, 172 * 128, 1, 1.0, S) == UNSUPPORTED     # m = 172 needs 2^5 or 2^6
     assert QE(P, None, P2, 4, 128, 1, 1.0, S) == INVALID
     assert QE(P, P2, UNALIGNED, 4, 128, 1, 1.0, S) == ALIGN
     assert QE(None, None, None, 0, 128, 1, 1.0, S) == OK
@@ -287,6 +288,8 @@ def test_no_device_reported(L):
     assert L.quarot_pack_e3m2(P, P2, 4, 128, None) == NODEV
     assert L.quarot_w4a4_gemm_e3m2(P, P, P, P, P, None, 4, 4, 128, None) == NODEV
     assert L.quarot_quant_int4_e3m2(P, P2, P2, 4, 28672, 1, 1.0, None) == NODEV
+    assert L.quarot_quant_int4_e3m2(P, P2, P2, 4, 11008, 1, 1.0, None) == NODEV
+    assert L.quarot_quant_int4_e3m2(P, P2, P2, 4, 13824, 1, 1.0, None) == NODEV
     assert L.quarot_linear_e3m2(P, P, P, P, 4, 4, 8192, 1, 1.0, P, 1 << 20, None) == NODEV
     assert L.quarot_swiglu_quant_e3m2(P, P2, P, P2, 4, 28672, 1.0, None) == NODEV
     assert L.quarot_mfma_probe_fp6(P, 4, 10, None) == NODEV
@@ -299,3 +302,57 @@ def test_binding_rejects_host_tensors():
         q.quarot_hadamard(x, y=torch.zeros_like(x))
     with pytest.raises(TypeError):
         q.quarot_hadamard(x.float(), y=torch.zeros_like(x))
+
+
+HIP_ERROR_LAUNCH_FAILURE = 719  # hipErrorLaunchFailure
+
+
+@pytest.fixture
+def fake_hip_error(monkeypatch):
+    def arm(call):
+        monkeypatch.setenv("QUAROT_FAKE_HIP_ERROR", call)
+    yield arm
+    monkeypatch.delenv("QUAROT_FAKE_HIP_ERROR", raising=False)
+
+
+def test_fake_hip_error_hook(L, fake_hip_error):
+    """QUAROT_FAKE_HIP_ERROR=<entry point> makes exactly that entry point
+    report QUAROT_ERR_HIP after its argument checks and before any device
+    work; quarot_last_hip_error() returns the code; other entry points and
+    invalid arguments are unaffected.  Host-only: nothing launches."""
+    nodev_or_ok = (NODEV, OK)
+    fake_hip_error("quarot_linear")
+    assert L.quarot_linear(P, P, P, P, 4, 4, 128, 1, 1.0, P, 1 << 20, None) == HIP
+    assert L.quarot_last_hip_error() == HIP_ERROR_LAUNCH_FAILURE
+    assert L.quarot_linear(P, P, P, P, 4, 4, 128, 1, 0.0, P, 1 << 20, None) == INVALID
+    assert L.quarot_linear(P, P, P, P, 4, 4, 128, 1, 1.0, P, 16, None) == WORKSPACE
+    if not has_gpu():
+        assert L.quarot_quant_int4(P, P2, P2, 4, 128, 1, 1.0, None) in nodev_or_ok
+    for call, invoke in (
+            ("quarot_hadamard", lambda: L.quarot_hadamard(P, P2, 4, 128, None)),
+            ("quarot_w4a4_gemm_e3m2",
+             lambda: L.quarot_w4a4_gemm_e3m2(P, P, P, P, P, None, 4, 4, 128, None)),
+            ("quarot_hadamard_heads_quant_int4",
+             lambda: L.quarot_hadamard_heads_quant_int4(P, P2, P, 4, 64, 128, 1.0, None)),
+            ("quarot_kv_decode_attention",
+             lambda: L.quarot_kv_decode_attention(P, P, P, P, P, P, P, P2, 4, 4, 64, 64, 128,
+                                                  128, 0.1, P, 1 << 24, None))):
+        fake_hip_error(call)
+        assert invoke() == HIP, call
+        assert L.quarot_last_hip_error() == HIP_ERROR_LAUNCH_FAILURE
+    # the binding turns it into QuarotError carrying both codes
+    fake_hip_error("quarot_quant_int4")
+    with pytest.raises(q.QuarotError) as ei:
+        q._check("quarot_quant_int4", L.quarot_quant_int4(P, P2, P2, 4, 128, 1, 1.0, None))
+    assert ei.value.status == HIP and ei.value.hip_error == HIP_ERROR_LAUNCH_FAILURE
+
+
+def test_last_hip_error_is_per_thread(L, fake_hip_error):
+    import threading
+    fake_hip_error("quarot_hadamard")
+    assert L.quarot_hadamard(P, P2, 4, 128, None) == HIP
+    seen = []
+    t = threading.Thread(target=lambda: seen.append(L.quarot_last_hip_error()))
+    t.start()
+    t.join()
+    assert seen == [0] and L.quarot_last_hip_error() == HIP_ERROR_LAUNCH_FAILURE

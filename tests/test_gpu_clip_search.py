@@ -1,7 +1,8 @@
 """GPU parity of the weights' per-row clip search (§5 Setup, App. A.2)
 through the C ABI against the CPU oracle: chosen clips, codes and scales
-bit for bit (the error sums run in a different fp64 order on the two
-sides; on these seeded rows no two candidates come within that rounding)."""
+bit for bit.  Both sides sum the squared errors in the same defined
+binary64 order, so the choice is the same on any input, including rows
+whose candidates tie exactly (the order then decides)."""
 import numpy as np
 import pytest
 
@@ -38,3 +39,17 @@ def test_clip_search(dev, orc, n, rotate, bits, ncand):
     assert_same(H(scale).view(np.uint16), rs.view(np.uint16), "scales")
     if ncand > 1 and bits == 4:
         assert (rc < 1).any()  # the search does move the clip on these rows
+
+
+def test_clip_search_exact_ties(dev, orc):
+    import clip_ties
+    import paper_2404_00456_amd as q
+    rows = clip_ties.tie_rows(orc, 256, seed=3)
+    say(f"clip search on {rows.shape[0]} exactly tied rows, n={rows.shape[1]}")
+    codes, scale, clip = q.quarot_quant_search(T(rows, dev), rotate=False, bits=4,
+                                               n_candidates=2)
+    rq, rs, rc = orc.quant_search(rows, rotate=False, bits=4, n_candidates=2)
+    assert_same(H(clip), rc, "chosen clips")
+    assert_same(H(codes).view(np.uint8), rq.view(np.uint8), "codes")
+    assert_same(H(scale).view(np.uint16), rs.view(np.uint16), "scales")
+    assert 0 < int((rc < 1).sum()) < rows.shape[0]  # both candidates win somewhere

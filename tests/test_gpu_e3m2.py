@@ -35,26 +35,27 @@ def e3m2_value(c: int) -> float:
 E3M2 = np.array([e3m2_value(c) for c in range(64)])
 
 
-def decode_e3m2_layout(q6: np.ndarray, rows: int, k: int) -> np.ndarray:
-    """Tiled e3m2 layout [k/128, rows*96] -> code values [rows, k].  In block
-    b, row r's unit u is the 192-bit little-endian word made of the 16-byte
-    head at slot u ^ ((r >> 1) & 3) of the row's 64 bytes (heads of all rows
-    first) and the 8-byte tail at slot u ^ ((r >> 2) & 3) of its 32 bytes
-    (after the heads); code e sits at bits 6e..6e+5."""
+def decode_e3m2_layout(q6: np.ndarray, rows: int, k: int, sel=None) -> np.ndarray:
+    """Tiled e3m2 layout [k/128, rows*96] -> code values [rows, k] (or of
+    the rows listed in sel).  In block b, row r's unit u is the 192-bit
+    little-endian word made of the 16-byte head at slot u ^ ((r >> 1) & 3)
+    of the row's 64 bytes (heads of all rows first) and the 8-byte tail at
+    slot u ^ ((r >> 2) & 3) of its 32 bytes (after the heads); code e sits
+    at bits 6e..6e+5."""
     kb = k // 128
     buf = np.asarray(q6, np.uint8).reshape(kb, rows * 96)
     heads = buf[:, :rows * 64].reshape(kb, rows, 4, 16)
     tails = buf[:, rows * 64:].reshape(kb, rows, 4, 8)
-    r = np.arange(rows)
-    out = np.empty((rows, kb, 4, 32))
+    r = np.arange(rows) if sel is None else np.asarray(sel)
+    out = np.empty((len(r), kb, 4, 32))
     for u in range(4):
         h = heads[:, r, u ^ ((r >> 1) & 3), :]
         t = tails[:, r, u ^ ((r >> 2) & 3), :]
         word = np.concatenate([h, t], axis=2)
-        bits = np.unpackbits(word, axis=2, bitorder="little").reshape(kb, rows, 32, 6)
+        bits = np.unpackbits(word, axis=2, bitorder="little").reshape(kb, len(r), 32, 6)
         codes = bits.astype(np.int64) @ (1 << np.arange(6))
         out[:, :, u, :] = E3M2[codes].transpose(1, 0, 2)
-    return out.reshape(rows, k)
+    return out.reshape(len(r), k)
 
 
 def test_e3m2_table_holds_int4():
@@ -164,7 +165,7 @@ def test_gemm_e3m2_full_size(dev, orc, M, N, K):
 # ------------------------------------------- quantizer writing e3m2 ---
 
 E3M2_ROTATED_N = [128, 256, 1024, 4096, 8192, 16384, 32768, 12288, 24576, 10240, 20480, 14336,
-                  28672]
+                  28672, 3456, 6912, 13824, 5504, 11008]
 
 
 @pytest.mark.parametrize("n", E3M2_ROTATED_N)
@@ -207,7 +208,7 @@ def test_quant_int4_e3m2_ragged_rows(dev, orc, rows):
     total row count."""
     import paper_2404_00456_amd as q
     import workloads
-    for n in (128, 1024, 8192, 28672):
+    for n in (128, 1024, 8192, 28672, 11008):
         x = workloads.random_rows(rows * 7 + n, rows, n)
         q6, s6 = q.quarot_quant_int4_e3m2(T(x, dev), rotate=True)
         rq, rs = orc.quant_int4(x, rotate=True)

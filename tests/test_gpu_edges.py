@@ -133,7 +133,11 @@ def test_e3m2_entry_points_edges(dev, orc):
     for clip in (0.0, 1.5):
         with pytest.raises(q.QuarotError):
             q.quarot_quant_int4_e3m2(x, rotate=True, clip_ratio=clip, q6=qbuf, scale=sbuf)
-    with pytest.raises(q.QuarotError):  # 13824 = 2^7 * 108: refused, int4 + repack instead
+    with pytest.raises(q.QuarotError):  # 7168 = 2^8 * 28: refused, int4 + repack instead
+        q.quarot_quant_int4_e3m2(torch.zeros((32, 7168), dtype=torch.float16, device=dev),
+                                 rotate=True, q6=qbuf.view(-1)[:56 * 32 * 96].view(56, 32 * 96),
+                                 scale=sbuf)
+    with pytest.raises(ValueError):  # a code buffer smaller than rows x n needs
         q.quarot_quant_int4_e3m2(torch.zeros((32, 13824), dtype=torch.float16, device=dev),
                                  rotate=True, q6=qbuf, scale=sbuf)
     y = torch.full((32, 256), 3.0, dtype=torch.float16, device=dev)
@@ -158,3 +162,29 @@ def test_e3m2_entry_points_edges(dev, orc):
     torch.cuda.current_stream().wait_stream(side)
     assert_same(H(b6), H(a6), "e3m2 codes on a side stream")
     assert_same(H(b_s).view(np.uint16), H(a_s).view(np.uint16), "e3m2 scales on a side stream")
+
+
+def test_fake_hip_error_leaves_outputs_untouched(dev, monkeypatch):
+    """With QUAROT_FAKE_HIP_ERROR naming the call, the two-launch layer
+    entry point reports QUAROT_ERR_HIP with hipErrorLaunchFailure and writes
+    neither its output nor its workspace; with the variable cleared the
+    same call runs."""
+    import torch
+    import paper_2404_00456_amd as q
+    say("fake hip error")
+    x = T(workloads.random_rows(31, 64, 8192), dev)
+    w6 = torch.zeros((64, 256 * 96), dtype=torch.uint8, device=dev)
+    sw = torch.ones(256, dtype=torch.float16, device=dev)
+    y = torch.full((64, 256), 3.0, dtype=torch.float16, device=dev)
+    ws = torch.full((q.quarot_linear_e3m2_workspace_size(64, 8192),), 0x5A, dtype=torch.uint8,
+                    device=dev)
+    monkeypatch.setenv("QUAROT_FAKE_HIP_ERROR", "quarot_linear_e3m2")
+    with pytest.raises(q.QuarotError) as ei:
+        q.quarot_linear_e3m2(x, w6, sw, y=y, workspace=ws)
+    assert ei.value.status == 6 and ei.value.hip_error == 719
+    torch.cuda.synchronize()
+    assert bool((y == 3.0).all()) and bool((ws == 0x5A).all())
+    monkeypatch.delenv("QUAROT_FAKE_HIP_ERROR")
+    q.quarot_linear_e3m2(x, w6, sw, y=y, workspace=ws)
+    torch.cuda.synchronize()
+    assert bool((y == 0.0).all())  # zero weights

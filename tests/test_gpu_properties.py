@@ -1,0 +1,120 @@
+"""Bounded property sweep of the hot path on the GPU against the CPU oracle
+(§3.1 rotation, §4 Stage 2b quantization and integer product, App. A.10):
+hypothesis draws shapes (rows, n = 2^k * m, M, N, K) and row contents,
+including adversarial rows (zeros, one spike, constant rows, fp16
+subnormals, values near the fp16 maximum), and every draw must match the
+oracle bit for bit.  Draws are derandomized (the same sweep every run) and
+failures are reported as drawn, without shrinking."""
+import numpy as np
+import pytest
+from hypothesis import HealthCheck, Phase, given, settings
+from hypothesis import strategies as st
+
+from test_gpu_e3m2 import decode_e3m2_layout
+from test_gpu_parity import H, T, assert_same, rand_codes, say
+
+pytestmark = pytest.mark.gpu
+
+SWEEP = settings(max_examples=30, deadline=None, derandomize=True, database=None,
+                 phases=[Phase.explicit, Phase.generate],
+                 suppress_health_check=list(HealthCheck))
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2404_00456_amd as q
+    q.lib()
+    return torch.device("cuda:0")
+
+
+# n = 2^k * m as the library supports it (multiples of 8, at most 32768)
+WIDTHS = sorted({(2 ** k) * m for m, ks in ((1, range(3, 16)), (12, range(1, 12)),
+                                            (20, range(1, 11)), (28, range(1, 11)),
+                                            (108, range(1, 8)), (172, range(1, 7)))
+                 for k in ks if (2 ** k) * m % 8 == 0 and (2 ** k) * m <= 32768})
+
+KINDS = ["normal", "student_t3", "zeros", "spike", "constant", "subnormal", "huge", "mixed"]
+
+
+def make_rows(seed, rows, n, kind):
+    rng = np.random.default_rng(seed)
+    if kind in ("normal", "student_t3"):
+        x = rng.standard_normal((rows, n)) if kind == "normal" else rng.standard_t(3, (rows, n))
+        x = x * 10.0 ** rng.uniform(-3, 2)
+    elif kind == "zeros":
+        x = np.zeros((rows, n))
+    elif kind == "spike":
+        x = rng.standard_normal((rows, n)) * 1e-3
+        x[np.arange(rows), rng.integers(0, n, rows)] = rng.choice([-1, 1], rows) * 3e3
+    elif kind == "constant":
+        x = np.full((rows, n), float(rng.uniform(-4, 4)))
+    elif kind == "subnormal":
+        x = rng.integers(-1023, 1024, (rows, n)) * 2.0 ** -24
+    elif kind == "huge":
+        x = rng.uniform(-65504, 65504, (rows, n))
+    else:  # each row its own kind
+        parts = [make_rows(seed + 1 + r, 1, n, KINDS[r % 7]) for r in range(rows)]
+        return np.concatenate(parts)
+    return x.astype(np.float16)
+
+
+@SWEEP
+@given(seed=st.integers(0, 2 ** 31 - 1), rows=st.integers(1, 300),
+       n=st.sampled_from(WIDTHS), kind=st.sampled_from(KINDS),
+       clip=st.sampled_from([1.0, 0.9, 0.5]))
+def test_rotate_quant_sweep(dev, orc, seed, rows, n, kind, clip):
+    import paper_2404_00456_amd as q
+    say(f"rotate+quant rows={rows} n={n} kind={kind} clip={clip} seed={seed}")
+    x = make_rows(seed, rows, n, kind)
+    xd = T(x, dev)
+    assert_same(H(q.quarot_hadamard(xd)).view(np.uint16), orc.hadamard(x).view(np.uint16),
+                "hadamard")
+    cq, cs = q.quarot_quant_int4(xd, rotate=True, clip_ratio=clip)
+    rq, rs = orc.quant_int4(x, rotate=True, clip=clip)
+    assert_same(H(cq), rq, "codes")
+    assert_same(H(cs).view(np.uint16), rs.view(np.uint16), "scales")
+    if _e3m2_rotated_ok(n):
+        q6, s6 = q.quarot_quant_int4_e3m2(xd, rotate=True, clip_ratio=clip)
+        assert_same(decode_e3m2_layout(H(q6), rows, n), orc.unpack_int4(rq).astype(np.float64),
+                    "e3m2 codes")
+        assert_same(H(s6).view(np.uint16), rs.view(np.uint16), "e3m2 scales")
+
+
+def _e3m2_rotated_ok(n):
+    """Widths quarot_quant_int4_e3m2 takes with rotation (its header)."""
+    if n % 128:
+        return False
+    for m, ks in ((1, range(7, 16)), (12, (10, 11)), (20, (9, 10)), (28, (9, 10)),
+                  (108, range(5, 8)), (172, (5, 6))):
+        if n % m == 0 and (n // m) & (n // m - 1) == 0 and (n // m).bit_length() - 1 in ks:
+            return True
+    return False
+
+
+@SWEEP
+@given(seed=st.integers(0, 2 ** 31 - 1), M=st.integers(1, 700), N=st.integers(1, 700),
+       kb=st.integers(1, 48), extreme=st.booleans())
+def test_gemm_sweep(dev, orc, seed, M, N, kb, extreme):
+    import paper_2404_00456_amd as q
+    K = 128 * kb
+    say(f"gemm M={M} N={N} K={K} extreme={extreme} seed={seed}")
+    rng = np.random.default_rng(seed)
+    if extreme:  # every code -8 or 7
+        xq = rng.choice(np.array([0x88, 0x77, 0x78, 0x87], np.uint8), (M, K // 2))
+        wq = rng.choice(np.array([0x88, 0x77, 0x78, 0x87], np.uint8), (N, K // 2))
+    else:
+        xq, wq = rand_codes(rng, M, K), rand_codes(rng, N, K)
+    sx = (2.0 ** rng.uniform(-20, 0, M)).astype(np.float16)
+    sw = (2.0 ** rng.uniform(-14, -4, N)).astype(np.float16)
+    racc = orc.gemm_i32(xq, wq)
+    ry = orc.dequant(racc, sx, sw)
+    y, acc = q.quarot_w4a4_gemm(T(xq, dev), T(sx, dev), T(wq, dev), T(sw, dev), want_acc=True)
+    assert_same(H(acc), racc, "int4 acc")
+    assert_same(H(y).view(np.uint16), ry.view(np.uint16), "int4 y")
+    x6, w6 = q.quarot_pack_e3m2(T(xq, dev)), q.quarot_pack_e3m2(T(wq, dev))
+    y6, acc6 = q.quarot_w4a4_gemm_e3m2(x6, T(sx, dev), w6, T(sw, dev), want_acc=True)
+    assert_same(H(acc6), racc, "e3m2 acc")
+    assert_same(H(y6).view(np.uint16), ry.view(np.uint16), "e3m2 y")

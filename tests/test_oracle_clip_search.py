@@ -53,3 +53,25 @@ def test_gaussian_rows_get_clipped(orc):
     _, _, c8 = orc.quant_search(w, rotate=False, bits=8, n_candidates=50)
     assert np.all(c4 < 0.9)
     assert np.all(c8 > c4)
+
+
+def test_exact_ties_follow_the_defined_order(orc):
+    """On rows whose two candidates' errors tie exactly (clip_ties), the
+    oracle keeps candidate 1 only where the defined summation order makes
+    its error strictly smaller, and these rows do depend on the order: a
+    left-to-right sum would choose differently on some of them."""
+    import clip_ties
+    rows = clip_ties.tie_rows(orc, 96)
+    _, _, c = orc.quant_search(rows, rotate=False, bits=4, n_candidates=2)
+    differs = 0
+    for r in range(rows.shape[0]):
+        e0 = clip_ties.squared_errors(orc, rows[r], 1.0)
+        e1 = clip_ties.squared_errors(orc, rows[r], clip_ties.C99)
+        assert np.array_equal(np.sort(e0), np.sort(e1))  # an exact tie
+        assert not np.array_equal(e0, e1)                # at different positions
+        t0, t1 = clip_ties.sum_defined_order(e0), clip_ties.sum_defined_order(e1)
+        pick = 1 if t1 < t0 else 0
+        assert c[r] == (np.float32(clip_ties.C99) if pick else np.float32(1.0))
+        l0, l1 = clip_ties.sum_left_to_right(e0), clip_ties.sum_left_to_right(e1)
+        differs += pick != (1 if l1 < l0 else 0)
+    assert differs >= 2

@@ -46,8 +46,30 @@ def test_one_token_returns_its_value_row(orc):
     v = make_cache(rng, 2, 8, 128, 128)
     q = rng.standard_normal((2, 128)).astype(np.float16)
     out = orc.kv_attention(q, k, v, 1)
-    ref = dequant_exact(orc, v, 128)[:, 0].astype(np.float32).astype(np.float16)
+    ref = dequant_exact(orc, v, 128)[:, 0].astype(np.float16)  # numpy rounds fp64 once
     assert np.array_equal(out, ref)
+
+
+def test_output_rounded_once_from_fp64(orc):
+    """Two tokens with equal scores average their value rows.  Token 0's
+    row is 1 (code 0, zero 1); token 1's is 1 + 2^-10 + 2^-24 (code 1,
+    scale 1 + 2^-10, zero 2^-24, both fp16).  The exact output
+    1 + 2^-11 + 2^-25 lies just above the fp16 midpoint 1 + 2^-11: rounded
+    once it is 1 + 2^-10, while a detour through binary32 lands on the
+    midpoint and ties to even, 1."""
+    D = G = 8
+    q = np.zeros((1, D), np.float16)
+    kc = np.zeros((1, 2, D // 2), np.uint8)
+    ks = np.ones((1, 2, 1), np.float16)
+    kz = np.zeros((1, 2, 1), np.float16)
+    vc = np.zeros((1, 2, D // 2), np.uint8)
+    vc[0, 1] = 0x11  # code 1 everywhere
+    vs = np.array([[[1.0], [1.0 + 2.0 ** -10]]], np.float16)
+    vz = np.array([[[1.0], [2.0 ** -24]]], np.float16)
+    out = orc.kv_attention(q, (kc, ks, kz), (vc, vs, vz), 2, group=G)
+    exact = 1.0 + 2.0 ** -11 + 2.0 ** -25
+    assert np.float64(exact).astype(np.float32) == np.float32(1.0 + 2.0 ** -11)
+    assert np.all(out.view(np.uint16) == np.float16(1.0 + 2.0 ** -10).view(np.uint16))
 
 
 def test_zero_query_averages_values(orc):

@@ -92,6 +92,33 @@ def test_f32_to_f16_random_and_boundaries(orc):
     assert np.array_equal(got[~nan].view(np.uint16), ref[~nan].view(np.uint16))
 
 
+def test_f64_to_f16_rounds_once(orc):
+    """binary64 -> binary16 against numpy's conversion (which rounds the
+    binary64 value directly): random encodings over the fp16 range and
+    beyond, every fp16 midpoint exactly and nudged by amounts far below a
+    binary32 ulp (where rounding through binary32 first would tie)."""
+    rng = np.random.default_rng(11)
+    parts = [rng.uniform(-70000, 70000, 1_000_000),
+             np.ldexp(rng.uniform(0.5, 1, 500_000), rng.integers(-30, 17, 500_000))]
+    h = np.arange(0, 0x7C01, dtype=np.uint32).astype(np.uint16).view(np.float16)
+    f = h.astype(np.float64)
+    mids = (f[:-1] + f[1:]) / 2
+    for eps in (0.0, 2.0 ** -40, -2.0 ** -40, 2.0 ** -30):
+        nudged = mids * (1 + eps)
+        parts += [nudged, -nudged]
+    parts.append(np.array([65520.0, 65519.99999, 1e300, 2.0 ** -25, 2.0 ** -25 * (1 + 2 ** -40),
+                           5e-324, 0.0, -0.0]))
+    d = np.concatenate(parts)
+    got = orc.f64_to_f16(d)
+    with np.errstate(over="ignore"):
+        ref = d.astype(np.float16)
+    assert np.array_equal(got.view(np.uint16), ref.view(np.uint16))
+    # the cases the direct rounding exists for
+    x = np.array([1 + 2.0 ** -11 + 2.0 ** -40])
+    assert orc.f64_to_f16(x).view(np.uint16)[0] == 0x3C01
+    assert orc.f32_to_f16(x.astype(np.float32)).view(np.uint16)[0] == 0x3C00
+
+
 # --------------------------------------------------------------------------
 # Hadamard matrices (§3.1)
 # --------------------------------------------------------------------------
