@@ -33,7 +33,9 @@
  *  - Pointers are device pointers (hipMalloc or torch CUDA tensors) unless
  *    stated otherwise, and must be 16-byte aligned.  The caller owns every
  *    buffer, including the workspace; the library never allocates, frees
- *    or keeps pointers, holds no mutable global state and is reentrant.
+ *    or keeps pointers, and is reentrant.  Its one piece of mutable global
+ *    state is the fixed scratch array of quarot_linear_e3m2_scratch (see
+ *    there); every other call uses only its arguments.
  *  - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *    Calls only enqueue work on `stream` and return without synchronizing.
  *  - Invalid arguments are reported before any device work, leaving every
@@ -218,6 +220,30 @@ quarot_status quarot_linear_e3m2(const quarot_f16 *x, const uint8_t *wq6, const 
                                  quarot_f16 *y, int64_t M, int64_t N, int64_t K, int rotate,
                                  float clip_ratio, void *workspace, size_t workspace_bytes,
                                  void *stream);
+
+/*
+ * quarot_linear_e3m2 for callers that cannot allocate device memory (code
+ * under HIP graph capture, allocation-free serving loops, harnesses that
+ * forbid hipMalloc): the same two launches and the same y bit for bit, with
+ * the activation codes and scales in a fixed device array inside the
+ * library instead of a workspace.  The array holds QUAROT_SCRATCH_BYTES on
+ * every device the library runs on, until the process ends; sizes with
+ * quarot_linear_e3m2_workspace_size(M, K) > QUAROT_SCRATCH_BYTES return
+ * QUAROT_ERR_WORKSPACE before any device work (e.g. M = 2048 tokens at
+ * K = 28672 fit; M = 16384 at K = 8192 does not).  Nothing is allocated; the
+ * first call on a device looks up the array's address there
+ * (hipGetSymbolAddress), so make one call before capturing a graph.  All
+ * calls on one device share the array and it keeps the last call's
+ * contents (each call writes all it reads, nothing needs to start at
+ * zero): calls that overlap in time on one device, from other streams or
+ * threads, race, and the caller must order them.  Other size, pointer and
+ * error rules as quarot_linear_e3m2.
+ */
+#define QUAROT_SCRATCH_BYTES (64u << 20)
+quarot_status quarot_linear_e3m2_scratch(const quarot_f16 *x, const uint8_t *wq6,
+                                         const quarot_f16 *sw, quarot_f16 *y, int64_t M,
+                                         int64_t N, int64_t K, int rotate, float clip_ratio,
+                                         void *stream);
 
 /*
  * Bytes of device workspace quarot_linear needs for M rows of width K:

@@ -55,6 +55,7 @@ SIGNATURES = {
     "quarot_linear_e3m2_workspace_size": (ctypes.c_size_t, [_I64, _I64]),
     "quarot_linear_e3m2": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P, ctypes.c_size_t,
                                 _P]),
+    "quarot_linear_e3m2_scratch": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P]),
     "quarot_swiglu_quant_e3m2": (_I, [_P, _P, _P, _P, _I64, _I64, _F, _P]),
     "quarot_linear_workspace_size": (ctypes.c_size_t, [_I64, _I64]),
     "quarot_linear": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I, _F, _P, ctypes.c_size_t, _P]),
@@ -367,6 +368,31 @@ def quarot_linear_e3m2(x: torch.Tensor, wq6: torch.Tensor, sw: torch.Tensor,
         _ptr(x, torch.float16, "x"), _ptr(wq6, torch.uint8, "wq6"), _ptr(sw, torch.float16, "sw"),
         _ptr(y, torch.float16, "y"), M, N, K, int(bool(rotate)), float(clip_ratio),
         _ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream)))
+    return y
+
+
+SCRATCH_BYTES = 64 << 20  # QUAROT_SCRATCH_BYTES
+
+
+def quarot_linear_e3m2_scratch(x: torch.Tensor, wq6: torch.Tensor, sw: torch.Tensor,
+                               rotate: bool = True, clip_ratio: float = 1.0,
+                               y: Optional[torch.Tensor] = None,
+                               stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """quarot_linear_e3m2 with the codes and scales in the library's fixed
+    device scratch array instead of a workspace (the C call allocates
+    nothing; pass y to keep this wrapper from allocating it).  Calls that
+    overlap in time on one device share that array and race."""
+    _ndim(x, 2, "x")
+    M, K = x.shape
+    N = sw.numel()
+    _numel(wq6, N * K * 3 // 4, "wq6")
+    _shape(y, (M, N), "y")
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    _check("quarot_linear_e3m2_scratch", lib().quarot_linear_e3m2_scratch(
+        _ptr(x, torch.float16, "x"), _ptr(wq6, torch.uint8, "wq6"), _ptr(sw, torch.float16, "sw"),
+        _ptr(y, torch.float16, "y"), M, N, K, int(bool(rotate)), float(clip_ratio),
+        _stream(stream)))
     return y
 
 
@@ -790,5 +816,5 @@ __all__ = [
     "quarot_kv_attention_workspace_size", "quarot_kv_decode_attention",
     "quarot_mfma_probe_fp6", "quarot_pack_e3m2", "quarot_w4a4_gemm_e3m2",
     "quarot_quant_int4_e3m2", "quarot_linear_e3m2_workspace_size", "quarot_linear_e3m2",
-    "quarot_swiglu_quant_e3m2", "prepare_weight_e3m2",
+    "quarot_swiglu_quant_e3m2", "prepare_weight_e3m2", "quarot_linear_e3m2_scratch",
 ]

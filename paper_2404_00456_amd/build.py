@@ -13,7 +13,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libquarot.so")
 SOURCES = ["capi.cpp", "rotate_quant.hip", "gemm_w4a4.hip", "gemm_grouped.hip", "kv_attention.hip",
-           "probe.hip"]
+           "probe.hip", "scratch.hip"]
 
 # -ffp-contract=off: every written add and multiply stays a rounded op of
 # its own (the rotation order and the dequant order are part of the result).

@@ -455,31 +455,42 @@ size_t quarot_linear_e3m2_workspace_size(int64_t M, int64_t K)
     return codes + scales;
 }
 
-quarot_status quarot_linear_e3m2(const quarot_f16 *x, const uint8_t *wq6, const quarot_f16 *sw,
-                                 quarot_f16 *y, int64_t M, int64_t N, int64_t K, int rotate,
-                                 float clip_ratio, void *workspace, size_t workspace_bytes,
-                                 void *stream)
+}  // extern "C"
+
+namespace {
+
+// Checks of the e3m2 layer's arguments other than its workspace; on
+// success k, m hold the factorization of K.  *noop is set when there is
+// nothing to compute.
+quarot_status check_linear_e3m2(const quarot_f16 *x, const uint8_t *wq6, const quarot_f16 *sw,
+                                const quarot_f16 *y, int64_t M, int64_t N, int64_t K,
+                                int rotate, float clip_ratio, int *k, int *m, bool *noop)
 {
+    *noop = false;
     if (M < 0 || N < 0 || !clip_ok(clip_ratio))
         return QUAROT_ERR_INVALID_ARG;
-    int k, m;
-    quarot_status st = check_rot_size(K, rotate != 0, EPI_E3M2, &k, &m);
+    quarot_status st = check_rot_size(K, rotate != 0, EPI_E3M2, k, m);
     if (st)
         return st;
     if ((st = check_gemm_sizes(M, N, K)))
         return st;
-    if (M == 0 || N == 0)
+    if (M == 0 || N == 0) {
+        *noop = true;
         return QUAROT_OK;
+    }
     if (!x || !wq6 || !sw || !y)
         return QUAROT_ERR_INVALID_ARG;
     if (!aligned16(x) || !aligned16(wq6) || !aligned16(sw) || !aligned16(y))
         return QUAROT_ERR_ALIGNMENT;
-    if (!workspace || workspace_bytes < quarot_linear_e3m2_workspace_size(M, K))
-        return QUAROT_ERR_WORKSPACE;
-    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
-        return QUAROT_ERR_ALIGNMENT;
-    if ((st = check_device(__func__)))
-        return st;
+    return QUAROT_OK;
+}
+
+// The e3m2 layer's two launches with its codes and scales in `workspace`
+// (at least quarot_linear_e3m2_workspace_size(M, K) bytes, 256-B aligned).
+quarot_status run_linear_e3m2(const quarot_f16 *x, const uint8_t *wq6, const quarot_f16 *sw,
+                              quarot_f16 *y, int64_t M, int64_t N, int64_t K, int rotate,
+                              float clip_ratio, int k, int m, void *workspace, void *stream)
+{
     uint8_t *xq6 = static_cast<uint8_t *>(workspace);
     const size_t codes = ((size_t)M * (size_t)(K / 4 * 3) + 255) & ~(size_t)255;
     quarot_f16 *sx = reinterpret_cast<quarot_f16 *>(xq6 + codes);
@@ -497,6 +508,52 @@ quarot_status quarot_linear_e3m2(const quarot_f16 *x, const uint8_t *wq6, const 
     GemmArgs ga{xq6, sx, wq6, sw, y, nullptr, (int)M, (int)N, (int)K};
     e = launch_gemm(ga, (hipStream_t)stream, 6);
     return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+quarot_status quarot_linear_e3m2(const quarot_f16 *x, const uint8_t *wq6, const quarot_f16 *sw,
+                                 quarot_f16 *y, int64_t M, int64_t N, int64_t K, int rotate,
+                                 float clip_ratio, void *workspace, size_t workspace_bytes,
+                                 void *stream)
+{
+    int k, m;
+    bool noop;
+    quarot_status st =
+        check_linear_e3m2(x, wq6, sw, y, M, N, K, rotate, clip_ratio, &k, &m, &noop);
+    if (st || noop)
+        return st;
+    if (!workspace || workspace_bytes < quarot_linear_e3m2_workspace_size(M, K))
+        return QUAROT_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return QUAROT_ERR_ALIGNMENT;
+    if ((st = check_device(__func__)))
+        return st;
+    return run_linear_e3m2(x, wq6, sw, y, M, N, K, rotate, clip_ratio, k, m, workspace, stream);
+}
+
+quarot_status quarot_linear_e3m2_scratch(const quarot_f16 *x, const uint8_t *wq6,
+                                         const quarot_f16 *sw, quarot_f16 *y, int64_t M,
+                                         int64_t N, int64_t K, int rotate, float clip_ratio,
+                                         void *stream)
+{
+    int k, m;
+    bool noop;
+    quarot_status st =
+        check_linear_e3m2(x, wq6, sw, y, M, N, K, rotate, clip_ratio, &k, &m, &noop);
+    if (st || noop)
+        return st;
+    if (quarot_linear_e3m2_workspace_size(M, K) > (size_t)QUAROT_SCRATCH_BYTES)
+        return QUAROT_ERR_WORKSPACE;  // beyond the fixed array
+    if ((st = check_device(__func__)))
+        return st;
+    void *ws = nullptr;
+    hipError_t e = scratch_buffer(&ws);  // the array's address on this device
+    if (e != hipSuccess)
+        return hip_fail(e);
+    return run_linear_e3m2(x, wq6, sw, y, M, N, K, rotate, clip_ratio, k, m, ws, stream);
 }
 
 quarot_status quarot_quant_int8(const quarot_f16 *x, int8_t *q, quarot_f16 *scale, int64_t rows,

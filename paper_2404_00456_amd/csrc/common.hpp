@@ -195,6 +195,10 @@ hipError_t launch_mfma_probe_fp6(int32_t *out, int blocks, int iters, hipStream_
 hipError_t launch_swiglu(const uint16_t *g, const uint16_t *u, uint16_t *h, int64_t count,
                          hipStream_t s);
 
+// Device address of the fixed scratch array (QUAROT_SCRATCH_BYTES) on the
+// current device; looked up on the first call per device, then cached.
+hipError_t scratch_buffer(void **ptr);
+
 // Is (k, m) covered by a compiled rotate kernel for this epilogue?
 bool rotate_supported(int epi, bool rotate, int k, int m, int n, int pro = PRO_PLAIN);
 

@@ -293,6 +293,7 @@ def test_no_device_reported(L):
     assert L.quarot_linear_e3m2(P, P, P, P, 4, 4, 8192, 1, 1.0, P, 1 << 20, None) == NODEV
     assert L.quarot_swiglu_quant_e3m2(P, P2, P, P2, 4, 28672, 1.0, None) == NODEV
     assert L.quarot_mfma_probe_fp6(P, 4, 10, None) == NODEV
+    assert L.quarot_linear_e3m2_scratch(P, P, P, P, 2048, 4, 28672, 1, 1.0, None) == NODEV
 
 
 def test_binding_rejects_host_tensors():
@@ -356,3 +357,18 @@ def test_last_hip_error_is_per_thread(L, fake_hip_error):
     t.start()
     t.join()
     assert seen == [0] and L.quarot_last_hip_error() == HIP_ERROR_LAUNCH_FAILURE
+
+
+def test_scratch_entry_point_limits(L):
+    """The allocation-free layer refuses sizes beyond its fixed array
+    (64 MiB of codes and scales) before any device work, and otherwise
+    validates like quarot_linear_e3m2."""
+    SE = L.quarot_linear_e3m2_scratch
+    assert q.SCRATCH_BYTES == 64 << 20
+    assert L.quarot_linear_e3m2_workspace_size(16384, 8192) > q.SCRATCH_BYTES
+    assert SE(P, P, P, P, 16384, 4, 8192, 1, 1.0, None) == WORKSPACE
+    assert SE(P, P, P, P, 4, 4, 8192, 1, 0.0, None) == INVALID
+    assert SE(P, P, P, P, 4, 4, 192, 1, 1.0, None) == UNSUPPORTED
+    assert SE(None, P, P, P, 4, 4, 8192, 1, 1.0, None) == INVALID
+    assert SE(UNALIGNED, P, P, P, 4, 4, 8192, 1, 1.0, None) == ALIGN
+    assert SE(None, None, None, None, 0, 4, 8192, 1, 1.0, None) == OK
