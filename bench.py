@@ -180,6 +180,171 @@ def bench_kv(q, workloads, torch, np, dev, stream, iters):
     return res
 
 
+def event_times_us(torch, stream, fns, iters):
+    """Per-launch durations (us) of each function in fns, run in turn
+    iters times, from HIP events on the launch stream."""
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)]
+          for _ in range(iters)]
+    for it in range(iters):
+        for j, fn in enumerate(fns):
+            ev[it][j].record(stream)
+            fn()
+        ev[it][len(fns)].record(stream)
+    torch.cuda.synchronize()
+    return [[ev[it][j].elapsed_time(ev[it][j + 1]) * 1e3 for it in range(iters)]
+            for j in range(len(fns))]
+
+
+def rotation_bounds(q, M, K, code_bits):
+    """(HBM-bound us, VALU-bound us) of rotate+quantize: algorithmic bytes at
+    8 TB/s, and log2(2^k) butterfly adds plus m - 1 m-factor adds per
+    element at the fp32 vector add rate."""
+    k2, m = q.quarot_hadamard_factor(K)
+    return (rotate_bytes(M, K, code_bits) / (PEAK_HBM_GBS * 1e9) * 1e6,
+            M * K * (k2 + m - 1) / PEAK_F32_ADDS * 1e6)
+
+
+def bench_layers_7b(q, workloads, torch, np, dev, stream, iters, keep=None):
+    """The Llama-2-7B layer shapes at sequence 2048 (M = 2048): up
+    4096 -> 11008 (H_4096) and down 11008 -> 4096 (H_64 x H_172), each as
+    the two launches of the e3m2 layer, per-kernel event times; and the
+    tiny layer (16 x 128 -> 256) as launch latency of the whole call."""
+    res = {}
+    for name in ("llama2_7b_up", "llama2_7b_down"):
+        wl = workloads.LINEAR[name]
+        log(f"generating {name}: M={wl.M} K={wl.K} N={wl.N}")
+        x, w, _ = workloads.linear_inputs(wl)
+        xd = torch.from_numpy(x).to(dev)
+        wd = torch.from_numpy(w).to(dev)
+        w6, sw = q.prepare_weight_e3m2(wd, rotate=True)
+        del wd
+        if keep is not None:
+            keep[name] = (x[:256].copy(), w)
+        x6 = torch.empty((wl.K // 128, wl.M * 96), dtype=torch.uint8, device=dev)
+        sx6 = torch.empty((wl.M,), dtype=torch.float16, device=dev)
+        y = torch.empty((wl.M, wl.N), dtype=torch.float16, device=dev)
+        rot = lambda: q.quarot_quant_int4_e3m2(xd, rotate=True, q6=x6, scale=sx6)
+        gem = lambda: q.quarot_w4a4_gemm_e3m2(x6, sx6, w6, sw, y=y)
+        for _ in range(3):
+            rot(), gem()
+        rt, gt = event_times_us(torch, stream, [rot, gem], iters)
+        # cold rotation: rotate across copies of X totalling > 512 MB (twice
+        # the last-level cache), so every launch reads its input from HBM
+        ncp = max(2, -(-(640 << 20) // (xd.numel() * 2)))
+        xs = [xd.clone() for _ in range(ncp)]
+        cold = [lambda xc=xc: q.quarot_quant_int4_e3m2(xc, rotate=True, q6=x6, scale=sx6)
+                for xc in xs]
+        ct = event_times_us(torch, stream, cold, 2)
+        del xs
+        r_us, g_us = float(np.mean(rt)), float(np.mean(gt))
+        c_us = float(np.mean([v for c in ct for v in c]))
+        hbm_us, valu_us = rotation_bounds(q, wl.M, wl.K, 6)
+        ops = 2 * wl.M * wl.N * wl.K
+        k2, m = q.quarot_hadamard_factor(wl.K)
+        res[name] = {
+            "workload": f"M={wl.M} K={wl.K} -> N={wl.N}, H_{2 ** k2}" + (f" x H_{m}" if m > 1 else ""),
+            "rotate_quant_us": round(r_us, 2), "rotate_quant_cold_us": round(c_us, 2),
+            "rotate_quant_GBps": round(rotate_bytes(wl.M, wl.K, 6) / (r_us * 1e-6) / 1e9, 1),
+            "rotate_quant_frac_hbm": round(hbm_us / r_us, 4),
+            "rotate_quant_frac_valu_bound": round(valu_us / r_us, 4),
+            "gemm_us": round(g_us, 2),
+            "gemm_us_p10_p50_p90": [round(float(np.percentile(gt, p)), 1) for p in (10, 50, 90)],
+            "gemm_TOPS": round(ops / (g_us * 1e-6) / 1e12, 1),
+            "gemm_frac_fp6_peak": round(ops / (g_us * 1e-6) / 1e12 / PEAK_FP6_TOPS, 4),
+            "linear_TOPS": round(ops / ((r_us + g_us) * 1e-6) / 1e12, 1),
+            "linear_frac_int8_peak": round(ops / ((r_us + g_us) * 1e-6) / 1e12 / PEAK_I8_TOPS, 4),
+        }
+        del xd, w6, sw, x6, sx6, y
+    # the tiny layer: launch latency of the two-launch call, back to back
+    wl = workloads.LINEAR["tiny"]
+    x, w, _ = workloads.linear_inputs(wl)
+    xd = torch.from_numpy(x).to(dev)
+    w6, sw = q.prepare_weight_e3m2(torch.from_numpy(w).to(dev), rotate=True)
+    ws = torch.empty(q.quarot_linear_e3m2_workspace_size(wl.M, wl.K), dtype=torch.uint8,
+                     device=dev)
+    y = torch.empty((wl.M, wl.N), dtype=torch.float16, device=dev)
+    call = lambda: q.quarot_linear_e3m2(xd, w6, sw, y=y, workspace=ws)
+    us = time_us(torch, stream, call, iters=200)
+    t0 = time.perf_counter()
+    for _ in range(200):
+        call()
+    host_us = (time.perf_counter() - t0) / 200 * 1e6
+    torch.cuda.synchronize()
+    res["tiny"] = {"workload": f"M={wl.M} K={wl.K} -> N={wl.N}, H_128 (two launches)",
+                   "us_per_call_gpu": round(us, 2), "us_per_call_host_enqueue": round(host_us, 2)}
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_oracle_per_config(workloads, np, inputs):
+    """The oracle on every workload, with all host threads and with one:
+    rotate+quantize (elements/s) and the integer product + dequant (int
+    ops/s) on a sample of token rows against all N weight rows (weights
+    prepared untimed), the KV quantize + dequantize on a sample of head
+    rows; each with the full workload's time extrapolated from the sample
+    (labelled as such).  inputs: name -> (token rows x, prepared wq, sw),
+    the workload's own draws (the tiny layer is drawn here)."""
+    import oracle as orc
+    allt = orc.max_threads()
+    out = {"cpu_model": cpu_model(), "threads_all": allt, "configs": {}}
+    sample = {"tiny": (16, 16), "llama2_7b_up": (64, 8), "llama2_7b_down": (64, 8),
+              "llama2_70b_up": (64, 4), "llama2_70b_down": (64, 4)}
+    for name, (r_all, r_one) in sample.items():
+        wl = workloads.LINEAR[name]
+        if name in inputs:
+            x, wq, sw = inputs[name]
+        elif name == "tiny":
+            x, w, _ = workloads.linear_inputs(wl)
+            wq, sw = orc.prepare_weight(w, rotate=True)
+        else:
+            continue
+        entry = {}
+        for th, R in ((allt, r_all), (1, r_one)):
+            orc.set_threads(th)
+            t = time.perf_counter()
+            xq, sx = orc.quant_int4(x[:R], rotate=True, clip=1.0)
+            tq = time.perf_counter() - t
+            t = time.perf_counter()
+            orc.dequant(orc.gemm_i32(xq, wq), sx, sw)
+            tg = time.perf_counter() - t
+            entry[f"threads_{th}"] = {
+                "sample_rows": R,
+                "rotate_quant_elems_per_s": round(R * wl.K / tq, 1),
+                "gemm_dequant_ops_per_s": round(2 * R * wl.N * wl.K / tg, 1),
+                "extrapolated_full_layer_s": round((tq + tg) * wl.M / R, 2)}
+        out["configs"][name] = entry
+    wl = workloads.KV["kv4_70b"]
+    k, _ = workloads.kv_inputs(wl, B=1, S=256)
+    kx = k.reshape(-1, wl.D)
+    entry = {}
+    for th, R in ((allt, kx.shape[0]), (1, 2048)):
+        orc.set_threads(th)
+        t = time.perf_counter()
+        cq, cs, cz = orc.kv_quant(kx[:R], group=wl.group, rotate=True, clip=wl.clip)
+        tq = time.perf_counter() - t
+        t = time.perf_counter()
+        orc.kv_dequant(cq, cs, cz, group=wl.group, inverse_rotate=False)
+        td = time.perf_counter() - t
+        entry[f"threads_{th}"] = {
+            "sample_rows": R, "quant_elems_per_s": round(R * wl.D / tq, 1),
+            "dequant_elems_per_s": round(R * wl.D / td, 1),
+            "extrapolated_full_KV_s": round((tq + td) * 2 * wl.rows / R, 2)}
+    out["configs"]["kv4_70b"] = entry
+    orc.set_threads(allt)
+    return out
+
+
 def time_us(torch, stream, fn, iters=10):
     fn()
     torch.cuda.synchronize()
@@ -290,6 +455,8 @@ def main():
     ap.add_argument("--kv-iters", type=int, default=5)
     ap.add_argument("--no-next", action="store_true",
                     help="skip the fused-prologue and 8-bit legs")
+    ap.add_argument("--no-7b", action="store_true",
+                    help="skip the Llama-2-7B layer shapes and the tiny layer")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB once (a plain copy "
                          "kernel of known size, to scale hardware byte counters)")
@@ -467,6 +634,30 @@ def main():
                 "mfma_probe_TOPS": round(probe6_tops, 1),
                 "gemm_frac_of_probe": round(gemm_tops / probe6_tops, 4)}
 
+    # the rotations warm (the same input back to back) and cold (copies of
+    # the input totalling > 512 MB, twice the last-level cache, in turn)
+    for li, L in enumerate(layers):
+        wl = L["wl"]
+        rot = lambda xd=L["xd"], L=L: q.quarot_quant_int4_e3m2(xd, rotate=True, q6=L["x6"],
+                                                               scale=L["sx6"])
+        warm = event_times_us(torch, stream, [rot], 10)[0]
+        ncp = max(2, -(-(640 << 20) // (L["xd"].numel() * 2)))
+        xs = [L["xd"]] + [L["xd"].clone() for _ in range(ncp - 1)]
+        cold = event_times_us(torch, stream,
+                              [lambda xc=xc, L=L: q.quarot_quant_int4_e3m2(
+                                  xc, rotate=True, q6=L["x6"], scale=L["sx6"]) for xc in xs], 3)
+        del xs
+        hbm_us, _ = rotation_bounds(q, wl.M, wl.K, 6)
+        w_us = float(np.mean(warm))
+        c_us = float(np.mean([v for c in cold for v in c]))
+        kernels[wl.name]["rotate_quant_warm_us"] = round(w_us, 2)
+        kernels[wl.name]["rotate_quant_cold_us"] = round(c_us, 2)
+        kernels[wl.name]["rotate_quant_cold_frac_hbm"] = round(hbm_us / c_us, 4)
+    torch.cuda.empty_cache()
+
+    drawn_7b = {}
+    small = None if args.no_7b else bench_layers_7b(q, workloads, torch, np, dev, stream,
+                                                      max(args.steps, 10), keep=drawn_7b)
     kv = None if args.no_kv else bench_kv(q, workloads, torch, np, dev, stream, args.kv_iters)
     nxt = None if args.no_next else bench_next(q, torch, dev, stream, layers)
 
@@ -480,6 +671,7 @@ def main():
         del src, dst
 
     cpu = None
+    cpu_all = None
     if not args.no_cpu_baseline:
         import oracle as orc
         R = args.cpu_rows
@@ -493,7 +685,13 @@ def main():
         cpu = {"value": sample_ops / dt / 1e12, "unit": "TOP/s", "cores": orc.max_threads(),
                "kind": "oracle",
                "sample": f"first {R} of {layers[0]['wl'].M} token rows of each layer "
-                         f"(rotate+quantize+GEMM+dequant), {dt:.1f} s"}
+                         f"(rotate+quantize+GEMM+dequant), {dt:.1f} s",
+               "cpu_model": cpu_model()}
+        log("cpu oracle per workload (all threads and one)")
+        inputs = {L["wl"].name: (L["x"][:256], *prep) for L, prep in zip(layers, preps)}
+        for name, (x7, w7) in drawn_7b.items():
+            inputs[name] = (x7, *orc.prepare_weight(w7, rotate=True))
+        cpu_all = cpu_oracle_per_config(workloads, np, inputs)
 
     traffic = gemm_traffic("k_gemm_w4a4_e3m2")
     out = {
@@ -526,9 +724,11 @@ def main():
         "kernels": kernels,
         "peak_i8": peak_i8,
         "peak_fp6": peak_fp6,
+        "llama2_7b_and_tiny": small,
         "kv": kv,
         "next": nxt,
         "cpu_baseline": cpu,
+        "cpu_oracle_per_workload": cpu_all,
     }
     print(json.dumps(out), flush=True)
 

@@ -134,18 +134,36 @@ struct HmTable {
     }
 };
 
-// Signs as doubles for the large-m kernel, which forms CB output columns
-// per pass: blk[p][r][q] = H[r][p*CB + q], so one pass reads the CB signs of
-// each input r as one contiguous scalar load.
-template <int M, int CB>
-struct HmColumnBlocks {
-    double blk[M / CB][M][CB];
-    constexpr HmColumnBlocks() : blk()
+// H_m as the B operand of v_mfma_i32_16x16x64_i8 for the large-m kernels,
+// which form the m-factor u = t . H_m on the int8 matrix cores: column tile
+// ct (16 columns), k-block kb (64 inputs), lane l holds 16 bytes,
+// byte e = H[kb*64 + (l/16)*16 + e][ct*16 + l%16] as int8 (+1 / -1), 0
+// past the edge.  The A operand (digits of t) uses the same lane / byte -> k
+// mapping, so the hardware's own k order within an instruction does not
+// matter.  Stored as dwords, 4 per lane.
+template <int M>
+struct HmMfmaB {
+    static constexpr int CT = (M + 15) / 16;
+    static constexpr int KB = (M + 63) / 64;
+    uint32_t w[CT][KB][64][4];
+    constexpr HmMfmaB() : w()
     {
         const Gs43Rows g{};
-        for (int r = 0; r < M; ++r)
-            for (int s = 0; s < M; ++s)
-                blk[s / CB][r][s % CB] = (double)(M == 172 ? gs172_sign(g, r, s) : hm_sign(M, r, s));
+        for (int ct = 0; ct < CT; ++ct)
+            for (int kb = 0; kb < KB; ++kb)
+                for (int l = 0; l < 64; ++l)
+                    for (int q = 0; q < 4; ++q) {
+                        uint32_t word = 0;
+                        for (int j = 0; j < 4; ++j) {
+                            const int r = kb * 64 + (l / 16) * 16 + 4 * q + j;
+                            const int c = ct * 16 + l % 16;
+                            int v = 0;
+                            if (r < M && c < M)
+                                v = M == 172 ? gs172_sign(g, r, c) : hm_sign(M, r, c);
+                            word |= (uint32_t)(v & 0xFF) << (8 * j);
+                        }
+                        w[ct][kb][l][q] = word;
+                    }
     }
 };
 

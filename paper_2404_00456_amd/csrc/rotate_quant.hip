@@ -31,9 +31,8 @@
 
 namespace quarot {
 
-constexpr int kLargeCB = 4;  // output columns per pass in k_rot_largem
-__constant__ HmColumnBlocks<108, kLargeCB> c_hm108 = HmColumnBlocks<108, kLargeCB>();
-__constant__ HmColumnBlocks<172, kLargeCB> c_hm172 = HmColumnBlocks<172, kLargeCB>();
+__constant__ HmMfmaB<108> c_hmb108 = HmMfmaB<108>();
+__constant__ HmMfmaB<172> c_hmb172 = HmMfmaB<172>();
 
 namespace {
 
@@ -778,92 +777,208 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
 // ------------------------------------------------------- m = 108, 172 -----
 
 template <int M>
-__device__ __forceinline__ const double *hm_blocks();
+__device__ __forceinline__ const uint4 *hm_mfma_b();
 template <>
-__device__ __forceinline__ const double *hm_blocks<108>()
+__device__ __forceinline__ const uint4 *hm_mfma_b<108>()
 {
-    return &c_hm108.blk[0][0][0];
+    return reinterpret_cast<const uint4 *>(&c_hmb108.w[0][0][0][0]);
 }
 template <>
-__device__ __forceinline__ const double *hm_blocks<172>()
+__device__ __forceinline__ const uint4 *hm_mfma_b<172>()
 {
-    return &c_hm172.blk[0][0][0];
+    return reinterpret_cast<const uint4 *>(&c_hmb172.w[0][0][0][0]);
 }
 
-// One row per block; thread g < A = n/M owns group g (placed at lane
-// position pos, see lane_pos).  The m-factor runs CB output columns per
-// pass, each an fp64 sum of +-t (exact, see mfactor_exact) rounded once.
-// The rotated row (before the scale) is staged in LDS as A rows of M+1
-// floats, with the lanes' sign sigma removed.
-template <int M, int W, int EPI, int PRO = PRO_PLAIN>
-__global__ __launch_bounds__(64 * W) void k_rot_largem(RotArgs a)
+// The exact integer N = t * 2^24 of an fp16 value t (bits h; |N| < 2^40 for
+// finite t) as 7 base-64 digits, N = sum_i d_i 64^i: d_0 .. d_5 in [0, 63]
+// (bits 6i .. 6i+5 of N in two's complement) and the signed top digit
+// d_6 = N >> 36 in [-16, 15].  Each fits an int8 byte.
+__device__ __forceinline__ void f16_digits(uint32_t h, uint32_t d[7])
 {
-    constexpr int CB = kLargeCB;
-    static_assert(M % CB == 0 && M % 4 == 0, "column blocking");
+    const uint32_t e = (h >> 10) & 31u;
+    const uint32_t mant = (h & 1023u) | (e ? 1024u : 0u);
+    const uint32_t sh = e ? e - 1u : 0u;
+    const int32_t sm = (h & 0x8000u) ? -(int32_t)mant : (int32_t)mant;
+    const int64_t N = (int64_t)sm << sh;
+    const uint32_t lo = (uint32_t)N, hi = (uint32_t)((uint64_t)N >> 32);
+    d[0] = lo & 63u;
+    d[1] = (lo >> 6) & 63u;
+    d[2] = (lo >> 12) & 63u;
+    d[3] = (lo >> 18) & 63u;
+    d[4] = (lo >> 24) & 63u;
+    d[5] = ((lo >> 30) | (hi << 2)) & 63u;
+    d[6] = (uint32_t)((int32_t)hi >> 4) & 0xFFu;
+}
+
+// Four fp16 inputs (raw bits) at element offset off of the row: the plain
+// row, or RN16(silu(gate) up) for the SwiGLU prologue.
+template <int PRO>
+__device__ __forceinline__ uint2 load_bits4(const RotArgs &a, int64_t off)
+{
+    if constexpr (PRO == PRO_PLAIN) {
+        return *reinterpret_cast<const uint2 *>(a.x + off);
+    } else {
+        float v[4];
+        load_row4<PRO>(a, off, v);
+        return make_uint2((uint32_t)f2h(v[0]) | ((uint32_t)f2h(v[1]) << 16),
+                          (uint32_t)f2h(v[2]) | ((uint32_t)f2h(v[3]) << 16));
+    }
+}
+
+// One row per block of four waves; the row's A = n / M groups of M
+// elements (element i = g M + b).
+//
+// m-factor on the int8 matrix cores.  It is a contraction, U = T . H_M
+// with T [A, M] the groups: every fp16 input is an integer multiple of
+// 2^-24, so N = t 2^24 is an integer below 2^40, and its base-64 digits
+// (f16_digits) are int8 operands of v_mfma_i32_16x16x64_i8 against the +-1
+// entries of H_M.  Digits 2p and 2p+1 accumulate into one int32 C_p (the
+// odd digit against 64 H_M, still int8): |C_p| <= M * 63 * 65 < 2^21.  Then
+// sum_b H[b][b'] N_b = sum_p C_p 2^(12 p), an integer below 2^48, is formed
+// exactly in binary64 and u = RN32(that * 2^-24): the exact sum rounded
+// once, as the definition asks, in whatever order the hardware adds.
+//
+// A wave takes row tiles of 16 groups (groups past A are zero); the MFMA
+// output puts groups 4 (l/16) + r (register r) and column ct*16 + l%16 in
+// lane l, so Walsh-Hadamard bits 0-1 of the group index are butterflies
+// between registers and bits 2-3 between lanes l and l ^ 16, l ^ 32; u is
+// then staged in LDS as A rows of M + 1 floats, where bits 4.. (across
+// tiles) run as butterflies on the staged row.  H_M's operand tiles sit in
+// LDS in front of the row.
+template <int M, int EPI, int PRO = PRO_PLAIN>
+__global__ __launch_bounds__(256, 2) void k_rot_largem(RotArgs a)
+{
+    constexpr int W = 4;
+    constexpr int CT = HmMfmaB<M>::CT, KB = HmMfmaB<M>::KB;
+    constexpr int CTP = 4;  // column tiles per pass (accumulator registers)
     constexpr int LD = M + 1;
-    extern __shared__ float rowbuf[];
+    static_assert(M % 4 == 0, "4-element loads");
+    typedef int v4i __attribute__((ext_vector_type(4)));
+    extern __shared__ __align__(16) uint8_t lds_raw[];
+    uint4 *hb = reinterpret_cast<uint4 *>(lds_raw);                 // [CT][KB][64]
+    float *rowbuf = reinterpret_cast<float *>(lds_raw + CT * KB * 1024);
     __shared__ float red[W];
-    const int tid = threadIdx.x, lane = tid & 63;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n = a.n, A = n / M;
     const int k = 31 - __clz(A);
     const int64_t row = blockIdx.x;
-    const int pos = lane_pos(lane);
-    const int g = (tid & ~63) | pos;  // this thread's group
-    const bool act = g < A;
-    const double *hb = hm_blocks<M>();
 
-    float t[M];
-    if (act) {
-        const int64_t xg = row * n + (int64_t)g * M;
-#pragma unroll
-        for (int p = 0; p < M / 4; ++p)
-            load_row4<PRO>(a, xg + 4 * p, &t[4 * p]);
-    } else {
-#pragma unroll
-        for (int b = 0; b < M; ++b)
-            t[b] = 0.0f;
-    }
-    const int klane = k < 6 ? k : 6;
-    // rolled: one pass is CB * M fma; unrolling all M/CB passes would not
-    // fit the instruction cache
-#pragma unroll 1
-    for (int cb = 0; cb < M / CB; ++cb) {
-        const double *sg = hb + cb * M * CB;  // signs [b][q] of columns cb*CB + q
-        double acc[CB];
-#pragma unroll
-        for (int q = 0; q < CB; ++q)
-            acc[q] = 0.0;
-#pragma unroll
-        for (int b = 0; b < M; ++b) {
-            const double tb = t[b];
-#pragma unroll
-            for (int q = 0; q < CB; ++q)
-                acc[q] = __builtin_fma(sg[b * CB + q], tb, acc[q]);  // exactly acc +- t[b]
-        }
-        float u[CB];
-#pragma unroll
-        for (int q = 0; q < CB; ++q)
-            u[q] = (float)acc[q];
-        // group bits below min(k, 6) across lanes; the count is uniform, so
-        // every lane of the wave takes the same branches
-        float sigma = 1.0f;
-        switch (klane) {
-        case 1: sigma = lane_stages<1, CB>(u, lane, pos & 1); break;
-        case 2: sigma = lane_stages<2, CB>(u, lane, pos & 3); break;
-        case 3: sigma = lane_stages<3, CB>(u, lane, pos & 7); break;
-        case 4: sigma = lane_stages<4, CB>(u, lane, pos & 15); break;
-        case 5: sigma = lane_stages<5, CB>(u, lane, pos & 31); break;
-        case 6: sigma = lane_stages<6, CB>(u, lane, pos); break;
-        default: break;
-        }
-        if (act)
-#pragma unroll
-            for (int q = 0; q < CB; ++q)
-                rowbuf[g * LD + cb * CB + q] = u[q] * sigma;
+    {
+        const uint4 *src = hm_mfma_b<M>();
+        for (int i = tid; i < CT * KB * 64; i += 64 * W)
+            hb[i] = src[i];
     }
     __syncthreads();
-    // group bits 6.. (across waves): butterflies on the staged row
-    for (int j = 6; j < k; ++j) {
+
+    const int RT = A >= 16 ? A / 16 : 1;  // row tiles of 16 groups
+    const int kreg = k < 4 ? k : 4;       // group bits done in registers / lanes
+    for (int rt = wave; rt < RT; rt += W) {
+        // A operands: digit d of the 16 inputs b = kb*64 + (lane/16)*16 + e
+        // of group rt*16 + lane%16, byte e (zeros past the row or the group)
+        const int g = rt * 16 + (lane & 15);
+        v4i dig[KB][7];
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+            uint32_t w[7][4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int b = kb * 64 + (lane >> 4) * 16 + 4 * q;
+                uint2 raw = make_uint2(0, 0);
+                if (g < A && b < M)
+                    raw = load_bits4<PRO>(a, row * n + (int64_t)g * M + b);
+                uint32_t d0[7], d1[7], d2[7], d3[7];
+                f16_digits(raw.x & 0xFFFFu, d0);
+                f16_digits(raw.x >> 16, d1);
+                f16_digits(raw.y & 0xFFFFu, d2);
+                f16_digits(raw.y >> 16, d3);
+#pragma unroll
+                for (int i = 0; i < 7; ++i)
+                    w[i][q] = d0[i] | (d1[i] << 8) | (d2[i] << 16) | (d3[i] << 24);
+            }
+#pragma unroll
+            for (int i = 0; i < 7; ++i)
+                dig[kb][i] = v4i{(int)w[i][0], (int)w[i][1], (int)w[i][2], (int)w[i][3]};
+        }
+#pragma unroll
+        for (int c0 = 0; c0 < CT; c0 += CTP) {
+            v4i acc[CTP][4];
+#pragma unroll
+            for (int c = 0; c < CTP; ++c)
+#pragma unroll
+                for (int p = 0; p < 4; ++p)
+                    acc[c][p] = v4i{0, 0, 0, 0};
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int c = 0; c < CTP; ++c) {
+                    if (c0 + c >= CT)
+                        continue;
+                    const uint4 hv = hb[((c0 + c) * KB + kb) * 64 + lane];
+                    // 64 H: each byte +-1 -> +-64 (bytes hold -1 as 0xFF, so
+                    // shifting the dword left by 6 and keeping bits 6-7 of
+                    // every byte gives 0xC0 / 0x40 with no carry between bytes)
+                    const v4i h1 = v4i{(int)hv.x, (int)hv.y, (int)hv.z, (int)hv.w};
+                    const v4i h64 = v4i{(int)((hv.x << 6) & 0xC0C0C0C0u), (int)((hv.y << 6) & 0xC0C0C0C0u),
+                                        (int)((hv.z << 6) & 0xC0C0C0C0u), (int)((hv.w << 6) & 0xC0C0C0C0u)};
+#pragma unroll
+                    for (int i = 0; i < 7; ++i)
+                        acc[c][i >> 1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
+                            dig[kb][i], (i & 1) ? h64 : h1, acc[c][i >> 1], 0, 0, 0);
+                }
+#pragma unroll
+            for (int c = 0; c < CTP; ++c) {
+                if (c0 + c >= CT)
+                    continue;
+                float u[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    double x = (double)acc[c][3][r];
+                    x = __builtin_fma(x, 4096.0, (double)acc[c][2][r]);
+                    x = __builtin_fma(x, 4096.0, (double)acc[c][1][r]);
+                    x = __builtin_fma(x, 4096.0, (double)acc[c][0][r]);
+                    u[r] = (float)(x * 0x1p-24);  // exact scaling, one rounding
+                }
+                // Walsh-Hadamard bits 0..kreg-1 of the group index, bit 0
+                // first: registers (bits 0, 1), then lanes (bits 2, 3)
+                if (kreg > 0) {
+                    const float p0 = u[0], p2 = u[2];
+                    u[0] = p0 + u[1];
+                    u[1] = p0 - u[1];
+                    u[2] = p2 + u[3];
+                    u[3] = p2 - u[3];
+                }
+                if (kreg > 1) {
+                    const float p0 = u[0], p1 = u[1];
+                    u[0] = p0 + u[2];
+                    u[1] = p1 + u[3];
+                    u[2] = p0 - u[2];
+                    u[3] = p1 - u[3];
+                }
+#pragma unroll
+                for (int j = 2; j < 4; ++j) {
+                    if (kreg > j) {
+                        const int mask = 16 << (j - 2);
+                        const bool hi = (lane & mask) != 0;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const float o = __shfl_xor(u[r], mask);
+                            u[r] = hi ? o - u[r] : u[r] + o;
+                        }
+                    }
+                }
+                const int col = (c0 + c) * 16 + (lane & 15);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int gg = rt * 16 + 4 * (lane >> 4) + r;
+                    if (gg < A && col < M)
+                        rowbuf[gg * LD + col] = u[r];
+                }
+            }
+        }
+    }
+    __syncthreads();
+    // group bits 4.. (across row tiles): butterflies on the staged row
+    for (int j = 4; j < k; ++j) {
         const int h = 1 << j;
         const int total = (A / 2) * M;
         for (int idx = tid; idx < total; idx += 64 * W) {
@@ -1212,12 +1327,17 @@ hipError_t go_smallm(const RotArgs &a, hipStream_t s)
     return hipGetLastError();
 }
 
-template <int M, int W, int EPI, int PRO>
+template <int M, int EPI, int PRO>
 hipError_t go_largem(const RotArgs &a, hipStream_t s)
 {
-    const size_t lds = (size_t)(a.n / M) * (M + 1) * sizeof(float);
-    hipLaunchKernelGGL((k_rot_largem<M, W, EPI, PRO>), dim3((unsigned)a.rows), dim3(64 * W), lds,
-                       s, a);
+    // H_M's operand tiles, then the staged row
+    const size_t lds = (size_t)HmMfmaB<M>::CT * HmMfmaB<M>::KB * 1024 +
+                       (size_t)(a.n / M) * (M + 1) * sizeof(float);
+    const void *fn = (const void *)k_rot_largem<M, EPI, PRO>;
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL((k_rot_largem<M, EPI, PRO>), dim3((unsigned)a.rows), dim3(256), lds, s, a);
     return hipGetLastError();
 }
 
@@ -1300,9 +1420,8 @@ hipError_t dispatch_rotated(const RotArgs &a, int k, int m, hipStream_t s)
         case 20: return dispatch_smallm_e3m2<20, PRO>(a, k, s);
         case 28: return dispatch_smallm_e3m2<28, PRO>(a, k, s);
         case 108:
-            return (k <= 6) ? go_largem<108, 1, EPI_E3M2, PRO>(a, s)
-                            : go_largem<108, 2, EPI_E3M2, PRO>(a, s);
-        case 172: return go_largem<172, 1, EPI_E3M2, PRO>(a, s);
+            return go_largem<108, EPI_E3M2, PRO>(a, s);
+        case 172: return go_largem<172, EPI_E3M2, PRO>(a, s);
         }
         return hipErrorInvalidValue;
     } else {
@@ -1311,8 +1430,8 @@ hipError_t dispatch_rotated(const RotArgs &a, int k, int m, hipStream_t s)
         case 12: return dispatch_smallm<12, 8, EPI, PRO>(a, k, s);
         case 20: return dispatch_smallm<20, 4, EPI, PRO>(a, k, s);
         case 28: return dispatch_smallm<28, 4, EPI, PRO>(a, k, s);
-        case 108: return (k <= 6) ? go_largem<108, 1, EPI, PRO>(a, s) : go_largem<108, 2, EPI, PRO>(a, s);
-        case 172: return go_largem<172, 1, EPI, PRO>(a, s);
+        case 108: return go_largem<108, EPI, PRO>(a, s);
+        case 172: return go_largem<172, EPI, PRO>(a, s);
         }
     }
     return hipErrorInvalidValue;
