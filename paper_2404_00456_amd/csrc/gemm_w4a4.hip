@@ -193,24 +193,34 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_k64(GemmArgs a)
 //    which makes the 16-byte reads of 8 consecutive rows hit 8 distinct bank
 //    groups.
 constexpr int S = 3;  // LDS ring stages
-// Scales of a tile (256 sx then 256 sw, fp16) live in LDS after the ring,
-// double buffered by tile parity.
-constexpr int SCALE_BYTES = 2 * (BM + BN) * 2;
+// Block tiles: TBM (m) x BN (n), TBM = 256 (eight waves) or 128 (four
+// waves, for grids too small to give every compute unit a 256 x 256 tile);
+// every wave computes 128 (m) x 64 (n).
+template <int TBM>
+struct Tile {
+    static constexpr int NW = TBM / 128 * (BN / WN);  // waves
+    static constexpr int THREADS = 64 * NW;
+    static constexpr int HEADS = (TBM + BN) * 64;     // e3m2 stage: offset of the tails
+    // Scales of a tile (TBM sx then BN sw, fp16) live in LDS after the ring,
+    // double buffered by tile parity.
+    static constexpr int SCALE_BYTES = 2 * (TBM + BN) * 2;
+};
 
 // Per code format: bytes per row per k-step, stage and ring sizes, DMAs per
-// wave per k-step.  4- and 8-bit codes: 64 bytes per row (32 KB stages).
-// e3m2 codes (BITS = 6): 96 bytes per row; a stage holds the 64-byte heads
-// of all 512 rows (X then W, laid out as the 4-bit stages), then their
-// 32-byte tails (X then W).
-template <int BITS>
+// wave per k-step.  4- and 8-bit codes: 64 bytes per row (32 KB stages for
+// 256 x 256 tiles).  e3m2 codes (BITS = 6): 96 bytes per row; a stage holds
+// the 64-byte heads of all TBM + BN rows (X then W, laid out as the 4-bit
+// stages), then their 32-byte tails (X then W).  DMA i < HPW of a wave moves
+// a 1 KB chunk of heads (16 rows), the others a chunk of tails (32 rows).
+template <int BITS, int TBM = 256>
 struct Ring {
     static constexpr int KB = BITS == 6 ? 96 : 64;
-    static constexpr int STAGE = (BM + BN) * KB;
+    static constexpr int STAGE = (TBM + BN) * KB;
     static constexpr int BYTES = S * STAGE;
-    static constexpr int DPW = STAGE / 1024 / (THREADS / 64);
-    static constexpr int LDS = BYTES + SCALE_BYTES;
+    static constexpr int HPW = (TBM + BN) * 64 / 1024 / Tile<TBM>::NW;
+    static constexpr int DPW = STAGE / 1024 / Tile<TBM>::NW;
+    static constexpr int LDS = BYTES + Tile<TBM>::SCALE_BYTES;
 };
-constexpr int HEADS = (BM + BN) * 64;  // e3m2 stage: offset of the tails
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) uint64_t lds_u64;
@@ -274,20 +284,26 @@ __device__ __forceinline__ int acc_int(T v)
 // (half the MFMA count of the 4-bit path, no widening), binary32
 // accumulators holding acc exactly.  Lane group g of an operand takes unit
 // g (its 16-byte head and 8-byte tail), the same k in A and B.
-template <int BITS>
+template <int BITS, int TBM = 256>
 __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
 {
     static_assert(BITS == 4 || BITS == 6 || BITS == 8, "int4, e3m2 or int8 codes");
-    typedef Ring<BITS> R;
+    static_assert(TBM == 256 || TBM == 128, "block tile 256 or 128 rows");
+    typedef Ring<BITS, TBM> R;
+    typedef Tile<TBM> TL;
     constexpr int KB = R::KB;
     constexpr int DPW = R::DPW;
+    constexpr int HPW = R::HPW;
+    constexpr int NW = TL::NW;
+    constexpr int HEADS = TL::HEADS;
+    constexpr int SCALE_BYTES = TL::SCALE_BYTES;
     constexpr int RING_STAGE = R::STAGE;
     constexpr int RING_BYTES = R::BYTES;
     typedef typename AccOf<BITS>::type Acc;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 2, wn = wave & 3;
     const int M = a.M, N = a.N, K = a.K;
-    const int TM = (M + BM - 1) / BM, TN = (N + BN - 1) / BN;
+    const int TM = (M + TBM - 1) / TBM, TN = (N + BN - 1) / BN;
     const int T = TM * TN;
     const int G = gridDim.x, b = blockIdx.x;
     const int64_t ldk = BITS == 4 ? K / 2 : K;  // row pitch (4- and 8-bit codes)
@@ -311,27 +327,34 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
         const int first = g * GM;
         const int gm = min(TM - first, GM);
         const int r = t - g * gsize;
-        m0 = (first + r % gm) * BM;
+        m0 = (first + r % gm) * TBM;
         n0 = (r / gm) * BN;
     };
 
-    // DMA sources: instruction i of wave w moves 16 rows of X (i < 2) or W
-    // (i >= 2): rows 16*(w + 8*(i&1)) + lane/4 land at unit lane%4 of their
-    // LDS row, so they fetch global unit (lane%4) ^ swizzle(row)
-    //
-    // e3m2 operands (tiled layout, see k_pack_e3m2): the same instructions
-    // i < 4 move heads, 64 bytes per row, already swizzled in memory, so
-    // lane l fetches unit l % 4 of its row; i = 4 (X) and 5 (W) move tails:
-    // wave w, rows 32 w + lane/2, 16 bytes each.  Every instruction reads
-    // 1 KB of consecutive bytes (rows past the matrix edge are clamped).
+    // DMA sources.  Head DMA i < HPW of wave w moves chunk c = w + NW i of
+    // the stage's heads: rows 16 c .. 16 c + 15 of the TBM X rows followed by
+    // the BN W rows (the first two of every wave are X chunks), row
+    // 16 c + lane/4 at unit lane%4 of its LDS row, so that it fetches global
+    // unit (lane%4) ^ swizzle(row).  e3m2 operands (tiled layout, see
+    // k_pack_e3m2): heads are already swizzled in memory, so lane l fetches
+    // unit l % 4 of its row; the remaining DMAs i = HPW + j move tail chunk
+    // c = w + NW j: rows 32 c + lane/2, 16 bytes each (the first of every
+    // wave is an X chunk).  Every instruction reads 1 KB of consecutive bytes
+    // (rows past the matrix edge are clamped).
     const int rsub = lane >> 2;
     const int cunit = (lane & 3) ^ ((lane >> 3) & 3);
-    static_assert(DPW == (BITS == 6 ? 6 : 4), "two X and two W chunks per wave (+ tails)");
+    static_assert(DPW == (BITS == 6 ? HPW + HPW / 2 : HPW), "heads (+ tails) per wave");
+    static_assert(TBM / 16 == 2 * NW && TBM / 32 == NW, "X chunks come first in every wave");
+    auto is_x = [&](int i) { return i < 2 || i == HPW; };  // compile-time after unrolling
+    auto chunk_row = [&](int i) -> int {  // first row of DMA i's chunk in its operand
+        const int c = wave + NW * (i < HPW ? i : i - HPW);
+        const int r = i < HPW ? 16 * c : 32 * c;
+        return is_x(i) ? r : r - TBM;
+    };
     int dst[DPW];
 #pragma unroll
     for (int i = 0; i < DPW; ++i)
-        dst[i] = i < 4 ? (i < 2 ? 0 : BM * BKB) + (wave + 8 * (i & 1)) * 1024
-                       : HEADS + (i == 4 ? 0 : BM * 32) + wave * 1024;
+        dst[i] = i < HPW ? (wave + NW * i) * 1024 : HEADS + (wave + NW * (i - HPW)) * 1024;
     // e3m2 DMAs in the SGPR-base form.  voff6: lane offset of DMA i inside
     // the tile's run of heads (or tails), rows past the matrix edge clamped;
     // base6: the run's wave-uniform start for k-step sk.
@@ -339,25 +362,25 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     // 4- and 8-bit codes (row-major, pitch ldk) use the same form: lane
     // offset r * ldk + unit (rows clamped), base x + m0 * ldk + sk * 64.
     auto voff6 = [&](int i, int m0, int n0) -> uint32_t {
-        const bool xop = i < 2 || i == 4;
+        const bool xop = is_x(i);
         const int lim = (xop ? M - m0 : N - n0) - 1;
-        if (i < 4) {
-            const int r = 16 * (wave + 8 * (i & 1)) + rsub;
+        if (i < HPW) {
+            const int r = chunk_row(i) + rsub;
             if constexpr (BITS != 6)
                 return (uint32_t)(min(r, lim) * (int)ldk + cunit * 16);
             return (uint32_t)(min(r, lim) * 64 + (lane & 3) * 16);
         }
-        const int r = 32 * wave + (lane >> 1);
+        const int r = chunk_row(i) + (lane >> 1);
         return (uint32_t)(min(r, lim) * 32 + (lane & 1) * 16);
     };
     auto base6 = [&](int i, int m0, int n0, int sk) -> const uint8_t * {
-        const bool xop = i < 2 || i == 4;
+        const bool xop = is_x(i);
         const int64_t org = xop ? m0 : n0;
         if constexpr (BITS != 6)
             return (xop ? a.xq : a.wq) + org * ldk + (int64_t)sk * BKB;
         const int64_t rows = xop ? M : N;
         const uint8_t *blk = (xop ? a.xq : a.wq) + (int64_t)sk * (rows * 96);
-        return i < 4 ? blk + org * 64 : blk + rows * 64 + org * 32;
+        return i < HPW ? blk + org * 64 : blk + rows * 64 + org * 32;
     };
     const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void *)lds;
     int dsts[DPW];  // LDS targets, wave-uniform (scalar registers)
@@ -375,31 +398,35 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     // k-block per step: scalar adds instead of per-step products
     const uint8_t *bcur[DPW];
     auto stride6 = [&](int i) -> int64_t {
-        return BITS == 6 ? (int64_t)(i < 2 || i == 4 ? M : N) * 96 : (int64_t)BKB;
+        return BITS == 6 ? (int64_t)(is_x(i) ? M : N) * 96 : (int64_t)BKB;
     };
 
     const int orow = lane & 15;
     const int ounit = ((lane >> 4) ^ ((orow >> 1) & 3)) << 4;
     const int brow = (wm * 128 + orow) * BKB + ounit;        // X slice rows (B operand)
-    const int arow = (BM + wn * WN + orow) * BKB + ounit;    // W slice rows (A operand)
+    const int arow = (TBM + wn * WN + orow) * BKB + ounit;   // W slice rows (A operand)
     // e3m2 tails: the 8 bytes of unit g of row r sit at slot g ^ ((r >> 2) & 3)
     // of the row's 32-byte tail (16-row slices start at multiples of 16)
     const int toff = 8 * ((lane >> 4) ^ ((orow >> 2) & 3));
     const int btail = HEADS + (wm * 128 + orow) * 32 + toff;
-    const int atail = HEADS + BM * 32 + (wn * WN + orow) * 32 + toff;
+    const int atail = HEADS + TBM * 32 + (wn * WN + orow) * 32 + toff;
 
     // Tiles wholly inside the matrices (and no int32 output) take the fast
-    // epilogue, with the scales staged in LDS: one 4-byte DMA per wave
-    // (waves w and w+4 fetch the same quarter: sx rows 0-127, 128-255, sw
-    // 0-127, 128-255), issued ahead of the tile's operand DMAs so that the
-    // k-loop's waits cover it.  Scale loads in the epilogue itself would
-    // wait for the next tile's operand DMAs in flight (vmcnt is in order).
+    // epilogue, with the scales staged in LDS: one 4-byte DMA per wave, of
+    // one 256-byte part (TBM / 128 parts of sx, then two of sw; with eight
+    // waves, waves w and w + 4 fetch the same part, with four the fourth
+    // fetches the first part again), issued ahead of the tile's operand DMAs
+    // so that the k-loop's waits cover it.  Scale loads in the epilogue
+    // itself would wait for the next tile's operand DMAs in flight (vmcnt is
+    // in order).
+    constexpr int XPARTS = TBM / 128, PARTS = XPARTS + 2;
     auto fast_tile = [&](int m0_, int n0_) {
-        return m0_ + BM <= M && n0_ + BN <= N && (N & 3) == 0 && a.acc == nullptr;
+        return m0_ + TBM <= M && n0_ + BN <= N && (N & 3) == 0 && a.acc == nullptr;
     };
     auto scale_dma = [&](int m0_, int n0_, int buf) {
-        const int part = wave & 3;
-        const uint16_t *gs = (part < 2 ? a.sx + m0_ + 128 * part : a.sw + n0_ + 128 * (part - 2));
+        const int part = wave % PARTS;
+        const uint16_t *gs = (part < XPARTS ? a.sx + m0_ + 128 * part
+                                            : a.sw + n0_ + 128 * (part - XPARTS));
         dma4(gs + 2 * lane,
              __builtin_amdgcn_readfirstlane(lds_base + RING_BYTES + buf * (SCALE_BYTES / 2) +
                                             part * 256));
@@ -665,7 +692,7 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
             // without the shift.
             const uint8_t *sc = lds + RING_BYTES + (it & 1) * (SCALE_BYTES / 2);
             const uint16_t *lsx = reinterpret_cast<const uint16_t *>(sc);
-            const uint16_t *lsw = lsx + BM;
+            const uint16_t *lsw = lsx + TBM;
             float sxs[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j)
@@ -760,22 +787,42 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));  // no DMA may outlive the block's LDS
 }
 
-__global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4(GemmArgs a)
+__global__ __launch_bounds__(Tile<256>::THREADS, 1) void k_gemm_w4a4(GemmArgs a)
 {
     extern __shared__ __align__(16) uint8_t lds[];
     gemm_main<4>(a, lds);
 }
 
-__global__ __launch_bounds__(THREADS, 1) void k_gemm_w8a8(GemmArgs a)
+__global__ __launch_bounds__(Tile<256>::THREADS, 1) void k_gemm_w8a8(GemmArgs a)
 {
     extern __shared__ __align__(16) uint8_t lds[];
     gemm_main<8>(a, lds);
 }
 
-__global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_e3m2(GemmArgs a)
+__global__ __launch_bounds__(Tile<256>::THREADS, 1) void k_gemm_w4a4_e3m2(GemmArgs a)
 {
     extern __shared__ __align__(16) uint8_t lds[];
     gemm_main<6>(a, lds);
+}
+
+// 128 x 256 block tiles (four waves): for grids with too few 256 x 256
+// tiles to keep every compute unit busy.
+__global__ __launch_bounds__(Tile<128>::THREADS, 1) void k_gemm_w4a4_m128(GemmArgs a)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    gemm_main<4, 128>(a, lds);
+}
+
+__global__ __launch_bounds__(Tile<128>::THREADS, 1) void k_gemm_w8a8_m128(GemmArgs a)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    gemm_main<8, 128>(a, lds);
+}
+
+__global__ __launch_bounds__(Tile<128>::THREADS, 1) void k_gemm_w4a4_e3m2_m128(GemmArgs a)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    gemm_main<6, 128>(a, lds);
 }
 
 // int4 codes (two per byte, low nibble first) -> the tiled e3m2 layout.
@@ -813,43 +860,65 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s, int bits)
 {
     if (a.M == 0 || a.N == 0)
         return hipSuccess;
-    const int TM = (a.M + BM - 1) / BM, TN = (a.N + BN - 1) / BN;
     const bool main = bits != 4 || (a.K % 128) == 0;
     const int ksteps = bits == 8 ? a.K / 64 : a.K / 128;
-    const void *fn = bits == 8   ? (const void *)k_gemm_w8a8
-                     : bits == 6 ? (const void *)k_gemm_w4a4_e3m2
-                     : main      ? (const void *)k_gemm_w4a4
-                                 : (const void *)k_gemm_w4a4_k64;
-    const int lds_bytes = bits == 6 ? Ring<6>::LDS : main ? Ring<4>::LDS : LDS_BYTES;
+    if (!main) {
+        const int TM = (a.M + BM - 1) / BM, TN = (a.N + BN - 1) / BN;
+        hipError_t e = hipFuncSetAttribute((const void *)k_gemm_w4a4_k64,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+        if (e != hipSuccess)
+            return e;
+        hipLaunchKernelGGL(k_gemm_w4a4_k64, dim3((unsigned)(TM * TN)), dim3(THREADS), LDS_BYTES,
+                           s, a);
+        return hipGetLastError();
+    }
+    // persistent: one block per CU (256 on MI355X), or fewer for small
+    // problems; the LDS ring allows one resident block per CU.  With fewer
+    // than S k-steps, one tile per block (see the kernel).
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+        cus = 256;
+    // 128-row block tiles when that takes less time over the CUs: with one
+    // wave per SIMD a 128 x 256 tile takes about 0.9 of a 256 x 256 tile's
+    // time (measured on the 7B down-projection shape: 74.6 against 81.8 us
+    // for one round each), so only grids that leave CUs idle gain (2048 x
+    // 4096 outputs: 128 large tiles for 256 CUs), not the 16384-token ones.
+    const int TN = (a.N + BN - 1) / BN;
+    const int64_t t256 = (int64_t)((a.M + 255) / 256) * TN, t128 = (int64_t)((a.M + 127) / 128) * TN;
+    const int64_t r256 = (t256 + cus - 1) / cus, r128 = (t128 + cus - 1) / cus;
+    const bool m128 = ksteps >= S && a.M > 128 && r128 * 90 < r256 * 100;
+    const int64_t tiles = m128 ? t128 : t256;
+    int grid = (int)((tiles < cus || ksteps < S) ? tiles : cus);
+    if (grid >= 8 && tiles % 8 == 0)
+        grid -= grid % 8;
+    const void *fn;
+    int lds_bytes, threads;
+    if (m128) {
+        fn = bits == 8 ? (const void *)k_gemm_w8a8_m128
+             : bits == 6 ? (const void *)k_gemm_w4a4_e3m2_m128
+                         : (const void *)k_gemm_w4a4_m128;
+        lds_bytes = bits == 6 ? Ring<6, 128>::LDS : Ring<4, 128>::LDS;
+        threads = Tile<128>::THREADS;
+    } else {
+        fn = bits == 8 ? (const void *)k_gemm_w8a8
+             : bits == 6 ? (const void *)k_gemm_w4a4_e3m2
+                         : (const void *)k_gemm_w4a4;
+        lds_bytes = bits == 6 ? Ring<6>::LDS : Ring<4>::LDS;
+        threads = Tile<256>::THREADS;
+    }
     // more than 64 KB of dynamic LDS: raise the kernel's limit (per call, so
     // that every device the caller uses gets it; the call is host-side only)
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
     if (e != hipSuccess)
         return e;
-    if (main) {
-        // persistent: one block per CU (256 on MI355X), or fewer for small
-        // problems; the LDS ring allows one resident block per CU.  With
-        // fewer than S k-steps, one tile per block (see the kernel).
-        int dev = 0, cus = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            cus <= 0)
-            cus = 256;
-        const int tiles = TM * TN;
-        int grid = (tiles < cus || ksteps < S) ? tiles : cus;
-        if (grid >= 8 && tiles % 8 == 0)
-            grid -= grid % 8;
-        if (bits == 8)
-            hipLaunchKernelGGL(k_gemm_w8a8, dim3((unsigned)grid), dim3(THREADS), lds_bytes, s, a);
-        else if (bits == 6)
-            hipLaunchKernelGGL(k_gemm_w4a4_e3m2, dim3((unsigned)grid), dim3(THREADS), lds_bytes,
-                               s, a);
-        else
-            hipLaunchKernelGGL(k_gemm_w4a4, dim3((unsigned)grid), dim3(THREADS), lds_bytes, s, a);
-    }
-    else
-        hipLaunchKernelGGL(k_gemm_w4a4_k64, dim3((unsigned)(TM * TN)), dim3(THREADS), lds_bytes, s,
-                           a);
+    GemmArgs args = a;
+    void *params[] = {&args};
+    e = hipLaunchKernel(fn, dim3((unsigned)grid), dim3((unsigned)threads), params,
+                        (size_t)lds_bytes, s);
+    if (e != hipSuccess)
+        return e;
     return hipGetLastError();
 }
 
