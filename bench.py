@@ -457,6 +457,9 @@ def main():
                     help="skip the fused-prologue and 8-bit legs")
     ap.add_argument("--no-7b", action="store_true",
                     help="skip the Llama-2-7B layer shapes and the tiny layer")
+    ap.add_argument("--only-7b", action="store_true",
+                    help="run only the Llama-2-7B layer shapes and the tiny layer (for "
+                         "profiling their kernels); prints their figures alone")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB once (a plain copy "
                          "kernel of known size, to scale hardware byte counters)")
@@ -474,6 +477,11 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.only_7b:
+        res = bench_layers_7b(q, workloads, torch, np, dev, torch.cuda.current_stream(),
+                              max(args.steps, 10))
+        print(json.dumps({"llama2_7b_and_tiny": res}), flush=True)
+        return
     layers = []
     for name in ("llama2_70b_up", "llama2_70b_down"):
         wl = workloads.LINEAR[name]

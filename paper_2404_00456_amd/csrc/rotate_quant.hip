@@ -25,6 +25,7 @@
 //   k_kv_dequant  4-bit KV cache back to fp16, optional inverse rotation.
 // Lane butterflies use the placement and sign bookkeeping of lane_stages().
 #include <algorithm>
+#include <type_traits>
 
 #include "common.hpp"
 #include "hadamard_factors.hpp"
@@ -789,25 +790,52 @@ __device__ __forceinline__ const uint4 *hm_mfma_b<172>()
     return reinterpret_cast<const uint4 *>(&c_hmb172.w[0][0][0][0]);
 }
 
-// The exact integer N = t * 2^24 of an fp16 value t (bits h; |N| < 2^40 for
-// finite t) as 7 base-64 digits, N = sum_i d_i 64^i: d_0 .. d_5 in [0, 63]
-// (bits 6i .. 6i+5 of N in two's complement) and the signed top digit
-// d_6 = N >> 36 in [-16, 15].  Each fits an int8 byte.
-__device__ __forceinline__ void f16_digits(uint32_t h, uint32_t d[7])
+// The exact integer N = t * 2^24 of an fp16 value t (bits h) as signed
+// base-64 digits, N = sum_k d_k 64^k, returned as a 64-bit word whose byte k
+// is d_k (int8).  t = +-mant 2^(sh - 24) with an 11-bit mant and sh in
+// [0, 29]; with q = sh / 6 and r = sh - 6 q, mant << r (below 2^17) has
+// three base-64 digits, which land at positions q .. q + 2 (q <= 4), all
+// of them negated for negative t.  Every digit lies in [-63, 63].
+__device__ __forceinline__ uint64_t f16_planes(uint32_t h)
 {
     const uint32_t e = (h >> 10) & 31u;
     const uint32_t mant = (h & 1023u) | (e ? 1024u : 0u);
     const uint32_t sh = e ? e - 1u : 0u;
-    const int32_t sm = (h & 0x8000u) ? -(int32_t)mant : (int32_t)mant;
-    const int64_t N = (int64_t)sm << sh;
-    const uint32_t lo = (uint32_t)N, hi = (uint32_t)((uint64_t)N >> 32);
-    d[0] = lo & 63u;
-    d[1] = (lo >> 6) & 63u;
-    d[2] = (lo >> 12) & 63u;
-    d[3] = (lo >> 18) & 63u;
-    d[4] = (lo >> 24) & 63u;
-    d[5] = ((lo >> 30) | (hi << 2)) & 63u;
-    d[6] = (uint32_t)((int32_t)hi >> 4) & 0xFFu;
+    const uint32_t q = (sh * 43u) >> 8;  // sh / 6 for sh < 30
+    const uint32_t mp = mant << (sh - 6u * q);
+    uint32_t d = (mp & 63u) | ((mp << 2) & 0x3F00u) | ((mp << 4) & 0x1F0000u);
+    // bytes below 0x80 negated in place: 0x80 - d borrows from no other byte
+    if (h & 0x8000u)
+        d = (0x80808080u - d) ^ 0x80808080u;
+    return (uint64_t)d << (8u * q);
+}
+
+// The digit planes of four fp16 values (raw bits in r.x, r.y, low half
+// first): w[k] holds digit k of the four values in its bytes 0..3.
+__device__ __forceinline__ void f16x4_planes(uint2 r, uint32_t w[7])
+{
+    const uint64_t p0 = f16_planes(r.x & 0xFFFFu), p1 = f16_planes(r.x >> 16);
+    const uint64_t p2 = f16_planes(r.y & 0xFFFFu), p3 = f16_planes(r.y >> 16);
+    const uint32_t l0 = (uint32_t)p0, l1 = (uint32_t)p1, l2 = (uint32_t)p2, l3 = (uint32_t)p3;
+    const uint32_t h0 = (uint32_t)(p0 >> 32), h1 = (uint32_t)(p1 >> 32);
+    const uint32_t h2 = (uint32_t)(p2 >> 32), h3 = (uint32_t)(p3 >> 32);
+    // v_perm_b32(s0, s1, sel): selector byte 0-3 picks s1's bytes, 4-7 s0's
+    // pairs: {digit j of v0, of v1, digit j+1 of v0, of v1}
+    const uint32_t a01 = __builtin_amdgcn_perm(l1, l0, 0x05010400u);
+    const uint32_t b01 = __builtin_amdgcn_perm(l1, l0, 0x07030602u);
+    const uint32_t c01 = __builtin_amdgcn_perm(h1, h0, 0x05010400u);
+    const uint32_t d01 = __builtin_amdgcn_perm(h1, h0, 0x0C0C0602u);
+    const uint32_t a23 = __builtin_amdgcn_perm(l3, l2, 0x05010400u);
+    const uint32_t b23 = __builtin_amdgcn_perm(l3, l2, 0x07030602u);
+    const uint32_t c23 = __builtin_amdgcn_perm(h3, h2, 0x05010400u);
+    const uint32_t d23 = __builtin_amdgcn_perm(h3, h2, 0x0C0C0602u);
+    w[0] = __builtin_amdgcn_perm(a23, a01, 0x05040100u);
+    w[1] = __builtin_amdgcn_perm(a23, a01, 0x07060302u);
+    w[2] = __builtin_amdgcn_perm(b23, b01, 0x05040100u);
+    w[3] = __builtin_amdgcn_perm(b23, b01, 0x07060302u);
+    w[4] = __builtin_amdgcn_perm(c23, c01, 0x05040100u);
+    w[5] = __builtin_amdgcn_perm(c23, c01, 0x07060302u);
+    w[6] = __builtin_amdgcn_perm(d23, d01, 0x05040100u);
 }
 
 // Four fp16 inputs (raw bits) at element offset off of the row: the plain
@@ -830,10 +858,11 @@ __device__ __forceinline__ uint2 load_bits4(const RotArgs &a, int64_t off)
 //
 // m-factor on the int8 matrix cores.  It is a contraction, U = T . H_M
 // with T [A, M] the groups: every fp16 input is an integer multiple of
-// 2^-24, so N = t 2^24 is an integer below 2^40, and its base-64 digits
-// (f16_digits) are int8 operands of v_mfma_i32_16x16x64_i8 against the +-1
-// entries of H_M.  Digits 2p and 2p+1 accumulate into one int32 C_p (the
-// odd digit against 64 H_M, still int8): |C_p| <= M * 63 * 65 < 2^21.  Then
+// 2^-24, so N = t 2^24 is an integer below 2^40, and its signed base-64
+// digits (f16_planes) are int8 operands of v_mfma_i32_16x16x64_i8 against
+// the +-1 entries of H_M.  Digits 2p and 2p+1 accumulate into one int32 C_p
+// (the odd digit against 64 H_M, still int8): |C_p| <= M * 63 * 65 < 2^21.
+// Then
 // sum_b H[b][b'] N_b = sum_p C_p 2^(12 p), an integer below 2^48, is formed
 // exactly in binary64 and u = RN32(that * 2^-24): the exact sum rounded
 // once, as the definition asks, in whatever order the hardware adds.
@@ -842,16 +871,17 @@ __device__ __forceinline__ uint2 load_bits4(const RotArgs &a, int64_t off)
 // output puts groups 4 (l/16) + r (register r) and column ct*16 + l%16 in
 // lane l, so Walsh-Hadamard bits 0-1 of the group index are butterflies
 // between registers and bits 2-3 between lanes l and l ^ 16, l ^ 32; u is
-// then staged in LDS as A rows of M + 1 floats, where bits 4.. (across
-// tiles) run as butterflies on the staged row.  H_M's operand tiles sit in
-// LDS in front of the row.
+// then staged in LDS as the row itself (element i = g M + b at i).  Bits
+// 4.. (across tiles) run in registers on the 2^(k-4) values of one column
+// of the groups a, a + 16, ..., which also gives the row's absmax; the
+// epilogue reads 8 consecutive elements with two 16-byte reads.  H_M's
+// operand tiles sit in LDS in front of the row.
 template <int M, int EPI, int PRO = PRO_PLAIN>
 __global__ __launch_bounds__(256, 2) void k_rot_largem(RotArgs a)
 {
     constexpr int W = 4;
     constexpr int CT = HmMfmaB<M>::CT, KB = HmMfmaB<M>::KB;
     constexpr int CTP = 4;  // column tiles per pass (accumulator registers)
-    constexpr int LD = M + 1;
     static_assert(M % 4 == 0, "4-element loads");
     typedef int v4i __attribute__((ext_vector_type(4)));
     extern __shared__ __align__(16) uint8_t lds_raw[];
@@ -882,18 +912,17 @@ __global__ __launch_bounds__(256, 2) void k_rot_largem(RotArgs a)
             uint32_t w[7][4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
+                // past the row or the group: load a valid quad, use zeros
                 const int b = kb * 64 + (lane >> 4) * 16 + 4 * q;
-                uint2 raw = make_uint2(0, 0);
-                if (g < A && b < M)
-                    raw = load_bits4<PRO>(a, row * n + (int64_t)g * M + b);
-                uint32_t d0[7], d1[7], d2[7], d3[7];
-                f16_digits(raw.x & 0xFFFFu, d0);
-                f16_digits(raw.x >> 16, d1);
-                f16_digits(raw.y & 0xFFFFu, d2);
-                f16_digits(raw.y >> 16, d3);
+                const bool ok = g < A && b < M;
+                const uint2 ld = load_bits4<PRO>(
+                    a, row * n + (int64_t)(ok ? g : 0) * M + (ok ? b : 0));
+                const uint2 raw = ok ? ld : make_uint2(0, 0);
+                uint32_t d[7];
+                f16x4_planes(raw, d);
 #pragma unroll
                 for (int i = 0; i < 7; ++i)
-                    w[i][q] = d0[i] | (d1[i] << 8) | (d2[i] << 16) | (d3[i] << 24);
+                    w[i][q] = d[i];
             }
 #pragma unroll
             for (int i = 0; i < 7; ++i)
@@ -971,47 +1000,68 @@ __global__ __launch_bounds__(256, 2) void k_rot_largem(RotArgs a)
                 for (int r = 0; r < 4; ++r) {
                     const int gg = rt * 16 + 4 * (lane >> 4) + r;
                     if (gg < A && col < M)
-                        rowbuf[gg * LD + col] = u[r];
+                        rowbuf[gg * M + col] = u[r];
                 }
             }
         }
     }
     __syncthreads();
-    // group bits 4.. (across row tiles): butterflies on the staged row
-    for (int j = 4; j < k; ++j) {
-        const int h = 1 << j;
-        const int total = (A / 2) * M;
-        for (int idx = tid; idx < total; idx += 64 * W) {
-            const int pr = idx / M, b = idx - pr * M;
-            const int p = (pr / h) * 2 * h + (pr % h), q = p + h;
-            const float up = rowbuf[p * LD + b], uq = rowbuf[q * LD + b];
-            rowbuf[p * LD + b] = up + uq;
-            rowbuf[q * LD + b] = up - uq;
-        }
-        __syncthreads();
-    }
+    // group bits 4.. (across row tiles) and the row's absmax: a thread takes
+    // column b of the groups a, a + 16, ... (a < 16), their 2^(k-4) values
     const float c = a.c;
+    float amax = 0.0f;
+    auto column_pass = [&](auto NJ_) {
+        constexpr int NJ = decltype(NJ_)::value;
+        const int NA = NJ > 1 ? 16 : A;
+        for (int idx = tid; idx < NA * M; idx += 64 * W) {
+            const int al = idx / M, b = idx - al * M;
+            float v[NJ];
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+                v[j] = rowbuf[(al + 16 * j) * M + b];
+#pragma unroll
+            for (int h = 1; h < NJ; h <<= 1)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    if (!(j & h)) {
+                        const float p = v[j], q = v[j + h];
+                        v[j] = p + q;
+                        v[j + h] = p - q;
+                    }
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                if constexpr (NJ > 1)
+                    rowbuf[(al + 16 * j) * M + b] = v[j];
+                amax = fmaxf(amax, fabsf(v[j] * c));  // |y|: the sign of a zero is moot
+            }
+        }
+    };
+    switch (k) {
+    case 7: column_pass(std::integral_constant<int, 8>()); break;
+    case 6: column_pass(std::integral_constant<int, 4>()); break;
+    case 5: column_pass(std::integral_constant<int, 2>()); break;
+    default: column_pass(std::integral_constant<int, 1>()); break;
+    }
+    __syncthreads();
     const int chunks = n / 8;
+    auto row8 = [&](int ch, float *y) {
+        const float4 p0 = *reinterpret_cast<const float4 *>(rowbuf + ch * 8);
+        const float4 p1 = *reinterpret_cast<const float4 *>(rowbuf + ch * 8 + 4);
+        y[0] = p0.x, y[1] = p0.y, y[2] = p0.z, y[3] = p0.w;
+        y[4] = p1.x, y[5] = p1.y, y[6] = p1.z, y[7] = p1.w;
+    };
     if constexpr (EPI == EPI_F16 || EPI == EPI_F32) {
         for (int ch = tid; ch < chunks; ch += 64 * W) {
             float y[8];
+            row8(ch, y);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
-                y[e] = __builtin_fmaf(rowbuf[gi * LD + b], c, 0.0f);  // zeros +0
-            }
+            for (int e = 0; e < 8; ++e)
+                y[e] = __builtin_fmaf(y[e], c, 0.0f);  // zeros +0
             store_y8<EPI>(a.out, row * n + ch * 8, y);
         }
     } else {
         static_assert(EPI == EPI_SYM || EPI == EPI_SYM8 || EPI == EPI_E3M2,
                       "large-m kernels serve activations");
-        float amax = 0.0f;
-        for (int ch = tid; ch < chunks; ch += 64 * W)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
-                amax = fmaxf(amax, fabsf(rowbuf[gi * LD + b] * c));  // |y|: sign of 0 moot
-            }
         static_for<6>([&](auto J) { amax = lane_max<J>(amax); });
         if (lane == 0)
             red[tid >> 6] = amax;
@@ -1027,11 +1077,10 @@ __global__ __launch_bounds__(256, 2) void k_rot_largem(RotArgs a)
         uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(n);
         for (int ch = tid; ch < chunks; ch += 64 * W) {
             float y[8];
+            row8(ch, y);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int i = ch * 8 + e, gi = i / M, b = i - gi * M;
-                y[e] = rowbuf[gi * LD + b] * c;
-            }
+            for (int e = 0; e < 8; ++e)
+                y[e] = y[e] * c;
             if constexpr (EPI == EPI_E3M2)
                 store_e3m2_8(static_cast<uint8_t *>(a.out), a.rows, row, ch * 8, y, dv);
             else
@@ -1332,7 +1381,7 @@ hipError_t go_largem(const RotArgs &a, hipStream_t s)
 {
     // H_M's operand tiles, then the staged row
     const size_t lds = (size_t)HmMfmaB<M>::CT * HmMfmaB<M>::KB * 1024 +
-                       (size_t)(a.n / M) * (M + 1) * sizeof(float);
+                       (size_t)a.n * sizeof(float);
     const void *fn = (const void *)k_rot_largem<M, EPI, PRO>;
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
