@@ -79,13 +79,17 @@ _SIGS = {
 
 
 def lib():
-    """Load (building first if needed) the oracle shared library."""
+    """Load (building first if needed) the oracle shared library.  The
+    environment variable QUAROT_ORACLE_LIB names another build of the same
+    source to load instead (the sanitizer test uses it)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB_PATH) or (
-                os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)):
-            build()
-        L = ctypes.CDLL(_LIB_PATH)
+        path = os.environ.get("QUAROT_ORACLE_LIB")
+        if not path:
+            path = _LIB_PATH
+            if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
+                build()
+        L = ctypes.CDLL(path)
         for name, (res, args) in _SIGS.items():
             fn = getattr(L, name)
             fn.restype = res

@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libquarot.so")
-SOURCES = ["capi.cpp", "rotate_quant.hip", "gemm_w4a4.hip", "gemm_grouped.hip", "kv_attention.hip",
+SOURCES = ["capi.cpp", "host_rules.cpp", "rotate_quant.hip", "gemm_w4a4.hip", "gemm_grouped.hip", "kv_attention.hip",
            "probe.hip", "scratch.hip"]
 
 # -ffp-contract=off: every written add and multiply stays a rounded op of

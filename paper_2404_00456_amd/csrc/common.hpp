@@ -27,12 +27,40 @@ enum Prologue : int {
 
 // ---- int4 codes as e3m2 numbers (the operand format of the fp6 GEMM) ----
 //
+// These encoders are also built for the host (a CPU test runs them over all
+// inputs against the format's definition), so the one device builtin they
+// use, v_perm_b32, has a host stand-in written from the instruction's
+// definition: the 8-byte pool {s0 (bytes 4-7), s1 (bytes 0-3)}, selector
+// byte 0-7 picks a pool byte, 8-11 replicates a sign bit, 12 gives 0x00
+// and larger values 0xFF.
+__host__ __device__ __forceinline__ uint32_t perm_b32(uint32_t s0, uint32_t s1, uint32_t sel)
+{
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_amdgcn_perm(s0, s1, sel);
+#else
+    const uint64_t pool = ((uint64_t)s0 << 32) | s1;
+    uint32_t d = 0;
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t c = (sel >> (8 * i)) & 0xFFu;
+        uint32_t byte;
+        if (c < 8)
+            byte = (uint32_t)(pool >> (8 * c)) & 0xFFu;
+        else if (c < 12)
+            byte = ((pool >> (c == 8 ? 15 : c == 9 ? 31 : c == 10 ? 47 : 63)) & 1u) ? 0xFFu : 0u;
+        else
+            byte = c == 12 ? 0x00u : 0xFFu;
+        d |= byte << (8 * i);
+    }
+    return d;
+#endif
+}
+//
 // e3m2: sign, 3 exponent bits (bias 3), 2 mantissa bits; every integer in
 // -8..8 is exact.  For such an integer q, the binary32 encoding b of q has
 // exponent field e and top mantissa bits m with 4 e + m = 4 (E + 124) + M
 // for q's e3m2 exponent field E and mantissa M (|q| >= 1), so the code is
 // (b >> 21 & 0x3FF) - 496, clamped at 0 for q = 0, plus the sign at bit 5.
-__device__ __forceinline__ uint32_t e3m2_of_bits(uint32_t b)
+__host__ __device__ __forceinline__ uint32_t e3m2_of_bits(uint32_t b)
 {
     const int mag = (int)((b >> 21) & 0x3FFu) - 4 * 124;
     return (uint32_t)(mag > 0 ? mag : 0) | ((b >> 26) & 0x20u);
@@ -48,17 +76,17 @@ __device__ __forceinline__ uint32_t e3m2_of_int(int q)
 // bits 32-47.  Byte lookups: v_perm_b32 picks, per byte, one of 8 table
 // bytes (the codes of q = 0..7, or of q = -8..-1), and the nibble's sign bit
 // chooses between the two lookups.
-__device__ __forceinline__ uint32_t e3m2_lut4(uint32_t x)  // 4 nibbles, one per byte
+__host__ __device__ __forceinline__ uint32_t e3m2_lut4(uint32_t x)  // 4 nibbles, one per byte
 {
     const uint32_t sel = x & 0x07070707u;
-    const uint32_t pos = __builtin_amdgcn_perm(0x17161514u, 0x12100C00u, sel);  // q = 0..7
-    const uint32_t neg = __builtin_amdgcn_perm(0x2C303234u, 0x35363738u, sel);  // q = -8..-1
+    const uint32_t pos = perm_b32(0x17161514u, 0x12100C00u, sel);  // q = 0..7
+    const uint32_t neg = perm_b32(0x2C303234u, 0x35363738u, sel);  // q = -8..-1
     const uint32_t m = x & 0x08080808u;
     const uint32_t mask = (m << 3) - (m >> 3);  // 0x3F in the bytes whose q < 0
     return (neg & mask) | (pos & ~mask);
 }
 
-__device__ __forceinline__ void e3m2_of_nibbles8(uint32_t w, uint32_t &lo, uint32_t &hi)
+__host__ __device__ __forceinline__ void e3m2_of_nibbles8(uint32_t w, uint32_t &lo, uint32_t &hi)
 {
     const uint32_t a = e3m2_lut4(w & 0x0F0F0F0Fu);         // codes 0, 2, 4, 6
     const uint32_t b = e3m2_lut4((w >> 4) & 0x0F0F0F0Fu);  // codes 1, 3, 5, 7
@@ -71,7 +99,7 @@ __device__ __forceinline__ void e3m2_of_nibbles8(uint32_t w, uint32_t &lo, uint3
 
 // 32 int4 codes (four nibble dwords) -> the 192-bit unit sum_e e3m2(q_e) << 6e
 // as six dwords.
-__device__ __forceinline__ void e3m2_unit(const uint32_t (&w)[4], uint32_t (&o)[6])
+__host__ __device__ __forceinline__ void e3m2_unit(const uint32_t (&w)[4], uint32_t (&o)[6])
 {
     uint32_t lo[4], hi[4];
 #pragma unroll
@@ -85,16 +113,66 @@ __device__ __forceinline__ void e3m2_unit(const uint32_t (&w)[4], uint32_t (&o)[
     o[5] = (lo[3] >> 16) | (hi[3] << 16);
 }
 
+// ---- exact integer digits of fp16 values (large-m rotation m-factor) ----
+
+// The exact integer N = t * 2^24 of an fp16 value t (bits h) as signed
+// base-64 digits, N = sum_k d_k 64^k, returned as a 64-bit word whose byte k
+// is d_k (int8).  t = +-mant 2^(sh - 24) with an 11-bit mant and sh in
+// [0, 29]; with q = sh / 6 and r = sh - 6 q, mant << r (below 2^17) has
+// three base-64 digits, which land at positions q .. q + 2 (q <= 4), all
+// of them negated for negative t.  Every digit lies in [-63, 63].
+__host__ __device__ __forceinline__ uint64_t f16_planes(uint32_t h)
+{
+    const uint32_t e = (h >> 10) & 31u;
+    const uint32_t mant = (h & 1023u) | (e ? 1024u : 0u);
+    const uint32_t sh = e ? e - 1u : 0u;
+    const uint32_t q = (sh * 43u) >> 8;  // sh / 6 for sh < 30
+    const uint32_t mp = mant << (sh - 6u * q);
+    uint32_t d = (mp & 63u) | ((mp << 2) & 0x3F00u) | ((mp << 4) & 0x1F0000u);
+    // bytes below 0x80 negated in place: 0x80 - d borrows from no other byte
+    if (h & 0x8000u)
+        d = (0x80808080u - d) ^ 0x80808080u;
+    return (uint64_t)d << (8u * q);
+}
+
+// The digit planes of four fp16 values (raw bits in r.x, r.y, low half
+// first): w[k] holds digit k of the four values in its bytes 0..3.
+__host__ __device__ __forceinline__ void f16x4_planes(uint2 r, uint32_t w[7])
+{
+    const uint64_t p0 = f16_planes(r.x & 0xFFFFu), p1 = f16_planes(r.x >> 16);
+    const uint64_t p2 = f16_planes(r.y & 0xFFFFu), p3 = f16_planes(r.y >> 16);
+    const uint32_t l0 = (uint32_t)p0, l1 = (uint32_t)p1, l2 = (uint32_t)p2, l3 = (uint32_t)p3;
+    const uint32_t h0 = (uint32_t)(p0 >> 32), h1 = (uint32_t)(p1 >> 32);
+    const uint32_t h2 = (uint32_t)(p2 >> 32), h3 = (uint32_t)(p3 >> 32);
+    // perm_b32(s0, s1, sel): selector byte 0-3 picks s1's bytes, 4-7 s0's
+    // pairs: {digit j of v0, of v1, digit j+1 of v0, of v1}
+    const uint32_t a01 = perm_b32(l1, l0, 0x05010400u);
+    const uint32_t b01 = perm_b32(l1, l0, 0x07030602u);
+    const uint32_t c01 = perm_b32(h1, h0, 0x05010400u);
+    const uint32_t d01 = perm_b32(h1, h0, 0x0C0C0602u);
+    const uint32_t a23 = perm_b32(l3, l2, 0x05010400u);
+    const uint32_t b23 = perm_b32(l3, l2, 0x07030602u);
+    const uint32_t c23 = perm_b32(h3, h2, 0x05010400u);
+    const uint32_t d23 = perm_b32(h3, h2, 0x0C0C0602u);
+    w[0] = perm_b32(a23, a01, 0x05040100u);
+    w[1] = perm_b32(a23, a01, 0x07060302u);
+    w[2] = perm_b32(b23, b01, 0x05040100u);
+    w[3] = perm_b32(b23, b01, 0x07060302u);
+    w[4] = perm_b32(c23, c01, 0x05040100u);
+    w[5] = perm_b32(c23, c01, 0x07060302u);
+    w[6] = perm_b32(d23, d01, 0x05040100u);
+}
+
 // Tiled e3m2 layout of a [rows, K] code matrix: K/128 blocks of rows * 96
 // bytes.  Unit u (k = 128 b + 32 u .. + 31) of row r: dwords 0-3 (head) at
 // e3m2_head, dwords 4-5 (tail) at e3m2_tail.  The row-dependent slot
 // swizzles make the GEMM's LDS reads of 16 rows hit distinct banks.
-__device__ __forceinline__ int64_t e3m2_head(int64_t rows, int64_t r, int b, int u)
+__host__ __device__ __forceinline__ int64_t e3m2_head(int64_t rows, int64_t r, int b, int u)
 {
     return (int64_t)b * rows * 96 + r * 64 + 16 * (u ^ (int)((r >> 1) & 3));
 }
 
-__device__ __forceinline__ int64_t e3m2_tail(int64_t rows, int64_t r, int b, int u)
+__host__ __device__ __forceinline__ int64_t e3m2_tail(int64_t rows, int64_t r, int b, int u)
 {
     return (int64_t)b * rows * 96 + rows * 64 + r * 32 + 8 * (u ^ (int)((r >> 2) & 3));
 }

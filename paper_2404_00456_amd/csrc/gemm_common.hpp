@@ -55,15 +55,15 @@ typedef __attribute__((address_space(3))) void lds_void;
 // own LDS-DMA builtin the waitcnt pass cannot tell the DMA target from the
 // stage being read and waits for every DMA before each LDS read, which
 // serializes the ring.  Here only the explicit s_waitcnt below orders it.
-// The kernel uses M0 for nothing else (checked in its ISA); the s_nop is
-// the wait state the ISA asks for between an SALU write of M0 and a VMEM
-// instruction with LDS destination.
+// M0 is declared clobbered, so the compiler keeps nothing of its own in it
+// across the block; the s_nop is the wait state the ISA asks for between an
+// SALU write of M0 and a VMEM instruction with LDS destination.
 __device__ __forceinline__ void dma16(const void *g, uint32_t lds_base)
 {
     asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                  :
                  : "v"(g), "s"(lds_base)
-                 : "memory");
+                 : "memory", "m0");
 }
 
 // dma16 in the SGPR-base form: lane l reads base + voff[l] (a wave-uniform
@@ -74,7 +74,7 @@ __device__ __forceinline__ void dma16s(uint32_t voff, const void *base, uint32_t
     asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                  :
                  : "v"(voff), "s"(base), "s"(lds_base)
-                 : "memory");
+                 : "memory", "m0");
 }
 
 // 4 bytes per lane into LDS at lds_base + 4 * lane (same rules as dma16).
@@ -83,7 +83,7 @@ __device__ __forceinline__ void dma4(const void *g, uint32_t lds_base)
     asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
                  :
                  : "v"(g), "s"(lds_base)
-                 : "memory");
+                 : "memory", "m0");
 }
 
 // s_waitcnt immediate: vmcnt(vm) expcnt(7) lgkmcnt(lgkm) in the gfx9 layout

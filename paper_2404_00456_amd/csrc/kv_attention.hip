@@ -276,14 +276,6 @@ hipError_t go_attn(const KvAttnArgs &a, hipStream_t s)
 
 }  // namespace
 
-int kv_attn_splits(int64_t nq, int64_t seq_len)
-{
-    // about 2048 blocks in flight, chunks of at least 256 tokens
-    const int64_t want = (2048 + nq - 1) / std::max<int64_t>(nq, 1);
-    const int64_t most = (seq_len + 255) / 256;
-    return (int)std::max<int64_t>(1, std::min(want, most));
-}
-
 hipError_t launch_kv_attention(const KvAttnArgs &a, hipStream_t s)
 {
     if (a.nq == 0)

@@ -790,54 +790,6 @@ __device__ __forceinline__ const uint4 *hm_mfma_b<172>()
     return reinterpret_cast<const uint4 *>(&c_hmb172.w[0][0][0][0]);
 }
 
-// The exact integer N = t * 2^24 of an fp16 value t (bits h) as signed
-// base-64 digits, N = sum_k d_k 64^k, returned as a 64-bit word whose byte k
-// is d_k (int8).  t = +-mant 2^(sh - 24) with an 11-bit mant and sh in
-// [0, 29]; with q = sh / 6 and r = sh - 6 q, mant << r (below 2^17) has
-// three base-64 digits, which land at positions q .. q + 2 (q <= 4), all
-// of them negated for negative t.  Every digit lies in [-63, 63].
-__device__ __forceinline__ uint64_t f16_planes(uint32_t h)
-{
-    const uint32_t e = (h >> 10) & 31u;
-    const uint32_t mant = (h & 1023u) | (e ? 1024u : 0u);
-    const uint32_t sh = e ? e - 1u : 0u;
-    const uint32_t q = (sh * 43u) >> 8;  // sh / 6 for sh < 30
-    const uint32_t mp = mant << (sh - 6u * q);
-    uint32_t d = (mp & 63u) | ((mp << 2) & 0x3F00u) | ((mp << 4) & 0x1F0000u);
-    // bytes below 0x80 negated in place: 0x80 - d borrows from no other byte
-    if (h & 0x8000u)
-        d = (0x80808080u - d) ^ 0x80808080u;
-    return (uint64_t)d << (8u * q);
-}
-
-// The digit planes of four fp16 values (raw bits in r.x, r.y, low half
-// first): w[k] holds digit k of the four values in its bytes 0..3.
-__device__ __forceinline__ void f16x4_planes(uint2 r, uint32_t w[7])
-{
-    const uint64_t p0 = f16_planes(r.x & 0xFFFFu), p1 = f16_planes(r.x >> 16);
-    const uint64_t p2 = f16_planes(r.y & 0xFFFFu), p3 = f16_planes(r.y >> 16);
-    const uint32_t l0 = (uint32_t)p0, l1 = (uint32_t)p1, l2 = (uint32_t)p2, l3 = (uint32_t)p3;
-    const uint32_t h0 = (uint32_t)(p0 >> 32), h1 = (uint32_t)(p1 >> 32);
-    const uint32_t h2 = (uint32_t)(p2 >> 32), h3 = (uint32_t)(p3 >> 32);
-    // v_perm_b32(s0, s1, sel): selector byte 0-3 picks s1's bytes, 4-7 s0's
-    // pairs: {digit j of v0, of v1, digit j+1 of v0, of v1}
-    const uint32_t a01 = __builtin_amdgcn_perm(l1, l0, 0x05010400u);
-    const uint32_t b01 = __builtin_amdgcn_perm(l1, l0, 0x07030602u);
-    const uint32_t c01 = __builtin_amdgcn_perm(h1, h0, 0x05010400u);
-    const uint32_t d01 = __builtin_amdgcn_perm(h1, h0, 0x0C0C0602u);
-    const uint32_t a23 = __builtin_amdgcn_perm(l3, l2, 0x05010400u);
-    const uint32_t b23 = __builtin_amdgcn_perm(l3, l2, 0x07030602u);
-    const uint32_t c23 = __builtin_amdgcn_perm(h3, h2, 0x05010400u);
-    const uint32_t d23 = __builtin_amdgcn_perm(h3, h2, 0x0C0C0602u);
-    w[0] = __builtin_amdgcn_perm(a23, a01, 0x05040100u);
-    w[1] = __builtin_amdgcn_perm(a23, a01, 0x07060302u);
-    w[2] = __builtin_amdgcn_perm(b23, b01, 0x05040100u);
-    w[3] = __builtin_amdgcn_perm(b23, b01, 0x07060302u);
-    w[4] = __builtin_amdgcn_perm(c23, c01, 0x05040100u);
-    w[5] = __builtin_amdgcn_perm(c23, c01, 0x07060302u);
-    w[6] = __builtin_amdgcn_perm(d23, d01, 0x05040100u);
-}
-
 // Four fp16 inputs (raw bits) at element offset off of the row: the plain
 // row, or RN16(silu(gate) up) for the SwiGLU prologue.
 template <int PRO>
@@ -1502,41 +1454,6 @@ hipError_t go_kvdeq(const KvDeqArgs &a, bool inv, hipStream_t s)
 
 }  // namespace
 
-bool rotate_supported(int epi, bool rotate, int k, int m, int n, int pro)
-{
-    if (n <= 0 || n % 8 != 0 || n > 32768)
-        return false;
-    if (pro == PRO_SWIGLU && ((epi != EPI_SYM && epi != EPI_E3M2) || !rotate))
-        return false;
-    if (epi == EPI_E3M2) {
-        if (n % 128)
-            return false;
-        if (!rotate)
-            return true;
-        switch (m) {
-        case 1: return k >= 7 && k <= 15;
-        case 12: return k == 10 || k == 11;
-        case 20:
-        case 28: return k == 9 || k == 10;
-        case 108: return k >= 5 && k <= 7;  // n a multiple of 128
-        case 172: return k >= 5 && k <= 6;
-        }
-        return false;
-    }
-    if (!rotate)
-        return epi == EPI_SYM || epi == EPI_SYM8 || (epi == EPI_KV && m == 1 && k >= 3 && k <= 9);
-    if (epi == EPI_KV)
-        return m == 1 && k >= 3 && k <= 9;
-    switch (m) {
-    case 1: return k >= 3 && k <= 15;
-    case 12: return k >= 1 && k <= 11;
-    case 20:
-    case 28: return k >= 1 && k <= 10;
-    case 108: return k >= 1 && k <= 7;
-    case 172: return k >= 1 && k <= 6;
-    }
-    return false;
-}
 
 hipError_t launch_rotate(const RotArgs &a, int epi, bool rotate, int k, int m, hipStream_t s,
                          int pro)
