@@ -19,8 +19,9 @@
 //                 lanes, then across the W waves (LDS), then across chunks.
 //   k_rot_smallm  m = 12, 20, 28: each lane owns whole groups of m elements;
 //                 the m-factor is an fp64 sum with shared partial sums.
-//   k_rot_largem  m = 108, 172: one group per lane, CB output columns of the
-//                 m-factor per pass in fp64, the rotated row staged in LDS.
+//   k_rot_largem  m = 108, 172: the m-factor as exact integer digit
+//                 products on the int8 matrix cores, the rotated row staged
+//                 in LDS.
 //   k_quant_plain quantization without rotation, any n multiple of 8.
 //   k_kv_dequant  4-bit KV cache back to fp16, optional inverse rotation.
 // Lane butterflies use the placement and sign bookkeeping of lane_stages().
