@@ -366,7 +366,8 @@ def bench_next(q, torch, dev, stream, layers):
     - the 8-bit GEMM (W8A8) on both FFN shapes, its codes from
       quarot_quant_int8 of the same activations and weights;
     - group-wise W4A4: the group quantizer (rotation to binary32, then
-      per-group scales) and the grouped GEMM on the FFN shapes.
+      per-group scales) and the grouped GEMM on the FFN shapes, on int4
+      operands and (groups of 128 and 256) on e3m2 operands.
     gate/up/attention-output rows are seeded torch.randn draws on the GPU."""
     M = 16384
     g = torch.Generator(device=dev)
@@ -433,10 +434,20 @@ def bench_next(q, torch, dev, stream, layers):
             us_g = time_us(torch, stream,
                            lambda: q.quarot_w4a4_gemm_grouped(xq, sx, wq, sw, group=G, y=y))
             ops = 2 * wl.M * wl.N * wl.K
-            gw[f"{wl.name}_g{G}"] = {
-                "quant_us": round(us_q, 1), "gemm_us": round(us_g, 1),
-                "gemm_TOPS": round(ops / (us_g * 1e-6) / 1e12, 1),
-                "frac_int8_peak": round(ops / (us_g * 1e-6) / 1e12 / PEAK_I8_TOPS, 4)}
+            ent = {"quant_us": round(us_q, 1), "gemm_us": round(us_g, 1),
+                   "gemm_TOPS": round(ops / (us_g * 1e-6) / 1e12, 1),
+                   "frac_int8_peak": round(ops / (us_g * 1e-6) / 1e12 / PEAK_I8_TOPS, 4)}
+            if G >= 128:
+                # the same codes as e3m2 operands on the fp6 matrix cores
+                # (repacked once, untimed, like the per-token path's weights)
+                xq6, wq6 = q.quarot_pack_e3m2(xq), q.quarot_pack_e3m2(wq)
+                us_6 = time_us(torch, stream, lambda: q.quarot_w4a4_gemm_grouped_e3m2(
+                    xq6, sx, wq6, sw, group=G, y=y))
+                ent["e3m2_gemm_us"] = round(us_6, 1)
+                ent["e3m2_gemm_TOPS"] = round(ops / (us_6 * 1e-6) / 1e12, 1)
+                ent["e3m2_frac_int8_peak"] = round(ops / (us_6 * 1e-6) / 1e12 / PEAK_I8_TOPS, 4)
+                del xq6, wq6
+            gw[f"{wl.name}_g{G}"] = ent
             del xq, sx, wq, sw
     res["w4a4_grouped"] = gw
     torch.cuda.empty_cache()

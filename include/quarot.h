@@ -368,6 +368,21 @@ quarot_status quarot_w4a4_gemm_grouped(const uint8_t *xq, const quarot_f16 *sx,
                                        void *stream);
 
 /*
+ * quarot_w4a4_gemm_grouped on operands in the tiled e3m2 layout of
+ * quarot_pack_e3m2 (xq6 [K/128, M*96], wq6 [K/128, N*96]; the same int4
+ * codes, each stored as the e3m2 number of its value): the same y, bit for
+ * bit, from the fp6 matrix instruction (each group's sum of code products
+ * is exact in binary32, so f32(acc_g) is that sum).
+ * group: 128 or 256 (64 is QUAROT_ERR_UNSUPPORTED_SIZE: one instruction
+ * spans 128 k); M and N multiples of 8; K a multiple of group,
+ * K <= 65536.  One launch.
+ */
+quarot_status quarot_w4a4_gemm_grouped_e3m2(const uint8_t *xq6, const quarot_f16 *sx,
+                                            const uint8_t *wq6, const quarot_f16 *sw,
+                                            quarot_f16 *y, int64_t M, int64_t N, int64_t K,
+                                            int64_t group, void *stream);
+
+/*
  * The group-wise linear layer: quarot_quant_int4_grouped of x [M, K] into
  * the workspace, then quarot_w4a4_gemm_grouped.  wq, sw come from
  * quarot_quant_int4_grouped of W [N, K] with the same group and rotate.

@@ -71,6 +71,7 @@ SIGNATURES = {
     "quarot_quant_int4_grouped": (_I, [_P, _P, _P, _I64, _I64, _I64, _I, _F, _P,
                                        ctypes.c_size_t, _P]),
     "quarot_w4a4_gemm_grouped": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _P]),
+    "quarot_w4a4_gemm_grouped_e3m2": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _P]),
     "quarot_linear_w4a4_grouped_workspace_size": (ctypes.c_size_t, [_I64, _I64, _I64, _I]),
     "quarot_linear_w4a4_grouped": (_I, [_P, _P, _P, _P, _I64, _I64, _I64, _I64, _I, _F, _P,
                                         ctypes.c_size_t, _P]),
@@ -595,6 +596,32 @@ def quarot_w4a4_gemm_grouped(xq: torch.Tensor, sx: torch.Tensor, wq: torch.Tenso
     return y
 
 
+def quarot_w4a4_gemm_grouped_e3m2(xq6: torch.Tensor, sx: torch.Tensor, wq6: torch.Tensor,
+                                  sw: torch.Tensor, group: int = 128,
+                                  y: Optional[torch.Tensor] = None,
+                                  stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """quarot_w4a4_gemm_grouped on operands in the tiled e3m2 layout
+    (xq6 [K/128, M*96], wq6 [K/128, N*96]); sx [K/group, M], sw [K/group, N]."""
+    _ndim(xq6, 2, "xq6")
+    _ndim(sx, 2, "sx")
+    _ndim(sw, 2, "sw")
+    M, N = sx.shape[1], sw.shape[1]
+    K = 128 * xq6.shape[0]
+    _group(group, K)
+    if xq6.shape[1] != M * 96 or tuple(wq6.shape) != (xq6.shape[0], N * 96):
+        raise ValueError("quarot_w4a4_gemm_grouped_e3m2: operand shapes do not match sx, sw")
+    _shape(sx, (K // group, M), "sx")
+    _shape(sw, (K // group, N), "sw")
+    _shape(y, (M, N), "y")
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=xq6.device)
+    _check("quarot_w4a4_gemm_grouped_e3m2", lib().quarot_w4a4_gemm_grouped_e3m2(
+        _ptr(xq6, torch.uint8, "xq6"), _ptr(sx, torch.float16, "sx"),
+        _ptr(wq6, torch.uint8, "wq6"), _ptr(sw, torch.float16, "sw"), _ptr(y, torch.float16, "y"),
+        M, N, K, int(group), _stream(stream)))
+    return y
+
+
 def quarot_linear_w4a4_grouped(x: torch.Tensor, wq: torch.Tensor, sw: torch.Tensor,
                                group: int = 128, rotate: bool = True, clip_ratio: float = 1.0,
                                y: Optional[torch.Tensor] = None,
@@ -810,7 +837,8 @@ __all__ = [
     "quarot_hadamard_factor_table", "quarot_linear_workspace_size", "quarot_hadamard",
     "quarot_quant_int4", "quarot_w4a4_gemm", "quarot_linear", "prepare_weight",
     "quarot_quant_int8", "quarot_w8a8_gemm", "quarot_linear_w8a8", "quarot_quant_search",
-    "quarot_quant_int4_grouped", "quarot_w4a4_gemm_grouped", "quarot_linear_w4a4_grouped",
+    "quarot_quant_int4_grouped", "quarot_w4a4_gemm_grouped",
+    "quarot_w4a4_gemm_grouped_e3m2", "quarot_linear_w4a4_grouped",
     "quarot_swiglu", "quarot_swiglu_quant_int4", "quarot_hadamard_heads", "quarot_hadamard_heads_quant_int4",
     "quarot_kv_quant", "quarot_kv_dequant", "quarot_kv_append",
     "quarot_kv_attention_workspace_size", "quarot_kv_decode_attention",

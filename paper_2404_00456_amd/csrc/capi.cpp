@@ -831,6 +831,27 @@ quarot_status quarot_w4a4_gemm_grouped(const uint8_t *xq, const quarot_f16 *sx,
     return e == hipSuccess ? QUAROT_OK : hip_fail(e);
 }
 
+quarot_status quarot_w4a4_gemm_grouped_e3m2(const uint8_t *xq6, const quarot_f16 *sx,
+                                            const uint8_t *wq6, const quarot_f16 *sw,
+                                            quarot_f16 *y, int64_t M, int64_t N, int64_t K,
+                                            int64_t group, void *stream)
+{
+    quarot_status st = check_gemm_grouped_sizes(M, N, K, group);
+    if (st)
+        return st;
+    if (group == 64 || M % 8 || N % 8)
+        return QUAROT_ERR_UNSUPPORTED_SIZE;
+    if (M == 0 || N == 0)
+        return QUAROT_OK;
+    if ((st = check_gemm(xq6, sx, wq6, sw, y, nullptr, M, N, K)))
+        return st;
+    if ((st = check_device(__func__)))
+        return st;
+    GemmArgs a{xq6, sx, wq6, sw, y, nullptr, (int)M, (int)N, (int)K};
+    hipError_t e = launch_gemm_grouped_e3m2(a, (int)group, (hipStream_t)stream);
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
 size_t quarot_linear_w4a4_grouped_workspace_size(int64_t M, int64_t K, int64_t group,
                                                  int rotate)
 {

@@ -261,6 +261,7 @@ hipError_t launch_pack_e3m2(const uint8_t *q4, uint8_t *q6, int64_t rows, int k,
 // Group-wise W4A4, groups of `group` (64, 128, 256) along K, K a multiple of
 // max(group, 128); a.sx [K/group, M], a.sw [K/group, N].
 hipError_t launch_gemm_grouped(const GemmArgs &a, int group, hipStream_t s);
+hipError_t launch_gemm_grouped_e3m2(const GemmArgs &a, int group, hipStream_t s);
 // Group-wise symmetric int4 of binary32 (f32_in) or fp16 rows: codes
 // [rows, n/2], scales group-major [n/group, rows].
 hipError_t launch_quant_grouped(const void *y, bool f32_in, uint8_t *q, uint16_t *scale,

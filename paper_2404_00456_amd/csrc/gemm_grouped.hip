@@ -679,6 +679,304 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_ring(GemmArgs 
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));  // no DMA may outlive the block's LDS
 }
 
+
+// ------------------------------------------------------------------------
+// Group-wise product on e3m2 operands (the tiled layout of k_pack_e3m2),
+// groups of 128 or 256.  A k-step is one 128-k block of the layout and a
+// group is GS / 128 consecutive k-steps.  One v_mfma_f32_16x16x128_f8f6f4
+// per 16 x 16 slice pair and k-step accumulates the group's products in a
+// binary32 temporary; every product of two codes is an integer of
+// magnitude <= 64 and |acc_g| <= 64 GS < 2^24, so the temporary is
+// f32(acc_g) exactly, and the dequant is two multiplies and an add per
+// output: t = RN(RN(tmp sx[g][m]) sw[g][n]), y_acc = y_acc + t.  No
+// widening, and half the MFMAs of the int4 path.
+//
+// Block tile 256 (m) x 128 (n), eight waves of 64 x 64 as in the int4 ring
+// kernel; a ring of RS stages, each holding the 64-byte heads of the 384
+// stage rows (X rows, then W rows), their 32-byte tails (same order), and
+// the step's group scales: sx in two 256-byte slots, sw in one, a fourth
+// slot for a dummy load.  DMAs of wave w per k-step (1 KB each except the
+// 256-byte scale loads; every instruction reads consecutive bytes):
+//   0, 1  X heads of stage rows 16 w .. + 15 and 128 + 16 w .. + 15
+//   2     W heads of W rows 16 w .. + 15
+//   3     X tails of stage rows 32 w .. + 31
+//   4     waves 0-3: W tails of W rows 32 w .. + 31; waves 4, 5: sx slots
+//         0, 1; wave 6: sw; wave 7: sw again into the dummy slot
+// so that every wave counts the same D = 5 loads in its vmcnt waits.
+template <int GS>
+struct GroupRing6 {
+    static constexpr int GST = GS / 128;           // k-steps per group
+    static constexpr int ROWS = BM + GBN;          // stage rows
+    static constexpr int HEADS = ROWS * 64;        // offset of the tails
+    static constexpr int SCL = HEADS + ROWS * 32;  // offset of the scale slots
+    static constexpr int STAGE = SCL + 4 * 256;
+    static constexpr int RS = 4;                   // ring stages
+    static constexpr int LDS = RS * STAGE;
+    static constexpr int D = 5;                    // loads per wave per k-step
+};
+
+template <int GS>
+__global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_e3m2(GemmArgs a)
+{
+    using C = GroupRing6<GS>;
+    static_assert(GS == 128 || GS == 256, "one or two k-blocks per group");
+    extern __shared__ __align__(16) uint8_t lds[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1, wn = wave & 1;  // 64 x 64 wave tiles
+    const int M = a.M, N = a.N, K = a.K;
+    const int TM = (M + BM - 1) / BM, TN = (N + GBN - 1) / GBN;
+    const int T = TM * TN;
+    const int G = gridDim.x, b = blockIdx.x;
+    const int KT = K / 128;
+
+    const bool xcd = (G % 8 == 0) && (T % 8 == 0) && G <= T;
+    auto tile_pos = [&](int it) -> int {
+        if (xcd) {
+            const int per_x = T / 8, gx = G / 8;
+            const int r = (b >> 3) + it * gx;
+            return r < per_x ? (b & 7) * per_x + r : -1;
+        }
+        const int t = b + it * G;
+        return t < T ? t : -1;
+    };
+    auto tile_mn = [&](int t, int &m0, int &n0) {
+        const int gsize = GM * TN;
+        const int g = t / gsize;
+        const int first = g * GM;
+        const int gm = min(TM - first, GM);
+        const int r = t - g * gsize;
+        m0 = (first + r % gm) * BM;
+        n0 = (r / gm) * GBN;
+    };
+
+    // Operand DMAs in the SGPR-base form: a per-lane 32-bit offset inside
+    // the tile's run of heads (row lane / 4, 16-byte unit lane % 4) or tails
+    // (row lane / 2, half lane % 2), rows past the matrix edge clamped, fixed
+    // per tile; and wave-uniform bases, advanced by one k-block per step.
+    const bool wtail = wave < 4;  // DMA 4 moves W tails (else scales)
+    uint32_t vo[5];
+    auto set_voff = [&](int m0, int n0) {
+        const int xl = M - 1 - m0, wl = N - 1 - n0;
+        vo[0] = (uint32_t)(min(16 * wave + (lane >> 2), xl) * 64 + (lane & 3) * 16);
+        vo[1] = (uint32_t)(min(128 + 16 * wave + (lane >> 2), xl) * 64 + (lane & 3) * 16);
+        vo[2] = (uint32_t)(min(16 * wave + (lane >> 2), wl) * 64 + (lane & 3) * 16);
+        vo[3] = (uint32_t)(min(32 * wave + (lane >> 1), xl) * 32 + (lane & 1) * 16);
+        vo[4] = (uint32_t)(min(32 * (wave & 3) + (lane >> 1), wl) * 32 + (lane & 1) * 16);
+    };
+    const int64_t xblk = (int64_t)M * 96, wblk = (int64_t)N * 96;
+    const uint8_t *bxh, *bwh, *bxt, *bwt;  // bases of the next DMA step
+    auto set_base = [&](int m0, int n0, int sk) {
+        bxh = a.xq + sk * xblk + (int64_t)m0 * 64;
+        bwh = a.wq + sk * wblk + (int64_t)n0 * 64;
+        bxt = a.xq + sk * xblk + (int64_t)M * 64 + (int64_t)m0 * 32;
+        bwt = a.wq + sk * wblk + (int64_t)N * 64 + (int64_t)n0 * 32;
+    };
+    const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void *)lds;
+    // scale load of waves 4-7 for k-step sk of the tile at (m0, n0): 2 fp16
+    // per lane, the element index clamped to an even one inside the vector
+    const int part = wave - 4;
+    auto scale_src = [&](int m0, int n0, int sk) -> const uint16_t * {
+        const int64_t g = sk / C::GST;
+        if (part < 2)
+            return a.sx + g * M + min(m0 + 128 * part + 2 * lane, M - 2);
+        return a.sw + g * N + min(n0 + 2 * lane, N - 2);
+    };
+    auto issue = [&](int sm0, int sn0, int sk, int stage) {
+        const uint32_t sb = lds_base + stage * C::STAGE;
+        dma16s(vo[0], bxh, sb + wave * 1024);
+        dma16s(vo[1], bxh, sb + (wave + 8) * 1024);
+        dma16s(vo[2], bwh, sb + (wave + 16) * 1024);
+        dma16s(vo[3], bxt, sb + C::HEADS + wave * 1024);
+        if (wtail)
+            dma16s(vo[4], bwt, sb + C::HEADS + (wave + 8) * 1024);
+        else
+            dma4(scale_src(sm0, sn0, sk), sb + C::SCL + part * 256);
+    };
+    auto advance = [&]() {
+        bxh += xblk;
+        bwh += wblk;
+        bxt += xblk;
+        bwt += wblk;
+    };
+
+    // LDS reads: X slice j (MFMA B operand) = stage rows wm 64 + 16 j + orow,
+    // W slice i (A operand) = stage rows BM + wn 64 + 16 i + orow; lane group
+    // q takes unit q of the 128-k block: its head at slot q ^ ((r >> 1) & 3),
+    // its tail at slot q ^ ((r >> 2) & 3) (slices start at multiples of 16)
+    const int orow = lane & 15, q = lane >> 4;
+    const int hsl = (q ^ ((orow >> 1) & 3)) << 4, tsl = 8 * (q ^ ((orow >> 2) & 3));
+    const int xh = (wm * 64 + orow) * 64 + hsl, xt = C::HEADS + (wm * 64 + orow) * 32 + tsl;
+    const int wh = (BM + wn * 64 + orow) * 64 + hsl;
+    const int wt = C::HEADS + (BM + wn * 64 + orow) * 32 + tsl;
+    auto rd = [&](const uint8_t *sb, int h, int t) -> Op6 {
+        Op6 o;
+        o.h = *reinterpret_cast<const uint4 *>(sb + h);
+        const uint64_t v = *(const volatile lds_u64 *)(lds_void *)(sb + t);
+        o.t = make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+        return o;
+    };
+
+    int t = tile_pos(0);
+    if (t < 0)
+        return;
+    int m0, n0;
+    tile_mn(t, m0, n0);
+    set_voff(m0, n0);
+    // global step g of this block lives in stage g % RS.  A step's operands
+    // are read from LDS during the step before it, so before step g starts
+    // the loads of step g + 1 must have landed for every wave: only the
+    // latest step's D loads stay in flight across a barrier.
+#pragma unroll
+    for (int s = 0; s < C::RS - 1; ++s) {
+        set_base(m0, n0, min(s, KT - 1));
+        issue(m0, n0, min(s, KT - 1), s);
+    }
+    set_base(m0, n0, C::RS - 1);
+    __asm__ volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::RS - 3) * C::D, 15));
+    __builtin_amdgcn_s_barrier();
+    __asm__ volatile("" ::: "memory");
+    Op6 X[4], W[4];
+    auto read_ops = [&](const uint8_t *sb) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            X[j] = rd(sb, xh + j * 16 * 64, xt + j * 16 * 32);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            W[i] = rd(sb, wh + i * 16 * 64, wt + i * 16 * 32);
+    };
+    read_ops(lds);
+
+    int g = 0;
+    for (int it = 0; t >= 0; ++it) {
+        const int tn_ = tile_pos(it + 1);
+        int m1 = 0, n1 = 0;
+        if (tn_ >= 0)
+            tile_mn(tn_, m1, n1);
+
+        float yacc[4][4][4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    yacc[j][i][r] = 0.0f;
+        v4f tt[4][4];
+
+        // one k-step; FIRST: the group's first (temporaries start at 0),
+        // LAST: its last (dequantize into yacc)
+        auto step = [&](int kt, auto FIRST, auto LAST) {
+            // DMA of global step g + RS - 1 into the stage of step g - 1
+            // (read during step g - 2): this tile's step kt + RS - 1, else
+            // the next tile's, else (no next tile) a harmless re-fetch
+            {
+                const bool here = kt + C::RS - 1 < KT;
+                const int stage = (g + C::RS - 1) % C::RS;
+                if (here || tn_ >= 0) {
+                    const int sk = here ? kt + C::RS - 1 : kt + C::RS - 1 - KT;
+                    if (kt + C::RS - 1 == KT) {
+                        set_voff(m1, n1);
+                        set_base(m1, n1, 0);
+                    }
+                    issue(here ? m0 : m1, here ? n0 : n1, sk, stage);
+                    advance();
+                } else {
+                    set_base(m0, n0, KT - 1);
+                    issue(m0, n0, KT - 1, stage);
+                }
+            }
+            const uint8_t *sb = lds + (g % C::RS) * C::STAGE;
+            // this step's scales (read first: LDS reads complete in order),
+            // sx of the lane's row per X slice, sw of its four columns per W
+            // slice
+            float sxv[4], swv[4][4];
+            if constexpr (decltype(LAST)::value) {
+                const uint16_t *lsc = reinterpret_cast<const uint16_t *>(sb + C::SCL);
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    sxv[j] = h2f(lsc[wm * 64 + j * 16 + orow]);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint2 w2 =
+                        *reinterpret_cast<const uint2 *>(lsc + 256 + wn * 64 + i * 16 + q * 4);
+                    swv[i][0] = h2f((uint16_t)w2.x);
+                    swv[i][1] = h2f((uint16_t)(w2.x >> 16));
+                    swv[i][2] = h2f((uint16_t)w2.y);
+                    swv[i][3] = h2f((uint16_t)(w2.y >> 16));
+                }
+            }
+            static_for<4>([&](auto JI) {
+                constexpr int j = decltype(JI)::value;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    tt[j][i] = mfma6(W[i], X[j], decltype(FIRST)::value ? v4f{0.0f, 0.0f, 0.0f, 0.0f}
+                                                                        : tt[j][i]);
+            });
+            __builtin_amdgcn_sched_barrier(0);
+            // the next step's operands into the same registers (the MFMAs
+            // above have taken theirs); their latency runs under the dequant
+            read_ops(lds + ((g + 1) % C::RS) * C::STAGE);
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (decltype(LAST)::value) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const float u = (tt[j][i][r] * sxv[j]) * swv[i][r];
+                            yacc[j][i][r] = yacc[j][i][r] + u;
+                            __asm__ volatile("" : "+v"(yacc[j][i][r]));
+                        }
+            }
+            // step g + 2 landed for this wave's loads (only step g + RS - 1
+            // may stay in flight; loads complete in order), every LDS read
+            // done; then for every wave
+            __asm__ volatile("" ::: "memory");
+            __builtin_amdgcn_s_waitcnt(waitcnt_imm((C::RS - 3) * C::D, 0));
+            __builtin_amdgcn_s_barrier();
+            __asm__ volatile("" ::: "memory");
+            ++g;
+        };
+        for (int kt = 0; kt < KT; kt += C::GST) {
+            if constexpr (C::GST == 1) {
+                step(kt, std::true_type{}, std::true_type{});
+            } else {
+                step(kt, std::true_type{}, std::false_type{});
+                step(kt + 1, std::false_type{}, std::true_type{});
+            }
+        }
+
+        // epilogue: lane holds n = nb + r (r < 4) of m = mb + orow per slice
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int m = m0 + wm * 64 + j * 16 + orow;
+            if (m >= M)
+                continue;
+            uint16_t *yrow = a.y + (int64_t)m * N;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int nb = n0 + wn * 64 + i * 16 + q * 4;
+                if (nb >= N)
+                    continue;  // N is a multiple of 8: a quad is all in or all out
+                const h2 lo = __builtin_convertvector((f2){yacc[j][i][0], yacc[j][i][1]}, h2);
+                const h2 hi = __builtin_convertvector((f2){yacc[j][i][2], yacc[j][i][3]}, h2);
+                uint2 pk;
+                pk.x = __builtin_bit_cast(uint32_t, lo);
+                pk.y = __builtin_bit_cast(uint32_t, hi);
+                *reinterpret_cast<uint2 *>(yrow + nb) = pk;
+            }
+        }
+
+        t = tn_;
+        m0 = m1;
+        n0 = n1;
+    }
+    __asm__ volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));  // no DMA may outlive the block's LDS
+}
 }  // namespace
 
 namespace {
@@ -718,6 +1016,32 @@ hipError_t gemm_grouped_as(const GemmArgs &a, hipStream_t s)
                        a);
     return hipGetLastError();
 }
+
+template <int GS>
+hipError_t gemm_grouped_e3m2_as(const GemmArgs &a, hipStream_t s)
+{
+    using C = GroupRing6<GS>;
+    if (a.K % GS || a.M % 8 || a.N % 8)
+        return hipErrorInvalidValue;
+    const int tiles = ((a.M + BM - 1) / BM) * ((a.N + GBN - 1) / GBN);
+    hipError_t e = hipFuncSetAttribute((const void *)k_gemm_w4a4_grouped_e3m2<GS>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+    if (e != hipSuccess)
+        return e;
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+        cus = 256;
+    // persistent: one block per CU, or one per tile when there are fewer
+    // tiles or fewer k-steps than ring stages
+    int grid = (tiles < cus || a.K / 128 < C::RS) ? tiles : cus;
+    if (grid >= 8 && tiles % 8 == 0)
+        grid -= grid % 8;
+    hipLaunchKernelGGL(k_gemm_w4a4_grouped_e3m2<GS>, dim3((unsigned)grid), dim3(THREADS), C::LDS,
+                       s, a);
+    return hipGetLastError();
+}
 }  // namespace
 
 hipError_t launch_gemm_grouped(const GemmArgs &a, int group, hipStream_t s)
@@ -728,6 +1052,17 @@ hipError_t launch_gemm_grouped(const GemmArgs &a, int group, hipStream_t s)
     case 64: return gemm_grouped_as<64>(a, s);
     case 128: return gemm_grouped_as<128>(a, s);
     case 256: return gemm_grouped_as<256>(a, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_grouped_e3m2(const GemmArgs &a, int group, hipStream_t s)
+{
+    if (a.M == 0 || a.N == 0)
+        return hipSuccess;
+    switch (group) {
+    case 128: return gemm_grouped_e3m2_as<128>(a, s);
+    case 256: return gemm_grouped_e3m2_as<256>(a, s);
     }
     return hipErrorInvalidValue;
 }

@@ -222,26 +222,6 @@ struct Ring {
     static constexpr int LDS = BYTES + Tile<TBM>::SCALE_BYTES;
 };
 
-typedef int v8i __attribute__((ext_vector_type(8)));
-typedef __attribute__((address_space(3))) uint64_t lds_u64;
-typedef float v4f __attribute__((ext_vector_type(4)));
-
-// One e3m2 operand slice of a lane: 32 codes, six dwords (head, tail).
-struct Op6 {
-    uint4 h;
-    uint2 t;
-};
-
-// v_mfma_f32_16x16x128_f8f6f4 with both operands e3m2 (format 3), no scale.
-// Every product of two codes is an integer of magnitude <= 64 and every
-// partial sum an integer below 2^24, so the binary32 accumulation is exact.
-__device__ __forceinline__ v4f mfma6(const Op6 &a, const Op6 &b, v4f c)
-{
-    const v8i av = {(int)a.h.x, (int)a.h.y, (int)a.h.z, (int)a.h.w, (int)a.t.x, (int)a.t.y, 0, 0};
-    const v8i bv = {(int)b.h.x, (int)b.h.y, (int)b.h.z, (int)b.h.w, (int)b.t.x, (int)b.t.y, 0, 0};
-    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(av, bv, c, 3, 3, 0, 0, 0, 0);
-}
-
 template <int BITS>
 struct AccOf {
     typedef v4i type;

@@ -80,6 +80,8 @@ int main()
            QUAROT_ERR_INVALID_ARG);
     EXPECT(quarot_quant_int4_grouped(H, B, H2, 4, 256, 96, 1, 1.0f, P, 1 << 20, nullptr) != 0, 1);
     EXPECT(quarot_w4a4_gemm_grouped(B, H, B, H, H2, 4, 4, 256, 32, nullptr) != 0, 1);
+    EXPECT(quarot_w4a4_gemm_grouped_e3m2(B, H, B, H, H2, 8, 8, 256, 64, nullptr) != 0, 1);
+    EXPECT(quarot_w4a4_gemm_grouped_e3m2(B, H, B, H, H2, 12, 8, 256, 128, nullptr) != 0, 1);
     EXPECT(quarot_kv_quant(H, B, H2, H2, 4, 128, 256, 1, 0.95f, nullptr),
            QUAROT_ERR_UNSUPPORTED_SIZE);
     EXPECT(quarot_kv_dequant(B, H, H, H2, 4, 96, 32, 0, nullptr) != 0, 1);

@@ -17,6 +17,7 @@ hipError_t launch_rotate(const RotArgs &, int, bool, int, int, hipStream_t, int)
 hipError_t launch_gemm(const GemmArgs &, hipStream_t, int) { return stub(); }
 hipError_t launch_pack_e3m2(const uint8_t *, uint8_t *, int64_t, int, hipStream_t) { return stub(); }
 hipError_t launch_gemm_grouped(const GemmArgs &, int, hipStream_t) { return stub(); }
+hipError_t launch_gemm_grouped_e3m2(const GemmArgs &, int, hipStream_t) { return stub(); }
 hipError_t launch_quant_grouped(const void *, bool, uint8_t *, uint16_t *, int64_t, int, int, float,
                                 hipStream_t)
 {

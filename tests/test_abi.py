@@ -219,6 +219,15 @@ def test_invalid_arguments_rejected_before_device(L):
     assert GG(P, None, P, P, P, 4, 4, 256, 128, S) == INVALID
     assert GG(P, P, P, P, UNALIGNED, 4, 4, 256, 128, S) == ALIGN
     assert GG(None, None, None, None, None, 0, 4, 256, 128, S) == OK
+    G6 = L.quarot_w4a4_gemm_grouped_e3m2
+    assert G6(P, P, P, P, P, 8, 8, 256, 64, S) == UNSUPPORTED    # one instruction spans 128 k
+    assert G6(P, P, P, P, P, 12, 8, 256, 128, S) == UNSUPPORTED  # M not a multiple of 8
+    assert G6(P, P, P, P, P, 8, 20, 256, 128, S) == UNSUPPORTED  # N not a multiple of 8
+    assert G6(P, P, P, P, P, 8, 8, 384, 256, S) == UNSUPPORTED   # K not a multiple of 256
+    assert G6(P, P, P, P, P, 8, 8, 256, 0, S) == INVALID
+    assert G6(P, None, P, P, P, 8, 8, 256, 128, S) == INVALID
+    assert G6(P, P, P, P, UNALIGNED, 8, 8, 256, 128, S) == ALIGN
+    assert G6(None, None, None, None, None, 0, 8, 256, 128, S) == OK
     LG = L.quarot_linear_w4a4_grouped
     need = L.quarot_linear_w4a4_grouped_workspace_size(3, 256, 128, 1)
     assert need == 512 + 256 + 3 * 256 * 4  # codes, scales, binary32 rows (256-B rounded)
@@ -280,6 +289,7 @@ def test_no_device_reported(L):
     assert L.quarot_quant_int4_grouped(P, P2, P, 4, 128, 128, 1, 1.0, P, 1 << 20,
                                        None) == NODEV
     assert L.quarot_w4a4_gemm_grouped(P, P, P, P, P, 4, 4, 256, 64, None) == NODEV
+    assert L.quarot_w4a4_gemm_grouped_e3m2(P, P, P, P, P, 8, 8, 256, 128, None) == NODEV
     cus, clk = ctypes.c_int(), ctypes.c_int()
     assert L.quarot_device_peaks(ctypes.byref(cus), ctypes.byref(clk)) == NODEV
     assert L.quarot_mfma_probe(P, 4, 10, None) == NODEV

@@ -97,6 +97,79 @@ def test_gemm_grouped_extremes(dev, orc):
     assert_fp16_close(H(y), ry, "grouped extremes")
 
 
+# ---- the same product on e3m2 operands (quarot_pack_e3m2 of the codes) ----
+
+def grouped_e3m2(q, dev, xq, sx, wq, sw, group):
+    return q.quarot_w4a4_gemm_grouped_e3m2(q.quarot_pack_e3m2(T(xq, dev)), T(sx, dev),
+                                           q.quarot_pack_e3m2(T(wq, dev)), T(sw, dev),
+                                           group=group)
+
+
+@pytest.mark.parametrize("M,N,K,group", [
+    # one tile, a single k-step or one group of two (fewer k-steps than ring
+    # stages: one tile per block)
+    (8, 8, 128, 128), (8, 8, 256, 256), (8, 16, 384, 128),
+    # ragged tiles in both directions, several groups
+    (264, 136, 2048, 128), (264, 136, 2048, 256), (520, 392, 1280, 128),
+    # 32 tiles with 2 / 3 / 4 k-steps
+    (1024, 1024, 256, 128), (1024, 1024, 384, 128), (1024, 1024, 512, 256),
+    # the largest K
+    (24, 8192, 65536, 128), (16, 264, 65536, 256)])
+def test_gemm_grouped_e3m2(dev, orc, M, N, K, group):
+    import paper_2404_00456_amd as q
+    say(f"grouped e3m2 gemm M={M} N={N} K={K} group={group}")
+    xq, sx, wq, sw = rand_group_case(M * 7 + N + K + group, M, N, K, group)
+    y = grouped_e3m2(q, dev, xq, sx, wq, sw, group)
+    ry = orc.gemm_grouped(xq, sx, wq, sw, group=group)
+    assert_fp16_close(H(y), ry, f"grouped e3m2 y M={M} N={N} K={K} G={group}")
+
+
+@pytest.mark.parametrize("M,N,K,group", [(2200, 8400, 1024, 128), (2304, 8448, 768, 256),
+                                         (4096, 4096, 2048, 128)])
+def test_gemm_grouped_e3m2_many_tiles(dev, orc, M, N, K, group):
+    """More 256 x 128 tiles than compute units (the persistent ring runs
+    across tiles), ragged edges; the oracle on sampled rows, and every output
+    against the int4-operand kernel."""
+    import paper_2404_00456_amd as q
+    say(f"grouped e3m2 gemm many tiles M={M} N={N} K={K} group={group}")
+    xq, sx, wq, sw = rand_group_case(M + 3 * N + K, M, N, K, group)
+    y = grouped_e3m2(q, dev, xq, sx, wq, sw, group)
+    y4 = q.quarot_w4a4_gemm_grouped(T(xq, dev), T(sx, dev), T(wq, dev), T(sw, dev), group=group)
+    rows = np.sort(np.random.default_rng(4).choice(M, 24, replace=False))
+    rows[0], rows[-1] = 0, M - 1
+    ry = orc.gemm_grouped(xq[rows], np.ascontiguousarray(sx[:, rows]), wq, sw, group=group)
+    yh = H(y)
+    assert_fp16_close(yh[rows], ry, f"grouped e3m2 y rows M={M} N={N} K={K} G={group}")
+    assert_same(yh.view(np.uint16), H(y4).view(np.uint16), "e3m2 == int4 operands")
+
+
+def test_gemm_grouped_e3m2_extremes(dev, orc):
+    """All -8 codes (|acc_g| = 64 G, the largest) and scales spanning fp16
+    subnormals."""
+    import paper_2404_00456_amd as q
+    M, N, K, group = 304, 264, 4096, 256
+    rng = np.random.default_rng(6)
+    xq = np.full((M, K // 2), 0x88, np.uint8)
+    wq = rng.integers(0, 256, size=(N, K // 2), dtype=np.uint8)
+    wq[0] = 0x88
+    sx = (2.0 ** rng.uniform(-24, -14, (K // group, M))).astype(np.float16)
+    sw = (2.0 ** rng.uniform(-14, -8, (K // group, N))).astype(np.float16)
+    y = grouped_e3m2(q, dev, xq, sx, wq, sw, group)
+    ry = orc.gemm_grouped(xq, sx, wq, sw, group=group)
+    assert (np.abs(ry.astype(np.float32)) < 2.0 ** -14).mean() > 0.05
+    assert_fp16_close(H(y), ry, "grouped e3m2 extremes")
+
+
+def test_gemm_grouped_e3m2_refusals(dev):
+    import paper_2404_00456_amd as q
+    xq, sx, wq, sw = rand_group_case(1, 16, 16, 256, 64)
+    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+        grouped_e3m2(q, dev, xq, sx, wq, sw, 64)
+    xq, sx, wq, sw = rand_group_case(1, 12, 16, 256, 128)
+    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+        grouped_e3m2(q, dev, xq, sx, wq, sw, 128)
+
+
 @pytest.mark.parametrize("name,group,sample", [("tiny", 64, None), ("llama2_7b_up", 128, 64),
                                                ("llama2_7b_down", 128, 48),
                                                ("llama2_7b_up", 256, 32),
@@ -130,3 +203,9 @@ def test_linear_grouped(dev, orc, name, group, sample):
     assert_fp16_close(H(y_d)[rows], ry, f"{name} grouped y")
     assert_same(H(y2_d)[rows].view(np.uint16), H(y_d)[rows].view(np.uint16),
                 f"{name} linear == quant + gemm")
+    if group >= 128 and wl.M % 8 == 0 and wl.N % 8 == 0:
+        y6_d = q.quarot_w4a4_gemm_grouped_e3m2(q.quarot_pack_e3m2(xq_d), sx_d,
+                                               q.quarot_pack_e3m2(wq_d), sw_d, group=group)
+        assert_fp16_close(H(y6_d)[rows], ry, f"{name} grouped y, e3m2 operands")
+        assert_same(H(y6_d).view(np.uint16), H(y_d).view(np.uint16),
+                    f"{name} e3m2 == int4 operands")
