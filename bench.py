@@ -30,6 +30,7 @@ Prints one JSON line.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -143,6 +144,7 @@ def bench_kv(q, workloads, torch, np, dev, stream, iters):
     attend()
     torch.cuda.synchronize()
     a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    quiet_host()
     a0.record(stream)
     for _ in range(10 * iters):
         attend()
@@ -151,6 +153,7 @@ def bench_kv(q, workloads, torch, np, dev, stream, iters):
     att_us = a0.elapsed_time(a1) / (10 * iters) * 1e3
     att_bytes = 2 * (rows * wl.D // 2 + rows * (wl.D // wl.group) * 4)  # K and V caches
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(iters)]
+    quiet_host()
     log(f"timing kv x{iters}")
     for it in range(iters):
         once(evs[it])
@@ -185,6 +188,7 @@ def event_times_us(torch, stream, fns, iters):
     iters times, from HIP events on the launch stream."""
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)]
           for _ in range(iters)]
+    quiet_host()
     for it in range(iters):
         for j, fn in enumerate(fns):
             ev[it][j].record(stream)
@@ -345,9 +349,18 @@ def cpu_oracle_per_config(workloads, np, inputs):
     return out
 
 
+def quiet_host():
+    """Collect Python's cyclic garbage now, outside any timed region.  The
+    collector is off for the whole run (main): a collection pass in the
+    middle of a timed loop stalls the host for tens of milliseconds, the GPU
+    runs dry, and the events count the idle time."""
+    gc.collect()
+
+
 def time_us(torch, stream, fn, iters=10):
     fn()
     torch.cuda.synchronize()
+    quiet_host()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(iters):
@@ -455,6 +468,7 @@ def bench_next(q, torch, dev, stream, layers):
 
 
 def main():
+    gc.disable()  # collections happen only at quiet_host(), between timed regions
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
@@ -557,6 +571,7 @@ def main():
     torch.cuda.synchronize()
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    quiet_host()
     log(f"timing {args.steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -571,6 +586,7 @@ def main():
     for _ in range(args.warmup):
         step_int4()
     ev4 = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    quiet_host()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
@@ -625,6 +641,7 @@ def main():
     probe_out = torch.empty(cus * 512, dtype=torch.int32, device=dev)
     probe_ops = q.quarot_mfma_probe(probe_out, cus, 2000)
     torch.cuda.synchronize()
+    quiet_host()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(10):
@@ -634,6 +651,7 @@ def main():
     probe_tops = probe_ops * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e12
     probe6_ops = q.quarot_mfma_probe_fp6(probe_out, cus, 2000)
     torch.cuda.synchronize()
+    quiet_host()
     e0.record(stream)
     for _ in range(10):
         q.quarot_mfma_probe_fp6(probe_out, cus, 2000)

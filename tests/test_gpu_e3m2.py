@@ -96,7 +96,12 @@ def _gemm_case(dev, orc, M, N, K, xq, wq, sx, sw):
                                    (300, 520, 1024), (513, 100, 4096), (64, 1000, 11008),
                                    (256, 256, 28672), (2, 3, 65536),
                                    (2048, 8448, 128), (2048, 8448, 256), (2048, 8448, 384),
-                                   (2304, 8448, 512), (2200, 8400, 1024)])
+                                   (2304, 8448, 512), (2200, 8400, 1024),
+                                   # whole 256 x 256 tiles and an even number of
+                                   # k-steps (four 128 x 128 waves per block):
+                                   # one tile, one per block, several per block
+                                   (512, 512, 1024), (2048, 8192, 1280), (4096, 8192, 512),
+                                   (8192, 4096, 768), (4352, 4352, 1536)])
 def test_gemm_e3m2_exact(dev, orc, M, N, K):
     """Ragged edges, k-step counts below, at and above the LDS ring depth,
     blocks that walk several tiles, the largest K."""
