@@ -920,16 +920,39 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_e3m2(GemmArgs 
             read_ops(lds + ((g + 1) % C::RS) * C::STAGE);
             __builtin_amdgcn_sched_barrier(0);
             if constexpr (decltype(LAST)::value) {
+                // per X slice, in three batches of 16 independent operations
+                // (multiply by sx, multiply by sw, add), so that consecutive
+                // VALU instructions of a wave do not wait on each other; each
+                // output still takes RN(RN(acc sx) sw), then one add
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+                for (int j = 0; j < 4; ++j) {
+                    float u[4][4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            u[i][r] = tt[j][i][r] * sxv[j];
+                    __asm__ volatile("" : "+v"(u[0][0]), "+v"(u[0][1]), "+v"(u[0][2]), "+v"(u[0][3]),
+                                     "+v"(u[1][0]), "+v"(u[1][1]), "+v"(u[1][2]), "+v"(u[1][3]),
+                                     "+v"(u[2][0]), "+v"(u[2][1]), "+v"(u[2][2]), "+v"(u[2][3]),
+                                     "+v"(u[3][0]), "+v"(u[3][1]), "+v"(u[3][2]), "+v"(u[3][3]));
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            u[i][r] = u[i][r] * swv[i][r];
+                    __asm__ volatile("" : "+v"(u[0][0]), "+v"(u[0][1]), "+v"(u[0][2]), "+v"(u[0][3]),
+                                     "+v"(u[1][0]), "+v"(u[1][1]), "+v"(u[1][2]), "+v"(u[1][3]),
+                                     "+v"(u[2][0]), "+v"(u[2][1]), "+v"(u[2][2]), "+v"(u[2][3]),
+                                     "+v"(u[3][0]), "+v"(u[3][1]), "+v"(u[3][2]), "+v"(u[3][3]));
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
-                            const float u = (tt[j][i][r] * sxv[j]) * swv[i][r];
-                            yacc[j][i][r] = yacc[j][i][r] + u;
+                            yacc[j][i][r] = yacc[j][i][r] + u[i][r];
                             __asm__ volatile("" : "+v"(yacc[j][i][r]));
                         }
+                }
             }
             // step g + 2 landed for this wave's loads (only step g + RS - 1
             // may stay in flight; loads complete in order), every LDS read
