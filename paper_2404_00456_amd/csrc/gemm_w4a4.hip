@@ -292,7 +292,18 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     // this block's tiles: logical positions b, b + G, ... within a
     // per-XCD ordering when the grid and the tile count allow it
     const bool xcd = (G % 8 == 0) && (T % 8 == 0) && G <= T;
+    // With 256 blocks and tile counts that are multiples of 16 both ways the
+    // chip works through 16 x 16-tile super-blocks, one per round: XCD x
+    // takes the 4 (m) x 8 (n) sub-block (x % 4, x / 4) of it, its 32 blocks
+    // one tile each, so an XCD's L2 serves 4 X and 8 W panels as in the
+    // order below, while the whole chip touches 16 X and 16 W panels per
+    // round instead of every X panel.  Rounds run along n within a row of
+    // super-blocks, in alternating directions, so that the X panels of a
+    // row and the W panels at its turns come back from the last-level cache.
+    const bool sblk = G == 256 && TM % 16 == 0 && TN % 16 == 0;
     auto tile_pos = [&](int it) -> int {  // it-th tile of this block, or -1
+        if (sblk)
+            return it < T / 256 ? it * 256 + b : -1;
         if (xcd) {
             const int per_x = T / 8, gx = G / 8;
             const int r = (b >> 3) + it * gx;
@@ -302,6 +313,14 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
         return t < T ? t : -1;
     };
     auto tile_mn = [&](int t, int &m0, int &n0) {
+        if (sblk) {
+            const int r = t >> 8, x = t & 7, s = (t >> 3) & 31;
+            const int nsb = TN / 16, mb = r / nsb, nr = r - mb * nsb;
+            const int nb = (mb & 1) ? nsb - 1 - nr : nr;
+            m0 = (mb * 16 + (x & 3) * 4 + (s & 3)) * TBM;
+            n0 = (nb * 16 + (x >> 2) * 8 + (s >> 2)) * BN;
+            return;
+        }
         const int gsize = GM * TN;
         const int g = t / gsize;
         const int first = g * GM;
