@@ -58,8 +58,8 @@ def log(*a):
 # kernel machine code they were taken with (its fingerprint); after any
 # change to it the figure is reported as null.
 GEMM_TRAFFIC = {
-    "k_gemm_w4a4": {"isa_sha256_16": "cd4bd1cd7a309196", "bytes_per_launch": 3.462e+09},
-    "k_gemm_w4a4_e3m2": {"isa_sha256_16": "4406ce9175bf81a2", "bytes_per_launch": 4.927e+09},
+    "k_gemm_w4a4": {"isa_sha256_16": "a959ef97d8288dd6", "bytes_per_launch": 3.470e+09},
+    "k_gemm_w4a4_e3m2": {"isa_sha256_16": "869819c9cf015403", "bytes_per_launch": 4.838e+09},
 }
 
 
