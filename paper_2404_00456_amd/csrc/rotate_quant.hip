@@ -33,6 +33,9 @@
 
 namespace quarot {
 
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef int v6i __attribute__((ext_vector_type(6)));
+
 __constant__ HmMfmaB<108> c_hmb108 = HmMfmaB<108>();
 __constant__ HmMfmaB<172> c_hmb172 = HmMfmaB<172>();
 
@@ -127,19 +130,13 @@ __device__ __forceinline__ uint32_t e3m2_code(float y, const Divisor &d)
     return d.ok ? e3m2_of_bits(__float_as_uint(r)) : 0u;
 }
 
-// Codes of the 8 elements i0 .. i0+7 (i0 a multiple of 8) of row r into the
-// tiled e3m2 layout: their 48 bits are bytes 6p .. 6p+5 of the 24 of unit u
-// (i0 = 128 b + 32 u + 8 p), whose bytes 0-15 are the head and 16-23 the
-// tail; each lane writes one dword and one short.
-__device__ __forceinline__ void store_e3m2_8(uint8_t *q, int64_t rows, int64_t r, int64_t i0,
-                                             const float *v, const Divisor &d)
+// The 48 code bits (lo, then the low 16 of hi) of the 8 elements i0 .. i0+7
+// (i0 a multiple of 8) of row r into the tiled e3m2 layout: bytes 6p .. 6p+5
+// of the 24 of unit u (i0 = 128 b + 32 u + 8 p), whose bytes 0-15 are the
+// head and 16-23 the tail; each lane writes one dword and one short.
+__device__ __forceinline__ void store_e3m2_48(uint8_t *q, int64_t rows, int64_t r, int64_t i0,
+                                              uint32_t lo, uint32_t hi)
 {
-    uint32_t c[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-        c[e] = e3m2_code(v[e], d);
-    const uint32_t lo = c[0] | (c[1] << 6) | (c[2] << 12) | (c[3] << 18) | (c[4] << 24) | (c[5] << 30);
-    const uint32_t hi = (c[5] >> 2) | (c[6] << 4) | (c[7] << 10);
     const int p = (int)(i0 >> 3) & 3, u = (int)(i0 >> 5) & 3, b = (int)(i0 >> 7);
     const int64_t h = e3m2_head(rows, r, b, u), t = e3m2_tail(rows, r, b, u);
     const bool odd = (p & 1) != 0;
@@ -149,6 +146,20 @@ __device__ __forceinline__ void store_e3m2_8(uint8_t *q, int64_t rows, int64_t r
     const int64_t sa = p == 0 ? h + 4 : p == 1 ? h + 6 : p == 2 ? t : t + 2;
     *reinterpret_cast<uint32_t *>(q + da) = dw;
     *reinterpret_cast<uint16_t *>(q + sa) = sh;
+}
+
+// The 8 codes of elements i0 .. i0+7 from their binary32 values, stored as
+// above (the paths that hold fewer than four chunks of a row per lane).
+__device__ __forceinline__ void store_e3m2_8(uint8_t *q, int64_t rows, int64_t r, int64_t i0,
+                                             const float *v, const Divisor &d)
+{
+    uint32_t c[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        c[e] = e3m2_code(v[e], d);
+    const uint32_t lo = c[0] | (c[1] << 6) | (c[2] << 12) | (c[3] << 18) | (c[4] << 24) | (c[5] << 30);
+    const uint32_t hi = (c[5] >> 2) | (c[6] << 4) | (c[7] << 10);
+    store_e3m2_48(q, rows, r, i0, lo, hi);
 }
 
 // The symmetric epilogues: scale divisor, row stride of the codes, and the
@@ -499,10 +510,64 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
         const uint16_t s16 = f2h(s32);
         const Divisor dv = make_divisor(h2f(s16));
         if constexpr (EPI == EPI_E3M2) {
+            // The codes as binary32 integers, four chunks (32 codes) at a
+            // time through the fp6 pack conversion: its 192-bit result holds
+            // code 2i of the first source and 2i + 1 of the second at bits
+            // 12 i and 12 i + 6, so with chunk c's even codes at first-source
+            // slots 4c .. 4c + 3 and its odd ones at the same second-source
+            // slots, the chunk's 8 codes are bits 48 c .. 48 c + 47 in order.
+            uint8_t *q6 = static_cast<uint8_t *>(a.out);
+            // With 16 or more lanes per row a lane's 8 codes sit at the same
+            // place p = pos mod 4 of unit (pos / 4) mod 4 of k-block
+            // (c W + w) L / 16 + pos / 64 for chunk c: from chunk to chunk its
+            // dword and short move by W L / 16 k-blocks.  (Shorter rows take
+            // store_e3m2_48 per chunk.)
+            constexpr bool STRIDED = L >= 16;
+            uint8_t *dp = nullptr, *sp = nullptr;
+            const int64_t kstep = (int64_t)(W * L / 16) * a.rows * 96;
+            const bool podd = (pos & 1) != 0;
+            if constexpr (STRIDED) {
+                const int p = pos & 3, u = (pos >> 2) & 3, b0 = w * L / 16 + (pos >> 4);
+                const int64_t h = e3m2_head(a.rows, row, b0, u), t = e3m2_tail(a.rows, row, b0, u);
+                dp = q6 + (p == 0 ? h : p == 1 ? h + 8 : p == 2 ? h + 12 : t + 4);
+                sp = q6 + (p == 0 ? h + 4 : p == 1 ? h + 6 : p == 2 ? t : t + 2);
+            }
 #pragma unroll
-            for (int cc = 0; cc < C; ++cc)
-                store_e3m2_8(static_cast<uint8_t *>(a.out), a.rows, row,
-                             ((cc * W + w) * L + pos) * 8, v[cc], dv);
+            for (int c0 = 0; c0 < C; c0 += 4) {
+                v16f ev, od;
+#pragma unroll
+                for (int c = 0; c < 4 && c0 + c < C; ++c)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const float t = fminf(fmaxf(quotient(v[c0 + c][e], dv), -8.0f), 7.0f);
+                        const float r = (t + 0x1.8p23f) - 0x1.8p23f;
+                        if (e & 1)
+                            od[4 * c + (e >> 1)] = r;
+                        else
+                            ev[4 * c + (e >> 1)] = r;
+                    }
+                v6i c6 = __builtin_amdgcn_cvt_scalef32_2xpk16_bf6_f32(ev, od, 1.0f);
+                if (!dv.ok)  // zero or infinite scale: codes 0
+                    c6 = v6i{0, 0, 0, 0, 0, 0};
+#pragma unroll
+                for (int c = 0; c < 4 && c0 + c < C; ++c) {
+                    const int d = 3 * (c >> 1);  // first dword of the chunk pair
+                    const uint32_t lo = (c & 1) ? __builtin_amdgcn_alignbit((uint32_t)c6[d + 2],
+                                                                           (uint32_t)c6[d + 1], 16)
+                                                : (uint32_t)c6[d];
+                    const uint32_t hi = (c & 1) ? (uint32_t)c6[d + 2] >> 16
+                                                : (uint32_t)c6[d + 1] & 0xFFFFu;
+                    if constexpr (STRIDED) {
+                        *reinterpret_cast<uint32_t *>(dp + (c0 + c) * kstep) =
+                            podd ? (lo >> 16) | (hi << 16) : lo;
+                        *reinterpret_cast<uint16_t *>(sp + (c0 + c) * kstep) =
+                            (uint16_t)(podd ? lo : hi);
+                    } else {
+                        store_e3m2_48(q6, a.rows, row, ((c0 + c) * W + w) * L * 8 + pos * 8, lo,
+                                      hi);
+                    }
+                }
+            }
         } else {
             uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(N);
 #pragma unroll
