@@ -120,16 +120,6 @@ __device__ __forceinline__ uint32_t sym8_code(float y, const Divisor &d, float q
     return d.ok ? c : 0u;
 }
 
-// The EPI_SYM code of y as an e3m2 number: the same clamp and rounding, with
-// the rounded value kept as a binary32 integer (t + 1.5 * 2^23 rounds t to
-// an integer; subtracting 1.5 * 2^23 again is exact).
-__device__ __forceinline__ uint32_t e3m2_code(float y, const Divisor &d)
-{
-    const float t = fminf(fmaxf(quotient(y, d), -8.0f), 7.0f);
-    const float r = (t + 0x1.8p23f) - 0x1.8p23f;
-    return d.ok ? e3m2_of_bits(__float_as_uint(r)) : 0u;
-}
-
 // The 48 code bits (lo, then the low 16 of hi) of the 8 elements i0 .. i0+7
 // (i0 a multiple of 8) of row r into the tiled e3m2 layout: bytes 6p .. 6p+5
 // of the 24 of unit u (i0 = 128 b + 32 u + 8 p), whose bytes 0-15 are the
@@ -148,19 +138,6 @@ __device__ __forceinline__ void store_e3m2_48(uint8_t *q, int64_t rows, int64_t 
     *reinterpret_cast<uint16_t *>(q + sa) = sh;
 }
 
-// The 8 codes of elements i0 .. i0+7 from their binary32 values, stored as
-// above (the paths that hold fewer than four chunks of a row per lane).
-__device__ __forceinline__ void store_e3m2_8(uint8_t *q, int64_t rows, int64_t r, int64_t i0,
-                                             const float *v, const Divisor &d)
-{
-    uint32_t c[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-        c[e] = e3m2_code(v[e], d);
-    const uint32_t lo = c[0] | (c[1] << 6) | (c[2] << 12) | (c[3] << 18) | (c[4] << 24) | (c[5] << 30);
-    const uint32_t hi = (c[5] >> 2) | (c[6] << 4) | (c[7] << 10);
-    store_e3m2_48(q, rows, r, i0, lo, hi);
-}
 
 // The symmetric epilogues: scale divisor, row stride of the codes, and the
 // codes of 8 (or 4) consecutive elements starting at element i0 of a row:
@@ -803,28 +780,39 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
         const uint16_t s16 = f2h(s32);
         const Divisor dv = make_divisor(h2f(s16));
         if constexpr (EPI == EPI_E3M2) {
-            // a lane's M codes do not fill whole 32-code units: the row's int4
-            // codes go through LDS, then each thread packs whole units
-            __shared__ uint4 stage[N / 32];
+            // a lane's M codes do not fill whole 32-code units: the row's
+            // codes go through LDS as signed bytes (the EPI_SYM decision:
+            // clamp to -8..7, ties to even; 0 for a zero or infinite scale),
+            // then each thread takes whole units: 32 bytes back to binary32
+            // and one fp6 pack conversion (code 2i from slot i of the first
+            // source, 2i + 1 from slot i of the second)
+            __shared__ uint4 stage[N / 16];
             uint8_t *st = reinterpret_cast<uint8_t *>(stage);
 #pragma unroll
             for (int cc = 0; cc < C; ++cc) {
                 const int g = (cc * W + w) * L + pos;
 #pragma unroll
                 for (int p = 0; p < M / 4; ++p)
-                    store_codes4<EPI_SYM>(st, g * M + 4 * p, &v[cc][4 * p], dv, qd);
+                    store_codes4<EPI_SYM8>(st, g * M + 4 * p, &v[cc][4 * p], dv, 7.0f);
             }
             __syncthreads();
             uint8_t *q = static_cast<uint8_t *>(a.out);
             for (int u = tid; u < N / 32; u += 64 * W) {
-                const uint4 in = stage[u];
-                const uint32_t wd[4] = {in.x, in.y, in.z, in.w};
-                uint32_t o[6];
-                e3m2_unit(wd, o);
+                const uint4 in0 = stage[2 * u], in1 = stage[2 * u + 1];
+                const uint32_t wd[8] = {in0.x, in0.y, in0.z, in0.w, in1.x, in1.y, in1.z, in1.w};
+                v16f ev, od;
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    ev[2 * k] = (float)(int8_t)(wd[k] & 0xFFu);
+                    od[2 * k] = (float)(int8_t)((wd[k] >> 8) & 0xFFu);
+                    ev[2 * k + 1] = (float)(int8_t)((wd[k] >> 16) & 0xFFu);
+                    od[2 * k + 1] = (float)(int8_t)(wd[k] >> 24);
+                }
+                const v6i o = __builtin_amdgcn_cvt_scalef32_2xpk16_bf6_f32(ev, od, 1.0f);
                 *reinterpret_cast<uint4 *>(q + e3m2_head(a.rows, row, u >> 2, u & 3)) =
-                    make_uint4(o[0], o[1], o[2], o[3]);
+                    make_uint4((uint32_t)o[0], (uint32_t)o[1], (uint32_t)o[2], (uint32_t)o[3]);
                 *reinterpret_cast<uint2 *>(q + e3m2_tail(a.rows, row, u >> 2, u & 3)) =
-                    make_uint2(o[4], o[5]);
+                    make_uint2((uint32_t)o[4], (uint32_t)o[5]);
             }
         } else {
             uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(N);
@@ -1092,17 +1080,45 @@ __global__ __launch_bounds__(256, 2) void k_rot_largem(RotArgs a)
         const float s32 = (amax * a.clip) / qd;
         const uint16_t s16 = f2h(s32);
         const Divisor dv = make_divisor(h2f(s16));
-        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(n);
-        for (int ch = tid; ch < chunks; ch += 64 * W) {
-            float y[8];
-            row8(ch, y);
+        if constexpr (EPI == EPI_E3M2) {
+            // a thread takes whole units (32 consecutive codes) through one
+            // fp6 pack conversion (code 2i from slot i of the first source,
+            // 2i + 1 from slot i of the second)
+            uint8_t *q6 = static_cast<uint8_t *>(a.out);
+            for (int u = tid; u < chunks / 4; u += 64 * W) {
+                v16f ev, od;
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                y[e] = y[e] * c;
-            if constexpr (EPI == EPI_E3M2)
-                store_e3m2_8(static_cast<uint8_t *>(a.out), a.rows, row, ch * 8, y, dv);
-            else
+                for (int k = 0; k < 4; ++k) {
+                    float y[8];
+                    row8(4 * u + k, y);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const float t = fminf(fmaxf(quotient(y[e] * c, dv), -8.0f), 7.0f);
+                        const float r = (t + 0x1.8p23f) - 0x1.8p23f;
+                        if (e & 1)
+                            od[4 * k + (e >> 1)] = r;
+                        else
+                            ev[4 * k + (e >> 1)] = r;
+                    }
+                }
+                v6i o = __builtin_amdgcn_cvt_scalef32_2xpk16_bf6_f32(ev, od, 1.0f);
+                if (!dv.ok)  // zero or infinite scale: codes 0
+                    o = v6i{0, 0, 0, 0, 0, 0};
+                *reinterpret_cast<uint4 *>(q6 + e3m2_head(a.rows, row, u >> 2, u & 3)) =
+                    make_uint4((uint32_t)o[0], (uint32_t)o[1], (uint32_t)o[2], (uint32_t)o[3]);
+                *reinterpret_cast<uint2 *>(q6 + e3m2_tail(a.rows, row, u >> 2, u & 3)) =
+                    make_uint2((uint32_t)o[4], (uint32_t)o[5]);
+            }
+        } else {
+            uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(n);
+            for (int ch = tid; ch < chunks; ch += 64 * W) {
+                float y[8];
+                row8(ch, y);
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    y[e] = y[e] * c;
                 store_codes8<EPI>(qr, ch * 8, y, dv, qd);
+            }
         }
         if (tid == 0)
             a.scale[row] = s16;
@@ -1136,14 +1152,40 @@ __global__ __launch_bounds__(256) void k_quant_plain(RotArgs a)
     const float s32 = (amax * a.clip) / qd;
     const uint16_t s16 = f2h(s32);
     const Divisor dv = make_divisor(h2f(s16));
-    uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(n);
-    for (int ch = tid; ch < chunks; ch += 256) {
-        float v[8];
-        load8(xr + ch * 8, v);
-        if constexpr (EPI == EPI_E3M2)
-            store_e3m2_8(static_cast<uint8_t *>(a.out), a.rows, row, ch * 8, v, dv);
-        else
+    if constexpr (EPI == EPI_E3M2) {
+        // whole units through one fp6 pack conversion, as in k_rot_largem
+        uint8_t *q6 = static_cast<uint8_t *>(a.out);
+        for (int u = tid; u < chunks / 4; u += 256) {
+            v16f ev, od;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                float v[8];
+                load8(xr + (4 * u + k) * 8, v);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float t = fminf(fmaxf(quotient(v[e], dv), -8.0f), 7.0f);
+                    const float r = (t + 0x1.8p23f) - 0x1.8p23f;
+                    if (e & 1)
+                        od[4 * k + (e >> 1)] = r;
+                    else
+                        ev[4 * k + (e >> 1)] = r;
+                }
+            }
+            v6i o = __builtin_amdgcn_cvt_scalef32_2xpk16_bf6_f32(ev, od, 1.0f);
+            if (!dv.ok)  // zero or infinite scale: codes 0
+                o = v6i{0, 0, 0, 0, 0, 0};
+            *reinterpret_cast<uint4 *>(q6 + e3m2_head(a.rows, row, u >> 2, u & 3)) =
+                make_uint4((uint32_t)o[0], (uint32_t)o[1], (uint32_t)o[2], (uint32_t)o[3]);
+            *reinterpret_cast<uint2 *>(q6 + e3m2_tail(a.rows, row, u >> 2, u & 3)) =
+                make_uint2((uint32_t)o[4], (uint32_t)o[5]);
+        }
+    } else {
+        uint8_t *qr = static_cast<uint8_t *>(a.out) + row * sym_row_bytes<EPI>(n);
+        for (int ch = tid; ch < chunks; ch += 256) {
+            float v[8];
+            load8(xr + ch * 8, v);
             store_codes8<EPI>(qr, ch * 8, v, dv, qd);
+        }
     }
     if (tid == 0)
         a.scale[row] = s16;
