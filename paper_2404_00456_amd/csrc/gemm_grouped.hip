@@ -680,6 +680,19 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_ring(GemmArgs 
 }
 
 
+// RN(a h) for a binary32 a and an fp16 h as fma(a, h, +0): one
+// v_fma_mix_f32 that takes h from its half of a register, no conversion.
+// It differs from the plain product only where that is -0, which it
+// returns as +0.  In the dequant below a zero first product makes the
+// second one a zero as well, and the second is added into a sum that
+// starts at +0; such a sum never becomes -0 (x + y is -0 in
+// round-to-nearest only when both are -0), so adding +0 instead of -0
+// leaves it as it is.
+__device__ __forceinline__ float mul_h(float a, _Float16 h)
+{
+    return __builtin_fmaf(a, (float)h, 0.0f);
+}
+
 // ------------------------------------------------------------------------
 // Group-wise product on e3m2 operands (the tiled layout of k_pack_e3m2),
 // groups of 128 or 256.  A k-step is one 128-k block of the layout and a
@@ -891,20 +904,22 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_e3m2(GemmArgs 
             // this step's scales (read first: LDS reads complete in order),
             // sx of the lane's row per X slice, sw of its four columns per W
             // slice
-            float sxv[4], swv[4][4];
+            // (kept as fp16: the multiplies take them as mixed-precision
+            // operands, so no conversions)
+            _Float16 sxv[4], swv[4][4];
             if constexpr (decltype(LAST)::value) {
-                const uint16_t *lsc = reinterpret_cast<const uint16_t *>(sb + C::SCL);
+                const _Float16 *lsc = reinterpret_cast<const _Float16 *>(sb + C::SCL);
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    sxv[j] = h2f(lsc[wm * 64 + j * 16 + orow]);
+                    sxv[j] = lsc[wm * 64 + j * 16 + orow];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const uint2 w2 =
                         *reinterpret_cast<const uint2 *>(lsc + 256 + wn * 64 + i * 16 + q * 4);
-                    swv[i][0] = h2f((uint16_t)w2.x);
-                    swv[i][1] = h2f((uint16_t)(w2.x >> 16));
-                    swv[i][2] = h2f((uint16_t)w2.y);
-                    swv[i][3] = h2f((uint16_t)(w2.y >> 16));
+                    swv[i][0] = __builtin_bit_cast(_Float16, (uint16_t)w2.x);
+                    swv[i][1] = __builtin_bit_cast(_Float16, (uint16_t)(w2.x >> 16));
+                    swv[i][2] = __builtin_bit_cast(_Float16, (uint16_t)w2.y);
+                    swv[i][3] = __builtin_bit_cast(_Float16, (uint16_t)(w2.y >> 16));
                 }
             }
             static_for<4>([&](auto JI) {
@@ -931,7 +946,7 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_e3m2(GemmArgs 
                     for (int i = 0; i < 4; ++i)
 #pragma unroll
                         for (int r = 0; r < 4; ++r)
-                            u[i][r] = tt[j][i][r] * sxv[j];
+                            u[i][r] = mul_h(tt[j][i][r], sxv[j]);
                     __asm__ volatile("" : "+v"(u[0][0]), "+v"(u[0][1]), "+v"(u[0][2]), "+v"(u[0][3]),
                                      "+v"(u[1][0]), "+v"(u[1][1]), "+v"(u[1][2]), "+v"(u[1][3]),
                                      "+v"(u[2][0]), "+v"(u[2][1]), "+v"(u[2][2]), "+v"(u[2][3]),
@@ -940,7 +955,7 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_e3m2(GemmArgs 
                     for (int i = 0; i < 4; ++i)
 #pragma unroll
                         for (int r = 0; r < 4; ++r)
-                            u[i][r] = u[i][r] * swv[i][r];
+                            u[i][r] = mul_h(u[i][r], swv[i][r]);
                     __asm__ volatile("" : "+v"(u[0][0]), "+v"(u[0][1]), "+v"(u[0][2]), "+v"(u[0][3]),
                                      "+v"(u[1][0]), "+v"(u[1][1]), "+v"(u[1][2]), "+v"(u[1][3]),
                                      "+v"(u[2][0]), "+v"(u[2][1]), "+v"(u[2][2]), "+v"(u[2][3]),
