@@ -429,6 +429,24 @@ __device__ __forceinline__ void dpp_minmax4(float &a, float &b, float &c, float 
 }
 #undef QUAROT_DPP_MINMAX4
 
+// The lane-pair maximum of mx and minimum of mn across position bit J = 0
+// or 1, one DPP-sourced instruction each (same hazard rule as above).
+template <int J>
+__device__ __forceinline__ void dpp_maxmin(float &mx, float &mn)
+{
+    static_assert(J == 0 || J == 1, "quad permutations only");
+    if constexpr (J == 0)
+        asm volatile("s_nop 1\n\t"
+                     "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+                     "v_min_f32_dpp %1, %1, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf"
+                     : "+v"(mx), "+v"(mn));
+    else
+        asm volatile("s_nop 1\n\t"
+                     "v_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+                     "v_min_f32_dpp %1, %1, %1 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf"
+                     : "+v"(mx), "+v"(mn));
+}
+
 // One Walsh-Hadamard stage across position bit J on R registers (R a
 // multiple of 4), s = pos_sign(pos, J).  J < 4: DPP as above (flips the
 // sign of the lanes with the bit set).  J = 4, 5 (lane ^ 16 by ds_swizzle,

@@ -104,11 +104,12 @@ __device__ __forceinline__ uint32_t sym_code(float y, const Divisor &d)
     return d.ok ? c : 0u;
 }
 
-// Asymmetric uint4 code: clamp(rint_even(RN(RN(y - zf) / sf)), 0, 15).
-__device__ __forceinline__ uint32_t asym_code(float y, const Divisor &d, float zf)
+// Asymmetric uint4 code: clamp(rint_even(RN(RN(y - zf) / sf)), 0, 15), as
+// the low nibble of the rounding sum's encoding (whose bits 4-21 are zero),
+// for packing; the caller applies the zero-or-infinite-scale rule (code 0).
+__device__ __forceinline__ uint32_t asym_code_bits(float y, const Divisor &d, float zf)
 {
-    const uint32_t c = round_bits(fminf(fmaxf(quotient(y - zf, d), 0.0f), 15.0f)) & 0xFu;
-    return d.ok ? c : 0u;
+    return round_bits(fminf(fmaxf(quotient(y - zf, d), 0.0f), 15.0f));
 }
 
 // Symmetric code with qmax levels a side, as a byte:
@@ -563,6 +564,30 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
         // chunk max and min as three-input max / min (v_max3 / v_min3: one
         // instruction per two values)
         float mx[C], mn[C];
+        if constexpr (KVROW) {
+            // the row is the group: the lane's chunks first, then its lanes
+            float x = v[0][0], y = v[0][0];
+#pragma unroll
+            for (int cc = 0; cc < C; ++cc)
+#pragma unroll
+                for (int e = (cc == 0); e < 8; ++e) {
+                    x = fmaxf(x, v[cc][e]);
+                    y = fminf(y, v[cc][e]);
+                }
+            static_for<LOGL>([&](auto J) {
+                if constexpr (J <= 1) {
+                    dpp_maxmin<J>(x, y);
+                } else {
+                    x = lane_max<J>(x);
+                    y = lane_min<J>(y);
+                }
+            });
+#pragma unroll
+            for (int cc = 0; cc < C; ++cc) {
+                mx[cc] = x;
+                mn[cc] = y;
+            }
+        } else {
 #pragma unroll
         for (int cc = 0; cc < C; ++cc) {
             const float *u = v[cc];
@@ -600,6 +625,7 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
                     mn[cc] = tn[cc];
                 }
             }
+        }
         const int64_t orow = row * a.ostride + a.ooff;  // Append: a cache position
         uint8_t *qr = static_cast<uint8_t *>(a.out) + orow * (N / 2);
         uint16_t s16 = 0, z16 = 0;
@@ -618,10 +644,21 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_pow2(RotArgs a)
                 dv = make_divisor(h2f(s16));
                 zf = h2f(z16);
             }
-            uint32_t pk = 0;
+            // codes in the low nibbles of their rounding sums' encodings
+            // (bits 4-15 of each are zero): pairs as bytes, bytes as
+            // halves, then the two halves, one v_lshl_or_b32 per step (the
+            // empty asm keeps the compiler from regrouping the ors)
+            uint32_t f[8], p[4];
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                pk |= asym_code(v[cc][e], dv, zf) << (4 * e);
+                f[e] = asym_code_bits(v[cc][e], dv, zf);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                p[k] = (f[2 * k + 1] << 4) | f[2 * k];
+                __asm__("" : "+v"(p[k]));
+            }
+            const uint32_t lo = (p[1] << 8) | p[0], hi = (p[3] << 8) | p[2];
+            const uint32_t pk = dv.ok ? perm_b32(hi, lo, 0x05040100u) : 0u;
             const int p8 = (cc * L + pos) * 8;  // first element of this chunk
             *reinterpret_cast<uint32_t *>(qr + p8 / 2) = pk;
             if (KVROW ? p8 == 0 : p8 % a.group == 0) {
