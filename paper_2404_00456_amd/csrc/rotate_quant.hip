@@ -1505,7 +1505,7 @@ hipError_t dispatch_pow2(const RotArgs &a, int k, hipStream_t s)
         case 10: return go_pow2<6, 1, 2, EPI, ROT, PRO, HEADS, KVROW>(a, s);
         case 11: return go_pow2<6, 1, 4, EPI, ROT, PRO, HEADS, KVROW>(a, s);
         case 12: return go_pow2<6, 1, 8, EPI, ROT, PRO, HEADS, KVROW>(a, s);
-        case 13: return go_pow2<6, 4, 4, EPI, ROT, PRO, HEADS, KVROW>(a, s);
+        case 13: return go_pow2<6, 2, 8, EPI, ROT, PRO, HEADS, KVROW>(a, s);
         case 14: return go_pow2<6, 4, 8, EPI, ROT, PRO, HEADS, KVROW>(a, s);
         case 15: return go_pow2<6, 8, 8, EPI, ROT, PRO, HEADS, KVROW>(a, s);
         }
