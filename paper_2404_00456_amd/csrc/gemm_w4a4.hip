@@ -456,12 +456,22 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
         if (tn_ >= 0)
             tile_mn(tn_, m1, n1);
 
+        // The 128-row e3m2 tile (four waves, one per SIMD, accumulators in
+        // AGPRs) does not clear its accumulators: its first k-step's MFMAs
+        // take a zero accumulator operand instead (the compiler peels that
+        // step), and the compiler then keeps the accumulators in place
+        // through the loop, where it otherwise moved 24 of them per k-step
+        // (7B down projection: 72 -> 64 us).  The 256-row tile measured
+        // the same or 1% slower that way and clears.
+        constexpr bool PEEL = BITS == 6 && TBM == 128;
         Acc acc[NI][8];
+        if constexpr (!PEEL) {
 #pragma unroll
-        for (int i = 0; i < NI; ++i)
+            for (int i = 0; i < NI; ++i)
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                acc[i][j] = Acc{0, 0, 0, 0};
+                for (int j = 0; j < 8; ++j)
+                    acc[i][j] = Acc{0, 0, 0, 0};
+        }
 
         auto read_step = [&](uint4 (&ops)[8 + NI], int stage) {
             const uint8_t *sb = lds + stage * RING_STAGE;
@@ -550,12 +560,13 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
                 const uint64_t t = *(const volatile lds_u64 *)(lds_void *)(sb + btail + j * 16 * 32);
                 B[j].t = make_uint2((uint32_t)t, (uint32_t)(t >> 32));
             };
-            auto quarter = [&](int i0, int j0) {
+            auto quarter = [&](int i0, int j0, bool first) {
 #pragma unroll
                 for (int i = i0; i < i0 + 2; ++i)
 #pragma unroll
                     for (int j = j0; j < j0 + 4; ++j)
-                        acc[i][j] = mfma6(A[i], B[j], acc[i][j]);
+                        acc[i][j] = mfma6(A[i], B[j],
+                                          PEEL && first ? v4f{0.0f, 0.0f, 0.0f, 0.0f} : acc[i][j]);
             };
             rdA(0, g % S);
             rdA(1, g % S);
@@ -567,7 +578,7 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
 #pragma unroll
                 for (int j = 4; j < 8; ++j)
                     rdB(j, cs);
-                quarter(0, 0);
+                quarter(0, 0, kt == 0);
 #pragma unroll
                 for (int k = 0; k < 8; ++k) {
                     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
@@ -576,7 +587,7 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
                 __builtin_amdgcn_sched_barrier(0);
                 rdA(2, cs);
                 rdA(3, cs);
-                quarter(0, 4);
+                quarter(0, 4, kt == 0);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     __builtin_amdgcn_sched_group_barrier(0x100, 1, 3);
@@ -613,7 +624,7 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
                 }
                 rdA(0, nx);
                 rdA(1, nx);
-                quarter(2, 0);
+                quarter(2, 0, kt == 0);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
@@ -624,7 +635,7 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
                     rdB(j, nx);
-                quarter(2, 4);
+                quarter(2, 4, kt == 0);
 #pragma unroll
                 for (int k = 0; k < 8; ++k) {
                     __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
