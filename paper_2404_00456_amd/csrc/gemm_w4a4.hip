@@ -534,7 +534,7 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
             // A[0..1] x B[0..3], A[0..1] x B[4..7], A[2..3] x B[0..3],
             // A[2..3] x B[4..7].  Every read lands in registers a quarter
             // has just freed, at least one quarter before its first use, so
-            // the operands are not double buffered (200 live VGPRs):
+            // the operands are not double buffered:
             //   quarter 1: read B[4..7] of this step
             //   quarter 2: read A[2..3] of this step
             //   barrier after quarter 2 (every read of this stage done)
