@@ -461,7 +461,7 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
         // take a zero accumulator operand instead (the compiler peels that
         // step), and the compiler then keeps the accumulators in place
         // through the loop, where it otherwise moved 24 of them per k-step
-        // (7B down projection: 72 -> 64 us).  The 256-row tile measured
+        // (M = 2048, N = 4096, K = 11008: 72 -> 64 us).  The 256-row tile measured
         // the same or 1% slower that way and clears.
         constexpr bool PEEL = BITS == 6 && TBM == 128;
         Acc acc[NI][8];
