@@ -753,11 +753,16 @@ __global__ __launch_bounds__(THREADS, 1) void k_gemm_w4a4_grouped_e3m2(GemmArgs 
         const int t = b + it * G;
         return t < T ? t : -1;
     };
+    // tiles in groups of 4 m-tiles: the 32 concurrent 256 x 128 tiles of an
+    // XCD then cover 4 X and 8 W panels (2048 rows) instead of 8 X and 4 W
+    // (2560 rows) with groups of 8, 20% fewer bytes through its L2
+    // (Llama-2-70B down shape, K = 28672: 4.45 -> 4.27 ms at G = 128)
+    constexpr int GM4 = 4;
     auto tile_mn = [&](int t, int &m0, int &n0) {
-        const int gsize = GM * TN;
+        const int gsize = GM4 * TN;
         const int g = t / gsize;
-        const int first = g * GM;
-        const int gm = min(TM - first, GM);
+        const int first = g * GM4;
+        const int gm = min(TM - first, GM4);
         const int r = t - g * gsize;
         m0 = (first + r % gm) * BM;
         n0 = (r / gm) * GBN;
