@@ -176,6 +176,18 @@ def bench_kv(q, workloads, torch, np, dev, stream, iters):
                "us": round(att_us, 1), "cache_bytes": att_bytes,
                "GBps": round(att_bytes / (att_us * 1e-6) / 1e9, 1),
                "frac_hbm": round(att_bytes / (att_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}}
+    # what a plain device-to-device copy of one K tensor (1 GiB read, 1 GiB
+    # written; the runtime's copy kernel through torch) reaches on this
+    # chip: the practical rate of a read-and-write stream, beside the
+    # published peak the fractions above use
+    src, dst = tens[0][0], tens[0][4]
+    dst.copy_(src)
+    c_us = float(np.median(event_times_us(torch, stream, [lambda: dst.copy_(src)], iters)[0]))
+    c_bytes = 2 * src.numel() * src.element_size()
+    res["device_copy_reference"] = {
+        "what": "1 GiB device-to-device copy (torch copy_, read + write)",
+        "us": round(c_us, 1), "GBps": round(c_bytes / (c_us * 1e-6) / 1e9, 1),
+        "frac_hbm": round(c_bytes / (c_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
     for t in tens:
         del t
     tens.clear()
