@@ -797,6 +797,413 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));  // no DMA may outlive the block's LDS
 }
 
+// ------------------------------------------------------------------------
+// e3m2 operands, 128 (m) x 256 (n) block tiles, the k-steps of a tile split
+// between two groups of four waves: group q takes the k-steps 2p + q
+// (p = 0 .. KT/2 - 1, KT even), each of its waves 128 (m) x 64 (n) as in
+// the kernel above, and the two partial sums meet in LDS at the end of the
+// tile.  Both partials are integers of magnitude below 2^24 held exactly in
+// binary32, so their sum is f32(acc) exactly.  Eight waves put two on each
+// SIMD, which the 128-row tile of the kernel above (one wave per SIMD) does
+// not: there the matrix cores idle while the single wave waits on its LDS
+// reads and barriers.  For grids with too few 256 x 256 tiles to fill the
+// chip.
+//
+// Ring: four 36 KB stages; k-step 2p + q in stage 2 (p % 2) + q, so each
+// group double-buffers its own k-steps: the DMA of step 2p + q + 4 (issued by
+// group q's waves, after the barrier of pair p) lands while pair p + 1 is
+// computed.  The ring does not run across tiles: at a tile's end it holds
+// the 128 KB exchange of partial sums, then the next tile's first two pairs
+// are issued before this tile's y stores.  Stage layout and DMA chunks are
+// those of the 128-row tile above (four waves per group).
+__device__ __forceinline__ void gemm_e3m2_ksplit(const GemmArgs &a, uint8_t *lds)
+{
+    constexpr int TBM = 128, NWG = 4;        // tile rows, waves per group
+    constexpr int HEADS = (TBM + BN) * 64;   // offset of the tails in a stage
+    constexpr int STAGE = (TBM + BN) * 96;   // 36 KB
+    constexpr int HPW = HEADS / 1024 / NWG;  // 6 head DMAs per wave and step
+    constexpr int DPW = STAGE / 1024 / NWG;  // 9 DMAs per wave and step
+    static_assert(4 * STAGE >= 2 * NWG * 16 * 1024, "the exchange fits in the ring");
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int q = wave >> 2, wn = wave & 3;  // k group, n slice of the wave
+    const int M = a.M, N = a.N, K = a.K;
+    const int TM = (M + TBM - 1) / TBM, TN = (N + BN - 1) / BN;
+    const int T = TM * TN;
+    const int G = gridDim.x, b = blockIdx.x;
+    const int P = K / 256;  // k-step pairs
+
+    // tile order of the kernel above
+    const bool xcd = (G % 8 == 0) && (T % 8 == 0) && G <= T;
+    const bool sblk = G == 256 && TM % 16 == 0 && TN % 16 == 0;
+    auto tile_pos = [&](int it) -> int {
+        if (sblk)
+            return it < T / 256 ? it * 256 + b : -1;
+        if (xcd) {
+            const int per_x = T / 8, gx = G / 8;
+            const int r = (b >> 3) + it * gx;
+            return r < per_x ? (b & 7) * per_x + r : -1;
+        }
+        const int t = b + it * G;
+        return t < T ? t : -1;
+    };
+    auto tile_mn = [&](int t, int &m0, int &n0) {
+        if (sblk) {
+            const int r = t >> 8, x = t & 7, s = (t >> 3) & 31;
+            const int nsb = TN / 16, mb = r / nsb, nr = r - mb * nsb;
+            const int nb = (mb & 1) ? nsb - 1 - nr : nr;
+            m0 = (mb * 16 + (x & 3) * 4 + (s & 3)) * TBM;
+            n0 = (nb * 16 + (x >> 2) * 8 + (s >> 2)) * BN;
+            return;
+        }
+        const int gsize = GM * TN;
+        const int g = t / gsize;
+        const int first = g * GM;
+        const int gm = min(TM - first, GM);
+        const int r = t - g * gsize;
+        m0 = (first + r % gm) * TBM;
+        n0 = (r / gm) * BN;
+    };
+
+    // DMAs of wave wn of group q for one k-step: head DMA i < HPW moves chunk
+    // c = wn + 4 i of the stage's heads (rows 16 c .. 16 c + 15 of the 128 X
+    // rows followed by the 256 W rows; i < 2 are X chunks), tail DMA
+    // i = HPW + j chunk c = wn + 4 j of the tails (rows 32 c .. 32 c + 31;
+    // j = 0 is the X chunk).  Lane offsets fixed per tile (rows past the
+    // matrix edge clamped), wave-uniform bases advanced by two k-blocks per
+    // pair.
+    auto is_x = [&](int i) { return i < 2 || i == HPW; };
+    auto chunk_row = [&](int i) -> int {
+        const int c = wn + NWG * (i < HPW ? i : i - HPW);
+        const int r = i < HPW ? 16 * c : 32 * c;
+        return is_x(i) ? r : r - TBM;
+    };
+    // (el: the lane index, laundered by the caller so that nothing derived
+    // from it is hoisted out of the tile loop and held through the k-loop)
+    auto voff = [&](int i, int m0, int n0, int el) -> uint32_t {
+        const int lim = (is_x(i) ? M - m0 : N - n0) - 1;
+        if (i < HPW)
+            return (uint32_t)(min(chunk_row(i) + (el >> 2), lim) * 64 + (el & 3) * 16);
+        return (uint32_t)(min(chunk_row(i) + (el >> 1), lim) * 32 + (el & 1) * 16);
+    };
+    // four wave-uniform bases (X heads, W heads, X tails, W tails) of the
+    // next k-step this group moves
+    const int64_t xblk = (int64_t)M * 96, wblk = (int64_t)N * 96;
+    const uint8_t *bxh, *bwh, *bxt, *bwt;
+    auto set_base = [&](int m0, int n0, int sk) {
+        bxh = a.xq + sk * xblk + (int64_t)m0 * 64;
+        bwh = a.wq + sk * wblk + (int64_t)n0 * 64;
+        bxt = a.xq + sk * xblk + (int64_t)M * 64 + (int64_t)m0 * 32;
+        bwt = a.wq + sk * wblk + (int64_t)N * 64 + (int64_t)n0 * 32;
+    };
+    const uint32_t wdst = (uint32_t)(uintptr_t)(lds_void *)lds + wn * 1024;
+    uint32_t vo[DPW];
+    // one k-step of this wave's DMAs into the stage at LDS offset so
+    auto issue = [&](int so) {
+#pragma unroll
+        for (int i = 0; i < DPW; ++i) {
+            const uint8_t *bs = i < HPW ? (is_x(i) ? bxh : bwh) : (is_x(i) ? bxt : bwt);
+            const int d = i < HPW ? i * NWG * 1024 : HEADS + (i - HPW) * NWG * 1024;
+            dma16s(vo[i], bs, wdst + so + d);
+        }
+    };
+    auto advance2 = [&]() {
+        bxh += 2 * xblk;
+        bwh += 2 * wblk;
+        bxt += 2 * xblk;
+        bwt += 2 * wblk;
+    };
+    // the tile's first two pairs (k-steps q and 2 + q) into stages q, 2 + q
+    auto start_tile = [&](int m0, int n0) {
+        int el = lane;
+        __asm__ volatile("" : "+v"(el));
+#pragma unroll
+        for (int i = 0; i < DPW; ++i)
+            vo[i] = voff(i, m0, n0, el);
+        set_base(m0, n0, q);
+        issue(q * STAGE);
+        advance2();
+        issue((2 + q) * STAGE);
+        advance2();
+    };
+
+    // LDS reads: X slice j (MFMA B operand) = stage row 16 j + orow, W slice
+    // i (A operand) = stage row TBM + 64 wn + 16 i + orow; lane group lane/16
+    // takes its unit of the 128-k block (head slot and tail slot swizzled as
+    // k_pack_e3m2 lays them out)
+    const int orow = lane & 15;
+    const int ounit = ((lane >> 4) ^ ((orow >> 1) & 3)) << 4;
+    const int toff = 8 * ((lane >> 4) ^ ((orow >> 2) & 3));
+    const int brow = orow * 64 + ounit, arow = (TBM + wn * WN + orow) * 64 + ounit;
+    const int btail = HEADS + orow * 32 + toff;
+    const int atail = HEADS + TBM * 32 + (wn * WN + orow) * 32 + toff;
+    Op6 A[NI], B[8];
+    auto rdA = [&](int i, int stage) {
+        const uint8_t *sb = lds + stage * STAGE;
+        A[i].h = *reinterpret_cast<const uint4 *>(sb + arow + i * 16 * 64);
+        const uint64_t t = *(const volatile lds_u64 *)(lds_void *)(sb + atail + i * 16 * 32);
+        A[i].t = make_uint2((uint32_t)t, (uint32_t)(t >> 32));
+    };
+    auto rdB = [&](int j, int stage) {
+        const uint8_t *sb = lds + stage * STAGE;
+        B[j].h = *reinterpret_cast<const uint4 *>(sb + brow + j * 16 * 64);
+        const uint64_t t = *(const volatile lds_u64 *)(lds_void *)(sb + btail + j * 16 * 32);
+        B[j].t = make_uint2((uint32_t)t, (uint32_t)(t >> 32));
+    };
+
+    int t = tile_pos(0);
+    if (t < 0)
+        return;
+    int m0, n0;
+    tile_mn(t, m0, n0);
+    start_tile(m0, n0);
+    // vm operations this wave issued after the current tile's first pair:
+    // its second pair, and the previous tile's y stores when they are known
+    // to be 16 (else 0: wait for everything)
+    int after = DPW;
+    for (int it = 0; t >= 0; ++it) {
+        const int tn_ = tile_pos(it + 1);
+        int m1 = 0, n1 = 0;
+        if (tn_ >= 0)
+            tile_mn(tn_, m1, n1);
+
+        v4f acc[NI][8];
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                acc[i][j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+
+        // pair 0 landed for every wave
+        __asm__ volatile("" ::: "memory");
+        if (after == DPW)
+            __builtin_amdgcn_s_waitcnt(waitcnt_imm(DPW, 15));
+        else if (after == DPW + 16)
+            __builtin_amdgcn_s_waitcnt(waitcnt_imm(DPW + 16, 15));
+        else
+            __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));
+        __builtin_amdgcn_s_barrier();
+        __asm__ volatile("" ::: "memory");
+        rdA(0, q);
+        rdA(1, q);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            rdB(j, q);
+
+        auto quarter = [&](int i0, int j0) {
+#pragma unroll
+            for (int i = i0; i < i0 + 2; ++i)
+#pragma unroll
+                for (int j = j0; j < j0 + 4; ++j)
+                    acc[i][j] = mfma6(A[i], B[j], acc[i][j]);
+        };
+        // pair p: the quarters, reads and fences of the kernel above; LAST:
+        // no next step to read
+        auto pair = [&](int p, auto LAST) {
+            const int cs = 2 * (p & 1) + q, nx = 2 * ((p + 1) & 1) + q;
+#pragma unroll
+            for (int j = 4; j < 8; ++j)
+                rdB(j, cs);
+            quarter(0, 0);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            rdA(2, cs);
+            rdA(3, cs);
+            quarter(0, 4);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 3);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 3);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 3);
+            __builtin_amdgcn_sched_barrier(0);
+            // this wave's DMAs of pair p + 1 landed and its reads of stage
+            // cs done; then for every wave
+            __asm__ volatile("" ::: "memory");
+            __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
+            __builtin_amdgcn_s_barrier();
+            __asm__ volatile("" ::: "memory");
+            if (p + 2 < P) {
+                issue(cs * STAGE);
+                advance2();
+            }
+            if constexpr (!decltype(LAST)::value) {
+                rdA(0, nx);
+                rdA(1, nx);
+            }
+            quarter(2, 0);
+            if constexpr (!decltype(LAST)::value) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (!decltype(LAST)::value) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    rdB(j, nx);
+            }
+            quarter(2, 4);
+            if constexpr (!decltype(LAST)::value) {
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        for (int p = 0; p < P - 1; ++p)
+            pair(p, std::false_type{});
+        pair(P - 1, std::true_type{});
+
+        // Every wave is past the last barrier: no ring reads or DMAs remain.
+        // Group q finishes m rows 64 q .. 64 q + 63 of the tile (slices
+        // j = 4 q .. 4 q + 3): the other group's partials of those rows come
+        // through LDS, 1 KB per (wave, slice pair), both directions at once.
+        // (QC: q as a compile-time constant, so that the accumulators are
+        // indexed statically.)
+        const bool fast = m0 + TBM <= M && n0 + BN <= N && (N & 3) == 0 && a.acc == nullptr;
+        auto finish = [&](auto QC) {
+            constexpr int Q = decltype(QC)::value, O = 1 - Q;
+            // the lane's epilogue offsets are derived here, from a copy of
+            // the lane index the compiler cannot see through: hoisted above
+            // the k-loop they would be held (spilled) through it
+            int el = lane;
+            __asm__ volatile("" : "+v"(el));
+            const int erow = el & 15, ecol = (el >> 4) * 4;
+            float sxs[4];
+            uint2 swp[NI];
+            if (fast) {
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+                    sxs[jj] = h2f(a.sx[m0 + 64 * Q + 16 * jj + erow]);
+#pragma unroll
+                for (int i = 0; i < NI; ++i)
+                    swp[i] = *reinterpret_cast<const uint2 *>(a.sw + n0 + wn * WN + i * 16 + ecol);
+            }
+            uint8_t *xw = lds + (O * NWG + wn) * 16 * 1024 + el * 16;
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+                    *reinterpret_cast<v4f *>(xw + (i * 4 + jj) * 1024) = acc[i][4 * O + jj];
+            __asm__ volatile("" ::: "memory");
+            __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, 0));
+            __builtin_amdgcn_s_barrier();
+            __asm__ volatile("" ::: "memory");
+            const uint8_t *xr = lds + (Q * NWG + wn) * 16 * 1024 + el * 16;
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+                    acc[i][4 * Q + jj] += *reinterpret_cast<const v4f *>(xr + (i * 4 + jj) * 1024);
+            __asm__ volatile("" ::: "memory");
+            __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, 0));
+            __builtin_amdgcn_s_barrier();
+            __asm__ volatile("" ::: "memory");
+
+            if (fast) {
+                // y = RN16(RN(RN(f32(acc) sx) sw)), packed before the next
+                // tile's DMAs are issued (so the scale loads are waited for
+                // alone) and stored after them
+                uint2 pk[4][NI];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                    for (int i = 0; i < NI; ++i) {
+                        const v4f v = acc[i][4 * Q + jj];
+                        float u0 = (v[0] * sxs[jj]) * h2f((uint16_t)swp[i].x);
+                        float u1 = (v[1] * sxs[jj]) * h2f((uint16_t)(swp[i].x >> 16));
+                        float u2 = (v[2] * sxs[jj]) * h2f((uint16_t)swp[i].y);
+                        float u3 = (v[3] * sxs[jj]) * h2f((uint16_t)(swp[i].y >> 16));
+                        // pinned so the multiply is not fused into the conversion
+                        __asm__ volatile("" : "+v"(u0), "+v"(u1), "+v"(u2), "+v"(u3));
+                        const h2 lo = __builtin_convertvector((f2){u0, u1}, h2);
+                        const h2 hi = __builtin_convertvector((f2){u2, u3}, h2);
+                        pk[jj][i] = make_uint2(__builtin_bit_cast(uint32_t, lo),
+                                               __builtin_bit_cast(uint32_t, hi));
+                    }
+                if (tn_ >= 0)
+                    start_tile(m1, n1);
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                    for (int i = 0; i < NI; ++i) {
+                        const int m = m0 + 64 * Q + 16 * jj + erow;
+                        const int nl = wn * WN + i * 16 + ecol;
+                        *reinterpret_cast<uint2 *>(a.y + (int64_t)m * N + n0 + nl) = pk[jj][i];
+                    }
+                after = DPW + 16;
+                return;
+            }
+            // edge tiles (and the int32 output): bounds per row and column
+            const bool vec = (N & 3) == 0;
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                const int nb = n0 + wn * WN + i * 16 + ecol;
+                float swf[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    swf[r] = h2f(a.sw[min(nb + r, N - 1)]);
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int m = m0 + 64 * Q + 16 * jj + erow;
+                    if (m >= M)
+                        continue;
+                    const float sxf = h2f(a.sx[m]);
+                    int iv[4];
+                    uint16_t hv[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        iv[r] = (int)acc[i][4 * Q + jj][r];
+                        const float tt = (float)iv[r] * sxf;
+                        hv[r] = f2h(tt * swf[r]);
+                    }
+                    uint16_t *yrow = a.y + (int64_t)m * N;
+                    int32_t *arw = a.acc ? a.acc + (int64_t)m * N : nullptr;
+                    if (vec && nb + 3 < N) {
+                        uint2 pk;
+                        pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
+                        pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
+                        *reinterpret_cast<uint2 *>(yrow + nb) = pk;
+                        if (arw)
+                            *reinterpret_cast<int4 *>(arw + nb) =
+                                make_int4(iv[0], iv[1], iv[2], iv[3]);
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            if (nb + r < N) {
+                                yrow[nb + r] = hv[r];
+                                if (arw)
+                                    arw[nb + r] = iv[r];
+                            }
+                    }
+                }
+            }
+            if (tn_ >= 0)
+                start_tile(m1, n1);
+            after = 0;
+        };
+        if (q == 0)
+            finish(std::integral_constant<int, 0>{});
+        else
+            finish(std::integral_constant<int, 1>{});
+        t = tn_;
+        m0 = m1;
+        n0 = n1;
+    }
+    __asm__ volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));  // no DMA may outlive the block's LDS
+}
+
 __global__ __launch_bounds__(Tile<256>::THREADS, 1) void k_gemm_w4a4(GemmArgs a)
 {
     extern __shared__ __align__(16) uint8_t lds[];
@@ -833,6 +1240,15 @@ __global__ __launch_bounds__(Tile<128>::THREADS, 1) void k_gemm_w4a4_e3m2_m128(G
 {
     extern __shared__ __align__(16) uint8_t lds[];
     gemm_main<6, 128>(a, lds);
+}
+
+// 128 x 256 e3m2 tiles, k-steps split between two groups of four waves
+constexpr int KSPLIT_THREADS = 512;
+constexpr int KSPLIT_LDS = 4 * (128 + BN) * 96;
+__global__ __launch_bounds__(KSPLIT_THREADS, 1) void k_gemm_w4a4_e3m2_ksplit(GemmArgs a)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    gemm_e3m2_ksplit(a, lds);
 }
 
 // int4 codes (two per byte, low nibble first) -> the tiled e3m2 layout.
@@ -898,14 +1314,24 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s, int bits)
     const int TN = (a.N + BN - 1) / BN;
     const int64_t t256 = (int64_t)((a.M + 255) / 256) * TN, t128 = (int64_t)((a.M + 127) / 128) * TN;
     const int64_t r256 = (t256 + cus - 1) / cus, r128 = (t128 + cus - 1) / cus;
-    const bool m128 = ksteps >= S && a.M > 128 && r128 * 90 < r256 * 100;
+    // e3m2 codes with K a multiple of 256: the 128-row tiles with the
+    // k-steps split between two wave groups, which take about KSPLIT_COST %
+    // of a 256 x 256 tile's time
+    constexpr int KSPLIT_COST = 70;
+    const bool ksplit =
+        bits == 6 && a.K % 256 == 0 && a.K >= 512 && a.M > 128 && r128 * KSPLIT_COST < r256 * 100;
+    const bool m128 = ksplit || (ksteps >= S && a.M > 128 && r128 * 90 < r256 * 100);
     const int64_t tiles = m128 ? t128 : t256;
     int grid = (int)((tiles < cus || ksteps < S) ? tiles : cus);
     if (grid >= 8 && tiles % 8 == 0)
         grid -= grid % 8;
     const void *fn;
     int lds_bytes, threads;
-    if (m128) {
+    if (ksplit) {
+        fn = (const void *)k_gemm_w4a4_e3m2_ksplit;
+        lds_bytes = KSPLIT_LDS;
+        threads = KSPLIT_THREADS;
+    } else if (m128) {
         fn = bits == 8 ? (const void *)k_gemm_w8a8_m128
              : bits == 6 ? (const void *)k_gemm_w4a4_e3m2_m128
                          : (const void *)k_gemm_w4a4_m128;

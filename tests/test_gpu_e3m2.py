@@ -167,6 +167,44 @@ def test_gemm_e3m2_full_size(dev, orc, M, N, K):
     assert_same(H(y6[rows]).view(np.uint16), ry.view(np.uint16), "full size sampled rows")
 
 
+@pytest.mark.parametrize("M,N,K", [(2048, 11008, 4096), (2048, 4096, 11008),
+                                   # 128-row tiles with split k-steps, one or
+                                   # two tiles per block, a ragged last column
+                                   # of tiles
+                                   (384, 33000, 512)])
+def test_gemm_e3m2_7b_shapes(dev, orc, M, N, K):
+    """Llama-2-7B FFN shapes at 2048 tokens, in the launch configuration the
+    benchmark times, and a grid whose blocks walk two 128-row tiles with
+    split k-steps: every acc and y equal to the int4 path's, and one seeded
+    row of every 128-row tile, plus the first and last, equal to the
+    oracle's, with and without the int32 output."""
+    import torch
+    import paper_2404_00456_amd as q
+    say(f"e3m2 gemm 7B shape M={M} N={N} K={K}")
+    g = torch.Generator(device=dev).manual_seed(M * 3 + N + K)
+    xq = torch.randint(0, 256, (M, K // 2), generator=g, device=dev, dtype=torch.uint8)
+    wq = torch.randint(0, 256, (N, K // 2), generator=g, device=dev, dtype=torch.uint8)
+    sx = (torch.rand(M, generator=g, device=dev) * 0.05 + 0.01).half()
+    sw = (torch.rand(N, generator=g, device=dev) * 0.002 + 0.0005).half()
+    x6, w6 = q.quarot_pack_e3m2(xq), q.quarot_pack_e3m2(wq)
+    y4, acc4 = q.quarot_w4a4_gemm(xq, sx, wq, sw, want_acc=True)
+    y6, acc6 = q.quarot_w4a4_gemm_e3m2(x6, sx, w6, sw, want_acc=True)
+    y6o = q.quarot_w4a4_gemm_e3m2(x6, sx, w6, sw)
+    torch.cuda.synchronize()
+    nd_acc = int((acc4 != acc6).sum().item())
+    nd_y = int((y4.view(torch.int16) != y6.view(torch.int16)).sum().item())
+    nd_yo = int((y4.view(torch.int16) != y6o.view(torch.int16)).sum().item())
+    say(f"7B shape e3m2 vs int4: acc {nd_acc}, y {nd_y}, y (no acc) {nd_yo} differing of {M * N}")
+    assert nd_acc == 0 and nd_y == 0 and nd_yo == 0
+    rng = np.random.default_rng(M + N + K)
+    rows = np.unique(np.concatenate([[0, M - 1], np.arange(0, M, 128) + rng.integers(0, 128, M // 128)]))
+    xs, ss = H(xq[rows]), H(sx[rows])
+    racc = orc.gemm_i32(xs, H(wq))
+    assert_same(H(acc6[rows]), racc, "7B shape sampled acc")
+    ry = orc.dequant(racc, ss, H(sw))
+    assert_same(H(y6o[rows]).view(np.uint16), ry.view(np.uint16), "7B shape sampled rows")
+
+
 # ------------------------------------------- quantizer writing e3m2 ---
 
 E3M2_ROTATED_N = [128, 256, 1024, 4096, 8192, 16384, 32768, 12288, 24576, 10240, 20480, 14336,
