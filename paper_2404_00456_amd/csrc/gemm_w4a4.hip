@@ -811,8 +811,8 @@ __device__ __forceinline__ void gemm_main(const GemmArgs &a, uint8_t *lds)
 //
 // Ring: four 36 KB stages; k-step 2p + q in stage 2 (p % 2) + q, so each
 // group double-buffers its own k-steps: the DMA of step 2p + q + 4 (issued by
-// group q's waves, after the barrier of pair p) lands while pair p + 1 is
-// computed.  The ring does not run across tiles: at a tile's end it holds
+// group q's waves after the barrier of pair p) must land by the barrier of
+// pair p + 1, after which that step's first operands are read.  The ring does not run across tiles: at a tile's end it holds
 // the 128 KB exchange of partial sums, then the next tile's first two pairs
 // are issued before this tile's y stores.  Stage layout and DMA chunks are
 // those of the 128-row tile above (four waves per group).
