@@ -20,6 +20,8 @@ import torch  # first: the library then binds to torch's HIP runtime
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libquarot.so")
+# the measurement library beside it (include/quarot_probe.h)
+PROBE_LIB_PATH = os.path.join(_HERE, "libquarot_probe.so")
 
 STATUS = {
     0: "QUAROT_OK",
@@ -41,9 +43,6 @@ SIGNATURES = {
     "quarot_status_string": (ctypes.c_char_p, [_I]),
     "quarot_last_hip_error": (_I, []),
     "quarot_version": (_I, []),
-    "quarot_device_peaks": (_I, [_P, _P]),
-    "quarot_mfma_probe_fp6": (_I, [_P, _I64, _I, _P]),
-    "quarot_mfma_probe": (_I, [_P, _I64, _I, _P]),
     "quarot_hadamard_factor": (_I, [_I64, _P, _P]),
     "quarot_hadamard_factor_table": (_I, [_I, _P]),
     "quarot_hadamard": (_I, [_P, _P, _I64, _I64, _P]),
@@ -87,7 +86,16 @@ SIGNATURES = {
                                         _I64, _I64, _F, _P, ctypes.c_size_t, _P]),
 }
 
+# name -> (restype, argtypes), exactly the declarations of include/quarot_probe.h
+PROBE_SIGNATURES = {
+    "quarot_device_peaks": (_I, [_P, _P]),
+    "quarot_mfma_probe": (_I, [_P, _I64, _I, _P]),
+    "quarot_mfma_probe_fp6": (_I, [_P, _I64, _I, _P]),
+    "quarot_probe_last_hip_error": (_I, []),
+}
+
 _lib = None
+_probe_lib = None
 
 
 class QuarotError(RuntimeError):
@@ -116,9 +124,30 @@ def lib() -> ctypes.CDLL:
     return _lib
 
 
+def probe_lib() -> ctypes.CDLL:
+    """The loaded measurement library; raises if it has not been built."""
+    global _probe_lib
+    if _probe_lib is None:
+        if not os.path.exists(PROBE_LIB_PATH):
+            raise RuntimeError(f"{PROBE_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2404_00456_amd.build`")
+        L = ctypes.CDLL(PROBE_LIB_PATH)
+        for name, (res, args) in PROBE_SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _probe_lib = L
+    return _probe_lib
+
+
 def _check(call: str, st: int):
     if st != 0:
         raise QuarotError(call, st, lib().quarot_last_hip_error() if st == 6 else 0)
+
+
+def _check_probe(call: str, st: int):
+    if st != 0:
+        raise QuarotError(call, st, probe_lib().quarot_probe_last_hip_error() if st == 6 else 0)
 
 
 def _ptr(t: Optional[torch.Tensor], dtype: torch.dtype, name: str):
@@ -185,7 +214,8 @@ def quarot_device_peaks() -> Tuple[int, int]:
     """(compute units, peak shader clock in kHz) of the current device."""
     cus = ctypes.c_int()
     clk = ctypes.c_int()
-    _check("quarot_device_peaks", lib().quarot_device_peaks(ctypes.byref(cus), ctypes.byref(clk)))
+    _check_probe("quarot_device_peaks",
+                 probe_lib().quarot_device_peaks(ctypes.byref(cus), ctypes.byref(clk)))
     return cus.value, clk.value
 
 
@@ -195,7 +225,7 @@ def quarot_mfma_probe(out: torch.Tensor, blocks: int, iters: int,
     (2 per multiply-add).  out: int32 device tensor of blocks * 512."""
     if out.numel() < blocks * 512:
         raise ValueError("out must hold blocks * 512 int32")
-    _check("quarot_mfma_probe", lib().quarot_mfma_probe(
+    _check_probe("quarot_mfma_probe", probe_lib().quarot_mfma_probe(
         _ptr(out, torch.int32, "out"), int(blocks), int(iters), _stream(stream)))
     return blocks * 8 * iters * 32 * 16384 * 2  # waves x MFMAs x multiply-adds x 2
 
@@ -206,7 +236,7 @@ def quarot_mfma_probe_fp6(out: torch.Tensor, blocks: int, iters: int,
     per multiply-add).  out: int32 device tensor of blocks * 512."""
     if out.numel() < blocks * 512:
         raise ValueError("out must hold blocks * 512 int32")
-    _check("quarot_mfma_probe_fp6", lib().quarot_mfma_probe_fp6(
+    _check_probe("quarot_mfma_probe_fp6", probe_lib().quarot_mfma_probe_fp6(
         _ptr(out, torch.int32, "out"), int(blocks), int(iters), _stream(stream)))
     return blocks * 8 * iters * 32 * 32768 * 2
 
@@ -832,7 +862,7 @@ def quarot_kv_decode_attention(q: torch.Tensor, k_cache, v_cache, seq_len: int,
 
 
 __all__ = [
-    "QuarotError", "lib", "quarot_version", "quarot_device_peaks", "quarot_mfma_probe",
+    "QuarotError", "lib", "probe_lib", "quarot_version", "quarot_device_peaks", "quarot_mfma_probe",
     "quarot_hadamard_factor",
     "quarot_hadamard_factor_table", "quarot_linear_workspace_size", "quarot_hadamard",
     "quarot_quant_int4", "quarot_w4a4_gemm", "quarot_linear", "prepare_weight",

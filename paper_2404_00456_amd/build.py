@@ -1,4 +1,5 @@
-"""Build libquarot.so (HIP for gfx950) in-tree with hipcc.
+"""Build libquarot.so (HIP for gfx950) and, beside it, the measurement
+library libquarot_probe.so in-tree with hipcc.
 
     python -m paper_2404_00456_amd.build
 """
@@ -13,7 +14,10 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libquarot.so")
 SOURCES = ["capi.cpp", "host_rules.cpp", "rotate_quant.hip", "gemm_w4a4.hip", "gemm_grouped.hip", "kv_attention.hip",
-           "probe.hip", "scratch.hip"]
+           "scratch.hip"]
+# MFMA-only rate probes and the device's peak clock (include/quarot_probe.h)
+PROBE_LIB = os.path.join(HERE, "libquarot_probe.so")
+PROBE_SOURCES = ["probe.hip"]
 
 # -ffp-contract=off: every written add and multiply stays a rounded op of
 # its own (the rotation order and the dequant order are part of the result).
@@ -56,9 +60,9 @@ def kernel_isa_sha(src: str, symbol: str) -> str:
     return hashlib.sha256(text.encode()).hexdigest()[:16]
 
 
-def build(verbose: bool = False) -> str:
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp"
+def _link(sources, lib: str, verbose: bool) -> None:
+    srcs = [os.path.join(CSRC, s) for s in sources]
+    tmp = lib + ".tmp"
     cmd = [hipcc(), *FLAGS, "-I", os.path.join(ROOT, "include"), *srcs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -66,8 +70,13 @@ def build(verbose: bool = False) -> str:
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("hipcc failed building libquarot.so")
-    os.replace(tmp, LIB)
+        raise RuntimeError("hipcc failed building " + os.path.basename(lib))
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    _link(SOURCES, LIB, verbose)
+    _link(PROBE_SOURCES, PROBE_LIB, verbose)
     # fingerprints of the per-token GEMMs' machine code, which the bench's
     # stored hardware byte counts refer to: one "name sha" line per kernel
     lines = []

@@ -177,56 +177,6 @@ int quarot_version(void)
     return 100;  // 0.1.0
 }
 
-quarot_status quarot_device_peaks(int *cu_count, int *max_clock_khz)
-{
-    if (!cu_count || !max_clock_khz)
-        return QUAROT_ERR_INVALID_ARG;
-    quarot_status st = check_device(__func__);
-    if (st)
-        return st;
-    int dev = 0, cus = 0, clk = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess)
-        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e == hipSuccess)
-        e = hipDeviceGetAttribute(&clk, hipDeviceAttributeClockRate, dev);
-    if (e != hipSuccess)
-        return hip_fail(e);
-    *cu_count = cus;
-    *max_clock_khz = clk;
-    return QUAROT_OK;
-}
-
-quarot_status quarot_mfma_probe(int32_t *out, int64_t blocks, int iters, void *stream)
-{
-    if (blocks <= 0 || blocks > (1 << 20) || iters <= 0 || iters > (1 << 20))
-        return QUAROT_ERR_INVALID_ARG;
-    if (!out)
-        return QUAROT_ERR_INVALID_ARG;
-    if (!aligned16(out))
-        return QUAROT_ERR_ALIGNMENT;
-    quarot_status st = check_device(__func__);
-    if (st)
-        return st;
-    hipError_t e = launch_mfma_probe(out, (int)blocks, iters, (hipStream_t)stream);
-    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
-}
-
-quarot_status quarot_mfma_probe_fp6(int32_t *out, int64_t blocks, int iters, void *stream)
-{
-    if (blocks <= 0 || blocks > (1 << 20) || iters <= 0 || iters > (1 << 20))
-        return QUAROT_ERR_INVALID_ARG;
-    if (!out)
-        return QUAROT_ERR_INVALID_ARG;
-    if (!aligned16(out))
-        return QUAROT_ERR_ALIGNMENT;
-    quarot_status st = check_device(__func__);
-    if (st)
-        return st;
-    hipError_t e = launch_mfma_probe_fp6(out, (int)blocks, iters, (hipStream_t)stream);
-    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
-}
-
 quarot_status quarot_hadamard_factor(int64_t n, int *log2_pow2, int *m)
 {
     if (!log2_pow2 || !m || n <= 0)

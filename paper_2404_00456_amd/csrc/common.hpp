@@ -267,10 +267,6 @@ hipError_t launch_gemm_grouped_e3m2(const GemmArgs &a, int group, hipStream_t s)
 hipError_t launch_quant_grouped(const void *y, bool f32_in, uint8_t *q, uint16_t *scale,
                                 int64_t rows, int n, int group, float clip, hipStream_t s);
 hipError_t launch_kv_dequant(const KvDeqArgs &a, bool inverse_rotate, hipStream_t s);
-// Measurement: blocks x 512 threads of int8-MFMA chains; out[blocks * 512].
-hipError_t launch_mfma_probe(int32_t *out, int blocks, int iters, hipStream_t s);
-// Measurement: the same with v_mfma_f32_16x16x128_f8f6f4 on e3m2 operands.
-hipError_t launch_mfma_probe_fp6(int32_t *out, int blocks, int iters, hipStream_t s);
 hipError_t launch_swiglu(const uint16_t *g, const uint16_t *u, uint16_t *h, int64_t count,
                          hipStream_t s);
 

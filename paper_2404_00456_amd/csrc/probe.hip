@@ -1,3 +1,4 @@
+// libquarot_probe (include/quarot_probe.h), built apart from libquarot.
 // Measurement utilities (not steps of the method): MFMA-only loops that give
 // the attainable rate of v_mfma_i32_16x16x64_i8 (the int4-operand GEMM's
 // instruction) and of v_mfma_f32_16x16x128_f8f6f4 on e3m2 operands (the
@@ -8,9 +9,13 @@
 // wave keeps 8 independent accumulators and cycles through 4 operand pairs
 // drawn from a per-lane hash, so the multipliers see changing data.  Each
 // thread writes one int32 (the accumulator sum) so nothing is dead code.
-#include "common.hpp"
+#include "../../include/quarot_probe.h"
 
-namespace quarot {
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
@@ -79,18 +84,90 @@ __global__ __launch_bounds__(512, 1) void k_mfma_probe_fp6(int32_t *out, int ite
     out[(int64_t)blockIdx.x * 512 + threadIdx.x] = __float_as_int(s);
 }
 
+thread_local int g_probe_hip_error = 0;
+
+quarot_status hip_fail(hipError_t e)
+{
+    g_probe_hip_error = (int)e;
+    return QUAROT_ERR_HIP;
+}
+
+// the current device is a gfx950
+quarot_status check_device()
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        g_probe_hip_error = (int)e;
+        return QUAROT_ERR_NO_DEVICE;
+    }
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) {
+        g_probe_hip_error = (int)e;
+        return QUAROT_ERR_NO_DEVICE;
+    }
+    return std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? QUAROT_OK : QUAROT_ERR_NO_DEVICE;
+}
+
+quarot_status check_probe(const int32_t *out, int64_t blocks, int iters)
+{
+    if (blocks <= 0 || blocks > (1 << 20) || iters <= 0 || iters > (1 << 20) || !out)
+        return QUAROT_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(out) & 15u)
+        return QUAROT_ERR_ALIGNMENT;
+    return check_device();
+}
+
 }  // namespace
 
-hipError_t launch_mfma_probe_fp6(int32_t *out, int blocks, int iters, hipStream_t s)
+extern "C" {
+
+quarot_status quarot_device_peaks(int *cu_count, int *max_clock_khz)
 {
-    hipLaunchKernelGGL(k_mfma_probe_fp6, dim3((unsigned)blocks), dim3(512), 0, s, out, iters);
-    return hipGetLastError();
+    if (!cu_count || !max_clock_khz)
+        return QUAROT_ERR_INVALID_ARG;
+    quarot_status st = check_device();
+    if (st)
+        return st;
+    int dev = 0, cus = 0, clk = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess)
+        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+        e = hipDeviceGetAttribute(&clk, hipDeviceAttributeClockRate, dev);
+    if (e != hipSuccess)
+        return hip_fail(e);
+    *cu_count = cus;
+    *max_clock_khz = clk;
+    return QUAROT_OK;
 }
 
-hipError_t launch_mfma_probe(int32_t *out, int blocks, int iters, hipStream_t s)
+quarot_status quarot_mfma_probe(int32_t *out, int64_t blocks, int iters, void *stream)
 {
-    hipLaunchKernelGGL(k_mfma_probe, dim3((unsigned)blocks), dim3(512), 0, s, out, iters);
-    return hipGetLastError();
+    quarot_status st = check_probe(out, blocks, iters);
+    if (st)
+        return st;
+    hipLaunchKernelGGL(k_mfma_probe, dim3((unsigned)blocks), dim3(512), 0, (hipStream_t)stream,
+                       out, iters);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
 }
 
-}  // namespace quarot
+quarot_status quarot_mfma_probe_fp6(int32_t *out, int64_t blocks, int iters, void *stream)
+{
+    quarot_status st = check_probe(out, blocks, iters);
+    if (st)
+        return st;
+    hipLaunchKernelGGL(k_mfma_probe_fp6, dim3((unsigned)blocks), dim3(512), 0,
+                       (hipStream_t)stream, out, iters);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? QUAROT_OK : hip_fail(e);
+}
+
+int quarot_probe_last_hip_error(void)
+{
+    return g_probe_hip_error;
+}
+
+}  // extern "C"

@@ -90,7 +90,6 @@ int main()
                                       P, 1 << 20, nullptr) != 0, 1);
     EXPECT(quarot_hadamard_heads(H, H2, 4, 3, 128, nullptr), QUAROT_ERR_UNSUPPORTED_SIZE);
     EXPECT(quarot_swiglu(H, H, H2, 7, nullptr) != 0, 1);
-    EXPECT(quarot_mfma_probe(static_cast<int32_t *>(P2), 0, 10, nullptr), QUAROT_ERR_INVALID_ARG);
 
     // valid calls with no device stop at the device check
     EXPECT(quarot_hadamard(H, H2, 4, 11008, nullptr), QUAROT_ERR_NO_DEVICE);

@@ -24,8 +24,6 @@ hipError_t launch_quant_grouped(const void *, bool, uint8_t *, uint16_t *, int64
     return stub();
 }
 hipError_t launch_kv_dequant(const KvDeqArgs &, bool, hipStream_t) { return stub(); }
-hipError_t launch_mfma_probe(int32_t *, int, int, hipStream_t) { return stub(); }
-hipError_t launch_mfma_probe_fp6(int32_t *, int, int, hipStream_t) { return stub(); }
 hipError_t launch_swiglu(const uint16_t *, const uint16_t *, uint16_t *, int64_t, hipStream_t)
 {
     return stub();

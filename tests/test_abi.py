@@ -1,6 +1,8 @@
 """C-ABI checks that need no GPU: the library loads, exports every symbol
-that include/quarot.h declares, answers host-only queries, and rejects bad
-arguments before touching any device.  No kernel is launched here."""
+that include/quarot.h declares (and the measurement library every symbol of
+include/quarot_probe.h, which libquarot itself does not export), answers
+host-only queries, and rejects bad arguments before touching any device.
+No kernel is launched here."""
 import ctypes
 import os
 import re
@@ -10,8 +12,9 @@ import pytest
 
 import paper_2404_00456_amd as q
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
-                      "include", "quarot.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+HEADER = os.path.join(INCLUDE, "quarot.h")
+PROBE_HEADER = os.path.join(INCLUDE, "quarot_probe.h")
 
 OK, INVALID, UNSUPPORTED, ALIGN, WORKSPACE, NODEV, HIP = range(7)
 
@@ -21,8 +24,8 @@ P2 = ctypes.c_void_p((1 << 20) + 4096)
 UNALIGNED = ctypes.c_void_p((1 << 20) + 8)
 
 
-def declared_functions():
-    src = open(HEADER).read()
+def declared_functions(header=HEADER):
+    src = open(header).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     return sorted(set(re.findall(r"\b(quarot_[a-z0-9_]+)\s*\(", src)))
 
@@ -37,6 +40,11 @@ def L():
     return q.lib()
 
 
+@pytest.fixture(scope="module")
+def PL():
+    return q.probe_lib()
+
+
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
     assert len(names) >= 12
@@ -44,6 +52,15 @@ def test_exports_every_declared_symbol(L):
         assert hasattr(L, name), name
     # and the binding declares exactly those signatures
     assert sorted(q.SIGNATURES) == names
+
+
+def test_probe_library_is_apart(L, PL):
+    names = declared_functions(PROBE_HEADER)
+    assert len(names) == 4
+    for name in names:
+        assert hasattr(PL, name), name
+        assert not hasattr(L, name), name  # measurement tools stay out of libquarot
+    assert sorted(q.PROBE_SIGNATURES) == names
 
 
 def test_status_strings(L):
@@ -189,12 +206,6 @@ def test_invalid_arguments_rejected_before_device(L):
     assert L.quarot_hadamard_heads(None, None, 0, 64, 128, S) == OK
     assert L.quarot_hadamard_heads_quant_int4(P, P2, None, 4, 64, 128, 1.0, S) == INVALID
     assert L.quarot_hadamard_heads_quant_int4(P, P2, P, 4, 64, 128, 2.0, S) == INVALID
-    # measurement utilities
-    assert L.quarot_device_peaks(None, None) == INVALID
-    assert L.quarot_mfma_probe(P, 0, 10, S) == INVALID
-    assert L.quarot_mfma_probe(P, 4, 0, S) == INVALID
-    assert L.quarot_mfma_probe(None, 4, 10, S) == INVALID
-    assert L.quarot_mfma_probe(UNALIGNED, 4, 10, S) == ALIGN
     # group-wise
     G = L.quarot_quant_int4_grouped
     assert G(P, P2, P, 4, 128, 0, 1, 1.0, P, 1 << 20, S) == INVALID
@@ -275,7 +286,25 @@ def test_invalid_arguments_rejected_before_device(L):
     assert SE(P, P2, P, P2, 4, 8192 + 128, 1.0, S) == UNSUPPORTED
     assert SE(P, P2, P, P2, 4, 28672, 0.0, S) == INVALID
     assert SE(P, None, P, P2, 4, 28672, 1.0, S) == INVALID
-    assert L.quarot_mfma_probe_fp6(P, 0, 10, S) == INVALID
+
+
+def test_probe_arguments_rejected_before_device(PL):
+    S = None
+    assert PL.quarot_device_peaks(None, None) == INVALID
+    for probe in (PL.quarot_mfma_probe, PL.quarot_mfma_probe_fp6):
+        assert probe(P, 0, 10, S) == INVALID
+        assert probe(P, 4, 0, S) == INVALID
+        assert probe(P, (1 << 20) + 1, 10, S) == INVALID
+        assert probe(None, 4, 10, S) == INVALID
+        assert probe(UNALIGNED, 4, 10, S) == ALIGN
+
+
+@pytest.mark.skipif(has_gpu(), reason="valid arguments would reach a real device")
+def test_probe_no_device_reported(PL):
+    cus, clk = ctypes.c_int(), ctypes.c_int()
+    assert PL.quarot_device_peaks(ctypes.byref(cus), ctypes.byref(clk)) == NODEV
+    assert PL.quarot_mfma_probe(P, 4, 10, None) == NODEV
+    assert PL.quarot_mfma_probe_fp6(P, 4, 10, None) == NODEV
 
 
 @pytest.mark.skipif(has_gpu(), reason="valid arguments would reach a real device")
@@ -290,9 +319,6 @@ def test_no_device_reported(L):
                                        None) == NODEV
     assert L.quarot_w4a4_gemm_grouped(P, P, P, P, P, 4, 4, 256, 64, None) == NODEV
     assert L.quarot_w4a4_gemm_grouped_e3m2(P, P, P, P, P, 8, 8, 256, 128, None) == NODEV
-    cus, clk = ctypes.c_int(), ctypes.c_int()
-    assert L.quarot_device_peaks(ctypes.byref(cus), ctypes.byref(clk)) == NODEV
-    assert L.quarot_mfma_probe(P, 4, 10, None) == NODEV
     assert L.quarot_linear_w4a4_grouped(P, P, P, P, 4, 4, 256, 256, 1, 1.0, P, 1 << 20,
                                         None) == NODEV
     assert L.quarot_pack_e3m2(P, P2, 4, 128, None) == NODEV
@@ -302,7 +328,6 @@ def test_no_device_reported(L):
     assert L.quarot_quant_int4_e3m2(P, P2, P2, 4, 13824, 1, 1.0, None) == NODEV
     assert L.quarot_linear_e3m2(P, P, P, P, 4, 4, 8192, 1, 1.0, P, 1 << 20, None) == NODEV
     assert L.quarot_swiglu_quant_e3m2(P, P2, P, P2, 4, 28672, 1.0, None) == NODEV
-    assert L.quarot_mfma_probe_fp6(P, 4, 10, None) == NODEV
     assert L.quarot_linear_e3m2_scratch(P, P, P, P, 2048, 4, 28672, 1, 1.0, None) == NODEV
 
 
