@@ -73,7 +73,9 @@ typedef enum {
     QUAROT_ERR_HIP = 6              /* a HIP runtime call failed */
 } quarot_status;
 
-/* Human-readable name of a status code (static string, never NULL). */
+/* Human-readable name of a status code (static string, never NULL).  Takes
+ * an int rather than quarot_status so that any integer, also one that is no
+ * status, is a valid argument ("QUAROT_ERR_UNKNOWN"). */
 const char *quarot_status_string(int status);
 
 /* Raw hipError_t of the last QUAROT_ERR_HIP on the calling thread (0 if none). */
