@@ -101,7 +101,12 @@ def _gemm_case(dev, orc, M, N, K, xq, wq, sx, sw):
                                    # k-steps (four 128 x 128 waves per block):
                                    # one tile, one per block, several per block
                                    (512, 512, 1024), (2048, 8192, 1280), (4096, 8192, 512),
-                                   (8192, 4096, 768), (4352, 4352, 1536)])
+                                   (8192, 4096, 768), (4352, 4352, 1536),
+                                   # 128-row tiles with split k-steps: the
+                                   # fewest pairs (K = 512), one row past a
+                                   # tile, N not a multiple of 4, one column
+                                   # of tiles
+                                   (129, 300, 512), (1000, 36, 768), (640, 1030, 2048)])
 def test_gemm_e3m2_exact(dev, orc, M, N, K):
     """Ragged edges, k-step counts below, at and above the LDS ring depth,
     blocks that walk several tiles, the largest K."""
