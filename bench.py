@@ -702,6 +702,16 @@ def main():
         kernels[wl.name]["rotate_quant_warm_us"] = round(w_us, 2)
         kernels[wl.name]["rotate_quant_cold_us"] = round(c_us, 2)
         kernels[wl.name]["rotate_quant_cold_frac_hbm"] = round(hbm_us / c_us, 4)
+        # the standalone rotation (fp16 in, fp16 out: 4 bytes per element)
+        yh = torch.empty_like(L["xd"])
+        had = event_times_us(torch, stream,
+                             [lambda xd=L["xd"], yh=yh: q.quarot_hadamard(xd, y=yh)], 10)[0]
+        del yh
+        h_us = float(np.mean(had))
+        h_gbs = wl.M * wl.K * 4 / (h_us * 1e-6) / 1e9
+        kernels[wl.name]["hadamard_fp16_us"] = round(h_us, 2)
+        kernels[wl.name]["hadamard_fp16_GBps"] = round(h_gbs, 1)
+        kernels[wl.name]["hadamard_fp16_frac_hbm"] = round(h_gbs / PEAK_HBM_GBS, 4)
     torch.cuda.empty_cache()
 
     drawn_7b = {}
