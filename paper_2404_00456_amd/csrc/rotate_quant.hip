@@ -735,6 +735,12 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
         w = wave;
     }
 
+    // LDS of the wave exchange below and, for fp16 output, of the row's
+    // staging before its stores
+    constexpr int XS_BYTES = W > 1 ? W * M * 64 * 4 : 16;
+    constexpr int ST_BYTES = (EPI == EPI_F16 && W > 1) ? N * 2 : 16;
+    __shared__ uint4 lbuf[(XS_BYTES > ST_BYTES ? XS_BYTES : ST_BYTES) / 16];
+
     float v[C][M];
 #pragma unroll
     for (int cc = 0; cc < C; ++cc) {
@@ -751,7 +757,7 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
     // group bits 0..LOGL-1 across lanes
     const float sigma = lane_stages<LOGL, C * M>(&v[0][0], lane, pos);
     if constexpr (W > 1) {
-        __shared__ float xs[W][M][64];
+        float(*xs)[M][64] = reinterpret_cast<float(*)[M][64]>(lbuf);
 #pragma unroll
         for (int j = 0; j < LOGW; ++j) {
             const int pw = w ^ (1 << j);
@@ -792,7 +798,23 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
                 v[cc][b] = v[cc][b] * sc;
         }
 
-    if constexpr (EPI == EPI_F16 || EPI == EPI_F32) {
+    if constexpr (EPI == EPI_F16 && W > 1) {
+        // a lane's M outputs sit 2 M bytes apart from the next lane's: the
+        // row goes through LDS (the exchange's, whose last reads are behind
+        // its barriers) and out as 16 consecutive bytes per lane
+        uint16_t *st = reinterpret_cast<uint16_t *>(lbuf);
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc) {
+            const int g = (cc * W + w) * L + pos;
+#pragma unroll
+            for (int p = 0; p < M / 4; ++p)
+                store4(st + g * M + 4 * p, &v[cc][4 * p]);
+        }
+        __syncthreads();
+        uint4 *dst = reinterpret_cast<uint4 *>(static_cast<uint16_t *>(a.out) + row * N);
+        for (int c = tid; c < N / 8; c += 64 * W)
+            dst[c] = lbuf[c];
+    } else if constexpr (EPI == EPI_F16 || EPI == EPI_F32) {
 #pragma unroll
         for (int cc = 0; cc < C; ++cc) {
             const int g = (cc * W + w) * L + pos;
