@@ -814,6 +814,25 @@ __global__ __launch_bounds__(W == 1 ? 256 : 64 * W) void k_rot_smallm(RotArgs a)
         uint4 *dst = reinterpret_cast<uint4 *>(static_cast<uint16_t *>(a.out) + row * N);
         for (int c = tid; c < N / 8; c += 64 * W)
             dst[c] = lbuf[c];
+    } else if constexpr (EPI == EPI_F32 && W > 1) {
+        // the same for binary32 output, one chunk cc (W L groups, M W L
+        // consecutive elements, the size of the exchange's buffer) at a time
+        float *st = reinterpret_cast<float *>(lbuf);
+        static_assert(M * W * 64 * 4 <= XS_BYTES, "a chunk fits the exchange buffer");
+#pragma unroll
+        for (int cc = 0; cc < C; ++cc) {
+            const int g = w * L + pos;  // group within the chunk
+#pragma unroll
+            for (int p = 0; p < M / 4; ++p)
+                *reinterpret_cast<float4 *>(st + g * M + 4 * p) =
+                    make_float4(v[cc][4 * p], v[cc][4 * p + 1], v[cc][4 * p + 2], v[cc][4 * p + 3]);
+            __syncthreads();
+            uint4 *dst = reinterpret_cast<uint4 *>(static_cast<float *>(a.out) + row * N +
+                                                   (int64_t)cc * (M * W * L));
+            for (int c = tid; c < M * W * L / 4; c += 64 * W)
+                dst[c] = lbuf[c];
+            __syncthreads();
+        }
     } else if constexpr (EPI == EPI_F16 || EPI == EPI_F32) {
 #pragma unroll
         for (int cc = 0; cc < C; ++cc) {
