@@ -25,7 +25,9 @@ def dev():
 @pytest.mark.parametrize("n,group,rotate,rows", [
     (4096, 128, True, 67), (4096, 64, True, 40), (4096, 256, True, 33), (11008, 128, True, 19),
     (8192, 256, False, 50), (128, 8, True, 300), (512, 512, True, 9), (28672, 128, True, 5),
-    (5120, 32, True, 17), (256, 16, False, 130)])
+    (5120, 32, True, 17), (256, 16, False, 130),
+    # multi-wave rows of m = 12, 20, 28 (binary32 rows staged through LDS)
+    (6144, 128, True, 7), (24576, 256, True, 3), (20480, 128, True, 4), (14336, 64, True, 6)])
 def test_group_quant(dev, orc, n, group, rotate, rows):
     import paper_2404_00456_amd as q
     say(f"group quant n={n} group={group} rotate={rotate} rows={rows}")
