@@ -210,6 +210,39 @@ def test_gemm_e3m2_7b_shapes(dev, orc, M, N, K):
     assert_same(H(y6o[rows]).view(np.uint16), ry.view(np.uint16), "7B shape sampled rows")
 
 
+@pytest.mark.parametrize("case", range(24))
+def test_gemm_e3m2_random_grids(dev, orc, case):
+    """Seeded random shapes with more than 128 rows and K a multiple of 256
+    (the tile walks of both e3m2 kernels, one to three tiles per block,
+    ragged edges): every acc and y equal to the int4 path's, with and
+    without the int32 output, and two seeded rows equal to the oracle's."""
+    import torch
+    import paper_2404_00456_amd as q
+    rng = np.random.default_rng(1000 + case)
+    M = int(rng.integers(129, 4097))
+    N = int(rng.integers(1, 8193))
+    K = 256 * int(rng.integers(2, 33))
+    say(f"e3m2 gemm random grid {case}: M={M} N={N} K={K}")
+    g = torch.Generator(device=dev).manual_seed(case)
+    xq = torch.randint(0, 256, (M, K // 2), generator=g, device=dev, dtype=torch.uint8)
+    wq = torch.randint(0, 256, (N, K // 2), generator=g, device=dev, dtype=torch.uint8)
+    sx = (torch.rand(M, generator=g, device=dev) * 0.05 + 0.001).half()
+    sw = (torch.rand(N, generator=g, device=dev) * 0.01 + 0.0001).half()
+    x6, w6 = q.quarot_pack_e3m2(xq), q.quarot_pack_e3m2(wq)
+    y4, a4 = q.quarot_w4a4_gemm(xq, sx, wq, sw, want_acc=True)
+    y6, a6 = q.quarot_w4a4_gemm_e3m2(x6, sx, w6, sw, want_acc=True)
+    y6o = q.quarot_w4a4_gemm_e3m2(x6, sx, w6, sw)
+    torch.cuda.synchronize()
+    assert int((a4 != a6).sum().item()) == 0
+    assert int((y4.view(torch.int16) != y6.view(torch.int16)).sum().item()) == 0
+    assert int((y4.view(torch.int16) != y6o.view(torch.int16)).sum().item()) == 0
+    rows = np.array(sorted({int(rng.integers(0, M)), M - 1}))
+    racc = orc.gemm_i32(H(xq[rows]), H(wq))
+    assert_same(H(a6[rows]), racc, "random grid sampled acc")
+    ry = orc.dequant(racc, H(sx[rows]), H(sw))
+    assert_same(H(y6o[rows]).view(np.uint16), ry.view(np.uint16), "random grid sampled rows")
+
+
 # ------------------------------------------- quantizer writing e3m2 ---
 
 E3M2_ROTATED_N = [128, 256, 1024, 4096, 8192, 16384, 32768, 12288, 24576, 10240, 20480, 14336,
