@@ -88,6 +88,21 @@ def test_hadamard_fp16(dev, orc, n):
     assert_fp16_close(y, orc.hadamard(x), f"hadamard n={n}")
 
 
+@pytest.mark.parametrize("n", [8192, 28672, 11008])
+def test_hadamard_fp16_many_rows(dev, orc, n):
+    """The standalone rotation over 2048 rows (every block of the grid busy
+    several times over): seeded sampled rows equal to the oracle's, the
+    first and last included."""
+    import paper_2404_00456_amd as q
+    rows = 2048
+    say(f"hadamard many rows n={n} rows={rows}")
+    x = workloads.random_rows(n + 11, rows, n, "normal")
+    y = H(q.quarot_hadamard(T(x, dev)))
+    rng = np.random.default_rng(n)
+    sel = np.unique(np.concatenate([[0, rows - 1], rng.integers(0, rows, 10)]))
+    assert_fp16_close(y[sel], orc.hadamard(x[sel]), f"hadamard many rows n={n}")
+
+
 @pytest.mark.parametrize("n", [8, 128, 1024, 8192, 32768, 24, 3072, 5120, 28672, 216, 11008])
 def test_hadamard_in_place(dev, orc, n):
     """x == y is allowed: every kernel family (power of two, exact small m,
