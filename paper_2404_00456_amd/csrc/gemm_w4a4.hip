@@ -24,6 +24,7 @@
 // XCDs round-robin) and, within an XCD, in groups of 8 m-tiles, so blocks
 // that share an L2 also share operand panels.
 #include "gemm_common.hpp"
+#include "gemm_plan.hpp"
 
 namespace quarot {
 namespace {
@@ -1286,45 +1287,23 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s, int bits)
 {
     if (a.M == 0 || a.N == 0)
         return hipSuccess;
-    const bool main = bits != 4 || (a.K % 128) == 0;
-    const int ksteps = bits == 8 ? a.K / 64 : a.K / 128;
-    if (!main) {
-        const int TM = (a.M + BM - 1) / BM, TN = (a.N + BN - 1) / BN;
-        hipError_t e = hipFuncSetAttribute((const void *)k_gemm_w4a4_k64,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
-        if (e != hipSuccess)
-            return e;
-        hipLaunchKernelGGL(k_gemm_w4a4_k64, dim3((unsigned)(TM * TN)), dim3(THREADS), LDS_BYTES,
-                           s, a);
-        return hipGetLastError();
-    }
-    // persistent: one block per CU (256 on MI355X), or fewer for small
-    // problems; the LDS ring allows one resident block per CU.  With fewer
-    // than S k-steps, one tile per block (see the kernel).
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         cus <= 0)
         cus = 256;
-    // 128-row block tiles when that takes less time over the CUs: with one
-    // wave per SIMD a 128 x 256 tile takes about 0.9 of a 256 x 256 tile's
-    // time (measured on the 7B down-projection shape: 74.6 against 81.8 us
-    // for one round each), so only grids that leave CUs idle gain (2048 x
-    // 4096 outputs: 128 large tiles for 256 CUs), not the 16384-token ones.
-    const int TN = (a.N + BN - 1) / BN;
-    const int64_t t256 = (int64_t)((a.M + 255) / 256) * TN, t128 = (int64_t)((a.M + 127) / 128) * TN;
-    const int64_t r256 = (t256 + cus - 1) / cus, r128 = (t128 + cus - 1) / cus;
-    // e3m2 codes with K a multiple of 256: the 128-row tiles with the
-    // k-steps split between two wave groups, which take about KSPLIT_COST %
-    // of a 256 x 256 tile's time
-    constexpr int KSPLIT_COST = 70;
-    const bool ksplit =
-        bits == 6 && a.K % 256 == 0 && a.K >= 512 && a.M > 128 && r128 * KSPLIT_COST < r256 * 100;
-    const bool m128 = ksplit || (ksteps >= S && a.M > 128 && r128 * 90 < r256 * 100);
-    const int64_t tiles = m128 ? t128 : t256;
-    int grid = (int)((tiles < cus || ksteps < S) ? tiles : cus);
-    if (grid >= 8 && tiles % 8 == 0)
-        grid -= grid % 8;
+    const GemmPlan plan = plan_gemm(a.M, a.N, a.K, bits, cus, S);
+    const int grid = plan.grid;
+    if (plan.kernel == GemmKernel::K64) {
+        hipError_t e = hipFuncSetAttribute((const void *)k_gemm_w4a4_k64,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+        if (e != hipSuccess)
+            return e;
+        hipLaunchKernelGGL(k_gemm_w4a4_k64, dim3((unsigned)grid), dim3(THREADS), LDS_BYTES, s, a);
+        return hipGetLastError();
+    }
+    const bool ksplit = plan.kernel == GemmKernel::Ksplit;
+    const bool m128 = plan.kernel == GemmKernel::Tile128;
     const void *fn;
     int lds_bytes, threads;
     if (ksplit) {
